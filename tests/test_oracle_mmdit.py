@@ -1,0 +1,135 @@
+"""Pins of the joint-attention (MMDiT-style) oracle, CPU only."""
+import math
+
+import numpy as np
+
+import synth
+from oracle import dit, mmdit
+from test_oracle_pins import brute_attention
+
+TINY = synth.reduced(synth.workload("mmdit1024"), hidden=16, heads=2, head_dim=8,
+                     depth=2, mlp_hidden=32, text_dim=6, text_tokens=3,
+                     latent_channels=2, requests=((4, 6),), freq_dim=8)
+
+
+def weights(w=TINY, seed=21, std=0.3):
+    rng = np.random.default_rng(seed)
+    return mmdit.as_dict(w, [rng.standard_normal(s) * std for _, s in mmdit.weight_layout(w)])
+
+
+def brute_rope(x, rows, cols, heads):
+    n, dm = x.shape
+    d = dm // heads
+    out = np.zeros_like(x)
+    for t in range(n):
+        for h in range(heads):
+            for half in range(2):
+                pos = rows[t] if half == 0 else cols[t]
+                for j in range(d // 4):
+                    a = h * d + half * (d // 2) + 2 * j
+                    ang = pos * 10000.0 ** (-j / (d // 4))
+                    out[t, a] = x[t, a] * math.cos(ang) - x[t, a + 1] * math.sin(ang)
+                    out[t, a + 1] = x[t, a] * math.sin(ang) + x[t, a + 1] * math.cos(ang)
+    return out
+
+
+def test_rope_brute_force_identity_and_norm():
+    rng = np.random.default_rng(0)
+    x = rng.standard_normal((12, 16))
+    rows, cols = mmdit.grid_positions(3, 4)
+    r = mmdit.rope_2d(x, rows, cols, 2)
+    assert np.allclose(r, brute_rope(x, rows, cols, 2), atol=1e-13)
+    assert np.allclose(r[0], x[0])                       # position (0, 0)
+    assert np.allclose(np.linalg.norm(r, axis=1), np.linalg.norm(x, axis=1))
+    # per-head, per-pair norms are preserved too
+    assert np.allclose(r[:, 0::2] ** 2 + r[:, 1::2] ** 2, x[:, 0::2] ** 2 + x[:, 1::2] ** 2)
+
+
+def test_rope_scores_depend_on_relative_position_only():
+    rng = np.random.default_rng(1)
+    q, k = rng.standard_normal((1, 16)), rng.standard_normal((1, 16))
+
+    def score(p, pp):
+        a = mmdit.rope_2d(q, [p[0]], [p[1]], 2)
+        b = mmdit.rope_2d(k, [pp[0]], [pp[1]], 2)
+        return float((a * b).sum())
+
+    base = score((1, 2), (4, 7))
+    assert math.isclose(base, score((3, 5), (6, 10)), rel_tol=1e-11)
+    assert math.isclose(base, score((0, 0), (3, 5)), rel_tol=1e-11)
+    assert not math.isclose(base, score((0, 0), (3, 6)), rel_tol=1e-6)
+
+
+def test_zero_gates_identity_both_streams():
+    W = weights()
+    D = TINY.hidden
+    for b in range(TINY.depth):
+        for s in mmdit.STREAMS:
+            for chunk in (2, 5):
+                W[f"blocks.{b}.{s}.ada.w"][chunk * D:(chunk + 1) * D] = 0
+                W[f"blocks.{b}.{s}.ada.b"][chunk * D:(chunk + 1) * D] = 0
+    rng = np.random.default_rng(2)
+    xt, xi = rng.standard_normal((3, D)), rng.standard_normal((6, D))
+    c = rng.standard_normal(D)
+    rows, cols = mmdit.grid_positions(2, 3)
+    for b in range(TINY.depth):
+        nt, ni = mmdit.joint_block(W, TINY, b, xt, xi, c, rows, cols)
+        assert np.array_equal(nt, xt) and np.array_equal(ni, xi)
+
+
+def test_joint_attention_brute_force_and_empty_text():
+    """Joint block attention equals brute-force attention over [text; image]."""
+    W = weights()
+    D, H = TINY.hidden, TINY.heads
+    rng = np.random.default_rng(3)
+    xt, xi = rng.standard_normal((3, D)), rng.standard_normal((6, D))
+    c = rng.standard_normal(D)
+    rows, cols = mmdit.grid_positions(2, 3)
+    nt, ni = mmdit.joint_block(W, TINY, 0, xt, xi, c, rows, cols)
+    # rebuild the image-stream output by brute force
+    qs, ks, vs = [], [], []
+    for s, x in (("txt", xt), ("img", xi)):
+        md = mmdit.stream_modulation(W, TINY, c, 0, s)
+        h = dit.modulate(dit.layer_norm(x, TINY.ln_eps), md["shift_msa"], md["scale_msa"])
+        qkv = h @ W[f"blocks.0.{s}.qkv.w"].T + W[f"blocks.0.{s}.qkv.b"]
+        q, k, v = qkv[:, :D], qkv[:, D:2 * D], qkv[:, 2 * D:]
+        if s == "img":
+            q, k = brute_rope(q, rows, cols, H), brute_rope(k, rows, cols, H)
+        qs.append(q), ks.append(k), vs.append(v)
+    o = brute_attention(np.vstack(qs), np.vstack(ks), np.vstack(vs), H)
+    md = mmdit.stream_modulation(W, TINY, c, 0, "img")
+    x = xi + md["gate_msa"] * (o[3:] @ W["blocks.0.img.o.w"].T + W["blocks.0.img.o.b"])
+    h = dit.modulate(dit.layer_norm(x, TINY.ln_eps), md["shift_mlp"], md["scale_mlp"])
+    u = dit.gelu_tanh(h @ W["blocks.0.img.fc1.w"].T + W["blocks.0.img.fc1.b"])
+    x = x + md["gate_mlp"] * (u @ W["blocks.0.img.fc2.w"].T + W["blocks.0.img.fc2.b"])
+    assert np.allclose(ni, x, atol=1e-12)
+    # no text tokens: the image stream is plain self-attention with RoPE
+    nt0, ni0 = mmdit.joint_block(W, TINY, 0, np.zeros((0, D)), xi, c, rows, cols)
+    assert nt0.shape == (0, D)
+    o = brute_attention(qs[1], ks[1], vs[1], H)
+    x = xi + md["gate_msa"] * (o @ W["blocks.0.img.o.w"].T + W["blocks.0.img.o.b"])
+    h = dit.modulate(dit.layer_norm(x, TINY.ln_eps), md["shift_mlp"], md["scale_mlp"])
+    u = dit.gelu_tanh(h @ W["blocks.0.img.fc1.w"].T + W["blocks.0.img.fc1.b"])
+    x = x + md["gate_mlp"] * (u @ W["blocks.0.img.fc2.w"].T + W["blocks.0.img.fc2.b"])
+    assert np.allclose(ni0, x, atol=1e-12)
+
+
+def test_forward_runs_and_embeds():
+    W = weights()
+    rng = np.random.default_rng(4)
+    lat = rng.standard_normal((2, 4, 6))
+    text = rng.standard_normal((3, 6))
+    v, xt, xi = mmdit.forward(W, TINY, lat, 1.0, text)
+    assert v.shape == lat.shape and xt.shape == (3, 16) and xi.shape == (6, 16)
+    _, xt0, xi0 = mmdit.forward(W, TINY, lat, 1.0, text, n_blocks=0)
+    assert np.allclose(xi0, dit.patchify(lat, 2) @ W["x_embed.w"].T + W["x_embed.b"])
+    assert np.allclose(xt0, text @ W["y_embed.w"].T + W["y_embed.b"])
+
+
+def test_layout_sizes():
+    w = synth.workload("mmdit1024")
+    n = sum(int(np.prod(s)) for _, s in mmdit.weight_layout(w))
+    D, F = 3072, 12288
+    per_block = 2 * (6 * D * D + 6 * D + 3 * D * D + 3 * D + D * D + D + F * D + F + D * F + D)
+    assert n == per_block * 19 + (D * 64 + D) + (D * 256 + D + D * D + D) + (D * 4096 + D) \
+        + (2 * D * D + 2 * D) + (64 * D + 64)
