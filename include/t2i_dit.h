@@ -1,0 +1,260 @@
+/*
+ * t2i_dit.h -- C ABI of the MI355X (gfx950) diffusion-transformer denoising step.
+ *
+ * ServerlessT2I (Sec. 4, Fig. "Flux function" and Fig. "workflow definition")
+ * treats the base diffusion model as a stateless model function: it loads its
+ * bf16 weights once, then each call takes `latents` and `prompt_embeds` and
+ * returns `noise_pred`; an orchestrator loop calls it once per denoising step
+ * and applies `denoise(noise_pred, latents)`.  The paper calls this inference
+ * compute-bound (Sec. 3.1) and requires identical results under fixed seeds
+ * (Sec. 4, "Function-as-a-Service Paradigm"; Sec. 8.1 "validated the identity
+ * of generated images").  This library is that model function and its loop:
+ *
+ *   t2i_dit_init    load: bind the caller's device weights and workspace
+ *   t2i_dit_step    one model evaluation (+ guidance, + optional Euler update)
+ *   t2i_dit_sample  the whole denoising loop, with the optional step-skip cache
+ *   t2i_cache_check the cache-skip decision of one step
+ *
+ * Conventions for every call:
+ *   - Device pointers are HIP device memory owned by the caller; host pointers
+ *     are ordinary host memory.  Each argument says which it is.
+ *   - `stream` is a hipStream_t passed as void* (NULL = the null stream).
+ *     Launches are asynchronous on it; calls return before the GPU finishes,
+ *     except where a call says it synchronises.
+ *   - Every call validates all arguments before launching anything, returns a
+ *     t2i_status and never aborts or throws; a failed call writes nothing.
+ *     t2i_last_error() gives a message for the last failure on a handle.
+ *   - A handle is used from one host thread and one stream at a time.  The
+ *     library keeps no global mutable state; distinct handles are independent.
+ *   - Identical inputs give bitwise-identical outputs (all reductions have a
+ *     fixed order).
+ */
+#ifndef T2I_DIT_H
+#define T2I_DIT_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  T2I_OK = 0,
+  T2I_ERR_INVALID_ARG = 1,   /* NULL pointer, bad enum, struct_size mismatch */
+  T2I_ERR_SHAPE = 2,         /* sizes inconsistent with the config or limits */
+  T2I_ERR_UNSUPPORTED = 3,   /* valid but not implemented (e.g. control_outputs) */
+  T2I_ERR_WORKSPACE = 4,     /* workspace or cache state too small */
+  T2I_ERR_OUT_OF_MEMORY = 5, /* host allocation failed */
+  T2I_ERR_DEVICE = 6         /* a HIP call failed; t2i_last_error has its text */
+} t2i_status;
+
+typedef enum { T2I_F32 = 0, T2I_BF16 = 1 } t2i_dtype;
+typedef enum { T2I_ARCH_CROSS_DIT = 0, T2I_ARCH_MMDIT = 1 } t2i_arch;
+typedef enum { T2I_CACHE_ACCUMULATE = 0, T2I_CACHE_PER_STEP = 1 } t2i_cache_mode;
+
+/* Most sequences one call may carry: requests times guidance branches. */
+#define T2I_MAX_SEQ 64
+/* Most requests one call may carry. */
+#define T2I_MAX_REQ 32
+
+/*
+ * Model shape.  `dtype` is the type of weights, text embeddings and of the
+ * GEMM / attention operands; accumulation, the residual stream, LayerNorm,
+ * softmax, modulation, the final layer and the sampler are always fp32.
+ *
+ * Architecture readings (the paper names the model families -- Flux, SD3.5,
+ * Z-Image, Sec. 8.1 -- but fixes no architecture):
+ *   T2I_ARCH_CROSS_DIT  adaLN-Zero DiT blocks: self-attention, cross-attention
+ *                       to projected text (ungated, query from the raw
+ *                       residual), MLP with tanh-GELU; fixed 2D sin-cos
+ *                       position embedding.
+ *   T2I_ARCH_MMDIT      joint attention over [text; image] with per-stream
+ *                       weights and 2D RoPE on image queries and keys.
+ */
+typedef struct t2i_dit_config {
+  uint32_t struct_size;      /* = sizeof(t2i_dit_config) */
+  int32_t arch;              /* t2i_arch */
+  int32_t dtype;             /* t2i_dtype */
+  int32_t latent_channels;   /* C */
+  int32_t patch;             /* p: tokens are p x p latent patches */
+  int32_t hidden;            /* D, multiple of 64 */
+  int32_t heads;             /* H, heads * head_dim == hidden */
+  int32_t head_dim;          /* d, multiple of 8, <= 128 */
+  int32_t depth;             /* number of blocks */
+  int32_t mlp_hidden;        /* F, multiple of 64 */
+  int32_t text_dim;          /* width of prompt_embeds, multiple of 64 */
+  int32_t text_tokens;       /* tokens per prompt (>= 1) */
+  int32_t freq_dim;          /* sinusoidal timestep width (even) */
+  int32_t max_tokens;        /* most image tokens one call carries, summed over
+                                requests and guidance branches */
+  int32_t max_requests;      /* most requests per call, <= T2I_MAX_REQ */
+  int32_t max_steps;         /* most steps of one t2i_dit_sample call */
+  float ln_eps;              /* LayerNorm epsilon */
+  float t_scale;             /* timestep multiplier before the sinusoid */
+} t2i_dit_config;
+
+typedef struct t2i_dit t2i_dit;  /* opaque handle, owned by the library */
+
+/*
+ * Weight table: the per-layer parameter lookup of the model function
+ * (Sec. 5.3, "Layer Lookup Table").  t2i_dit_weight_count gives its length and
+ * t2i_dit_weight_desc the name, shape (up to 4 dims, unused dims 0) and dtype
+ * of entry i.  Linear weights are [out, in] row-major (the input dimension is
+ * contiguous).  Returns 0 / T2I_ERR_* on a bad config or index.
+ */
+size_t t2i_dit_weight_count(const t2i_dit_config* cfg);
+t2i_status t2i_dit_weight_desc(const t2i_dit_config* cfg, size_t i,
+                               char name[64], int64_t shape[4], int32_t* dtype);
+
+/* Device workspace the handle needs, in bytes (0 on a bad config). */
+size_t t2i_dit_workspace_bytes(const t2i_dit_config* cfg);
+
+/*
+ * Device bytes of the cache-skip state for a request mix: n_req requests with
+ * tokens_per_req[r] image tokens each (host array) and `branches` guidance
+ * branches (1, or 2 under classifier-free guidance).
+ */
+size_t t2i_cache_state_bytes(const t2i_dit_config* cfg, int32_t n_req,
+                             const int32_t* tokens_per_req, int32_t branches);
+
+/*
+ * Create a handle (the model function's load_model).
+ *   weights   host array of t2i_dit_weight_count(cfg) device pointers, each to
+ *             a tensor of the shape and dtype t2i_dit_weight_desc gives.
+ *             Borrowed: they must stay valid and unchanged for the handle's
+ *             life (t2i_dit_rebind_weights replaces them).
+ *   workspace device buffer of ws_bytes >= t2i_dit_workspace_bytes(cfg),
+ *             256-byte aligned, borrowed for the handle's life.
+ * Touches no device memory; `stream` is unused and may be NULL.
+ */
+t2i_status t2i_dit_init(const t2i_dit_config* cfg, const void* const* weights,
+                        void* workspace, size_t ws_bytes, void* stream,
+                        t2i_dit** out);
+
+/* Replace the weight pointers (same shapes and dtypes) of a live handle. */
+t2i_status t2i_dit_rebind_weights(t2i_dit* h, const void* const* weights,
+                                  void* stream);
+
+/*
+ * One model evaluation for a batch of requests (the model function's
+ * `execute`), with classifier-free guidance and an optional Euler update.
+ *
+ * Request r has a latent of [C, lat_h[r], lat_w[r]] fp32 (both multiples of
+ * p); the latents of all requests are packed back to back in `latents`.
+ * Under guidance (guidance != 1) every request runs a conditional branch on its
+ * text and an unconditional branch on all-zero text embeddings, and
+ * v = v_u + guidance * (v_c - v_u).
+ */
+typedef struct t2i_step_args {
+  uint32_t struct_size;        /* = sizeof(t2i_step_args) */
+  int32_t n_req;               /* 1 .. max_requests */
+  const int32_t* lat_h;        /* host [n_req] */
+  const int32_t* lat_w;        /* host [n_req] */
+  const double* t;             /* host [n_req] model time of each request */
+  const double* t_next;        /* host [n_req], or NULL: no Euler update;
+                                  else latents += (t_next - t) * v in place */
+  float* latents;              /* device, packed fp32 latents */
+  const void* prompt_embeds;   /* device [n_req, text_tokens, text_dim], dtype */
+  float guidance;              /* 1 = no guidance */
+  float* noise_pred;           /* device, packed like latents, or NULL */
+  int32_t n_blocks;            /* < 0: all blocks; else run only the first
+                                  n_blocks (diagnostics; then the final layer
+                                  reads the partial residual stream) */
+  float* hidden_out;           /* device or NULL: receives the residual stream
+                                  after the blocks, fp32 [rows, hidden], rows
+                                  ordered branch-major then request; MMDiT
+                                  appends the text stream after the image */
+  const uint8_t* skip;         /* host [n_req] or NULL: 1 = reuse the cached
+                                  residual instead of running the blocks */
+  void* cache_state;           /* device or NULL: when given, computed requests
+                                  store their residual for later skips */
+  size_t cache_state_bytes;
+  const void* control_outputs; /* reserved, must be NULL */
+} t2i_step_args;
+
+t2i_status t2i_dit_step(t2i_dit* h, const t2i_step_args* args, void* stream);
+
+/*
+ * Cache-skip decision of step `step` of an n_steps loop (reading of the
+ * step-skip cache the paper names: the relative L1 change of block 0's
+ * modulated input between consecutive steps, accumulated until it reaches
+ * tau, first and last steps always computed).  Computes m_k from the current
+ * latents, d_k = sum|m_k - m_{k-1}| / sum|m_{k-1}| per request with fp64
+ * sums in a fixed order, updates the accumulator, stores m_k.  A check at
+ * step 0 resets the request's state.  Synchronises `stream` once to return
+ * the decisions in host memory.
+ */
+typedef struct t2i_cache_args {
+  uint32_t struct_size;        /* = sizeof(t2i_cache_args) */
+  int32_t n_req;
+  const int32_t* lat_h;        /* host [n_req] */
+  const int32_t* lat_w;        /* host [n_req] */
+  const double* t;             /* host [n_req] */
+  const float* latents;        /* device, packed fp32 latents */
+  int32_t step, n_steps;       /* 0 <= step < n_steps */
+  double tau;                  /* <= 0: never skip */
+  int32_t mode;                /* t2i_cache_mode */
+  int32_t branches;            /* 1, or 2 under guidance */
+  void* cache_state;           /* device, t2i_cache_state_bytes() */
+  size_t cache_state_bytes;
+  double* rel_l1;              /* host [n_req] out: d_k (NaN at step 0) */
+  uint8_t* skip;               /* host [n_req] out: 1 = skip the blocks */
+} t2i_cache_args;
+
+t2i_status t2i_cache_check(t2i_dit* h, const t2i_cache_args* args, void* stream);
+
+/*
+ * The denoising loop: for k = start_step .. n_steps-1, optionally a cache
+ * check, then one step with the Euler update from t_k to t_{k+1}.
+ * Conditioning (timestep embeddings and every block's modulation for every
+ * step) and the text projections are computed once per call.
+ */
+typedef struct t2i_sample_args {
+  uint32_t struct_size;        /* = sizeof(t2i_sample_args) */
+  int32_t n_req;
+  const int32_t* lat_h;        /* host [n_req] */
+  const int32_t* lat_w;        /* host [n_req] */
+  int32_t n_steps;             /* 1 .. max_steps */
+  int32_t start_step;          /* resume point, 0 .. n_steps-1 */
+  const double* timesteps;     /* host [(n_steps+1) * n_req], row k holds t_k
+                                  of every request; NULL = t_k = 1 - k/n_steps */
+  float* latents;              /* device, updated in place */
+  const void* prompt_embeds;   /* device [n_req, text_tokens, text_dim] */
+  float guidance;
+  double cache_tau;            /* <= 0 disables the cache */
+  int32_t cache_mode;          /* t2i_cache_mode */
+  void* cache_state;           /* device, needed when cache_tau > 0 */
+  size_t cache_state_bytes;
+  uint8_t* skip_log;           /* host [n_steps * n_req] or NULL */
+  double* rel_l1_log;          /* host [n_steps * n_req] or NULL */
+} t2i_sample_args;
+
+/* Synchronises `stream` once per step when cache_tau > 0, else never. */
+t2i_status t2i_dit_sample(t2i_dit* h, const t2i_sample_args* args, void* stream);
+
+/*
+ * Kernel timing (tracing aid).  When a class's bit is set in `class_mask`,
+ * every launch of that class on a handle's calls is bracketed by two HIP
+ * events recorded on the call's stream.  t2i_dit_profile resets the counters
+ * (mask 0 disables timing); t2i_dit_profile_read synchronises on the last
+ * recorded event and returns the summed device time and the launch count.
+ */
+typedef enum {
+  T2I_K_GEMM_QKV = 0, T2I_K_ATTN_SELF = 1, T2I_K_GEMM_O = 2, T2I_K_GEMM_XQ = 3,
+  T2I_K_ATTN_CROSS = 4, T2I_K_GEMM_XO = 5, T2I_K_LN = 6, T2I_K_GEMM_FC1 = 7,
+  T2I_K_GEMM_FC2 = 8, T2I_K_COUNT = 9
+} t2i_kernel_class;
+
+t2i_status t2i_dit_profile(t2i_dit* h, uint32_t class_mask);
+t2i_status t2i_dit_profile_read(t2i_dit* h, int32_t kernel_class, double* total_ms,
+                                int64_t* launches);
+
+void t2i_dit_destroy(t2i_dit* h);
+const char* t2i_status_str(t2i_status s);
+const char* t2i_last_error(const t2i_dit* h);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* T2I_DIT_H */

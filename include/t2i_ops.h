@@ -1,0 +1,76 @@
+/*
+ * t2i_ops.h -- kernel-level entry points of the denoising step.
+ *
+ * The same kernels t2i_dit_step launches, exposed one by one so that each can
+ * be checked against its definition in isolation.  Conventions are those of
+ * t2i_dit.h: device pointers are caller-owned HIP memory, `stream` is a
+ * hipStream_t as void*, launches are asynchronous, arguments are validated
+ * before any launch, errors come back as t2i_status (text in
+ * t2i_ops_last_error(), per host thread).
+ */
+#ifndef T2I_OPS_H
+#define T2I_OPS_H
+
+#include <stdint.h>
+#include "t2i_dit.h"
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* Epilogues of the linear layer y = A W^T + b. */
+typedef enum {
+  T2I_EPI_STORE = 0,       /* out = y */
+  T2I_EPI_GELU = 1,        /* out = GELU_tanh(y) */
+  T2I_EPI_SILU = 2,        /* out = SiLU(y) */
+  T2I_EPI_RESID = 3,       /* resid += y  (fp32), resid_copy = bf16(resid) */
+  T2I_EPI_RESID_GATED = 4  /* resid += gate (.) y, gate a [N] fp32 vector */
+} t2i_epilogue;
+
+/*
+ * Linear layer (DiT projections, Sec. 4's model `forward`): y = A W^T + b,
+ * A [M, K] with row stride lda, W [N, K] with row stride ldw, b [N].
+ *   dtype T2I_BF16: A, W, b bf16, MFMA with fp32 accumulation, K % 64 == 0,
+ *                   lda, ldw % 8 == 0.  `out` is bf16.
+ *   dtype T2I_F32 : A, W, b, out fp32.
+ * For T2I_EPI_RESID*: `resid` is fp32 [M, N] (stride ldr) updated in place,
+ * `resid_copy` (bf16 [M, N], stride ldr, or NULL) receives its new value;
+ * `out` is unused.  `gate` is fp32 [N] (T2I_EPI_RESID_GATED only).
+ */
+t2i_status t2i_op_linear(int32_t dtype, int32_t epilogue, int32_t M, int32_t N,
+                         int32_t K, const void* A, int32_t lda, const void* W,
+                         int32_t ldw, const void* bias, void* out, int32_t ldo,
+                         float* resid, int32_t ldr, void* resid_copy,
+                         const float* gate, void* stream);
+
+/*
+ * Multi-head attention softmax(Q K^T / sqrt(d)) V over packed variable-length
+ * sequences: query sequence s holds rows q_start[s] .. q_start[s]+q_len[s]-1
+ * of Q and attends to rows k_start[s] .. +k_len[s]-1 of K and V (host arrays
+ * of n_seq <= T2I_MAX_SEQ entries, k_len >= 1).  Head h of a row occupies
+ * columns h*d .. h*d+d-1.  Q, K, V, O are dtype (bf16 or fp32) with row
+ * strides ldq, ldk, ldv, ldo (multiples of 8).
+ */
+t2i_status t2i_op_attention(int32_t dtype, int32_t heads, int32_t head_dim,
+                            int32_t n_seq, const int32_t* q_start,
+                            const int32_t* q_len, const int32_t* k_start,
+                            const int32_t* k_len, const void* q, int32_t ldq,
+                            const void* k, int32_t ldk, const void* v,
+                            int32_t ldv, void* o, int32_t ldo, void* stream);
+
+/*
+ * LayerNorm (no affine, biased variance) fused with adaLN modulation:
+ * out = (x - mean) / sqrt(var + eps) * (1 + scale) + shift per row of
+ * x [rows, D] fp32; shift, scale fp32 [D]; out dtype (bf16 or fp32) [rows, D].
+ */
+t2i_status t2i_op_ln_modulate(int32_t dtype, int32_t rows, int32_t D,
+                              const float* x, const float* shift,
+                              const float* scale, float eps, void* out,
+                              void* stream);
+
+const char* t2i_ops_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* T2I_OPS_H */

@@ -213,6 +213,26 @@ def block(W, w, b, x, y, mod):
     return x + mod["gate_mlp"] * linear(u, W[p + "mlp.fc2.w"], W[p + "mlp.fc2.b"])
 
 
+def block_rows(W, w, b, x, y, mod, rows):
+    """Output rows ``rows`` of :func:`block` (self-attention keys and values
+    from every row of ``x``); every other step acts on each row alone, so this
+    equals ``block(...)[rows]`` while evaluating far fewer rows."""
+    p = f"blocks.{b}."
+    D, H = w.hidden, w.heads
+    h = modulate(layer_norm(x, w.ln_eps), mod["shift_msa"], mod["scale_msa"])
+    qkv = linear(h, W[p + "attn.qkv.w"], W[p + "attn.qkv.b"])
+    xr = x[rows]
+    o = attention(qkv[rows, :D], qkv[:, D:2 * D], qkv[:, 2 * D:], H)
+    xr = xr + mod["gate_msa"] * linear(o, W[p + "attn.o.w"], W[p + "attn.o.b"])
+    q = linear(xr, W[p + "xattn.q.w"], W[p + "xattn.q.b"])
+    kv = linear(y, W[p + "xattn.kv.w"], W[p + "xattn.kv.b"])
+    o = attention(q, kv[:, :D], kv[:, D:], H)
+    xr = xr + linear(o, W[p + "xattn.o.w"], W[p + "xattn.o.b"])
+    h = modulate(layer_norm(xr, w.ln_eps), mod["shift_mlp"], mod["scale_mlp"])
+    u = gelu_tanh(linear(h, W[p + "mlp.fc1.w"], W[p + "mlp.fc1.b"]))
+    return xr + mod["gate_mlp"] * linear(u, W[p + "mlp.fc2.w"], W[p + "mlp.fc2.b"])
+
+
 def run_blocks(W, w, x, y, c, first=0, last=None):
     """Blocks ``first ... last-1`` on the residual stream."""
     last = w.depth if last is None else last

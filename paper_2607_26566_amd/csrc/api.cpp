@@ -1,0 +1,879 @@
+// C ABI of the denoising step: argument validation, workspace layout and the
+// launch sequence of one step / one sampling loop on the caller's stream.
+// Nothing here computes model values on the host: every number of the path is
+// produced by the kernels in gemm.hip, attention.hip and pointwise.hip.
+#include <hip/hip_runtime.h>
+
+#include <cmath>
+#include <cstdio>
+#include <cstring>
+#include <string>
+#include <vector>
+
+#include "../../include/t2i_dit.h"
+#include "../../include/t2i_ops.h"
+#include "t2i_internal.h"
+
+using namespace t2i;
+
+namespace {
+
+constexpr size_t kAlign = 256;
+size_t align_up(size_t v) { return (v + kAlign - 1) / kAlign * kAlign; }
+
+// ---------------------------------------------------------------------------
+// weight table
+
+struct WDesc {
+  std::string name;
+  int64_t shape[4];
+  int nd;
+};
+
+std::vector<WDesc> weight_table(const t2i_dit_config& c) {
+  std::vector<WDesc> t;
+  auto add = [&](const std::string& n, int64_t a, int64_t b = 0) {
+    WDesc d;
+    d.name = n;
+    d.shape[0] = a;
+    d.shape[1] = b;
+    d.shape[2] = d.shape[3] = 0;
+    d.nd = b ? 2 : 1;
+    t.push_back(d);
+  };
+  const int64_t D = c.hidden, F = c.mlp_hidden, P = (int64_t)c.patch * c.patch * c.latent_channels;
+  add("x_embed.w", D, P);
+  add("x_embed.b", D);
+  add("t_embed.w1", D, c.freq_dim);
+  add("t_embed.b1", D);
+  add("t_embed.w2", D, D);
+  add("t_embed.b2", D);
+  add("y_embed.w", D, c.text_dim);
+  add("y_embed.b", D);
+  for (int b = 0; b < c.depth; ++b) {
+    const std::string p = "blocks." + std::to_string(b) + ".";
+    if (c.arch == T2I_ARCH_CROSS_DIT) {
+      add(p + "ada.w", 6 * D, D);
+      add(p + "ada.b", 6 * D);
+      add(p + "attn.qkv.w", 3 * D, D);
+      add(p + "attn.qkv.b", 3 * D);
+      add(p + "attn.o.w", D, D);
+      add(p + "attn.o.b", D);
+      add(p + "xattn.q.w", D, D);
+      add(p + "xattn.q.b", D);
+      add(p + "xattn.kv.w", 2 * D, D);
+      add(p + "xattn.kv.b", 2 * D);
+      add(p + "xattn.o.w", D, D);
+      add(p + "xattn.o.b", D);
+      add(p + "mlp.fc1.w", F, D);
+      add(p + "mlp.fc1.b", F);
+      add(p + "mlp.fc2.w", D, F);
+      add(p + "mlp.fc2.b", D);
+    } else {
+      for (const char* s : {"txt", "img"}) {
+        const std::string q = p + s + ".";
+        add(q + "ada.w", 6 * D, D);
+        add(q + "ada.b", 6 * D);
+        add(q + "qkv.w", 3 * D, D);
+        add(q + "qkv.b", 3 * D);
+        add(q + "o.w", D, D);
+        add(q + "o.b", D);
+        add(q + "fc1.w", F, D);
+        add(q + "fc1.b", F);
+        add(q + "fc2.w", D, F);
+        add(q + "fc2.b", D);
+      }
+    }
+  }
+  add("final.ada.w", 2 * D, D);
+  add("final.ada.b", 2 * D);
+  add("final.out.w", P, D);
+  add("final.out.b", P);
+  return t;
+}
+
+// indices into the table
+enum { W_PE = 0, B_PE, W_T1, B_T1, W_T2, B_T2, W_Y, B_Y, W_BLOCK0 };
+enum { X_ADA = 0, X_ADA_B, X_QKV, X_QKV_B, X_O, X_O_B, X_XQ, X_XQ_B, X_XKV, X_XKV_B, X_XO, X_XO_B,
+       X_FC1, X_FC1_B, X_FC2, X_FC2_B, X_PER_BLOCK };
+enum { J_ADA = 0, J_ADA_B, J_QKV, J_QKV_B, J_O, J_O_B, J_FC1, J_FC1_B, J_FC2, J_FC2_B, J_PER_STREAM };
+
+int per_block(const t2i_dit_config& c) {
+  return c.arch == T2I_ARCH_CROSS_DIT ? X_PER_BLOCK : 2 * J_PER_STREAM;
+}
+int final_base(const t2i_dit_config& c) { return W_BLOCK0 + c.depth * per_block(c); }
+int mod_width(const t2i_dit_config& c) {
+  const int per = c.arch == T2I_ARCH_CROSS_DIT ? 6 : 12;
+  return c.depth * per * c.hidden + 2 * c.hidden;
+}
+
+const char* check_config(const t2i_dit_config* c) {
+  if (!c) return "config is NULL";
+  if (c->struct_size != sizeof(t2i_dit_config)) return "config struct_size mismatch";
+  if (c->arch != T2I_ARCH_CROSS_DIT && c->arch != T2I_ARCH_MMDIT) return "bad arch";
+  if (c->dtype != T2I_F32 && c->dtype != T2I_BF16) return "bad dtype";
+  if (c->latent_channels < 1 || c->patch < 1) return "bad latent_channels/patch";
+  if (c->patch * c->patch * c->latent_channels > 64) return "p*p*C must be <= 64";
+  if (c->hidden < 64 || c->hidden % 64 || c->hidden > 3072) return "hidden must be a multiple of 64 in [64, 3072]";
+  if (c->heads < 1 || c->heads * c->head_dim != c->hidden) return "heads * head_dim != hidden";
+  if (c->head_dim != 32 && c->head_dim != 64 && c->head_dim != 72 && c->head_dim != 128 && c->head_dim != 8)
+    return "head_dim must be one of 8, 32, 64, 72, 128";
+  if (c->depth < 1 || c->depth > 256) return "bad depth";
+  if (c->mlp_hidden < 64 || c->mlp_hidden % 64) return "mlp_hidden must be a positive multiple of 64";
+  if (c->text_dim < 64 || c->text_dim % 64) return "text_dim must be a positive multiple of 64";
+  if (c->text_tokens < 1 || c->text_tokens > 4096) return "bad text_tokens";
+  if (c->freq_dim < 2 || c->freq_dim % 2) return "freq_dim must be even";
+  if (c->max_tokens < 1) return "bad max_tokens";
+  if (c->max_requests < 1 || c->max_requests > T2I_MAX_REQ) return "bad max_requests";
+  if (c->max_steps < 1 || c->max_steps > 10000) return "bad max_steps";
+  if (!(c->ln_eps > 0.f) || !(c->t_scale > 0.f)) return "bad ln_eps/t_scale";
+  if (c->arch == T2I_ARCH_MMDIT && c->dtype != T2I_BF16) return "MMDiT runs in bf16 only";
+  return nullptr;
+}
+
+// ---------------------------------------------------------------------------
+// workspace layout
+
+struct Layout {
+  size_t x, x0, h, xb, qkv, o, u, ytxt, kv, tfreq, th1, tsc, mod, partial, total;
+};
+
+Layout layout(const t2i_dit_config& c) {
+  Layout L{};
+  const size_t A = c.dtype == T2I_BF16 ? 2 : 4;
+  const size_t D = c.hidden, F = c.mlp_hidden;
+  const size_t txt_rows = (size_t)(c.max_requests + 1) * c.text_tokens;
+  size_t rows = c.max_tokens;
+  if (c.arch == T2I_ARCH_MMDIT) rows += (size_t)c.max_requests * c.text_tokens;
+  const size_t Tt = (size_t)c.max_steps * c.max_requests;
+  size_t off = 0;
+  auto take = [&](size_t bytes) {
+    size_t o = off;
+    off = align_up(off + bytes);
+    return o;
+  };
+  L.x = take(rows * D * 4);
+  L.x0 = take(rows * D * 4);
+  L.h = take(rows * D * A);
+  L.xb = take(c.dtype == T2I_BF16 ? rows * D * 2 : 0);
+  L.qkv = take(rows * 3 * D * A);
+  L.o = take(rows * D * A);
+  L.u = take(rows * F * A);
+  L.ytxt = take(txt_rows * D * A);
+  L.kv = take(c.arch == T2I_ARCH_CROSS_DIT ? (size_t)c.depth * txt_rows * 2 * D * A : 0);
+  L.tfreq = take(Tt * c.freq_dim * 4);
+  L.th1 = take(Tt * D * 4);
+  L.tsc = take(Tt * D * 4);
+  L.mod = take(Tt * mod_width(c) * 4);
+  L.partial = take(((size_t)c.max_tokens / kCacheRowsPerBlock + c.max_requests + 1) * 2 * 8);
+  L.total = off;
+  return L;
+}
+
+}  // namespace
+
+// ---------------------------------------------------------------------------
+
+struct t2i_dit {
+  t2i_dit_config cfg;
+  std::vector<const void*> w;
+  char* ws = nullptr;
+  size_t ws_bytes = 0;
+  Layout L{};
+  std::string err;
+  std::vector<CacheHeader> hdr_host;
+  // kernel timing
+  uint32_t prof_mask = 0;
+  std::vector<hipEvent_t> ev_pool;               // created on demand, reused
+  size_t ev_used = 0;
+  std::vector<std::pair<int, size_t>> ev_pairs;  // (class, index of start event)
+
+  ~t2i_dit() {
+    for (hipEvent_t e : ev_pool) (void)hipEventDestroy(e);
+  }
+
+  template <typename T>
+  T* at(size_t off) const { return (T*)(ws + off); }
+  bool bf() const { return cfg.dtype == T2I_BF16; }
+  size_t act() const { return bf() ? 2 : 4; }
+};
+
+namespace {
+
+thread_local std::string g_ops_err;
+
+t2i_status fail(t2i_dit* h, t2i_status s, const std::string& msg) {
+  if (h) h->err = msg;
+  return s;
+}
+
+#define HIP_TRY(h, expr)                                                              \
+  do {                                                                                \
+    hipError_t e_ = (expr);                                                           \
+    if (e_ != hipSuccess)                                                             \
+      return fail((h), T2I_ERR_DEVICE, std::string(#expr ": ") + hipGetErrorString(e_)); \
+  } while (0)
+
+// One call's request geometry.
+struct Plan {
+  int n_req = 0, branches = 1, T_img = 0, rows = 0, txt_rows = 0;
+  float guidance = 1.f;
+  ReqMap rm{};
+  SeqMap img{};      // image rows (branch-major) -> sequence -> modulation row
+  AttnMap self{}, cross{};
+  size_t lat_floats = 0;
+};
+
+t2i_status build_plan(t2i_dit* h, int n_req, const int32_t* lat_h, const int32_t* lat_w,
+                      float guidance, Plan& P) {
+  const t2i_dit_config& c = h->cfg;
+  if (n_req < 1 || n_req > c.max_requests) return fail(h, T2I_ERR_SHAPE, "n_req out of range");
+  if (!lat_h || !lat_w) return fail(h, T2I_ERR_INVALID_ARG, "lat_h/lat_w is NULL");
+  if (!std::isfinite(guidance)) return fail(h, T2I_ERR_INVALID_ARG, "guidance not finite");
+  P.n_req = n_req;
+  P.guidance = guidance;
+  P.branches = guidance == 1.f ? 1 : 2;
+  if (n_req * P.branches > kMaxSeq) return fail(h, T2I_ERR_SHAPE, "too many sequences");
+  int tok = 0;
+  size_t lat = 0;
+  P.rm.n = n_req;
+  for (int r = 0; r < n_req; ++r) {
+    if (lat_h[r] < c.patch || lat_w[r] < c.patch || lat_h[r] % c.patch || lat_w[r] % c.patch)
+      return fail(h, T2I_ERR_SHAPE, "latent size must be a positive multiple of patch");
+    if (lat_h[r] > 4096 || lat_w[r] > 4096) return fail(h, T2I_ERR_SHAPE, "latent too large");
+    const int n = (lat_h[r] / c.patch) * (lat_w[r] / c.patch);
+    P.rm.tok_off[r] = tok;
+    P.rm.lat_off[r] = (int)lat;
+    P.rm.h[r] = lat_h[r];
+    P.rm.w[r] = lat_w[r];
+    P.rm.modrow[r] = r;
+    P.rm.dt[r] = 0.f;
+    tok += n;
+    lat += (size_t)c.latent_channels * lat_h[r] * lat_w[r];
+  }
+  P.rm.tok_off[n_req] = tok;
+  P.rm.tokens_total = tok;
+  P.rm.branches = P.branches;
+  P.T_img = tok;
+  P.rows = tok * P.branches;
+  P.lat_floats = lat;
+  if (P.rows > c.max_tokens) return fail(h, T2I_ERR_SHAPE, "image tokens exceed max_tokens");
+  const int M = c.text_tokens;
+  P.txt_rows = n_req * M + (P.branches == 2 ? M : 0);
+  const int BQ = attention_query_tile(h->bf(), c.head_dim);
+  P.img.n = n_req * P.branches;
+  P.self.n = P.cross.n = P.img.n;
+  int tiles = 0;
+  for (int br = 0; br < P.branches; ++br)
+    for (int r = 0; r < n_req; ++r) {
+      const int s = br * n_req + r;
+      const int start = br * tok + P.rm.tok_off[r];
+      const int len = P.rm.tok_off[r + 1] - P.rm.tok_off[r];
+      P.img.start[s] = start;
+      P.img.modrow[s] = r;
+      P.self.q_start[s] = P.cross.q_start[s] = start;
+      P.self.q_len[s] = P.cross.q_len[s] = len;
+      P.self.k_start[s] = start;
+      P.self.k_len[s] = len;
+      P.cross.k_start[s] = br == 0 ? r * M : n_req * M;
+      P.cross.k_len[s] = M;
+      P.self.tile_start[s] = P.cross.tile_start[s] = tiles;
+      tiles += (len + BQ - 1) / BQ;
+    }
+  P.img.start[P.img.n] = P.rows;
+  P.self.tile_start[P.self.n] = P.cross.tile_start[P.cross.n] = tiles;
+  return T2I_OK;
+}
+
+void set_modrows(Plan& P, int base) {
+  for (int r = 0; r < P.n_req; ++r) P.rm.modrow[r] = base + r;
+  for (int s = 0; s < P.img.n; ++s) P.img.modrow[s] = base + (s % P.n_req);
+}
+
+Epi make_epi() {
+  Epi e;
+  std::memset(&e, 0, sizeof(e));
+  return e;
+}
+
+// y = A W^T + b with the config's operand type.
+hipError_t linear(t2i_dit* h, const void* A, int lda, int wi, int M, int N, int K, int kind,
+                  Epi epi, hipStream_t st) {
+  const void* W = h->w[wi];
+  const void* B = h->w[wi + 1];
+  if (h->bf())
+    return launch_gemm_bf16((const bf16*)A, lda, (const bf16*)W, K, (const bf16*)B, M, N, K, kind,
+                            epi, st);
+  return launch_gemm_f32((const float*)A, lda, W, K, false, B, M, N, K, kind, epi, st);
+}
+
+// Conditioning of `rows` timesteps (rows <= max_steps * max_requests):
+// silu(c) into tsc and every block's adaLN chunks into the modulation table.
+t2i_status conditioning(t2i_dit* h, const double* t_host, int rows, int n_blocks_mod,
+                        hipStream_t st) {
+  const t2i_dit_config& c = h->cfg;
+  const int D = c.hidden, fd = c.freq_dim;
+  float* tfreq = h->at<float>(h->L.tfreq);
+  float* th1 = h->at<float>(h->L.th1);
+  float* tsc = h->at<float>(h->L.tsc);
+  float* mod = h->at<float>(h->L.mod);
+  const bool wb = h->bf();
+  HIP_TRY(h, launch_timestep_freq(t_host, rows, fd, (double)c.t_scale, tfreq, st));
+  Epi e = make_epi();
+  e.out = th1;
+  e.ldo = D;
+  HIP_TRY(h, launch_gemm_f32(tfreq, fd, h->w[W_T1], fd, wb, h->w[B_T1], rows, D, fd, EPI_SILU, e, st));
+  e.out = tsc;
+  HIP_TRY(h, launch_gemm_f32(th1, D, h->w[W_T2], D, wb, h->w[B_T2], rows, D, D, EPI_SILU, e, st));
+  const int mw = mod_width(c);
+  const int pb = per_block(c);
+  e.ldo = mw;
+  for (int b = 0; b < n_blocks_mod; ++b) {
+    if (c.arch == T2I_ARCH_CROSS_DIT) {
+      e.out = mod + (size_t)b * 6 * D;
+      const int wi = W_BLOCK0 + b * pb + X_ADA;
+      HIP_TRY(h, launch_gemm_f32(tsc, D, h->w[wi], D, wb, h->w[wi + 1], rows, 6 * D, D, EPI_STORE, e, st));
+    } else {
+      for (int s = 0; s < 2; ++s) {
+        e.out = mod + (size_t)b * 12 * D + (size_t)s * 6 * D;
+        const int wi = W_BLOCK0 + b * pb + s * J_PER_STREAM + J_ADA;
+        HIP_TRY(h, launch_gemm_f32(tsc, D, h->w[wi], D, wb, h->w[wi + 1], rows, 6 * D, D, EPI_STORE, e, st));
+      }
+    }
+  }
+  e.out = mod + (size_t)(mw - 2 * D);
+  const int fb = final_base(c);
+  HIP_TRY(h, launch_gemm_f32(tsc, D, h->w[fb], D, wb, h->w[fb + 1], rows, 2 * D, D, EPI_STORE, e, st));
+  return T2I_OK;
+}
+
+// Text projection and (cross-DiT) every block's text K/V.
+t2i_status text_prep(t2i_dit* h, const Plan& P, const void* prompt, hipStream_t st) {
+  const t2i_dit_config& c = h->cfg;
+  const int D = c.hidden, M = c.text_tokens;
+  char* ytxt = h->at<char>(h->L.ytxt);
+  Epi e = make_epi();
+  e.out = ytxt;
+  e.ldo = D;
+  HIP_TRY(h, linear(h, prompt, c.text_dim, W_Y, P.n_req * M, D, c.text_dim, EPI_STORE, e, st));
+  if (P.branches == 2)
+    HIP_TRY(h, launch_broadcast_rows(h->w[B_Y], h->bf(), M, D,
+                                     ytxt + (size_t)P.n_req * M * D * h->act(), st));
+  if (c.arch != T2I_ARCH_CROSS_DIT) return T2I_OK;
+  const size_t txt_rows_max = (size_t)(c.max_requests + 1) * M;
+  for (int b = 0; b < c.depth; ++b) {
+    e.out = h->at<char>(h->L.kv) + (size_t)b * txt_rows_max * 2 * D * h->act();
+    e.ldo = 2 * D;
+    HIP_TRY(h, linear(h, ytxt, D, W_BLOCK0 + b * X_PER_BLOCK + X_XKV, P.txt_rows, 2 * D, D,
+                      EPI_STORE, e, st));
+  }
+  return T2I_OK;
+}
+
+// Event pair around one launch of a timed kernel class.
+hipError_t prof_mark(t2i_dit* h, int cls, bool start, hipStream_t st) {
+  if (!(h->prof_mask & (1u << cls))) return hipSuccess;
+  if (h->ev_used == h->ev_pool.size()) {
+    hipEvent_t e;
+    hipError_t err = hipEventCreate(&e);
+    if (err != hipSuccess) return err;
+    h->ev_pool.push_back(e);
+  }
+  const size_t i = h->ev_used++;
+  if (start) h->ev_pairs.push_back({cls, i});
+  return hipEventRecord(h->ev_pool[i], st);
+}
+
+#define TIMED(h, cls, st, expr)                      \
+  do {                                               \
+    HIP_TRY(h, prof_mark(h, cls, true, st));         \
+    HIP_TRY(h, expr);                                \
+    HIP_TRY(h, prof_mark(h, cls, false, st));        \
+  } while (0)
+
+// Cross-DiT blocks [0, nb) over all image rows of the plan.
+t2i_status run_blocks_cross(t2i_dit* h, const Plan& P, int nb, hipStream_t st) {
+  const t2i_dit_config& c = h->cfg;
+  const int D = c.hidden, F = c.mlp_hidden, R = P.rows, mw = mod_width(c);
+  const bool bf = h->bf();
+  float* x = h->at<float>(h->L.x);
+  char* hb = h->at<char>(h->L.h);
+  char* qkv = h->at<char>(h->L.qkv);
+  char* o = h->at<char>(h->L.o);
+  char* u = h->at<char>(h->L.u);
+  bf16* xb = bf ? h->at<bf16>(h->L.xb) : nullptr;
+  const float* mod = h->at<float>(h->L.mod);
+  const size_t A = h->act();
+  const size_t txt_rows_max = (size_t)(c.max_requests + 1) * c.text_tokens;
+  for (int b = 0; b < nb; ++b) {
+    const int wb = W_BLOCK0 + b * X_PER_BLOCK;
+    const int mo = b * 6 * D;
+    // self-attention
+    TIMED(h, T2I_K_LN, st, launch_ln_modulate(bf, R, D, x, D, mod, mw, mo + 0 * D, mo + 1 * D,
+                                               P.img, hb, D, c.ln_eps, st));
+    Epi e = make_epi();
+    e.out = qkv;
+    e.ldo = 3 * D;
+    TIMED(h, T2I_K_GEMM_QKV, st, linear(h, hb, D, wb + X_QKV, R, 3 * D, D, EPI_STORE, e, st));
+    TIMED(h, T2I_K_ATTN_SELF, st,
+          launch_attention(bf, c.heads, c.head_dim, P.self, qkv, 3 * D, qkv + D * A, 3 * D,
+                           qkv + 2 * D * A, 3 * D, o, D, st));
+    e = make_epi();
+    e.x = x;
+    e.ldx = D;
+    e.xb = xb;
+    e.gate = mod + mo + 2 * D;
+    e.ld_gate = mw;
+    e.map = P.img;
+    TIMED(h, T2I_K_GEMM_O, st, linear(h, o, D, wb + X_O, R, D, D, EPI_RESID_GATED, e, st));
+    // cross-attention (query from the raw residual, ungated)
+    e = make_epi();
+    e.out = qkv;
+    e.ldo = D;
+    TIMED(h, T2I_K_GEMM_XQ, st,
+          linear(h, bf ? (const void*)xb : (const void*)x, D, wb + X_XQ, R, D, D, EPI_STORE, e, st));
+    const char* kv = h->at<char>(h->L.kv) + (size_t)b * txt_rows_max * 2 * D * A;
+    TIMED(h, T2I_K_ATTN_CROSS, st,
+          launch_attention(bf, c.heads, c.head_dim, P.cross, qkv, D, kv, 2 * D, kv + D * A, 2 * D,
+                           o, D, st));
+    e = make_epi();
+    e.x = x;
+    e.ldx = D;
+    TIMED(h, T2I_K_GEMM_XO, st, linear(h, o, D, wb + X_XO, R, D, D, EPI_RESID, e, st));
+    // MLP
+    TIMED(h, T2I_K_LN, st, launch_ln_modulate(bf, R, D, x, D, mod, mw, mo + 3 * D, mo + 4 * D,
+                                               P.img, hb, D, c.ln_eps, st));
+    e = make_epi();
+    e.out = u;
+    e.ldo = F;
+    TIMED(h, T2I_K_GEMM_FC1, st, linear(h, hb, D, wb + X_FC1, R, F, D, EPI_GELU, e, st));
+    e = make_epi();
+    e.x = x;
+    e.ldx = D;
+    e.gate = mod + mo + 5 * D;
+    e.ld_gate = mw;
+    e.map = P.img;
+    TIMED(h, T2I_K_GEMM_FC2, st, linear(h, u, F, wb + X_FC2, R, D, F, EPI_RESID_GATED, e, st));
+  }
+  return T2I_OK;
+}
+
+t2i_status run_blocks(t2i_dit* h, const Plan& P, int nb, hipStream_t st) {
+  if (h->cfg.arch == T2I_ARCH_CROSS_DIT) return run_blocks_cross(h, P, nb, st);
+  return fail(h, T2I_ERR_UNSUPPORTED, "MMDiT blocks are not built yet");
+}
+
+size_t cache_bytes(const t2i_dit_config& c, int n_req, int tokens, int branches) {
+  return align_up((size_t)n_req * sizeof(CacheHeader)) + align_up((size_t)tokens * c.hidden * 4) +
+         (size_t)branches * tokens * c.hidden * 4;
+}
+
+struct CachePtrs {
+  CacheHeader* hdr;
+  float* m_prev;
+  float* R;
+};
+
+CachePtrs cache_ptrs(const t2i_dit_config& c, void* base, int n_req, int tokens) {
+  CachePtrs p;
+  char* b = (char*)base;
+  p.hdr = (CacheHeader*)b;
+  p.m_prev = (float*)(b + align_up((size_t)n_req * sizeof(CacheHeader)));
+  p.R = (float*)((char*)p.m_prev + align_up((size_t)tokens * c.hidden * 4));
+  return p;
+}
+
+// Cache check on x0 (already embedded) with modulation rows set in P.
+t2i_status cache_check_impl(t2i_dit* h, const Plan& P, int step, int n_steps, double tau,
+                            int mode, void* state, double* rel_l1, uint8_t* skip, hipStream_t st) {
+  const t2i_dit_config& c = h->cfg;
+  CachePtrs cp = cache_ptrs(c, state, P.n_req, P.T_img);
+  double* partial = h->at<double>(h->L.partial);
+  HIP_TRY(h, launch_cache_signal(h->at<float>(h->L.x0), P.rm, h->at<float>(h->L.mod),
+                                 mod_width(c), 0, c.hidden, c.hidden, c.ln_eps, cp.m_prev, cp.hdr,
+                                 step, partial, st));
+  HIP_TRY(h, launch_cache_decide(P.rm, partial, cp.hdr, step, n_steps, tau, mode, st));
+  h->hdr_host.resize(P.n_req);
+  HIP_TRY(h, hipMemcpyAsync(h->hdr_host.data(), cp.hdr, sizeof(CacheHeader) * P.n_req,
+                            hipMemcpyDeviceToHost, st));
+  HIP_TRY(h, hipStreamSynchronize(st));
+  for (int r = 0; r < P.n_req; ++r) {
+    if (rel_l1) rel_l1[r] = h->hdr_host[r].d;
+    if (skip) skip[r] = (uint8_t)(h->hdr_host[r].skip ? 1 : 0);
+  }
+  return T2I_OK;
+}
+
+// Embed, blocks (or cached residual), final layer for one step whose
+// conditioning rows start at `modbase`.
+t2i_status step_body(t2i_dit* h, Plan& P, const float* latents_in, float* latents,
+                     float* noise_pred, int nb, float* hidden_out, const uint8_t* skip,
+                     void* cache_state, hipStream_t st) {
+  const t2i_dit_config& c = h->cfg;
+  const int D = c.hidden;
+  float* x = h->at<float>(h->L.x);
+  float* x0 = h->at<float>(h->L.x0);
+  const bool pe = c.arch == T2I_ARCH_CROSS_DIT;
+  HIP_TRY(h, launch_embed(latents_in, P.rm, h->w[W_PE], h->w[B_PE], h->bf(), D,
+                          c.latent_channels, c.patch, pe, x0, x, P.branches, st));
+  uint32_t skip_mask = 0, compute_mask = 0;
+  for (int r = 0; r < P.n_req; ++r) {
+    if (skip && skip[r]) skip_mask |= 1u << r;
+    else compute_mask |= 1u << r;
+  }
+  if (compute_mask) {
+    t2i_status s = run_blocks(h, P, nb, st);
+    if (s != T2I_OK) return s;
+  }
+  if (cache_state) {
+    CachePtrs cp = cache_ptrs(c, cache_state, P.n_req, P.T_img);
+    if (skip_mask) HIP_TRY(h, launch_apply_residual(x0, cp.R, x, P.rm, skip_mask, D, st));
+    if (compute_mask)
+      HIP_TRY(h, launch_store_residual(x0, x, cp.R, P.rm, compute_mask, D, cp.hdr, st));
+  }
+  if (hidden_out)
+    HIP_TRY(h, hipMemcpyAsync(hidden_out, x, (size_t)P.rows * D * 4, hipMemcpyDeviceToDevice, st));
+  const int mw = mod_width(c);
+  const int fb = final_base(c);
+  HIP_TRY(h, launch_final_layer(x, P.rm, h->w[fb + 2], h->w[fb + 3], h->bf(), h->at<float>(h->L.mod),
+                                mw, mw - 2 * D, mw - D, D, c.latent_channels, c.patch, c.ln_eps,
+                                P.guidance, latents, noise_pred, st));
+  return T2I_OK;
+}
+
+}  // namespace
+
+// ===========================================================================
+// exported
+
+extern "C" {
+
+const char* t2i_status_str(t2i_status s) {
+  switch (s) {
+    case T2I_OK: return "ok";
+    case T2I_ERR_INVALID_ARG: return "invalid argument";
+    case T2I_ERR_SHAPE: return "shape error";
+    case T2I_ERR_UNSUPPORTED: return "unsupported";
+    case T2I_ERR_WORKSPACE: return "workspace too small";
+    case T2I_ERR_OUT_OF_MEMORY: return "out of memory";
+    case T2I_ERR_DEVICE: return "device error";
+  }
+  return "unknown status";
+}
+
+const char* t2i_last_error(const t2i_dit* h) { return h ? h->err.c_str() : "NULL handle"; }
+
+size_t t2i_dit_weight_count(const t2i_dit_config* cfg) {
+  if (check_config(cfg)) return 0;
+  return (size_t)final_base(*cfg) + 4;
+}
+
+t2i_status t2i_dit_weight_desc(const t2i_dit_config* cfg, size_t i, char name[64],
+                               int64_t shape[4], int32_t* dtype) {
+  if (check_config(cfg)) return T2I_ERR_INVALID_ARG;
+  if (!name || !shape || !dtype) return T2I_ERR_INVALID_ARG;
+  std::vector<WDesc> t = weight_table(*cfg);
+  if (i >= t.size()) return T2I_ERR_SHAPE;
+  std::snprintf(name, 64, "%s", t[i].name.c_str());
+  for (int k = 0; k < 4; ++k) shape[k] = t[i].shape[k];
+  *dtype = cfg->dtype;
+  return T2I_OK;
+}
+
+size_t t2i_dit_workspace_bytes(const t2i_dit_config* cfg) {
+  if (check_config(cfg)) return 0;
+  return layout(*cfg).total;
+}
+
+size_t t2i_cache_state_bytes(const t2i_dit_config* cfg, int32_t n_req,
+                             const int32_t* tokens_per_req, int32_t branches) {
+  if (check_config(cfg) || n_req < 1 || n_req > cfg->max_requests || !tokens_per_req ||
+      (branches != 1 && branches != 2))
+    return 0;
+  long tok = 0;
+  for (int r = 0; r < n_req; ++r) {
+    if (tokens_per_req[r] < 1) return 0;
+    tok += tokens_per_req[r];
+  }
+  return cache_bytes(*cfg, n_req, (int)tok, branches);
+}
+
+t2i_status t2i_dit_init(const t2i_dit_config* cfg, const void* const* weights, void* workspace,
+                        size_t ws_bytes, void* stream, t2i_dit** out) {
+  (void)stream;
+  if (!out) return T2I_ERR_INVALID_ARG;
+  *out = nullptr;
+  if (check_config(cfg)) return T2I_ERR_INVALID_ARG;
+  if (!weights || !workspace) return T2I_ERR_INVALID_ARG;
+  if ((uintptr_t)workspace % kAlign) return T2I_ERR_INVALID_ARG;
+  const size_t need = layout(*cfg).total;
+  if (ws_bytes < need) return T2I_ERR_WORKSPACE;
+  const size_t n = (size_t)final_base(*cfg) + 4;
+  for (size_t i = 0; i < n; ++i)
+    if (!weights[i]) return T2I_ERR_INVALID_ARG;
+  t2i_dit* h = new (std::nothrow) t2i_dit();
+  if (!h) return T2I_ERR_OUT_OF_MEMORY;
+  h->cfg = *cfg;
+  h->w.assign(weights, weights + n);
+  h->ws = (char*)workspace;
+  h->ws_bytes = ws_bytes;
+  h->L = layout(*cfg);
+  *out = h;
+  return T2I_OK;
+}
+
+t2i_status t2i_dit_rebind_weights(t2i_dit* h, const void* const* weights, void* stream) {
+  (void)stream;
+  if (!h || !weights) return T2I_ERR_INVALID_ARG;
+  for (size_t i = 0; i < h->w.size(); ++i)
+    if (!weights[i]) return fail(h, T2I_ERR_INVALID_ARG, "NULL weight pointer");
+  h->w.assign(weights, weights + h->w.size());
+  return T2I_OK;
+}
+
+void t2i_dit_destroy(t2i_dit* h) { delete h; }
+
+t2i_status t2i_dit_profile(t2i_dit* h, uint32_t class_mask) {
+  if (!h) return T2I_ERR_INVALID_ARG;
+  if (class_mask >> T2I_K_COUNT) return fail(h, T2I_ERR_INVALID_ARG, "bad class mask");
+  h->prof_mask = class_mask;
+  h->ev_used = 0;
+  h->ev_pairs.clear();
+  return T2I_OK;
+}
+
+t2i_status t2i_dit_profile_read(t2i_dit* h, int32_t cls, double* total_ms, int64_t* launches) {
+  if (!h || !total_ms || !launches) return T2I_ERR_INVALID_ARG;
+  if (cls < 0 || cls >= T2I_K_COUNT) return fail(h, T2I_ERR_INVALID_ARG, "bad kernel class");
+  if (h->ev_used) HIP_TRY(h, hipEventSynchronize(h->ev_pool[h->ev_used - 1]));
+  double tot = 0.0;
+  int64_t n = 0;
+  for (const auto& pr : h->ev_pairs) {
+    if (pr.first != cls) continue;
+    float ms = 0.f;
+    HIP_TRY(h, hipEventElapsedTime(&ms, h->ev_pool[pr.second], h->ev_pool[pr.second + 1]));
+    tot += ms;
+    ++n;
+  }
+  *total_ms = tot;
+  *launches = n;
+  return T2I_OK;
+}
+
+t2i_status t2i_dit_step(t2i_dit* h, const t2i_step_args* a, void* stream) {
+  if (!h) return T2I_ERR_INVALID_ARG;
+  if (!a || a->struct_size != sizeof(t2i_step_args))
+    return fail(h, T2I_ERR_INVALID_ARG, "step args NULL or struct_size mismatch");
+  if (a->control_outputs) return fail(h, T2I_ERR_UNSUPPORTED, "control_outputs is reserved");
+  if (!a->t || !a->latents || !a->prompt_embeds)
+    return fail(h, T2I_ERR_INVALID_ARG, "t, latents and prompt_embeds are required");
+  const t2i_dit_config& c = h->cfg;
+  Plan P;
+  t2i_status s = build_plan(h, a->n_req, a->lat_h, a->lat_w, a->guidance, P);
+  if (s != T2I_OK) return s;
+  const int nb = a->n_blocks < 0 ? c.depth : a->n_blocks;
+  if (nb > c.depth) return fail(h, T2I_ERR_SHAPE, "n_blocks > depth");
+  if (a->skip && !a->cache_state)
+    return fail(h, T2I_ERR_INVALID_ARG, "skip decisions need cache_state");
+  if (a->cache_state &&
+      a->cache_state_bytes < cache_bytes(c, P.n_req, P.T_img, P.branches))
+    return fail(h, T2I_ERR_WORKSPACE, "cache_state too small");
+  for (int r = 0; r < P.n_req; ++r) {
+    if (!std::isfinite(a->t[r])) return fail(h, T2I_ERR_INVALID_ARG, "t not finite");
+    if (a->t_next) {
+      if (!std::isfinite(a->t_next[r])) return fail(h, T2I_ERR_INVALID_ARG, "t_next not finite");
+      P.rm.dt[r] = (float)(a->t_next[r] - a->t[r]);
+    }
+  }
+  hipStream_t st = (hipStream_t)stream;
+  set_modrows(P, 0);
+  if ((s = conditioning(h, a->t, P.n_req, c.depth, st)) != T2I_OK) return s;
+  if ((s = text_prep(h, P, a->prompt_embeds, st)) != T2I_OK) return s;
+  return step_body(h, P, a->latents, a->latents, a->noise_pred, nb, a->hidden_out, a->skip,
+                   a->cache_state, st);
+}
+
+t2i_status t2i_cache_check(t2i_dit* h, const t2i_cache_args* a, void* stream) {
+  if (!h) return T2I_ERR_INVALID_ARG;
+  if (!a || a->struct_size != sizeof(t2i_cache_args))
+    return fail(h, T2I_ERR_INVALID_ARG, "cache args NULL or struct_size mismatch");
+  if (!a->t || !a->latents || !a->cache_state || !a->rel_l1 || !a->skip)
+    return fail(h, T2I_ERR_INVALID_ARG, "missing pointer");
+  if (a->step < 0 || a->step >= a->n_steps) return fail(h, T2I_ERR_SHAPE, "bad step");
+  if (a->mode != T2I_CACHE_ACCUMULATE && a->mode != T2I_CACHE_PER_STEP)
+    return fail(h, T2I_ERR_INVALID_ARG, "bad mode");
+  if (a->branches != 1 && a->branches != 2) return fail(h, T2I_ERR_INVALID_ARG, "bad branches");
+  Plan P;
+  t2i_status s = build_plan(h, a->n_req, a->lat_h, a->lat_w, a->branches == 2 ? 2.f : 1.f, P);
+  if (s != T2I_OK) return s;
+  const t2i_dit_config& c = h->cfg;
+  if (a->cache_state_bytes < cache_bytes(c, P.n_req, P.T_img, P.branches))
+    return fail(h, T2I_ERR_WORKSPACE, "cache_state too small");
+  hipStream_t st = (hipStream_t)stream;
+  set_modrows(P, 0);
+  if ((s = conditioning(h, a->t, P.n_req, 1, st)) != T2I_OK) return s;
+  HIP_TRY(h, launch_embed(a->latents, P.rm, h->w[W_PE], h->w[B_PE], h->bf(), c.hidden,
+                          c.latent_channels, c.patch, c.arch == T2I_ARCH_CROSS_DIT,
+                          h->at<float>(h->L.x0), h->at<float>(h->L.x), 0, st));
+  return cache_check_impl(h, P, a->step, a->n_steps, a->tau, a->mode, a->cache_state, a->rel_l1,
+                          a->skip, st);
+}
+
+t2i_status t2i_dit_sample(t2i_dit* h, const t2i_sample_args* a, void* stream) {
+  if (!h) return T2I_ERR_INVALID_ARG;
+  if (!a || a->struct_size != sizeof(t2i_sample_args))
+    return fail(h, T2I_ERR_INVALID_ARG, "sample args NULL or struct_size mismatch");
+  if (!a->latents || !a->prompt_embeds) return fail(h, T2I_ERR_INVALID_ARG, "missing pointer");
+  const t2i_dit_config& c = h->cfg;
+  if (a->n_steps < 1 || a->n_steps > c.max_steps) return fail(h, T2I_ERR_SHAPE, "n_steps out of range");
+  if (a->start_step < 0 || a->start_step >= a->n_steps) return fail(h, T2I_ERR_SHAPE, "bad start_step");
+  const bool use_cache = a->cache_tau > 0.0;
+  if (use_cache && (!a->cache_state)) return fail(h, T2I_ERR_INVALID_ARG, "cache needs cache_state");
+  if (a->cache_mode != T2I_CACHE_ACCUMULATE && a->cache_mode != T2I_CACHE_PER_STEP)
+    return fail(h, T2I_ERR_INVALID_ARG, "bad cache_mode");
+  Plan P;
+  t2i_status s = build_plan(h, a->n_req, a->lat_h, a->lat_w, a->guidance, P);
+  if (s != T2I_OK) return s;
+  if (use_cache && a->cache_state_bytes < cache_bytes(c, P.n_req, P.T_img, P.branches))
+    return fail(h, T2I_ERR_WORKSPACE, "cache_state too small");
+  const int n = a->n_steps, R = P.n_req;
+  std::vector<double> ts((size_t)(n + 1) * R);
+  for (int k = 0; k <= n; ++k)
+    for (int r = 0; r < R; ++r) {
+      const double v = a->timesteps ? a->timesteps[(size_t)k * R + r] : 1.0 - (double)k / n;
+      if (!std::isfinite(v)) return fail(h, T2I_ERR_INVALID_ARG, "timestep not finite");
+      ts[(size_t)k * R + r] = v;
+    }
+  hipStream_t st = (hipStream_t)stream;
+  // conditioning rows k*R + r for every step k < n
+  if ((s = conditioning(h, ts.data(), n * R, c.depth, st)) != T2I_OK) return s;
+  if ((s = text_prep(h, P, a->prompt_embeds, st)) != T2I_OK) return s;
+  std::vector<uint8_t> skip(R, 0);
+  std::vector<double> rel(R, 0.0);
+  for (int k = a->start_step; k < n; ++k) {
+    set_modrows(P, k * R);
+    for (int r = 0; r < R; ++r)
+      P.rm.dt[r] = (float)(ts[(size_t)(k + 1) * R + r] - ts[(size_t)k * R + r]);
+    if (use_cache) {
+      HIP_TRY(h, launch_embed(a->latents, P.rm, h->w[W_PE], h->w[B_PE], h->bf(), c.hidden,
+                              c.latent_channels, c.patch, c.arch == T2I_ARCH_CROSS_DIT,
+                              h->at<float>(h->L.x0), h->at<float>(h->L.x), 0, st));
+      if ((s = cache_check_impl(h, P, k, n, a->cache_tau, a->cache_mode, a->cache_state,
+                                rel.data(), skip.data(), st)) != T2I_OK)
+        return s;
+    }
+    for (int r = 0; r < R; ++r) {
+      if (a->skip_log) a->skip_log[(size_t)k * R + r] = skip[r];
+      if (a->rel_l1_log) a->rel_l1_log[(size_t)k * R + r] = use_cache ? rel[r] : NAN;
+    }
+    if ((s = step_body(h, P, a->latents, a->latents, nullptr, c.depth, nullptr,
+                       use_cache ? skip.data() : nullptr, use_cache ? a->cache_state : nullptr,
+                       st)) != T2I_OK)
+      return s;
+  }
+  return T2I_OK;
+}
+
+// ---------------------------------------------------------------------------
+// kernel-level entry points
+
+const char* t2i_ops_last_error(void) { return g_ops_err.c_str(); }
+
+static t2i_status ops_fail(t2i_status s, const std::string& m) {
+  g_ops_err = m;
+  return s;
+}
+
+t2i_status t2i_op_linear(int32_t dtype, int32_t epilogue, int32_t M, int32_t N, int32_t K,
+                         const void* A, int32_t lda, const void* W, int32_t ldw, const void* bias,
+                         void* out, int32_t ldo, float* resid, int32_t ldr, void* resid_copy,
+                         const float* gate, void* stream) {
+  if (dtype != T2I_F32 && dtype != T2I_BF16) return ops_fail(T2I_ERR_INVALID_ARG, "bad dtype");
+  if (epilogue < T2I_EPI_STORE || epilogue > T2I_EPI_RESID_GATED)
+    return ops_fail(T2I_ERR_INVALID_ARG, "bad epilogue");
+  if (M < 1 || N < 1 || K < 1) return ops_fail(T2I_ERR_SHAPE, "empty GEMM");
+  if (!A || !W || !bias) return ops_fail(T2I_ERR_INVALID_ARG, "NULL operand");
+  if (lda < K || ldw < K) return ops_fail(T2I_ERR_SHAPE, "leading dimension < K");
+  const bool res = epilogue >= T2I_EPI_RESID;
+  if (res && (!resid || ldr < N)) return ops_fail(T2I_ERR_INVALID_ARG, "bad residual");
+  if (!res && (!out || ldo < N)) return ops_fail(T2I_ERR_INVALID_ARG, "bad out");
+  if (epilogue == T2I_EPI_RESID_GATED && !gate) return ops_fail(T2I_ERR_INVALID_ARG, "NULL gate");
+  if (dtype == T2I_BF16 && (K % 64 || lda % 8 || ldw % 8))
+    return ops_fail(T2I_ERR_SHAPE, "bf16 GEMM needs K % 64 == 0 and lda, ldw % 8 == 0");
+  Epi e = make_epi();
+  e.out = out;
+  e.ldo = ldo;
+  e.x = resid;
+  e.ldx = ldr;
+  e.xb = (bf16*)resid_copy;
+  e.gate = gate;
+  e.ld_gate = 0;
+  e.map.n = 1;
+  e.map.start[0] = 0;
+  e.map.start[1] = M;
+  e.map.modrow[0] = 0;
+  hipStream_t st = (hipStream_t)stream;
+  hipError_t err = dtype == T2I_BF16
+                       ? launch_gemm_bf16((const bf16*)A, lda, (const bf16*)W, ldw, (const bf16*)bias,
+                                          M, N, K, epilogue, e, st)
+                       : launch_gemm_f32((const float*)A, lda, W, ldw, false, bias, M, N, K,
+                                         epilogue, e, st);
+  if (err != hipSuccess) return ops_fail(T2I_ERR_DEVICE, hipGetErrorString(err));
+  return T2I_OK;
+}
+
+t2i_status t2i_op_attention(int32_t dtype, int32_t heads, int32_t head_dim, int32_t n_seq,
+                            const int32_t* q_start, const int32_t* q_len, const int32_t* k_start,
+                            const int32_t* k_len, const void* q, int32_t ldq, const void* k,
+                            int32_t ldk, const void* v, int32_t ldv, void* o, int32_t ldo,
+                            void* stream) {
+  if (dtype != T2I_F32 && dtype != T2I_BF16) return ops_fail(T2I_ERR_INVALID_ARG, "bad dtype");
+  if (heads < 1 || (head_dim != 8 && head_dim != 32 && head_dim != 64 && head_dim != 72 &&
+                    head_dim != 128))
+    return ops_fail(T2I_ERR_SHAPE, "unsupported head_dim");
+  if (n_seq < 1 || n_seq > kMaxSeq) return ops_fail(T2I_ERR_SHAPE, "bad n_seq");
+  if (!q_start || !q_len || !k_start || !k_len || !q || !k || !v || !o)
+    return ops_fail(T2I_ERR_INVALID_ARG, "NULL pointer");
+  const int w = heads * head_dim;
+  if (ldq < w || ldk < w || ldv < w || ldo < w || ldq % 8 || ldk % 8 || ldv % 8 || ldo % 8)
+    return ops_fail(T2I_ERR_SHAPE, "bad leading dimension");
+  AttnMap m;
+  std::memset(&m, 0, sizeof(m));
+  m.n = n_seq;
+  const int BQ = attention_query_tile(dtype == T2I_BF16, head_dim);
+  int tiles = 0;
+  for (int s = 0; s < n_seq; ++s) {
+    if (q_start[s] < 0 || q_len[s] < 0 || k_start[s] < 0 || k_len[s] < 1)
+      return ops_fail(T2I_ERR_SHAPE, "bad sequence bounds");
+    m.q_start[s] = q_start[s];
+    m.q_len[s] = q_len[s];
+    m.k_start[s] = k_start[s];
+    m.k_len[s] = k_len[s];
+    m.tile_start[s] = tiles;
+    tiles += (q_len[s] + BQ - 1) / BQ;
+  }
+  m.tile_start[n_seq] = tiles;
+  hipError_t err = launch_attention(dtype == T2I_BF16, heads, head_dim, m, q, ldq, k, ldk, v, ldv,
+                                    o, ldo, (hipStream_t)stream);
+  if (err != hipSuccess) return ops_fail(T2I_ERR_DEVICE, hipGetErrorString(err));
+  return T2I_OK;
+}
+
+t2i_status t2i_op_ln_modulate(int32_t dtype, int32_t rows, int32_t D, const float* x,
+                              const float* shift, const float* scale, float eps, void* out,
+                              void* stream) {
+  if (dtype != T2I_F32 && dtype != T2I_BF16) return ops_fail(T2I_ERR_INVALID_ARG, "bad dtype");
+  if (rows < 1 || D < 4 || D % 4 || D > 3072) return ops_fail(T2I_ERR_SHAPE, "bad shape");
+  if (!x || !shift || !scale || !out) return ops_fail(T2I_ERR_INVALID_ARG, "NULL pointer");
+  if (scale != shift + D) return ops_fail(T2I_ERR_INVALID_ARG, "scale must follow shift (scale == shift + D)");
+  SeqMap m;
+  std::memset(&m, 0, sizeof(m));
+  m.n = 1;
+  m.start[1] = rows;
+  hipError_t err = launch_ln_modulate(dtype == T2I_BF16, rows, D, x, D, shift, 2 * D, 0, D, m, out,
+                                      D, eps, (hipStream_t)stream);
+  if (err != hipSuccess) return ops_fail(T2I_ERR_DEVICE, hipGetErrorString(err));
+  return T2I_OK;
+}
+
+}  // extern "C"

@@ -1,0 +1,285 @@
+// Multi-head attention over packed variable-length sequences (self-attention,
+// cross-attention to text, joint attention) on gfx950.
+//
+// attn_bf16_kernel: flash-style, one workgroup = 4 waves = 128 queries of one
+// head of one sequence; each wave owns 32 queries (two 16-query MFMA tiles).
+// Keys/values stream through LDS 64 at a time.  Everything is arranged so that
+// a lane always holds data of ONE query:
+//   * scores are computed transposed, S^T = K Q^T, with v_mfma_f32_16x16x32_bf16
+//     (A = K fragment, B = Q fragment kept in registers for the whole loop):
+//     the C fragment gives lane l the scores of query (l & 15) against keys
+//     4*(l >> 4) + 0..3 of each 16-key tile;
+//   * the output is accumulated transposed, O^T = V^T P^T: the B operand is
+//     exactly the lane's own probabilities (8 keys of two adjacent 16-key
+//     tiles), the A operand is read from a V^T tile in LDS, and the C fragment
+//     again gives lane l query (l & 15) -- so the online-softmax rescale of the
+//     output needs no data exchange between lanes.
+// The row max needs two cross-lane steps per tile (the 4 lanes of a query);
+// row sums are kept per lane and combined once at the end.  The head
+// dimension is padded with zeros to a multiple of 32 for Q K^T and to a
+// multiple of 16 for P V (72 -> 96 / 80); the padding never reaches memory.
+//
+// attn_f32_kernel: plain fp32 online softmax, one thread per query, for the
+// fp32 model.
+#include "t2i_internal.h"
+
+namespace t2i {
+
+__device__ __forceinline__ int xcd_remap_attn(int b, int nb) {
+  const int q = nb >> 3, r = nb & 7;
+  const int x = b & 7, j = b >> 3;
+  return (x < r ? x * (q + 1) : r * (q + 1) + (x - r) * q) + j;
+}
+
+// Flattened tile -> (head, sequence, query tile).  Tiles of one head and one
+// sequence are consecutive so that they land on one XCD and share K/V in L2.
+__device__ __forceinline__ void decode_tile(const AttnMap& m, int heads, int L, int& h, int& s,
+                                            int& j) {
+  const int total = m.tile_start[m.n];
+  h = L / total;
+  const int t = L - h * total;
+  s = 0;
+#pragma unroll 1
+  for (int i = 1; i < m.n; ++i) s += (t >= m.tile_start[i]) ? 1 : 0;
+  j = t - m.tile_start[s];
+}
+
+template <int HD>
+__global__ __launch_bounds__(256) void attn_bf16_kernel(AttnMap map, int heads,
+                                                        const bf16* __restrict__ Q, int ldq,
+                                                        const bf16* __restrict__ K, int ldk,
+                                                        const bf16* __restrict__ V, int ldv,
+                                                        bf16* __restrict__ O, int ldo,
+                                                        float scale_log2) {
+  constexpr int BQ = 128, BKV = 64, QT = 2;
+  constexpr int DC = (HD + 31) / 32;   // 32-wide chunks of d for Q K^T
+  constexpr int HDP = DC * 32;
+  constexpr int DT = (HD + 15) / 16;   // 16-wide tiles of d for P V
+  constexpr int HDO = DT * 16;
+  constexpr int KP = HDP + 8;          // LDS pitch of a K row (bf16)
+  constexpr int VP = BKV + 8;          // LDS pitch of a V^T row (bf16)
+  constexpr int CPR = HD / 8;          // 16-byte chunks per K/V row
+  __shared__ bf16 Ks[BKV * KP];
+  __shared__ bf16 Vt[HDO * VP];
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  int h, s, j;
+  decode_tile(map, heads, xcd_remap_attn(blockIdx.x, gridDim.x), h, s, j);
+  const int q_beg = map.q_start[s], q_end = q_beg + map.q_len[s];
+  const int k_beg = map.k_start[s], k_end = k_beg + map.k_len[s];
+  const int qrow0 = q_beg + j * BQ + wave * 32;
+  const int g = lane >> 4, fr = lane & 15;
+
+  // zero the LDS tiles once: padding columns / rows stay zero
+  for (int i = tid; i < BKV * KP; i += 256) Ks[i] = (bf16)0.f;
+  for (int i = tid; i < HDO * VP; i += 256) Vt[i] = (bf16)0.f;
+
+  // Q fragments (B operand of S^T): query qrow0 + qt*16 + fr, d = c*32 + g*8 .. +7
+  bf16x8 qf[QT][DC];
+#pragma unroll
+  for (int qt = 0; qt < QT; ++qt) {
+    const int qr = qrow0 + qt * 16 + fr;
+#pragma unroll
+    for (int c = 0; c < DC; ++c) {
+      const int d = c * 32 + g * 8;
+      if (qr < q_end && d < HD)
+        qf[qt][c] = *(const bf16x8*)(Q + (size_t)qr * ldq + h * HD + d);
+      else
+        qf[qt][c] = bf16x8{};
+    }
+  }
+
+  f32x4 o[QT][DT];
+  float m_run[QT], l_run[QT];
+#pragma unroll
+  for (int qt = 0; qt < QT; ++qt) {
+    m_run[qt] = -INFINITY;
+    l_run[qt] = 0.f;
+#pragma unroll
+    for (int dt = 0; dt < DT; ++dt) o[qt][dt] = f32x4{0.f, 0.f, 0.f, 0.f};
+  }
+
+  for (int kv0 = k_beg; kv0 < k_end; kv0 += BKV) {
+    __syncthreads();   // previous tile fully consumed (and zero-init done)
+    for (int c = tid; c < BKV * CPR; c += 256) {
+      const int key = c / CPR, dc = (c - key * CPR) * 8;
+      const int gk = kv0 + key;
+      bf16x8 kv = bf16x8{}, vv = bf16x8{};
+      if (gk < k_end) {
+        kv = *(const bf16x8*)(K + (size_t)gk * ldk + h * HD + dc);
+        vv = *(const bf16x8*)(V + (size_t)gk * ldv + h * HD + dc);
+      }
+      *(bf16x8*)&Ks[key * KP + dc] = kv;
+#pragma unroll
+      for (int e = 0; e < 8; ++e) Vt[(dc + e) * VP + key] = vv[e];
+    }
+    __syncthreads();
+    const bool ragged = kv0 + BKV > k_end;
+
+#pragma unroll
+    for (int qt = 0; qt < QT; ++qt) {
+      f32x4 sc[4];
+#pragma unroll
+      for (int kt = 0; kt < 4; ++kt) {
+        sc[kt] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int c = 0; c < DC; ++c) {
+          const bf16x8 kf = *(const bf16x8*)&Ks[(kt * 16 + fr) * KP + c * 32 + g * 8];
+          sc[kt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf, qf[qt][c], sc[kt], 0, 0, 0);
+        }
+      }
+      if (ragged) {
+#pragma unroll
+        for (int kt = 0; kt < 4; ++kt)
+#pragma unroll
+          for (int r = 0; r < 4; ++r)
+            if (kv0 + kt * 16 + g * 4 + r >= k_end) sc[kt][r] = -INFINITY;
+      }
+      float mx = -INFINITY;
+#pragma unroll
+      for (int kt = 0; kt < 4; ++kt)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) mx = fmaxf(mx, sc[kt][r]);
+      mx = fmaxf(mx, __shfl_xor(mx, 16, 64));
+      mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
+      const float m_new = fmaxf(m_run[qt], mx * scale_log2);
+      const float alpha = __builtin_amdgcn_exp2f(m_run[qt] - m_new);
+      m_run[qt] = m_new;
+      float psum = 0.f;
+      bf16x8 pf[2];
+#pragma unroll
+      for (int kt = 0; kt < 4; ++kt) {
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const float p = __builtin_amdgcn_exp2f(sc[kt][r] * scale_log2 - m_new);
+          psum += p;
+          pf[kt >> 1][(kt & 1) * 4 + r] = (bf16)p;
+        }
+      }
+      l_run[qt] = l_run[qt] * alpha + psum;
+#pragma unroll
+      for (int dt = 0; dt < DT; ++dt) {
+        o[qt][dt] *= alpha;
+#pragma unroll
+        for (int kc = 0; kc < 2; ++kc) {
+          const bf16* vrow = &Vt[(dt * 16 + fr) * VP + kc * 32 + g * 4];
+          const bf16x4 lo = *(const bf16x4*)vrow;
+          const bf16x4 hi = *(const bf16x4*)(vrow + 16);
+          const bf16x8 vf = bf16x8{lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
+          o[qt][dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vf, pf[kc], o[qt][dt], 0, 0, 0);
+        }
+      }
+    }
+  }
+
+#pragma unroll
+  for (int qt = 0; qt < QT; ++qt) {
+    float l = l_run[qt];
+    l += __shfl_xor(l, 16, 64);
+    l += __shfl_xor(l, 32, 64);
+    const float inv = 1.0f / l;
+    const int qr = qrow0 + qt * 16 + fr;
+    if (qr >= q_end) continue;
+#pragma unroll
+    for (int dt = 0; dt < DT; ++dt) {
+      const int d = dt * 16 + g * 4;
+      if (d < HD) {
+        bf16x4 w;
+#pragma unroll
+        for (int r = 0; r < 4; ++r) w[r] = (bf16)(o[qt][dt][r] * inv);
+        *(bf16x4*)(O + (size_t)qr * ldo + h * HD + d) = w;
+      }
+    }
+  }
+}
+
+// ---------------------------------------------------------------------------
+
+template <int HD>
+__global__ __launch_bounds__(64) void attn_f32_kernel(AttnMap map, int heads,
+                                                      const float* __restrict__ Q, int ldq,
+                                                      const float* __restrict__ K, int ldk,
+                                                      const float* __restrict__ V, int ldv,
+                                                      float* __restrict__ O, int ldo, float scale) {
+  constexpr int BQ = 64, BKV = 32;
+  __shared__ float Ks[BKV][HD];
+  __shared__ float Vs[BKV][HD];
+  int h, s, j;
+  decode_tile(map, heads, blockIdx.x, h, s, j);
+  const int q_beg = map.q_start[s], q_end = q_beg + map.q_len[s];
+  const int k_beg = map.k_start[s], k_end = k_beg + map.k_len[s];
+  const int qr = q_beg + j * BQ + threadIdx.x;
+  const bool active = qr < q_end;
+  float q[HD], acc[HD];
+#pragma unroll
+  for (int d = 0; d < HD; ++d) {
+    q[d] = active ? Q[(size_t)qr * ldq + h * HD + d] : 0.f;
+    acc[d] = 0.f;
+  }
+  float m = -INFINITY, l = 0.f;
+  for (int kv0 = k_beg; kv0 < k_end; kv0 += BKV) {
+    __syncthreads();
+    for (int i = threadIdx.x; i < BKV * HD; i += 64) {
+      const int key = i / HD, d = i - key * HD, gk = kv0 + key;
+      Ks[key][d] = gk < k_end ? K[(size_t)gk * ldk + h * HD + d] : 0.f;
+      Vs[key][d] = gk < k_end ? V[(size_t)gk * ldv + h * HD + d] : 0.f;
+    }
+    __syncthreads();
+    const int nk = min(BKV, k_end - kv0);
+    for (int key = 0; key < nk; ++key) {
+      float sdot = 0.f;
+#pragma unroll
+      for (int d = 0; d < HD; ++d) sdot = fmaf(q[d], Ks[key][d], sdot);
+      sdot *= scale;
+      const float m_new = fmaxf(m, sdot);
+      const float corr = expf(m - m_new);
+      const float p = expf(sdot - m_new);
+      l = l * corr + p;
+#pragma unroll
+      for (int d = 0; d < HD; ++d) acc[d] = acc[d] * corr + p * Vs[key][d];
+      m = m_new;
+    }
+  }
+  if (active) {
+    const float inv = 1.0f / l;
+#pragma unroll
+    for (int d = 0; d < HD; ++d) O[(size_t)qr * ldo + h * HD + d] = acc[d] * inv;
+  }
+}
+
+int attention_query_tile(bool bf16_io, int /*head_dim*/) { return bf16_io ? 128 : 64; }
+
+template <int HD>
+static hipError_t launch_hd(bool bf16_io, int heads, const AttnMap& map, const void* q, int ldq,
+                            const void* k, int ldk, const void* v, int ldv, void* o, int ldo,
+                            hipStream_t st) {
+  const int tiles = map.tile_start[map.n] * heads;
+  if (tiles == 0) return hipSuccess;
+  if (bf16_io) {
+    const float scale_log2 = 1.4426950408889634f / sqrtf((float)HD);
+    hipLaunchKernelGGL(attn_bf16_kernel<HD>, dim3(tiles), dim3(256), 0, st, map, heads,
+                       (const bf16*)q, ldq, (const bf16*)k, ldk, (const bf16*)v, ldv, (bf16*)o, ldo,
+                       scale_log2);
+  } else {
+    const float scale = 1.0f / sqrtf((float)HD);
+    hipLaunchKernelGGL(attn_f32_kernel<HD>, dim3(tiles), dim3(64), 0, st, map, heads,
+                       (const float*)q, ldq, (const float*)k, ldk, (const float*)v, ldv, (float*)o,
+                       ldo, scale);
+  }
+  return hipGetLastError();
+}
+
+hipError_t launch_attention(bool bf16_io, int heads, int head_dim, const AttnMap& map,
+                            const void* q, int ldq, const void* k, int ldk, const void* v, int ldv,
+                            void* o, int ldo, hipStream_t st) {
+  switch (head_dim) {
+    case 8: return launch_hd<8>(bf16_io, heads, map, q, ldq, k, ldk, v, ldv, o, ldo, st);
+    case 32: return launch_hd<32>(bf16_io, heads, map, q, ldq, k, ldk, v, ldv, o, ldo, st);
+    case 64: return launch_hd<64>(bf16_io, heads, map, q, ldq, k, ldk, v, ldv, o, ldo, st);
+    case 72: return launch_hd<72>(bf16_io, heads, map, q, ldq, k, ldk, v, ldv, o, ldo, st);
+    case 128: return launch_hd<128>(bf16_io, heads, map, q, ldq, k, ldk, v, ldv, o, ldo, st);
+    default: return hipErrorInvalidValue;
+  }
+}
+
+}  // namespace t2i

@@ -1,0 +1,237 @@
+// Linear layers y = A W^T + b of the DiT block (qkv, out, cross-q, cross-out,
+// fc1, fc2, text projections) on gfx950.
+//
+//  * gemm_bf16_kernel: bf16 operands, fp32 accumulation on MFMA
+//    (v_mfma_f32_16x16x32_bf16).  A workgroup of 4 waves owns a BM x BN output
+//    tile; each wave a (BM/2) x (BN/2) quadrant.  K advances 64 at a time
+//    through double-buffered LDS tiles (row pitch 72 bf16 = 144 B, so the 16
+//    rows a fragment load touches fall in distinct bank groups); the next K
+//    tile is fetched from HBM into registers while MFMA works on the current
+//    one.  Workgroups are numbered so that each XCD (dispatched round-robin)
+//    receives a contiguous run of output tiles: tiles sharing A rows share
+//    that XCD's L2.
+//  * gemm_f32_kernel: SIMT fp32 FMA for the fp32 model and the small
+//    conditioning GEMMs (timestep MLP, adaLN table), weights fp32 or bf16.
+//
+// Epilogues (bias always added): store, GELU-tanh, SiLU, residual add,
+// gated residual add (gate row chosen by the row's sequence).
+#include "t2i_internal.h"
+
+namespace t2i {
+
+// Map launch order -> tile order so XCD x (blocks b with b % 8 == x) owns the
+// contiguous tile range of its share.
+__device__ __forceinline__ int xcd_remap(int b, int nb) {
+  const int q = nb >> 3, r = nb & 7;
+  const int x = b & 7, j = b >> 3;
+  return (x < r ? x * (q + 1) : r * (q + 1) + (x - r) * q) + j;
+}
+
+template <int BM, int BN, int KIND>
+__global__ __launch_bounds__(256) void gemm_bf16_kernel(
+    const bf16* __restrict__ A, int lda, const bf16* __restrict__ W, int ldw,
+    const bf16* __restrict__ bias, int M, int N, int K, Epi epi, int tiles_n) {
+  constexpr int BK = 64;
+  constexpr int LDK = BK + 8;
+  constexpr int WM = BM / 2, WN = BN / 2;
+  constexpr int TM = WM / 16, TN = WN / 16;
+  constexpr int ACH = BM * BK / 8 / 256;   // 16-byte chunks per thread
+  constexpr int BCH = BN * BK / 8 / 256;
+  __shared__ bf16 As[2][BM * LDK];
+  __shared__ bf16 Bs[2][BN * LDK];
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int wm = wave >> 1, wn = wave & 1;
+  const int tile = xcd_remap(blockIdx.x, gridDim.x);
+  const int m0 = (tile / tiles_n) * BM, n0 = (tile % tiles_n) * BN;
+
+  const int lrow = tid >> 3, lk = (tid & 7) * 8;
+  const bf16* Ap[ACH];
+  const bf16* Bp[BCH];
+#pragma unroll
+  for (int i = 0; i < ACH; ++i) Ap[i] = A + (size_t)min(m0 + lrow + 32 * i, M - 1) * lda + lk;
+#pragma unroll
+  for (int i = 0; i < BCH; ++i) Bp[i] = W + (size_t)min(n0 + lrow + 32 * i, N - 1) * ldw + lk;
+
+  bf16x8 ra[ACH], rb[BCH];
+  auto gload = [&](int k0) {
+#pragma unroll
+    for (int i = 0; i < ACH; ++i) ra[i] = *(const bf16x8*)(Ap[i] + k0);
+#pragma unroll
+    for (int i = 0; i < BCH; ++i) rb[i] = *(const bf16x8*)(Bp[i] + k0);
+  };
+  auto sstore = [&](int buf) {
+#pragma unroll
+    for (int i = 0; i < ACH; ++i) *(bf16x8*)&As[buf][(lrow + 32 * i) * LDK + lk] = ra[i];
+#pragma unroll
+    for (int i = 0; i < BCH; ++i) *(bf16x8*)&Bs[buf][(lrow + 32 * i) * LDK + lk] = rb[i];
+  };
+
+  f32x4 acc[TM][TN];
+#pragma unroll
+  for (int i = 0; i < TM; ++i)
+#pragma unroll
+    for (int j = 0; j < TN; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+  const int KT = K / BK;
+  gload(0);
+  sstore(0);
+  __syncthreads();
+  const int fr = lane & 15, fk = (lane >> 4) * 8;
+  for (int kt = 0; kt < KT; ++kt) {
+    const int buf = kt & 1;
+    if (kt + 1 < KT) gload((kt + 1) * BK);
+#pragma unroll
+    for (int kk = 0; kk < BK; kk += 32) {
+      bf16x8 af[TM], bfr[TN];
+#pragma unroll
+      for (int i = 0; i < TM; ++i)
+        af[i] = *(const bf16x8*)&As[buf][(wm * WM + i * 16 + fr) * LDK + kk + fk];
+#pragma unroll
+      for (int j = 0; j < TN; ++j)
+        bfr[j] = *(const bf16x8*)&Bs[buf][(wn * WN + j * 16 + fr) * LDK + kk + fk];
+#pragma unroll
+      for (int i = 0; i < TM; ++i)
+#pragma unroll
+        for (int j = 0; j < TN; ++j)
+          acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af[i], bfr[j], acc[i][j], 0, 0, 0);
+    }
+    if (kt + 1 < KT) sstore(buf ^ 1);
+    __syncthreads();
+  }
+
+  // C fragment layout: lane holds column (lane & 15), rows 4*(lane >> 4) + 0..3.
+#pragma unroll
+  for (int j = 0; j < TN; ++j) {
+    const int n = n0 + wn * WN + j * 16 + fr;
+    if (n >= N) continue;
+    const float b = (float)bias[n];
+#pragma unroll
+    for (int i = 0; i < TM; ++i) {
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int m = m0 + wm * WM + i * 16 + (lane >> 4) * 4 + r;
+        if (m < M) epi_apply<bf16>(epi, KIND, m, n, acc[i][j][r] + b);
+      }
+    }
+  }
+}
+
+template <int BM, int BN>
+static hipError_t gemm_bf16_dispatch(const bf16* A, int lda, const bf16* W, int ldw,
+                                     const bf16* bias, int M, int N, int K, int kind,
+                                     const Epi& epi, hipStream_t st) {
+  const int tn = (N + BN - 1) / BN, tm = (M + BM - 1) / BM;
+  dim3 grid(tm * tn), block(256);
+  switch (kind) {
+    case EPI_STORE:
+      hipLaunchKernelGGL((gemm_bf16_kernel<BM, BN, EPI_STORE>), grid, block, 0, st, A, lda, W, ldw, bias, M, N, K, epi, tn);
+      break;
+    case EPI_GELU:
+      hipLaunchKernelGGL((gemm_bf16_kernel<BM, BN, EPI_GELU>), grid, block, 0, st, A, lda, W, ldw, bias, M, N, K, epi, tn);
+      break;
+    case EPI_SILU:
+      hipLaunchKernelGGL((gemm_bf16_kernel<BM, BN, EPI_SILU>), grid, block, 0, st, A, lda, W, ldw, bias, M, N, K, epi, tn);
+      break;
+    case EPI_RESID:
+      hipLaunchKernelGGL((gemm_bf16_kernel<BM, BN, EPI_RESID>), grid, block, 0, st, A, lda, W, ldw, bias, M, N, K, epi, tn);
+      break;
+    default:
+      hipLaunchKernelGGL((gemm_bf16_kernel<BM, BN, EPI_RESID_GATED>), grid, block, 0, st, A, lda, W, ldw, bias, M, N, K, epi, tn);
+      break;
+  }
+  return hipGetLastError();
+}
+
+hipError_t launch_gemm_bf16(const bf16* A, int lda, const bf16* W, int ldw, const bf16* bias,
+                            int M, int N, int K, int kind, const Epi& epi, hipStream_t st) {
+  if (M <= 0 || N <= 0) return hipSuccess;
+  return gemm_bf16_dispatch<128, 128>(A, lda, W, ldw, bias, M, N, K, kind, epi, st);
+}
+
+// ---------------------------------------------------------------------------
+
+template <typename TW, int KIND>
+__global__ __launch_bounds__(256) void gemm_f32_kernel(
+    const float* __restrict__ A, int lda, const TW* __restrict__ W, int ldw,
+    const TW* __restrict__ bias, int M, int N, int K, Epi epi) {
+  constexpr int BM = 64, BN = 64, BK = 16;
+  __shared__ float As[BK][BM + 4];
+  __shared__ float Bs[BK][BN + 4];
+  const int tid = threadIdx.x, tx = tid & 15, ty = tid >> 4;
+  const int m0 = blockIdx.y * BM, n0 = blockIdx.x * BN;
+  float acc[4][4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+#pragma unroll
+    for (int j = 0; j < 4; ++j) acc[i][j] = 0.f;
+
+  for (int k0 = 0; k0 < K; k0 += BK) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int idx = tid + 256 * i, r = idx >> 4, kk = idx & 15;
+      const int m = m0 + r, n = n0 + r, k = k0 + kk;
+      As[kk][r] = (m < M && k < K) ? A[(size_t)m * lda + k] : 0.f;
+      Bs[kk][r] = (n < N && k < K) ? to_f32(W[(size_t)n * ldw + k]) : 0.f;
+    }
+    __syncthreads();
+#pragma unroll
+    for (int kk = 0; kk < BK; ++kk) {
+      float a[4], b[4];
+#pragma unroll
+      for (int i = 0; i < 4; ++i) a[i] = As[kk][ty * 4 + i];
+#pragma unroll
+      for (int j = 0; j < 4; ++j) b[j] = Bs[kk][tx * 4 + j];
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int j = 0; j < 4; ++j) acc[i][j] = fmaf(a[i], b[j], acc[i][j]);
+    }
+    __syncthreads();
+  }
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const int m = m0 + ty * 4 + i;
+    if (m >= M) continue;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int n = n0 + tx * 4 + j;
+      if (n < N) epi_apply<float>(epi, KIND, m, n, acc[i][j] + to_f32(bias[n]));
+    }
+  }
+}
+
+template <typename TW>
+static hipError_t gemm_f32_dispatch(const float* A, int lda, const TW* W, int ldw, const TW* bias,
+                                    int M, int N, int K, int kind, const Epi& epi, hipStream_t st) {
+  dim3 grid((N + 63) / 64, (M + 63) / 64), block(256);
+  switch (kind) {
+    case EPI_STORE:
+      hipLaunchKernelGGL((gemm_f32_kernel<TW, EPI_STORE>), grid, block, 0, st, A, lda, W, ldw, bias, M, N, K, epi);
+      break;
+    case EPI_GELU:
+      hipLaunchKernelGGL((gemm_f32_kernel<TW, EPI_GELU>), grid, block, 0, st, A, lda, W, ldw, bias, M, N, K, epi);
+      break;
+    case EPI_SILU:
+      hipLaunchKernelGGL((gemm_f32_kernel<TW, EPI_SILU>), grid, block, 0, st, A, lda, W, ldw, bias, M, N, K, epi);
+      break;
+    case EPI_RESID:
+      hipLaunchKernelGGL((gemm_f32_kernel<TW, EPI_RESID>), grid, block, 0, st, A, lda, W, ldw, bias, M, N, K, epi);
+      break;
+    default:
+      hipLaunchKernelGGL((gemm_f32_kernel<TW, EPI_RESID_GATED>), grid, block, 0, st, A, lda, W, ldw, bias, M, N, K, epi);
+      break;
+  }
+  return hipGetLastError();
+}
+
+hipError_t launch_gemm_f32(const float* A, int lda, const void* W, int ldw, bool w_bf16,
+                           const void* bias, int M, int N, int K, int kind, const Epi& epi,
+                           hipStream_t st) {
+  if (M <= 0 || N <= 0) return hipSuccess;
+  if (w_bf16)
+    return gemm_f32_dispatch<bf16>(A, lda, (const bf16*)W, ldw, (const bf16*)bias, M, N, K, kind, epi, st);
+  return gemm_f32_dispatch<float>(A, lda, (const float*)W, ldw, (const float*)bias, M, N, K, kind, epi, st);
+}
+
+}  // namespace t2i

@@ -1,0 +1,505 @@
+// HBM-bound kernels of the denoising step on gfx950: patch + position
+// embedding, timestep sinusoid, LayerNorm fused with adaLN modulation, the
+// final layer fused with unpatchify + classifier-free guidance + Euler update,
+// and the step-skip cache reductions.
+//
+// Row kernels use one 64-lane wave per row with float4 loads (a row of
+// D = 1152 floats is 4.5 KB: lane i reads float4 i, i+64, ...), so every load
+// instruction of a wave covers 1 KB of contiguous memory.  Reductions run in
+// registers with a fixed butterfly order, so results are bitwise reproducible.
+#include <algorithm>
+
+#include "t2i_internal.h"
+
+namespace t2i {
+
+constexpr int kMaxV4 = 12;   // float4 per lane: rows up to 3072 wide
+
+// ---------------------------------------------------------------------------
+// LayerNorm (biased variance, no affine) + modulation.
+
+template <typename OutT>
+__global__ __launch_bounds__(256) void ln_mod_kernel(const float* __restrict__ x, int ldx, int rows,
+                                                     int D, const float* __restrict__ mod,
+                                                     int ld_mod, int shift_off, int scale_off,
+                                                     SeqMap map, OutT* __restrict__ out, int ldo,
+                                                     float eps) {
+  const int lane = threadIdx.x & 63;
+  const int row = blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (row >= rows) return;
+  const float4* xr = (const float4*)(x + (size_t)row * ldx);
+  const int nv = D >> 2;
+  float4 v[kMaxV4];
+  float s = 0.f;
+#pragma unroll
+  for (int i = 0; i < kMaxV4; ++i) {
+    const int c = lane + 64 * i;
+    if (c < nv) {
+      v[i] = xr[c];
+      s += (v[i].x + v[i].y) + (v[i].z + v[i].w);
+    }
+  }
+  const float mean = wave_sum(s) / (float)D;
+  float q = 0.f;
+#pragma unroll
+  for (int i = 0; i < kMaxV4; ++i) {
+    const int c = lane + 64 * i;
+    if (c < nv) {
+      const float a = v[i].x - mean, b = v[i].y - mean, cc = v[i].z - mean, d = v[i].w - mean;
+      q += (a * a + b * b) + (cc * cc + d * d);
+    }
+  }
+  const float rstd = 1.0f / sqrtf(wave_sum(q) / (float)D + eps);
+  const float* md = mod + (size_t)map.modrow[seq_of_row(map, row)] * ld_mod;
+  const float4* sh = (const float4*)(md + shift_off);
+  const float4* sc = (const float4*)(md + scale_off);
+  OutT* orow = out + (size_t)row * ldo;
+#pragma unroll
+  for (int i = 0; i < kMaxV4; ++i) {
+    const int c = lane + 64 * i;
+    if (c < nv) {
+      const float4 a = sh[c], b = sc[c];
+      orow[4 * c + 0] = from_f32<OutT>((v[i].x - mean) * rstd * (1.f + b.x) + a.x);
+      orow[4 * c + 1] = from_f32<OutT>((v[i].y - mean) * rstd * (1.f + b.y) + a.y);
+      orow[4 * c + 2] = from_f32<OutT>((v[i].z - mean) * rstd * (1.f + b.z) + a.z);
+      orow[4 * c + 3] = from_f32<OutT>((v[i].w - mean) * rstd * (1.f + b.w) + a.w);
+    }
+  }
+}
+
+hipError_t launch_ln_modulate(bool bf16_out, int rows, int D, const float* x, int ldx,
+                              const float* mod, int ld_mod, int shift_off, int scale_off,
+                              const SeqMap& map, void* out, int ldo, float eps, hipStream_t st) {
+  if (rows <= 0) return hipSuccess;
+  dim3 grid((rows + 3) / 4), block(256);
+  if (bf16_out)
+    hipLaunchKernelGGL(ln_mod_kernel<bf16>, grid, block, 0, st, x, ldx, rows, D, mod, ld_mod,
+                       shift_off, scale_off, map, (bf16*)out, ldo, eps);
+  else
+    hipLaunchKernelGGL(ln_mod_kernel<float>, grid, block, 0, st, x, ldx, rows, D, mod, ld_mod,
+                       shift_off, scale_off, map, (float*)out, ldo, eps);
+  return hipGetLastError();
+}
+
+// ---------------------------------------------------------------------------
+// Patchify + patch embedding (+ 2D sin-cos position embedding).
+// Token i*(w/p)+j of a request reads latent [c, i*p+a, j*p+b] as feature
+// (a*p+b)*C+c.  Writes x0 (one copy) and `copies` copies into x (one per
+// guidance branch, branch-major).
+
+template <typename TW>
+__global__ __launch_bounds__(256) void embed_kernel(const float* __restrict__ lat, ReqMap rm,
+                                                    const TW* __restrict__ w_pe,
+                                                    const TW* __restrict__ b_pe, int D, int C,
+                                                    int p, int pos_embed, float* __restrict__ x0,
+                                                    float* __restrict__ x, int copies) {
+  const int P = p * p * C;
+  const long total = (long)rm.tokens_total * D;
+  for (long idx = blockIdx.x * 256L + threadIdx.x; idx < total; idx += (long)gridDim.x * 256) {
+    const int tok = (int)(idx / D), d = (int)(idx - (long)tok * D);
+    const int r = req_of_token(rm, tok);
+    const int lt = tok - rm.tok_off[r];
+    const int W = rm.w[r], H = rm.h[r], gw = W / p;
+    const int gi = lt / gw, gj = lt - gi * gw;
+    const float* L = lat + rm.lat_off[r];
+    float acc = to_f32(b_pe[d]);
+    const TW* wr = w_pe + (size_t)d * P;
+    for (int a = 0; a < p; ++a)
+      for (int b = 0; b < p; ++b)
+        for (int c = 0; c < C; ++c)
+          acc = fmaf(to_f32(wr[(a * p + b) * C + c]),
+                     L[(size_t)c * H * W + (size_t)(gi * p + a) * W + gj * p + b], acc);
+    if (pos_embed) {
+      // first D/2 channels: row gi, last D/2: column gj; within a half the
+      // first D/4 are sin(pos w_k), the next D/4 cos(pos w_k), w_k = 10000^(-k/(D/4))
+      const int half = D / 2, qd = D / 4;
+      const int k = d % half;
+      const int pos = d < half ? gi : gj;
+      const int f = k % qd;
+      const double ang = (double)pos * pow(10000.0, -(double)f / (double)qd);
+      acc += (float)(k < qd ? sin(ang) : cos(ang));
+    }
+    x0[(size_t)tok * D + d] = acc;
+    for (int cp = 0; cp < copies; ++cp) x[((size_t)cp * rm.tokens_total + tok) * D + d] = acc;
+  }
+}
+
+hipError_t launch_embed(const float* lat, const ReqMap& rm, const void* w_pe, const void* b_pe,
+                        bool w_bf16, int D, int C, int p, bool pos_embed, float* x0, float* x,
+                        int copies, hipStream_t st) {
+  const long total = (long)rm.tokens_total * D;
+  if (total == 0) return hipSuccess;
+  const int grid = (int)std::min<long>((total + 255) / 256, 8192);
+  if (w_bf16)
+    hipLaunchKernelGGL(embed_kernel<bf16>, dim3(grid), dim3(256), 0, st, lat, rm, (const bf16*)w_pe,
+                       (const bf16*)b_pe, D, C, p, pos_embed ? 1 : 0, x0, x, copies);
+  else
+    hipLaunchKernelGGL(embed_kernel<float>, dim3(grid), dim3(256), 0, st, lat, rm,
+                       (const float*)w_pe, (const float*)b_pe, D, C, p, pos_embed ? 1 : 0, x0, x,
+                       copies);
+  return hipGetLastError();
+}
+
+// ---------------------------------------------------------------------------
+// Timestep sinusoid: row r, s = t_scale * t[r]: [cos(s f_k) | sin(s f_k)],
+// f_k = exp(-ln(10000) k / half), evaluated in fp64.
+
+__global__ void timestep_freq_kernel(TVals tv, int freq_dim, double t_scale,
+                                     float* __restrict__ out) {
+  const int half = freq_dim / 2;
+  const int idx = blockIdx.x * blockDim.x + threadIdx.x;
+  if (idx >= tv.n * freq_dim) return;
+  const int r = idx / freq_dim, k = idx - r * freq_dim;
+  const int kk = k < half ? k : k - half;
+  const double f = exp(-log(10000.0) * (double)kk / (double)half);
+  const double a = t_scale * tv.t[r] * f;
+  out[idx] = (float)(k < half ? cos(a) : sin(a));
+}
+
+hipError_t launch_timestep_freq(const double* t, int rows, int freq_dim, double t_scale,
+                                float* out, hipStream_t st) {
+  for (int r0 = 0; r0 < rows; r0 += kTValsChunk) {
+    TVals tv;
+    tv.n = std::min(kTValsChunk, rows - r0);
+    for (int i = 0; i < tv.n; ++i) tv.t[i] = t[r0 + i];
+    const int n = tv.n * freq_dim;
+    hipLaunchKernelGGL(timestep_freq_kernel, dim3((n + 255) / 256), dim3(256), 0, st, tv, freq_dim,
+                       t_scale, out + (size_t)r0 * freq_dim);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+  }
+  return hipSuccess;
+}
+
+// dst[r][:] = src[:] (bf16 or fp32 rows of width D)
+__global__ void broadcast_rows_kernel(const uint16_t* __restrict__ src16,
+                                      const float* __restrict__ src32, int rows, int D,
+                                      uint16_t* __restrict__ dst16, float* __restrict__ dst32) {
+  const long n = (long)rows * D;
+  for (long i = blockIdx.x * 256L + threadIdx.x; i < n; i += (long)gridDim.x * 256) {
+    const int d = (int)(i % D);
+    if (src16) dst16[i] = src16[d];
+    else dst32[i] = src32[d];
+  }
+}
+
+hipError_t launch_broadcast_rows(const void* src, bool bf16_io, int rows, int D, void* dst,
+                                 hipStream_t st) {
+  const long n = (long)rows * D;
+  if (n == 0) return hipSuccess;
+  const int grid = (int)std::min<long>((n + 255) / 256, 4096);
+  hipLaunchKernelGGL(broadcast_rows_kernel, dim3(grid), dim3(256), 0, st,
+                     bf16_io ? (const uint16_t*)src : nullptr, bf16_io ? nullptr : (const float*)src,
+                     rows, D, bf16_io ? (uint16_t*)dst : nullptr, bf16_io ? nullptr : (float*)dst);
+  return hipGetLastError();
+}
+
+// ---------------------------------------------------------------------------
+// Final layer: per image token and guidance branch,
+//   out = LNmod(x; shift, scale) W_out^T + b_out     (P = p*p*C outputs)
+// then v = v_u + g (v_c - v_u), unpatchify, noise_pred = v, latent += dt v.
+// One wave per token; lane f < P ends up holding output feature f.
+
+template <typename TW>
+__global__ __launch_bounds__(256) void final_kernel(const float* __restrict__ x, ReqMap rm,
+                                                    const TW* __restrict__ w_out,
+                                                    const TW* __restrict__ b_out,
+                                                    const float* __restrict__ mod, int ld_mod,
+                                                    int shift_off, int scale_off, int D, int C,
+                                                    int p, float eps, float guidance,
+                                                    float* __restrict__ lat,
+                                                    float* __restrict__ noise_pred) {
+  const int lane = threadIdx.x & 63;
+  const int tok = blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (tok >= rm.tokens_total) return;
+  const int r = req_of_token(rm, tok);
+  const int P = p * p * C;
+  const int nv = D >> 2;
+  const float* md = mod + (size_t)rm.modrow[r] * ld_mod;
+  const float4* sh = (const float4*)(md + shift_off);
+  const float4* sc = (const float4*)(md + scale_off);
+  float mine[2] = {0.f, 0.f};
+  for (int br = 0; br < rm.branches; ++br) {
+    const float4* xr = (const float4*)(x + ((size_t)br * rm.tokens_total + tok) * D);
+    float4 v[kMaxV4];
+    float s = 0.f;
+#pragma unroll
+    for (int i = 0; i < kMaxV4; ++i) {
+      const int c = lane + 64 * i;
+      if (c < nv) {
+        v[i] = xr[c];
+        s += (v[i].x + v[i].y) + (v[i].z + v[i].w);
+      }
+    }
+    const float mean = wave_sum(s) / (float)D;
+    float q = 0.f;
+#pragma unroll
+    for (int i = 0; i < kMaxV4; ++i) {
+      const int c = lane + 64 * i;
+      if (c < nv) {
+        const float a = v[i].x - mean, b = v[i].y - mean, cc = v[i].z - mean, d = v[i].w - mean;
+        q += (a * a + b * b) + (cc * cc + d * d);
+      }
+    }
+    const float rstd = 1.0f / sqrtf(wave_sum(q) / (float)D + eps);
+#pragma unroll
+    for (int i = 0; i < kMaxV4; ++i) {
+      const int c = lane + 64 * i;
+      if (c < nv) {
+        const float4 a = sh[c], b = sc[c];
+        v[i].x = (v[i].x - mean) * rstd * (1.f + b.x) + a.x;
+        v[i].y = (v[i].y - mean) * rstd * (1.f + b.y) + a.y;
+        v[i].z = (v[i].z - mean) * rstd * (1.f + b.z) + a.z;
+        v[i].w = (v[i].w - mean) * rstd * (1.f + b.w) + a.w;
+      }
+    }
+    for (int f = 0; f < P; ++f) {
+      const TW* wr = w_out + (size_t)f * D;
+      float part = 0.f;
+#pragma unroll
+      for (int i = 0; i < kMaxV4; ++i) {
+        const int c = lane + 64 * i;
+        if (c < nv) {
+          part = fmaf(v[i].x, to_f32(wr[4 * c + 0]), part);
+          part = fmaf(v[i].y, to_f32(wr[4 * c + 1]), part);
+          part = fmaf(v[i].z, to_f32(wr[4 * c + 2]), part);
+          part = fmaf(v[i].w, to_f32(wr[4 * c + 3]), part);
+        }
+      }
+      const float tot = wave_sum(part) + to_f32(b_out[f]);
+      if (lane == f) mine[br] = tot;
+    }
+  }
+  if (lane >= P) return;
+  const float vel = rm.branches == 2 ? mine[1] + guidance * (mine[0] - mine[1]) : mine[0];
+  const int f = lane;
+  const int a = f / (p * C), b = (f / C) % p, c = f % C;
+  const int lt = tok - rm.tok_off[r];
+  const int W = rm.w[r], H = rm.h[r], gw = W / p;
+  const int gi = lt / gw, gj = lt - gi * gw;
+  const size_t li = (size_t)rm.lat_off[r] + (size_t)c * H * W + (size_t)(gi * p + a) * W + gj * p + b;
+  if (noise_pred) noise_pred[li] = vel;
+  const float dt = rm.dt[r];
+  if (dt != 0.f) lat[li] = lat[li] + dt * vel;
+}
+
+hipError_t launch_final_layer(const float* x, const ReqMap& rm, const void* w_out,
+                              const void* b_out, bool w_bf16, const float* mod, int ld_mod,
+                              int shift_off, int scale_off, int D, int C, int p, float eps,
+                              float guidance, float* latents, float* noise_pred, hipStream_t st) {
+  if (rm.tokens_total == 0) return hipSuccess;
+  dim3 grid((rm.tokens_total + 3) / 4), block(256);
+  if (w_bf16)
+    hipLaunchKernelGGL(final_kernel<bf16>, grid, block, 0, st, x, rm, (const bf16*)w_out,
+                       (const bf16*)b_out, mod, ld_mod, shift_off, scale_off, D, C, p, eps,
+                       guidance, latents, noise_pred);
+  else
+    hipLaunchKernelGGL(final_kernel<float>, grid, block, 0, st, x, rm, (const float*)w_out,
+                       (const float*)b_out, mod, ld_mod, shift_off, scale_off, D, C, p, eps,
+                       guidance, latents, noise_pred);
+  return hipGetLastError();
+}
+
+// ---------------------------------------------------------------------------
+// Step-skip cache.
+//
+// cache_signal_kernel: workgroup = 16 rows of one request.  m = LNmod(x0;
+// block-0 shift_msa, scale_msa) in fp32; partial[blk] = (sum|m - m_prev|,
+// sum|m_prev|) in fp64 (lane order, butterfly, then waves 0..3); m_prev := m.
+// cache_decide_kernel: one thread per request sums its partials in block
+// order and applies the rule.
+
+int cache_partial_blocks(const ReqMap& rm) {
+  int n = 0;
+  for (int r = 0; r < rm.n; ++r)
+    n += (rm.tok_off[r + 1] - rm.tok_off[r] + kCacheRowsPerBlock - 1) / kCacheRowsPerBlock;
+  return n;
+}
+
+__global__ __launch_bounds__(256) void cache_signal_kernel(
+    const float* __restrict__ x0, ReqMap rm, const float* __restrict__ mod, int ld_mod,
+    int shift_off, int scale_off, int D, float eps, float* __restrict__ m_prev,
+    const CacheHeader* __restrict__ hdr, int step, double* __restrict__ partial) {
+  __shared__ double red[4][2];
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  // block -> (request, row chunk)
+  int r = 0, base = 0;
+  for (;;) {
+    const int nb = (rm.tok_off[r + 1] - rm.tok_off[r] + kCacheRowsPerBlock - 1) / kCacheRowsPerBlock;
+    if ((int)blockIdx.x < base + nb || r == rm.n - 1) break;
+    base += nb;
+    ++r;
+  }
+  const int chunk = blockIdx.x - base;
+  const bool have_prev = step > 0 && hdr[r].has_m;
+  const float* md = mod + (size_t)rm.modrow[r] * ld_mod;
+  const float4* sh = (const float4*)(md + shift_off);
+  const float4* sc = (const float4*)(md + scale_off);
+  const int nv = D >> 2;
+  double num = 0.0, den = 0.0;
+  for (int rr = 0; rr < kCacheRowsPerBlock / 4; ++rr) {
+    const int tok = rm.tok_off[r] + chunk * kCacheRowsPerBlock + wave * (kCacheRowsPerBlock / 4) + rr;
+    if (tok >= rm.tok_off[r + 1]) break;
+    const float4* xr = (const float4*)(x0 + (size_t)tok * D);
+    float4* mr = (float4*)(m_prev + (size_t)tok * D);
+    float4 v[kMaxV4];
+    float s = 0.f;
+#pragma unroll
+    for (int i = 0; i < kMaxV4; ++i) {
+      const int c = lane + 64 * i;
+      if (c < nv) {
+        v[i] = xr[c];
+        s += (v[i].x + v[i].y) + (v[i].z + v[i].w);
+      }
+    }
+    const float mean = wave_sum(s) / (float)D;
+    float q = 0.f;
+#pragma unroll
+    for (int i = 0; i < kMaxV4; ++i) {
+      const int c = lane + 64 * i;
+      if (c < nv) {
+        const float a = v[i].x - mean, b = v[i].y - mean, cc = v[i].z - mean, d = v[i].w - mean;
+        q += (a * a + b * b) + (cc * cc + d * d);
+      }
+    }
+    const float rstd = 1.0f / sqrtf(wave_sum(q) / (float)D + eps);
+#pragma unroll
+    for (int i = 0; i < kMaxV4; ++i) {
+      const int c = lane + 64 * i;
+      if (c < nv) {
+        const float4 a = sh[c], b = sc[c];
+        float4 m;
+        m.x = (v[i].x - mean) * rstd * (1.f + b.x) + a.x;
+        m.y = (v[i].y - mean) * rstd * (1.f + b.y) + a.y;
+        m.z = (v[i].z - mean) * rstd * (1.f + b.z) + a.z;
+        m.w = (v[i].w - mean) * rstd * (1.f + b.w) + a.w;
+        if (have_prev) {
+          const float4 o = mr[c];
+          num += (double)fabsf(m.x - o.x) + (double)fabsf(m.y - o.y) +
+                 (double)fabsf(m.z - o.z) + (double)fabsf(m.w - o.w);
+          den += (double)fabsf(o.x) + (double)fabsf(o.y) + (double)fabsf(o.z) + (double)fabsf(o.w);
+        }
+        mr[c] = m;
+      }
+    }
+  }
+  num = wave_sum(num);
+  den = wave_sum(den);
+  if (lane == 0) {
+    red[wave][0] = num;
+    red[wave][1] = den;
+  }
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    partial[2 * blockIdx.x + 0] = ((red[0][0] + red[1][0]) + red[2][0]) + red[3][0];
+    partial[2 * blockIdx.x + 1] = ((red[0][1] + red[1][1]) + red[2][1]) + red[3][1];
+  }
+}
+
+__global__ void cache_decide_kernel(ReqMap rm, const double* __restrict__ partial,
+                                    CacheHeader* __restrict__ hdr, int step, int n_steps,
+                                    double tau, int mode) {
+  const int r = threadIdx.x;
+  if (r >= rm.n) return;
+  int b0 = 0;
+  for (int i = 0; i < r; ++i)
+    b0 += (rm.tok_off[i + 1] - rm.tok_off[i] + kCacheRowsPerBlock - 1) / kCacheRowsPerBlock;
+  const int nb = (rm.tok_off[r + 1] - rm.tok_off[r] + kCacheRowsPerBlock - 1) / kCacheRowsPerBlock;
+  CacheHeader hd = hdr[r];
+  if (step == 0) {
+    hd.acc = 0.0;
+    hd.has_m = 0;
+    hd.has_r = 0;
+  }
+  double d = __longlong_as_double(0x7ff8000000000000LL);   // NaN: no predecessor
+  if (hd.has_m) {
+    double num = 0.0, den = 0.0;
+    for (int b = 0; b < nb; ++b) {
+      num += partial[2 * (b0 + b) + 0];
+      den += partial[2 * (b0 + b) + 1];
+    }
+    d = num / den;
+  }
+  int skip = 0;
+  double acc = hd.acc;
+  if (tau > 0.0 && step != 0 && step != n_steps - 1 && hd.has_r && hd.has_m) {
+    if (mode == 0) {
+      acc = acc + d;
+      skip = acc < tau;
+    } else {
+      acc = d;
+      skip = d < tau;
+    }
+  }
+  if (!skip) acc = 0.0;
+  hd.acc = acc;
+  hd.d = d;
+  hd.skip = skip;
+  hd.has_m = 1;
+  hdr[r] = hd;
+}
+
+hipError_t launch_cache_signal(const float* x0, const ReqMap& rm, const float* mod, int ld_mod,
+                               int shift_off, int scale_off, int D, float eps, float* m_prev,
+                               CacheHeader* hdr, int step, double* partial, hipStream_t st) {
+  const int nb = cache_partial_blocks(rm);
+  if (nb == 0) return hipSuccess;
+  hipLaunchKernelGGL(cache_signal_kernel, dim3(nb), dim3(256), 0, st, x0, rm, mod, ld_mod,
+                     shift_off, scale_off, D, eps, m_prev, hdr, step, partial);
+  return hipGetLastError();
+}
+
+hipError_t launch_cache_decide(const ReqMap& rm, const double* partial, CacheHeader* hdr,
+                               int step, int n_steps, double tau, int mode, hipStream_t st) {
+  hipLaunchKernelGGL(cache_decide_kernel, dim3(1), dim3(64), 0, st, rm, partial, hdr, step,
+                     n_steps, tau, mode);
+  return hipGetLastError();
+}
+
+// x[b][tok] = x0[tok] + R[b][tok] (skip_mask) / R[b][tok] = x[b][tok] - x0[tok] (store_mask)
+__global__ void residual_kernel(const float* __restrict__ x0, const float* __restrict__ R_in,
+                                float* __restrict__ x, float* __restrict__ R_out, ReqMap rm,
+                                uint32_t mask, int D, int store, CacheHeader* __restrict__ hdr) {
+  const int nv = D >> 2;
+  const long per_branch = (long)rm.tokens_total * nv;
+  const long total = per_branch * rm.branches;
+  if (store && blockIdx.x == 0 && threadIdx.x < (unsigned)rm.n && ((mask >> threadIdx.x) & 1u))
+    hdr[threadIdx.x].has_r = 1;
+  for (long i = blockIdx.x * 256L + threadIdx.x; i < total; i += (long)gridDim.x * 256) {
+    const int br = (int)(i / per_branch);
+    const long j = i - (long)br * per_branch;
+    const int tok = (int)(j / nv);
+    const int r = req_of_token(rm, tok);
+    if (!((mask >> r) & 1u)) continue;
+    const float4 a = ((const float4*)x0)[j];
+    if (store) {
+      const float4 b = ((const float4*)x)[i];
+      ((float4*)R_out)[i] = float4{b.x - a.x, b.y - a.y, b.z - a.z, b.w - a.w};
+    } else {
+      const float4 b = ((const float4*)R_in)[i];
+      ((float4*)x)[i] = float4{a.x + b.x, a.y + b.y, a.z + b.z, a.w + b.w};
+    }
+  }
+}
+
+hipError_t launch_apply_residual(const float* x0, const float* R, float* x, const ReqMap& rm,
+                                 uint32_t skip_mask, int D, hipStream_t st) {
+  const long total = (long)rm.tokens_total * (D / 4) * rm.branches;
+  if (total == 0 || skip_mask == 0) return hipSuccess;
+  const int grid = (int)std::min<long>((total + 255) / 256, 8192);
+  hipLaunchKernelGGL(residual_kernel, dim3(grid), dim3(256), 0, st, x0, R, x, (float*)nullptr, rm,
+                     skip_mask, D, 0, (CacheHeader*)nullptr);
+  return hipGetLastError();
+}
+
+hipError_t launch_store_residual(const float* x0, const float* x, float* R, const ReqMap& rm,
+                                 uint32_t store_mask, int D, CacheHeader* hdr, hipStream_t st) {
+  const long total = (long)rm.tokens_total * (D / 4) * rm.branches;
+  if (total == 0 || store_mask == 0) return hipSuccess;
+  const int grid = (int)std::min<long>((total + 255) / 256, 8192);
+  hipLaunchKernelGGL(residual_kernel, dim3(grid), dim3(256), 0, st, x0, (const float*)nullptr,
+                     (float*)x, R, rm, store_mask, D, 1, hdr);
+  return hipGetLastError();
+}
+
+}  // namespace t2i

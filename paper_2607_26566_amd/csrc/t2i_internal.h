@@ -1,0 +1,199 @@
+// Internal declarations shared by the gfx950 kernels and the host orchestration.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace t2i {
+
+typedef __bf16 bf16;
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+
+constexpr int kMaxSeq = 64;
+constexpr int kMaxReq = 32;
+constexpr int kWave = 64;
+
+// ---------------------------------------------------------------------------
+// Small tables passed to kernels by value (no device copies, no memcpy).
+
+// Packed rows -> sequence.  Sequence s owns rows [start[s], start[s+1]); its
+// modulation-table row is modrow[s].
+struct SeqMap {
+  int n;
+  int start[kMaxSeq + 1];
+  int modrow[kMaxSeq];
+};
+
+// Variable-length attention: query sequence s reads Q rows [q_start, +q_len)
+// and K/V rows [k_start, +k_len).  tile_start[s] is the first query tile of s
+// in the flattened tile space of one head (prefix sum of ceil(q_len/BQ)).
+struct AttnMap {
+  int n;
+  int q_start[kMaxSeq], q_len[kMaxSeq], k_start[kMaxSeq], k_len[kMaxSeq];
+  int tile_start[kMaxSeq + 1];
+};
+
+// Per-request geometry for the image-side kernels.
+struct ReqMap {
+  int n;                    // requests
+  int tokens_total;         // image tokens of all requests (one branch)
+  int branches;             // 1 or 2
+  int tok_off[kMaxReq + 1]; // first token of request r within a branch
+  int lat_off[kMaxReq];     // first float of request r's latent
+  int h[kMaxReq], w[kMaxReq];
+  int modrow[kMaxReq];      // modulation-table row of request r
+  float dt[kMaxReq];        // Euler step t_next - t (0 = no update)
+};
+
+// Timestep values handed to a kernel by value (host array, no copy).
+constexpr int kTValsChunk = 64;
+struct TVals {
+  int n;
+  double t[kTValsChunk];
+};
+
+__device__ __forceinline__ int seq_of_row(const SeqMap& m, int row) {
+  int s = 0;
+  #pragma unroll 1
+  for (int i = 1; i < m.n; ++i) s += (row >= m.start[i]) ? 1 : 0;
+  return s;
+}
+
+__device__ __forceinline__ int req_of_token(const ReqMap& m, int tok) {
+  int r = 0;
+  #pragma unroll 1
+  for (int i = 1; i < m.n; ++i) r += (tok >= m.tok_off[i]) ? 1 : 0;
+  return r;
+}
+
+// ---------------------------------------------------------------------------
+// Conversions and reductions.
+
+__device__ __forceinline__ float to_f32(float v) { return v; }
+__device__ __forceinline__ float to_f32(bf16 v) { return (float)v; }
+template <typename T> __device__ __forceinline__ T from_f32(float v);
+template <> __device__ __forceinline__ float from_f32<float>(float v) { return v; }
+template <> __device__ __forceinline__ bf16 from_f32<bf16>(float v) { return (bf16)v; }
+
+__device__ __forceinline__ float wave_sum(float v) {
+  #pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) v += __shfl_xor(v, o, kWave);
+  return v;
+}
+__device__ __forceinline__ double wave_sum(double v) {
+  #pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) v += __shfl_xor(v, o, kWave);
+  return v;
+}
+
+// GELU with the tanh approximation, written as u * sigmoid(2z):
+// 0.5 u (1 + tanh z) = u / (1 + exp(-2z)),  z = sqrt(2/pi) (u + 0.044715 u^3).
+__device__ __forceinline__ float gelu_tanh(float u) {
+  const float k0 = 0.7978845608028654f;   // sqrt(2/pi)
+  float z = k0 * (u + 0.044715f * u * u * u);
+  return u / (1.0f + __expf(-2.0f * z));
+}
+
+__device__ __forceinline__ float silu(float v) { return v / (1.0f + __expf(-v)); }
+
+// ---------------------------------------------------------------------------
+// Linear-layer epilogue.
+
+enum EpiKind { EPI_STORE = 0, EPI_GELU = 1, EPI_SILU = 2, EPI_RESID = 3, EPI_RESID_GATED = 4 };
+
+struct Epi {
+  void* out;          // STORE / GELU / SILU destination
+  int ldo;
+  float* x;           // fp32 residual for RESID kinds
+  int ldx;
+  bf16* xb;           // optional bf16 copy of the updated residual (stride ldx)
+  const float* gate;  // gate rows: gate[modrow(seq(row)) * ld_gate + col]
+  int ld_gate;
+  SeqMap map;
+};
+
+template <typename OutT>
+__device__ __forceinline__ void epi_apply(const Epi& e, int kind, int m, int n, float y) {
+  if (kind == EPI_STORE) {
+    ((OutT*)e.out)[(size_t)m * e.ldo + n] = from_f32<OutT>(y);
+  } else if (kind == EPI_GELU) {
+    ((OutT*)e.out)[(size_t)m * e.ldo + n] = from_f32<OutT>(gelu_tanh(y));
+  } else if (kind == EPI_SILU) {
+    ((OutT*)e.out)[(size_t)m * e.ldo + n] = from_f32<OutT>(silu(y));
+  } else {
+    float g = 1.0f;
+    if (kind == EPI_RESID_GATED) {
+      int s = seq_of_row(e.map, m);
+      g = e.gate[(size_t)e.map.modrow[s] * e.ld_gate + n];
+    }
+    size_t i = (size_t)m * e.ldx + n;
+    float nx = e.x[i] + g * y;
+    e.x[i] = nx;
+    if (e.xb) e.xb[i] = (bf16)nx;
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Launchers (defined in the kernel files; all asynchronous on `st`).
+
+hipError_t launch_gemm_bf16(const bf16* A, int lda, const bf16* W, int ldw, const bf16* bias,
+                            int M, int N, int K, int kind, const Epi& epi, hipStream_t st);
+
+// SIMT fp32-accumulating GEMM: A fp32, W fp32 or bf16 (w_bf16), bias like W,
+// output fp32 for STORE kinds.
+hipError_t launch_gemm_f32(const float* A, int lda, const void* W, int ldw, bool w_bf16,
+                           const void* bias, int M, int N, int K, int kind, const Epi& epi,
+                           hipStream_t st);
+
+hipError_t launch_attention(bool bf16_io, int heads, int head_dim, const AttnMap& map,
+                            const void* q, int ldq, const void* k, int ldk, const void* v,
+                            int ldv, void* o, int ldo, hipStream_t st);
+int attention_query_tile(bool bf16_io, int head_dim);
+
+hipError_t launch_ln_modulate(bool bf16_out, int rows, int D, const float* x, int ldx,
+                              const float* mod, int ld_mod, int shift_off, int scale_off,
+                              const SeqMap& map, void* out, int ldo, float eps, hipStream_t st);
+
+hipError_t launch_embed(const float* lat, const ReqMap& rm, const void* w_pe, const void* b_pe,
+                        bool w_bf16, int D, int C, int p, bool pos_embed, float* x0, float* x,
+                        int copies, hipStream_t st);
+
+// t: HOST array of `rows` timesteps (launched in chunks of kTValsChunk).
+hipError_t launch_timestep_freq(const double* t, int rows, int freq_dim, double t_scale,
+                                float* out, hipStream_t st);
+
+hipError_t launch_broadcast_rows(const void* src, bool bf16_io, int rows, int D, void* dst,
+                                 hipStream_t st);
+
+hipError_t launch_final_layer(const float* x, const ReqMap& rm, const void* w_out,
+                              const void* b_out, bool w_bf16, const float* mod, int ld_mod,
+                              int shift_off, int scale_off, int D, int C, int p, float eps,
+                              float guidance, float* latents, float* noise_pred, hipStream_t st);
+
+// Cache-skip support.
+struct CacheHeader {      // one per request, in the caller's cache-state buffer
+  double acc;             // accumulated relative L1 change
+  double d;               // last d_k
+  int32_t has_m;          // m_prev valid
+  int32_t has_r;          // residual valid
+  int32_t skip;           // last decision
+  int32_t pad;
+};
+constexpr int kCacheRowsPerBlock = 16;
+
+int cache_partial_blocks(const ReqMap& rm);
+hipError_t launch_cache_signal(const float* x0, const ReqMap& rm, const float* mod, int ld_mod,
+                               int shift_off, int scale_off, int D, float eps, float* m_prev,
+                               CacheHeader* hdr, int step, double* partial, hipStream_t st);
+hipError_t launch_cache_decide(const ReqMap& rm, const double* partial, CacheHeader* hdr,
+                               int step, int n_steps, double tau, int mode, hipStream_t st);
+// x[b][tok] = x0[tok] + R[b][tok] for requests with skip_mask[r]
+hipError_t launch_apply_residual(const float* x0, const float* R, float* x, const ReqMap& rm,
+                                 uint32_t skip_mask, int D, hipStream_t st);
+// R[b][tok] = x[b][tok] - x0[tok] for requests with store_mask[r]; sets has_r
+hipError_t launch_store_residual(const float* x0, const float* x, float* R, const ReqMap& rm,
+                                 uint32_t store_mask, int D, CacheHeader* hdr, hipStream_t st);
+
+}  // namespace t2i

@@ -1,0 +1,187 @@
+"""The C-ABI library on the host: loads, exports every declared symbol, agrees
+with the oracle on the weight table, and rejects bad arguments before any
+launch.  No call here reaches the GPU."""
+import ctypes as C
+import os
+import re
+
+import pytest
+
+import synth
+import paper_2607_26566_amd as t2i
+from paper_2607_26566_amd import _lib
+from oracle import dit, mmdit
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def declared_functions():
+    names = set()
+    for h in os.listdir(os.path.join(ROOT, "include")):
+        if not h.endswith(".h"):
+            continue
+        text = open(os.path.join(ROOT, "include", h)).read()
+        text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+        names |= set(re.findall(r"\b(t2i_\w+)\s*\(", text))
+    return names
+
+
+def test_library_exports_every_declared_symbol():
+    lib = t2i.load()
+    declared = declared_functions()
+    assert len(declared) >= 16
+    for name in declared:
+        assert hasattr(lib, name), name
+        assert name in _lib.SIGNATURES, name
+
+
+def test_struct_sizes_match_header_layout():
+    # field order and types mirror include/t2i_dit.h; sizes are what the
+    # library checks through struct_size
+    assert C.sizeof(_lib.t2i_dit_config) == 18 * 4
+    assert C.sizeof(_lib.t2i_step_args) % 8 == 0
+
+
+@pytest.mark.parametrize("name", ["tiny_f32", "dit512", "dit1024_cfg", "packed8"])
+def test_weight_table_matches_oracle(name):
+    w = synth.workload(name)
+    cfg = t2i.Config.from_shape(w)
+    assert t2i.weight_table(cfg) == [(n, tuple(s)) for n, s in dit.weight_layout(w)]
+
+
+def test_mmdit_weight_table_matches_oracle():
+    w = synth.workload("mmdit1024")
+    cfg = t2i.Config.from_shape(w)
+    assert t2i.weight_table(cfg) == [(n, tuple(s)) for n, s in mmdit.weight_layout(w)]
+
+
+def test_workspace_and_cache_sizes():
+    lib = t2i.load()
+    w = synth.workload("dit1024_cfg")
+    cfg = t2i.Config.from_shape(w)
+    ws = lib.t2i_dit_workspace_bytes(cfg.ref())
+    # at least the fp32 residual stream and its block-input copy, qkv and fc1 activations
+    T, D, F = 8192, 1152, 4608
+    assert ws >= T * D * 4 * 2 + T * 3 * D * 2 + T * F * 2
+    assert ws < 2 * 1024 ** 3
+    toks = (C.c_int32 * 1)(4096)
+    cs = lib.t2i_cache_state_bytes(cfg.ref(), 1, toks, 2)
+    assert cs >= 4096 * D * 4 * 3
+    assert lib.t2i_cache_state_bytes(cfg.ref(), 1, toks, 3) == 0
+
+
+def test_invalid_configs_are_rejected():
+    lib = t2i.load()
+    w = synth.workload("dit512")
+    for field, bad in [("hidden", 100), ("heads", 7), ("head_dim", 40), ("max_requests", 99),
+                       ("dtype", 5), ("patch", 0), ("text_tokens", 0)]:
+        cfg = t2i.Config.from_shape(w)
+        setattr(cfg.c, field, bad)
+        assert lib.t2i_dit_weight_count(cfg.ref()) == 0, field
+        assert lib.t2i_dit_workspace_bytes(cfg.ref()) == 0, field
+    cfg = t2i.Config.from_shape(w)
+    cfg.c.struct_size = 12
+    assert lib.t2i_dit_weight_count(cfg.ref()) == 0
+
+
+def _fake_handle(w):
+    """A handle bound to fake device addresses: valid only for calls that fail
+    validation before touching the GPU."""
+    lib = t2i.load()
+    cfg = t2i.Config.from_shape(w)
+    n = lib.t2i_dit_weight_count(cfg.ref())
+    ptrs = (C.c_void_p * n)(*[0x1000 * (i + 1) for i in range(n)])
+    ws = lib.t2i_dit_workspace_bytes(cfg.ref())
+    h = C.c_void_p()
+    assert lib.t2i_dit_init(cfg.ref(), ptrs, C.c_void_p(1 << 20), ws - 1, None, C.byref(h)) == 4
+    assert lib.t2i_dit_init(cfg.ref(), ptrs, C.c_void_p((1 << 20) + 8), ws, None, C.byref(h)) == 1
+    assert lib.t2i_dit_init(cfg.ref(), ptrs, C.c_void_p(1 << 20), ws, None, C.byref(h)) == 0
+    return lib, cfg, h
+
+
+def test_step_argument_errors_return_status():
+    w = synth.workload("dit512")
+    lib, cfg, h = _fake_handle(w)
+    try:
+        a = _lib.t2i_step_args()
+        a.struct_size = C.sizeof(a) - 8
+        assert lib.t2i_dit_step(h, C.byref(a), None) == 1
+        a.struct_size = C.sizeof(a)
+        a.n_req = 1
+        hh = (C.c_int32 * 1)(64)
+        ww = (C.c_int32 * 1)(63)                      # not a multiple of the patch
+        t = (C.c_double * 1)(1.0)
+        a.lat_h, a.lat_w, a.t = hh, ww, t
+        a.latents = 0x2000
+        a.prompt_embeds = 0x3000
+        a.guidance = 1.0
+        a.n_blocks = -1
+        assert lib.t2i_dit_step(h, C.byref(a), None) == 2
+        assert b"multiple of patch" in lib.t2i_last_error(h)
+        ww[0] = 64
+        a.n_req = 0
+        assert lib.t2i_dit_step(h, C.byref(a), None) == 2
+        a.n_req = 1
+        a.n_blocks = 29
+        assert lib.t2i_dit_step(h, C.byref(a), None) == 2
+        a.n_blocks = -1
+        a.control_outputs = 0x4000
+        assert lib.t2i_dit_step(h, C.byref(a), None) == 3
+        a.control_outputs = None
+        hh[0] = 128                                     # 4096 tokens > max_tokens 1024
+        assert lib.t2i_dit_step(h, C.byref(a), None) == 2
+        hh[0] = 64
+        t[0] = float("nan")
+        assert lib.t2i_dit_step(h, C.byref(a), None) == 1
+        a.t = None
+        assert lib.t2i_dit_step(h, C.byref(a), None) == 1
+    finally:
+        lib.t2i_dit_destroy(h)
+
+
+def test_sample_and_cache_argument_errors():
+    w = synth.workload("packed8")
+    lib, cfg, h = _fake_handle(w)
+    try:
+        s = _lib.t2i_sample_args()
+        s.struct_size = C.sizeof(s)
+        s.n_req = 8
+        hs = (C.c_int32 * 8)(*[r[0] for r in w.requests])
+        s.lat_h = s.lat_w = hs
+        s.latents, s.prompt_embeds = 0x2000, 0x3000
+        s.guidance = 1.0
+        s.n_steps = 21                                  # > max_steps
+        assert lib.t2i_dit_sample(h, C.byref(s), None) == 2
+        s.n_steps = 20
+        s.start_step = 20
+        assert lib.t2i_dit_sample(h, C.byref(s), None) == 2
+        s.start_step = 0
+        s.cache_tau = 0.1                               # cache without state
+        assert lib.t2i_dit_sample(h, C.byref(s), None) == 1
+        s.cache_state = 0x5000
+        s.cache_state_bytes = 16                        # too small
+        assert lib.t2i_dit_sample(h, C.byref(s), None) == 4
+        s.cache_mode = 7
+        assert lib.t2i_dit_sample(h, C.byref(s), None) == 1
+        c = _lib.t2i_cache_args()
+        c.struct_size = C.sizeof(c)
+        assert lib.t2i_cache_check(h, C.byref(c), None) == 1
+    finally:
+        lib.t2i_dit_destroy(h)
+
+
+def test_op_argument_errors():
+    lib = t2i.load()
+    # bf16 GEMM needs K % 64 == 0
+    assert lib.t2i_op_linear(1, 0, 4, 4, 40, 0x1000, 40, 0x2000, 40, 0x3000, 0x4000, 4,
+                             None, 0, None, None, None) == 2
+    assert b"K % 64" in lib.t2i_ops_last_error()
+    assert lib.t2i_op_linear(1, 9, 4, 4, 64, 0x1000, 64, 0x2000, 64, 0x3000, 0x4000, 4,
+                             None, 0, None, None, None) == 1
+    qs = (C.c_int32 * 1)(0)
+    ql = (C.c_int32 * 1)(4)
+    kl = (C.c_int32 * 1)(0)                              # no keys
+    assert lib.t2i_op_attention(1, 2, 72, 1, qs, ql, qs, kl, 0x1000, 144, 0x2000, 144,
+                                0x3000, 144, 0x4000, 144, None) == 2
+    assert lib.t2i_op_attention(1, 2, 48, 1, qs, ql, qs, ql, 0x1000, 96, 0x2000, 96,
+                                0x3000, 96, 0x4000, 96, None) == 2

@@ -1,0 +1,185 @@
+"""Kernel-level parity of the HIP path against the oracle's definitions.
+
+Each case calls one kernel through the C ABI (``include/t2i_ops.h``) on
+seeded bf16/fp32 inputs and compares with the oracle computing the same
+operation in float64 from the same (bf16-rounded) values."""
+import ctypes as C
+
+import numpy as np
+import pytest
+import torch
+
+import synth
+import paper_2607_26566_amd as t2i
+from paper_2607_26566_amd import _lib
+from oracle import dit
+from gpu_common import DEV, rel_l2, say, to_dev, to_host
+
+pytestmark = pytest.mark.gpu
+
+
+def _stream():
+    return C.c_void_p(torch.cuda.current_stream().cuda_stream)
+
+
+def rnd(seed, shape, std=1.0, bf=True):
+    a = synth.normal(seed, (7,), shape, std)
+    return synth.round_bf16(a) if bf else a
+
+
+def run_linear(dtype, epi, A, W, b, resid=None, gate=None, with_copy=False):
+    lib = t2i.load()
+    M, K = A.shape
+    N = W.shape[0]
+    dt = "bf16" if dtype == _lib.T2I_BF16 else "f32"
+    dA, dW, db = to_dev(A, dt), to_dev(W, dt), to_dev(b, dt)
+    out = torch.zeros((M, N), dtype=dA.dtype, device=DEV)
+    dR = torch.from_numpy(resid.astype(np.float32)).to(DEV) if resid is not None else None
+    dC = torch.zeros((M, N), dtype=torch.bfloat16, device=DEV) if with_copy else None
+    dG = torch.from_numpy(gate.astype(np.float32)).to(DEV) if gate is not None else None
+    st = lib.t2i_op_linear(dtype, epi, M, N, K, dA.data_ptr(), K, dW.data_ptr(), K, db.data_ptr(),
+                           out.data_ptr(), N, dR.data_ptr() if dR is not None else None, N,
+                           dC.data_ptr() if dC is not None else None,
+                           dG.data_ptr() if dG is not None else None, _stream())
+    _lib.check(st)
+    torch.cuda.synchronize()
+    return out, dR, dC
+
+
+GEMM_SHAPES = [(300, 192, 128), (1000, 1152, 1152), (64, 3456, 1152), (8192, 1152, 4608),
+               (129, 4608, 1152), (240, 2304, 1152), (1, 128, 64)]
+
+
+@pytest.mark.parametrize("M,N,K", GEMM_SHAPES)
+def test_linear_bf16_store_and_gelu(M, N, K):
+    say(f"linear bf16 {M}x{N}x{K}")
+    A, W, b = rnd(1, (M, K)), rnd(2, (N, K), 0.05), rnd(3, (N,), 0.1)
+    ref = dit.linear(A.astype(np.float64), W.astype(np.float64), b.astype(np.float64))
+    out, _, _ = run_linear(_lib.T2I_BF16, _lib.T2I_EPI_STORE, A, W, b)
+    assert rel_l2(to_host(out), ref) < 3e-3
+    out, _, _ = run_linear(_lib.T2I_BF16, _lib.T2I_EPI_GELU, A, W, b)
+    assert rel_l2(to_host(out), dit.gelu_tanh(ref)) < 3e-3
+
+
+@pytest.mark.parametrize("M,N,K", [(300, 192, 128), (1000, 1152, 4608), (8192, 1152, 1152)])
+def test_linear_bf16_residual_epilogues(M, N, K):
+    say(f"linear bf16 residual {M}x{N}x{K}")
+    A, W, b = rnd(4, (M, K)), rnd(5, (N, K), 0.05), rnd(6, (N,), 0.1)
+    x0 = rnd(8, (M, N), bf=False)
+    gate = rnd(9, (N,), 0.5, bf=False)
+    ref = dit.linear(A.astype(np.float64), W.astype(np.float64), b.astype(np.float64))
+    _, x, xc = run_linear(_lib.T2I_BF16, _lib.T2I_EPI_RESID, A, W, b, resid=x0, with_copy=True)
+    xg = x.cpu().numpy()
+    assert rel_l2(xg.astype(np.float64) - x0, ref) < 1e-4
+    assert np.array_equal(xc.float().cpu().numpy(), synth.round_bf16(xg))
+    _, x, _ = run_linear(_lib.T2I_BF16, _lib.T2I_EPI_RESID_GATED, A, W, b, resid=x0, gate=gate)
+    assert rel_l2(x.cpu().numpy().astype(np.float64) - x0, gate * ref) < 1e-4
+
+
+@pytest.mark.parametrize("M,N,K,epi", [(64, 128, 256, 0), (100, 520, 128, 2), (77, 33, 90, 4)])
+def test_linear_f32(M, N, K, epi):
+    A, W, b = rnd(10, (M, K), bf=False), rnd(11, (N, K), 0.05, bf=False), rnd(12, (N,), 0.1, bf=False)
+    x0 = rnd(13, (M, N), bf=False)
+    gate = rnd(14, (N,), 0.5, bf=False)
+    ref = dit.linear(A.astype(np.float64), W.astype(np.float64), b.astype(np.float64))
+    out, x, _ = run_linear(_lib.T2I_F32, epi, A, W, b, resid=x0 if epi >= 3 else None,
+                           gate=gate if epi == 4 else None)
+    if epi == 0:
+        assert rel_l2(to_host(out), ref) < 1e-6
+    elif epi == 2:
+        assert rel_l2(to_host(out), dit.silu(ref)) < 1e-6
+    else:
+        assert rel_l2(x.cpu().numpy().astype(np.float64) - x0, gate * ref) < 1e-6
+
+
+def run_attention(dtype, heads, d, seqs, q, k, v):
+    lib = t2i.load()
+    n = len(seqs)
+    qs, ql, ks, kl = ((C.c_int32 * n)(*[s[i] for s in seqs]) for i in range(4))
+    dt = "bf16" if dtype == _lib.T2I_BF16 else "f32"
+    dq, dk, dv = to_dev(q, dt), to_dev(k, dt), to_dev(v, dt)
+    o = torch.zeros(dq.shape, dtype=dq.dtype, device=DEV)
+    w = heads * d
+    st = lib.t2i_op_attention(dtype, heads, d, n, qs, ql, ks, kl, dq.data_ptr(), w, dk.data_ptr(),
+                              w, dv.data_ptr(), w, o.data_ptr(), w, _stream())
+    _lib.check(st)
+    torch.cuda.synchronize()
+    return to_host(o)
+
+
+def attention_ref(seqs, q, k, v, heads):
+    out = np.zeros(q.shape)
+    for (q0, nq, k0, nk) in seqs:
+        out[q0:q0 + nq] = dit.attention(q[q0:q0 + nq].astype(np.float64),
+                                        k[k0:k0 + nk].astype(np.float64),
+                                        v[k0:k0 + nk].astype(np.float64), heads)
+    return out
+
+
+ATTN_CASES = [
+    ("self-ragged", 4, 72, [(0, 333, 0, 333)], 333, 333),
+    ("varlen", 2, 72, [(0, 256, 0, 256), (256, 1024, 256, 1024), (1280, 77, 1280, 77)], 1357, 1357),
+    ("cross-120", 4, 72, [(0, 500, 0, 120), (500, 300, 120, 120)], 800, 240),
+    ("single-key", 2, 72, [(0, 130, 0, 1)], 130, 1),
+    ("d128", 3, 128, [(0, 200, 0, 260)], 200, 260),
+    ("d64", 2, 64, [(0, 129, 0, 64)], 129, 64),
+]
+
+
+@pytest.mark.parametrize("name,H,d,seqs,nq,nk", ATTN_CASES, ids=[c[0] for c in ATTN_CASES])
+def test_attention_bf16(name, H, d, seqs, nq, nk):
+    say(f"attention bf16 {name}")
+    q, k, v = rnd(20, (nq, H * d)), rnd(21, (nk, H * d)), rnd(22, (nk, H * d))
+    got = run_attention(_lib.T2I_BF16, H, d, seqs, q, k, v)
+    ref = attention_ref(seqs, q, k, v, H)
+    err = rel_l2(got, ref)
+    say(f"  rel_l2 {err:.2e}")
+    assert err < 6e-3
+
+
+def test_attention_bf16_identical_keys_give_mean():
+    H, d, n = 2, 72, 300
+    q = rnd(23, (n, H * d))
+    k = np.tile(rnd(24, (1, H * d)), (n, 1))
+    v = rnd(25, (n, H * d))
+    got = run_attention(_lib.T2I_BF16, H, d, [(0, n, 0, n)], q, k, v)
+    ref = np.tile(v.astype(np.float64).mean(axis=0), (n, 1))
+    assert rel_l2(got, ref) < 6e-3
+
+
+def test_attention_bf16_full_size_sampled_rows():
+    """1024 px self-attention: 2 sequences x 4096 tokens, 16 heads of 72."""
+    H, d, n = 16, 72, 4096
+    q, k, v = rnd(26, (2 * n, H * d)), rnd(27, (2 * n, H * d)), rnd(28, (2 * n, H * d))
+    seqs = [(0, n, 0, n), (n, n, n, n)]
+    got = run_attention(_lib.T2I_BF16, H, d, seqs, q, k, v)
+    rows = np.r_[np.arange(0, 2 * n, 97), n - 1, 2 * n - 1]
+    ref = np.zeros((len(rows), H * d))
+    for i, r in enumerate(rows):
+        s0 = 0 if r < n else n
+        ref[i] = dit.attention(q[r:r + 1].astype(np.float64), k[s0:s0 + n].astype(np.float64),
+                               v[s0:s0 + n].astype(np.float64), H)[0]
+    assert rel_l2(got[rows], ref) < 6e-3
+
+
+@pytest.mark.parametrize("H,d,seqs,nq,nk", [(2, 64, [(0, 64, 0, 64)], 64, 64),
+                                            (2, 64, [(0, 64, 0, 16), (64, 10, 16, 16)], 74, 32)])
+def test_attention_f32(H, d, seqs, nq, nk):
+    q, k, v = (rnd(s, (n, H * d), bf=False) for s, n in ((30, nq), (31, nk), (32, nk)))
+    got = run_attention(_lib.T2I_F32, H, d, seqs, q, k, v)
+    assert rel_l2(got, attention_ref(seqs, q, k, v, H)) < 1e-6
+
+
+@pytest.mark.parametrize("dtype,rows,D", [(1, 1000, 1152), (0, 64, 128), (1, 7, 3072)])
+def test_ln_modulate(dtype, rows, D):
+    lib = t2i.load()
+    x = rnd(40, (rows, D), bf=False) * 2 + 0.5
+    mod = rnd(41, (2, D), 0.3, bf=False)
+    dx = torch.from_numpy(x.astype(np.float32)).to(DEV)
+    dm = torch.from_numpy(mod.astype(np.float32)).to(DEV)
+    out = torch.zeros((rows, D), dtype=torch.bfloat16 if dtype == 1 else torch.float32, device=DEV)
+    _lib.check(lib.t2i_op_ln_modulate(dtype, rows, D, dx.data_ptr(), dm.data_ptr(),
+                                      dm.data_ptr() + 4 * D, 1e-6, out.data_ptr(), _stream()))
+    torch.cuda.synchronize()
+    ref = dit.modulate(dit.layer_norm(x.astype(np.float64), 1e-6), mod[0], mod[1])
+    assert rel_l2(to_host(out), ref) < (3e-3 if dtype == 1 else 1e-6)

@@ -261,6 +261,17 @@ def test_block_brute_force():
         assert np.allclose(got, brute_block(W, TINY, b, x, y, c), rtol=1e-11, atol=1e-12)
 
 
+def test_block_rows_equals_block_subset():
+    W = tiny_weights()
+    rng = np.random.default_rng(18)
+    x = rng.standard_normal((9, TINY.hidden))
+    y = rng.standard_normal((3, TINY.hidden))
+    mod = dit.block_modulation(W, TINY, rng.standard_normal(TINY.hidden), 1)
+    full = dit.block(W, TINY, 1, x, y, mod)
+    rows = np.array([7, 0, 4])
+    assert np.allclose(dit.block_rows(W, TINY, 1, x, y, mod, rows), full[rows], rtol=1e-13, atol=1e-14)
+
+
 def test_zero_gates_make_block_identity():
     """adaLN-Zero with zero gates is an identity block.
 
