@@ -48,8 +48,12 @@ t2i_status t2i_op_linear(int32_t dtype, int32_t epilogue, int32_t M, int32_t N,
  * sequences: query sequence s holds rows q_start[s] .. q_start[s]+q_len[s]-1
  * of Q and attends to rows k_start[s] .. +k_len[s]-1 of K and V (host arrays
  * of n_seq <= T2I_MAX_SEQ entries, k_len >= 1).  Head h of a row occupies
- * columns h*d .. h*d+d-1.  Q, K, V, O are dtype (bf16 or fp32) with row
- * strides ldq, ldk, ldv, ldo (multiples of 8).
+ * columns h*d .. h*d+d-1.  Q, K, O are dtype (bf16 or fp32) with row strides
+ * ldq, ldk, ldo (multiples of 8).
+ *   fp32: V is row-major like K, row stride ldv.
+ *   bf16: V is given transposed, V^T [heads*head_dim][ldv] (the key index is
+ *         contiguous), the layout the fused qkv projection writes; every
+ *         k_start must be a multiple of 8 and k_start + k_len <= ldv.
  */
 t2i_status t2i_op_attention(int32_t dtype, int32_t heads, int32_t head_dim,
                             int32_t n_seq, const int32_t* q_start,

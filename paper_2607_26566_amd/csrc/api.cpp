@@ -122,12 +122,13 @@ const char* check_config(const t2i_dit_config* c) {
   if (c->mlp_hidden < 64 || c->mlp_hidden % 64) return "mlp_hidden must be a positive multiple of 64";
   if (c->text_dim < 64 || c->text_dim % 64) return "text_dim must be a positive multiple of 64";
   if (c->text_tokens < 1 || c->text_tokens > 4096) return "bad text_tokens";
-  if (c->freq_dim < 2 || c->freq_dim % 2) return "freq_dim must be even";
+  if (c->freq_dim < 8 || c->freq_dim % 8) return "freq_dim must be a positive multiple of 8";
   if (c->max_tokens < 1) return "bad max_tokens";
   if (c->max_requests < 1 || c->max_requests > T2I_MAX_REQ) return "bad max_requests";
   if (c->max_steps < 1 || c->max_steps > 10000) return "bad max_steps";
   if (!(c->ln_eps > 0.f) || !(c->t_scale > 0.f)) return "bad ln_eps/t_scale";
   if (c->arch == T2I_ARCH_MMDIT && c->dtype != T2I_BF16) return "MMDiT runs in bf16 only";
+  if (c->dtype == T2I_BF16 && c->text_tokens % 8) return "bf16 models need text_tokens % 8 == 0";
   return nullptr;
 }
 
@@ -135,7 +136,8 @@ const char* check_config(const t2i_dit_config* c) {
 // workspace layout
 
 struct Layout {
-  size_t x, x0, h, xb, qkv, o, u, ytxt, kv, tfreq, th1, tsc, mod, partial, total;
+  size_t x, x0, h, xb, qkv, vt, o, u, ytxt, kv, vtt, tfreq, th1, tsc, mod, partial, total;
+  int ldvt = 0, ldvt_txt = 0;   // token strides of the transposed V buffers
 };
 
 Layout layout(const t2i_dit_config& c) {
@@ -157,10 +159,16 @@ Layout layout(const t2i_dit_config& c) {
   L.h = take(rows * D * A);
   L.xb = take(c.dtype == T2I_BF16 ? rows * D * 2 : 0);
   L.qkv = take(rows * 3 * D * A);
+  // bf16 attention reads V transposed: [D][ldvt], token index contiguous
+  L.ldvt = (int)((rows + 63) / 64 * 64);
+  L.ldvt_txt = (int)((txt_rows + 63) / 64 * 64);
+  const bool bfv = c.dtype == T2I_BF16;
+  L.vt = take(bfv ? D * (size_t)L.ldvt * 2 : 0);
   L.o = take(rows * D * A);
   L.u = take(rows * F * A);
   L.ytxt = take(txt_rows * D * A);
   L.kv = take(c.arch == T2I_ARCH_CROSS_DIT ? (size_t)c.depth * txt_rows * 2 * D * A : 0);
+  L.vtt = take(c.arch == T2I_ARCH_CROSS_DIT && bfv ? (size_t)c.depth * D * L.ldvt_txt * 2 : 0);
   L.tfreq = take(Tt * c.freq_dim * 4);
   L.th1 = take(Tt * D * 4);
   L.tsc = take(Tt * D * 4);
@@ -242,6 +250,8 @@ t2i_status build_plan(t2i_dit* h, int n_req, const int32_t* lat_h, const int32_t
       return fail(h, T2I_ERR_SHAPE, "latent size must be a positive multiple of patch");
     if (lat_h[r] > 4096 || lat_w[r] > 4096) return fail(h, T2I_ERR_SHAPE, "latent too large");
     const int n = (lat_h[r] / c.patch) * (lat_w[r] / c.patch);
+    if (h->bf() && n % 8)
+      return fail(h, T2I_ERR_SHAPE, "bf16 models need image tokens per request % 8 == 0");
     P.rm.tok_off[r] = tok;
     P.rm.lat_off[r] = (int)lat;
     P.rm.h[r] = lat_h[r];
@@ -322,9 +332,9 @@ t2i_status conditioning(t2i_dit* h, const double* t_host, int rows, int n_blocks
   Epi e = make_epi();
   e.out = th1;
   e.ldo = D;
-  HIP_TRY(h, launch_gemm_f32(tfreq, fd, h->w[W_T1], fd, wb, h->w[B_T1], rows, D, fd, EPI_SILU, e, st));
+  HIP_TRY(h, launch_linear_rows(tfreq, fd, h->w[W_T1], fd, wb, h->w[B_T1], rows, D, fd, EPI_SILU, e, st));
   e.out = tsc;
-  HIP_TRY(h, launch_gemm_f32(th1, D, h->w[W_T2], D, wb, h->w[B_T2], rows, D, D, EPI_SILU, e, st));
+  HIP_TRY(h, launch_linear_rows(th1, D, h->w[W_T2], D, wb, h->w[B_T2], rows, D, D, EPI_SILU, e, st));
   const int mw = mod_width(c);
   const int pb = per_block(c);
   e.ldo = mw;
@@ -332,18 +342,18 @@ t2i_status conditioning(t2i_dit* h, const double* t_host, int rows, int n_blocks
     if (c.arch == T2I_ARCH_CROSS_DIT) {
       e.out = mod + (size_t)b * 6 * D;
       const int wi = W_BLOCK0 + b * pb + X_ADA;
-      HIP_TRY(h, launch_gemm_f32(tsc, D, h->w[wi], D, wb, h->w[wi + 1], rows, 6 * D, D, EPI_STORE, e, st));
+      HIP_TRY(h, launch_linear_rows(tsc, D, h->w[wi], D, wb, h->w[wi + 1], rows, 6 * D, D, EPI_STORE, e, st));
     } else {
       for (int s = 0; s < 2; ++s) {
         e.out = mod + (size_t)b * 12 * D + (size_t)s * 6 * D;
         const int wi = W_BLOCK0 + b * pb + s * J_PER_STREAM + J_ADA;
-        HIP_TRY(h, launch_gemm_f32(tsc, D, h->w[wi], D, wb, h->w[wi + 1], rows, 6 * D, D, EPI_STORE, e, st));
+        HIP_TRY(h, launch_linear_rows(tsc, D, h->w[wi], D, wb, h->w[wi + 1], rows, 6 * D, D, EPI_STORE, e, st));
       }
     }
   }
   e.out = mod + (size_t)(mw - 2 * D);
   const int fb = final_base(c);
-  HIP_TRY(h, launch_gemm_f32(tsc, D, h->w[fb], D, wb, h->w[fb + 1], rows, 2 * D, D, EPI_STORE, e, st));
+  HIP_TRY(h, launch_linear_rows(tsc, D, h->w[fb], D, wb, h->w[fb + 1], rows, 2 * D, D, EPI_STORE, e, st));
   return T2I_OK;
 }
 
@@ -364,8 +374,16 @@ t2i_status text_prep(t2i_dit* h, const Plan& P, const void* prompt, hipStream_t 
   for (int b = 0; b < c.depth; ++b) {
     e.out = h->at<char>(h->L.kv) + (size_t)b * txt_rows_max * 2 * D * h->act();
     e.ldo = 2 * D;
+    int kind = EPI_STORE;
+    if (h->bf()) {   // k row-major [rows, D], v transposed [D][ldvt_txt]
+      kind = EPI_SPLIT_VT;
+      e.ldo = D;
+      e.vt = h->at<bf16>(h->L.vtt) + (size_t)b * D * h->L.ldvt_txt;
+      e.ldvt = h->L.ldvt_txt;
+      e.vcol0 = D;
+    }
     HIP_TRY(h, linear(h, ytxt, D, W_BLOCK0 + b * X_PER_BLOCK + X_XKV, P.txt_rows, 2 * D, D,
-                      EPI_STORE, e, st));
+                      kind, e, st));
   }
   return T2I_OK;
 }
@@ -402,6 +420,7 @@ t2i_status run_blocks_cross(t2i_dit* h, const Plan& P, int nb, hipStream_t st) {
   char* o = h->at<char>(h->L.o);
   char* u = h->at<char>(h->L.u);
   bf16* xb = bf ? h->at<bf16>(h->L.xb) : nullptr;
+  bf16* vt = bf ? h->at<bf16>(h->L.vt) : nullptr;
   const float* mod = h->at<float>(h->L.mod);
   const size_t A = h->act();
   const size_t txt_rows_max = (size_t)(c.max_requests + 1) * c.text_tokens;
@@ -413,11 +432,22 @@ t2i_status run_blocks_cross(t2i_dit* h, const Plan& P, int nb, hipStream_t st) {
                                                P.img, hb, D, c.ln_eps, st));
     Epi e = make_epi();
     e.out = qkv;
-    e.ldo = 3 * D;
-    TIMED(h, T2I_K_GEMM_QKV, st, linear(h, hb, D, wb + X_QKV, R, 3 * D, D, EPI_STORE, e, st));
-    TIMED(h, T2I_K_ATTN_SELF, st,
-          launch_attention(bf, c.heads, c.head_dim, P.self, qkv, 3 * D, qkv + D * A, 3 * D,
-                           qkv + 2 * D * A, 3 * D, o, D, st));
+    if (bf) {   // q|k row-major [R, 2D], v transposed [D][ldvt]
+      e.ldo = 2 * D;
+      e.vt = vt;
+      e.ldvt = h->L.ldvt;
+      e.vcol0 = 2 * D;
+      TIMED(h, T2I_K_GEMM_QKV, st, linear(h, hb, D, wb + X_QKV, R, 3 * D, D, EPI_SPLIT_VT, e, st));
+      TIMED(h, T2I_K_ATTN_SELF, st,
+            launch_attention(bf, c.heads, c.head_dim, P.self, qkv, 2 * D, qkv + D * A, 2 * D, vt,
+                             h->L.ldvt, o, D, st));
+    } else {
+      e.ldo = 3 * D;
+      TIMED(h, T2I_K_GEMM_QKV, st, linear(h, hb, D, wb + X_QKV, R, 3 * D, D, EPI_STORE, e, st));
+      TIMED(h, T2I_K_ATTN_SELF, st,
+            launch_attention(bf, c.heads, c.head_dim, P.self, qkv, 3 * D, qkv + D * A, 3 * D,
+                             qkv + 2 * D * A, 3 * D, o, D, st));
+    }
     e = make_epi();
     e.x = x;
     e.ldx = D;
@@ -433,9 +463,15 @@ t2i_status run_blocks_cross(t2i_dit* h, const Plan& P, int nb, hipStream_t st) {
     TIMED(h, T2I_K_GEMM_XQ, st,
           linear(h, bf ? (const void*)xb : (const void*)x, D, wb + X_XQ, R, D, D, EPI_STORE, e, st));
     const char* kv = h->at<char>(h->L.kv) + (size_t)b * txt_rows_max * 2 * D * A;
-    TIMED(h, T2I_K_ATTN_CROSS, st,
-          launch_attention(bf, c.heads, c.head_dim, P.cross, qkv, D, kv, 2 * D, kv + D * A, 2 * D,
-                           o, D, st));
+    if (bf)
+      TIMED(h, T2I_K_ATTN_CROSS, st,
+            launch_attention(bf, c.heads, c.head_dim, P.cross, qkv, D, kv, D,
+                             h->at<bf16>(h->L.vtt) + (size_t)b * D * h->L.ldvt_txt,
+                             h->L.ldvt_txt, o, D, st));
+    else
+      TIMED(h, T2I_K_ATTN_CROSS, st,
+            launch_attention(bf, c.heads, c.head_dim, P.cross, qkv, D, kv, 2 * D, kv + D * A,
+                             2 * D, o, D, st));
     e = make_epi();
     e.x = x;
     e.ldx = D;
@@ -835,7 +871,8 @@ t2i_status t2i_op_attention(int32_t dtype, int32_t heads, int32_t head_dim, int3
   if (!q_start || !q_len || !k_start || !k_len || !q || !k || !v || !o)
     return ops_fail(T2I_ERR_INVALID_ARG, "NULL pointer");
   const int w = heads * head_dim;
-  if (ldq < w || ldk < w || ldv < w || ldo < w || ldq % 8 || ldk % 8 || ldv % 8 || ldo % 8)
+  if (ldq < w || ldk < w || ldo < w || ldq % 8 || ldk % 8 || ldv % 8 || ldo % 8 ||
+      (dtype == T2I_F32 && ldv < w))
     return ops_fail(T2I_ERR_SHAPE, "bad leading dimension");
   AttnMap m;
   std::memset(&m, 0, sizeof(m));
@@ -845,6 +882,8 @@ t2i_status t2i_op_attention(int32_t dtype, int32_t heads, int32_t head_dim, int3
   for (int s = 0; s < n_seq; ++s) {
     if (q_start[s] < 0 || q_len[s] < 0 || k_start[s] < 0 || k_len[s] < 1)
       return ops_fail(T2I_ERR_SHAPE, "bad sequence bounds");
+    if (dtype == T2I_BF16 && (k_start[s] % 8 || (long)k_start[s] + k_len[s] > ldv))
+      return ops_fail(T2I_ERR_SHAPE, "bf16 attention needs k_start % 8 == 0 and keys within ldv");
     m.q_start[s] = q_start[s];
     m.q_len[s] = q_len[s];
     m.k_start[s] = k_start[s];

@@ -44,35 +44,83 @@ __device__ __forceinline__ void decode_tile(const AttnMap& m, int heads, int L, 
   j = t - m.tile_start[s];
 }
 
-template <int HD>
-__global__ __launch_bounds__(256) void attn_bf16_kernel(AttnMap map, int heads,
-                                                        const bf16* __restrict__ Q, int ldq,
-                                                        const bf16* __restrict__ K, int ldk,
-                                                        const bf16* __restrict__ V, int ldv,
-                                                        bf16* __restrict__ O, int ldo,
-                                                        float scale_log2) {
-  constexpr int BQ = 128, BKV = 64, QT = 2;
+template <int HD, int QT>
+__global__ __launch_bounds__(256, 2) void attn_bf16_kernel(AttnMap map, int heads,
+                                                           const bf16* __restrict__ Q, int ldq,
+                                                           const bf16* __restrict__ K, int ldk,
+                                                           const bf16* __restrict__ Vt, int ldvt,
+                                                           bf16* __restrict__ O, int ldo,
+                                                           float scale_log2) {
+  constexpr int BQ = 4 * QT * 16, BKV = 64;
   constexpr int DC = (HD + 31) / 32;   // 32-wide chunks of d for Q K^T
   constexpr int HDP = DC * 32;
   constexpr int DT = (HD + 15) / 16;   // 16-wide tiles of d for P V
   constexpr int HDO = DT * 16;
+  constexpr bool ONES = HD < HDO;      // a spare V^T row carries the row sums
   constexpr int KP = HDP + 8;          // LDS pitch of a K row (bf16)
   constexpr int VP = BKV + 8;          // LDS pitch of a V^T row (bf16)
-  constexpr int CPR = HD / 8;          // 16-byte chunks per K/V row
-  __shared__ bf16 Ks[BKV * KP];
-  __shared__ bf16 Vt[HDO * VP];
+  constexpr int CPR = HD / 8;          // 16-byte chunks per K row
+  constexpr int KCH = BKV * CPR, VCH = HD * (BKV / 8);
+  constexpr int KPT = (KCH + 255) / 256, VPT = (VCH + 255) / 256;
+  __shared__ bf16 Ks[2][BKV * KP];
+  __shared__ bf16 Vs[2][HDO * VP];
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   int h, s, j;
   decode_tile(map, heads, xcd_remap_attn(blockIdx.x, gridDim.x), h, s, j);
   const int q_beg = map.q_start[s], q_end = q_beg + map.q_len[s];
   const int k_beg = map.k_start[s], k_end = k_beg + map.k_len[s];
-  const int qrow0 = q_beg + j * BQ + wave * 32;
+  const int qrow0 = q_beg + j * BQ + wave * (QT * 16);
   const int g = lane >> 4, fr = lane & 15;
 
-  // zero the LDS tiles once: padding columns / rows stay zero
-  for (int i = tid; i < BKV * KP; i += 256) Ks[i] = (bf16)0.f;
-  for (int i = tid; i < HDO * VP; i += 256) Vt[i] = (bf16)0.f;
+  // zero both buffers once: K padding columns and V^T padding rows stay zero
+  for (int i = tid; i < 2 * BKV * KP; i += 256) (&Ks[0][0])[i] = (bf16)0.f;
+  for (int i = tid; i < 2 * HDO * VP; i += 256) (&Vs[0][0])[i] = (bf16)0.f;
+
+  bf16x8 kr[KPT], vr[VPT];
+  auto gload = [&](int kv0) {
+#pragma unroll
+    for (int i = 0; i < KPT; ++i) {
+      const int c = tid + 256 * i;
+      kr[i] = bf16x8{};
+      if (c < KCH) {
+        const int key = c / CPR, dc = (c - key * CPR) * 8, gk = kv0 + key;
+        if (gk < k_end) kr[i] = *(const bf16x8*)(K + (size_t)gk * ldk + h * HD + dc);
+      }
+    }
+#pragma unroll
+    for (int i = 0; i < VPT; ++i) {
+      const int c = tid + 256 * i;
+      vr[i] = bf16x8{};
+      if (c < VCH) {
+        const int d = c >> 3, gk = kv0 + (c & 7) * 8;
+        if (gk < k_end) {
+          vr[i] = *(const bf16x8*)(Vt + (size_t)(h * HD + d) * ldvt + gk);
+          if (gk + 8 > k_end) {
+#pragma unroll
+            for (int e = 0; e < 8; ++e)
+              if (gk + e >= k_end) vr[i][e] = (bf16)0.f;
+          }
+        }
+      }
+    }
+  };
+  auto sstore = [&](int buf, int kv0) {
+#pragma unroll
+    for (int i = 0; i < KPT; ++i) {
+      const int c = tid + 256 * i;
+      if (c < KCH) {
+        const int key = c / CPR, dc = (c - key * CPR) * 8;
+        *(bf16x8*)&Ks[buf][key * KP + dc] = kr[i];
+      }
+    }
+#pragma unroll
+    for (int i = 0; i < VPT; ++i) {
+      const int c = tid + 256 * i;
+      if (c < VCH) *(bf16x8*)&Vs[buf][(c >> 3) * VP + (c & 7) * 8] = vr[i];
+    }
+    if (ONES && tid < BKV) Vs[buf][HD * VP + tid] = (bf16)(kv0 + tid < k_end ? 1.f : 0.f);
+  };
 
   // Q fragments (B operand of S^T): query qrow0 + qt*16 + fr, d = c*32 + g*8 .. +7
   bf16x8 qf[QT][DC];
@@ -99,32 +147,30 @@ __global__ __launch_bounds__(256) void attn_bf16_kernel(AttnMap map, int heads,
     for (int dt = 0; dt < DT; ++dt) o[qt][dt] = f32x4{0.f, 0.f, 0.f, 0.f};
   }
 
+  __syncthreads();          // zero-fill done before the first tile lands
+  gload(k_beg);
+  sstore(0, k_beg);
+  __syncthreads();
+  int buf = 0;
   for (int kv0 = k_beg; kv0 < k_end; kv0 += BKV) {
-    __syncthreads();   // previous tile fully consumed (and zero-init done)
-    for (int c = tid; c < BKV * CPR; c += 256) {
-      const int key = c / CPR, dc = (c - key * CPR) * 8;
-      const int gk = kv0 + key;
-      bf16x8 kv = bf16x8{}, vv = bf16x8{};
-      if (gk < k_end) {
-        kv = *(const bf16x8*)(K + (size_t)gk * ldk + h * HD + dc);
-        vv = *(const bf16x8*)(V + (size_t)gk * ldv + h * HD + dc);
-      }
-      *(bf16x8*)&Ks[key * KP + dc] = kv;
-#pragma unroll
-      for (int e = 0; e < 8; ++e) Vt[(dc + e) * VP + key] = vv[e];
-    }
-    __syncthreads();
+    const bool next = kv0 + BKV < k_end;
+    if (next) gload(kv0 + BKV);
     const bool ragged = kv0 + BKV > k_end;
-
+    const bf16* Kb = Ks[buf];
+    const bf16* Vb = Vs[buf];
 #pragma unroll
     for (int qt = 0; qt < QT; ++qt) {
+      // re-read the K / V^T fragments for every query tile instead of keeping
+      // all of them live across tiles (register pressure, not LDS traffic,
+      // limits this kernel)
+      asm volatile("" ::: "memory");
       f32x4 sc[4];
 #pragma unroll
       for (int kt = 0; kt < 4; ++kt) {
         sc[kt] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
         for (int c = 0; c < DC; ++c) {
-          const bf16x8 kf = *(const bf16x8*)&Ks[(kt * 16 + fr) * KP + c * 32 + g * 8];
+          const bf16x8 kf = *(const bf16x8*)&Kb[(kt * 16 + fr) * KP + c * 32 + g * 8];
           sc[kt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf, qf[qt][c], sc[kt], 0, 0, 0);
         }
       }
@@ -138,31 +184,39 @@ __global__ __launch_bounds__(256) void attn_bf16_kernel(AttnMap map, int heads,
       float mx = -INFINITY;
 #pragma unroll
       for (int kt = 0; kt < 4; ++kt)
-#pragma unroll
-        for (int r = 0; r < 4; ++r) mx = fmaxf(mx, sc[kt][r]);
+        mx = fmaxf(fmaxf(mx, fmaxf(sc[kt][0], sc[kt][1])), fmaxf(sc[kt][2], sc[kt][3]));
       mx = fmaxf(mx, __shfl_xor(mx, 16, 64));
       mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
-      const float m_new = fmaxf(m_run[qt], mx * scale_log2);
-      const float alpha = __builtin_amdgcn_exp2f(m_run[qt] - m_new);
-      m_run[qt] = m_new;
+      const float mt = mx * scale_log2;
+      // keep a stale maximum while the tile's stays within 2^8 of it: the
+      // probabilities stay <= 256 and the result is unchanged (the same
+      // maximum scales numerator and denominator)
+      if (__any(mt > m_run[qt] + 8.0f)) {
+        const float m_new = fmaxf(m_run[qt], mt);
+        const float alpha = __builtin_amdgcn_exp2f(m_run[qt] - m_new);
+        m_run[qt] = m_new;
+        l_run[qt] *= alpha;
+#pragma unroll
+        for (int dt = 0; dt < DT; ++dt) o[qt][dt] *= alpha;
+      }
+      const float mr = m_run[qt];
       float psum = 0.f;
       bf16x8 pf[2];
 #pragma unroll
       for (int kt = 0; kt < 4; ++kt) {
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
-          const float p = __builtin_amdgcn_exp2f(sc[kt][r] * scale_log2 - m_new);
-          psum += p;
+          const float p = __builtin_amdgcn_exp2f(fmaf(sc[kt][r], scale_log2, -mr));
+          if (!ONES) psum += p;
           pf[kt >> 1][(kt & 1) * 4 + r] = (bf16)p;
         }
       }
-      l_run[qt] = l_run[qt] * alpha + psum;
+      if (!ONES) l_run[qt] += psum;
 #pragma unroll
       for (int dt = 0; dt < DT; ++dt) {
-        o[qt][dt] *= alpha;
 #pragma unroll
         for (int kc = 0; kc < 2; ++kc) {
-          const bf16* vrow = &Vt[(dt * 16 + fr) * VP + kc * 32 + g * 4];
+          const bf16* vrow = &Vb[(dt * 16 + fr) * VP + kc * 32 + g * 4];
           const bf16x4 lo = *(const bf16x4*)vrow;
           const bf16x4 hi = *(const bf16x4*)(vrow + 16);
           const bf16x8 vf = bf16x8{lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
@@ -170,13 +224,24 @@ __global__ __launch_bounds__(256) void attn_bf16_kernel(AttnMap map, int heads,
         }
       }
     }
+    if (next) sstore(buf ^ 1, kv0 + BKV);
+    __syncthreads();
+    buf ^= 1;
   }
 
 #pragma unroll
   for (int qt = 0; qt < QT; ++qt) {
-    float l = l_run[qt];
-    l += __shfl_xor(l, 16, 64);
-    l += __shfl_xor(l, 32, 64);
+    float l;
+    if (ONES) {
+      // row HD of O^T = sum of the probabilities: tile HD/16, row HD%16, held
+      // by the lanes with g = (HD%16)/4 as component (HD%16)%4
+      constexpr int LT = HD / 16, LR = HD % 16;
+      l = __shfl(o[qt][LT][LR % 4], (LR / 4) * 16 + fr, 64);
+    } else {
+      l = l_run[qt];
+      l += __shfl_xor(l, 16, 64);
+      l += __shfl_xor(l, 32, 64);
+    }
     const float inv = 1.0f / l;
     const int qr = qrow0 + qt * 16 + fr;
     if (qr >= q_end) continue;
@@ -247,7 +312,13 @@ __global__ __launch_bounds__(64) void attn_f32_kernel(AttnMap map, int heads,
   }
 }
 
-int attention_query_tile(bool bf16_io, int /*head_dim*/) { return bf16_io ? 128 : 64; }
+// 16-query tiles per wave: 4 (64 queries) while the output accumulators fit
+// next to everything else in 256 registers, 2 for the widest heads
+constexpr int query_tiles(int hd) { return hd > 96 ? 2 : 4; }
+int attention_query_tile(bool bf16_io, int head_dim) {
+  if (!bf16_io) return 64;
+  return 4 * 16 * (head_dim > 96 ? 2 : 4);
+}
 
 template <int HD>
 static hipError_t launch_hd(bool bf16_io, int heads, const AttnMap& map, const void* q, int ldq,
@@ -257,7 +328,7 @@ static hipError_t launch_hd(bool bf16_io, int heads, const AttnMap& map, const v
   if (tiles == 0) return hipSuccess;
   if (bf16_io) {
     const float scale_log2 = 1.4426950408889634f / sqrtf((float)HD);
-    hipLaunchKernelGGL(attn_bf16_kernel<HD>, dim3(tiles), dim3(256), 0, st, map, heads,
+    hipLaunchKernelGGL((attn_bf16_kernel<HD, query_tiles(HD)>), dim3(tiles), dim3(256), 0, st, map, heads,
                        (const bf16*)q, ldq, (const bf16*)k, ldk, (const bf16*)v, ldv, (bf16*)o, ldo,
                        scale_log2);
   } else {

@@ -10,11 +10,16 @@
 //    one.  Workgroups are numbered so that each XCD (dispatched round-robin)
 //    receives a contiguous run of output tiles: tiles sharing A rows share
 //    that XCD's L2.
-//  * gemm_f32_kernel: SIMT fp32 FMA for the fp32 model and the small
-//    conditioning GEMMs (timestep MLP, adaLN table), weights fp32 or bf16.
+//  * gemm_f32_kernel: SIMT fp32 FMA for the fp32 model's layers.
+//  * linear_rows_kernel: the conditioning GEMMs (timestep MLP, adaLN table),
+//    8 timesteps per pass, weight-streaming and HBM-bound; its per-element
+//    summation order does not depend on the number of timesteps, so a
+//    sample's batched table equals the per-step tables bitwise.
 //
 // Epilogues (bias always added): store, GELU-tanh, SiLU, residual add,
-// gated residual add (gate row chosen by the row's sequence).
+// gated residual add (gate row chosen by the row's sequence), and split-store
+// for fused q|k|v projections: q and k row-major, v transposed (V^T[d][token],
+// four tokens per 8-byte store) so attention can stage V^T tiles directly.
 #include "t2i_internal.h"
 
 namespace t2i {
@@ -108,9 +113,18 @@ __global__ __launch_bounds__(256) void gemm_bf16_kernel(
     const float b = (float)bias[n];
 #pragma unroll
     for (int i = 0; i < TM; ++i) {
+      const int mb = m0 + wm * WM + i * 16 + (lane >> 4) * 4;
+      if (KIND == EPI_SPLIT_VT && n >= epi.vcol0 && mb + 3 < M) {
+        // four consecutive tokens of one V column: one 8-byte store into V^T
+        bf16x4 v4;
+#pragma unroll
+        for (int r = 0; r < 4; ++r) v4[r] = (bf16)(acc[i][j][r] + b);
+        *(bf16x4*)(epi.vt + (size_t)(n - epi.vcol0) * epi.ldvt + mb) = v4;
+        continue;
+      }
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
-        const int m = m0 + wm * WM + i * 16 + (lane >> 4) * 4 + r;
+        const int m = mb + r;
         if (m < M) epi_apply<bf16>(epi, KIND, m, n, acc[i][j][r] + b);
       }
     }
@@ -135,6 +149,9 @@ static hipError_t gemm_bf16_dispatch(const bf16* A, int lda, const bf16* W, int 
       break;
     case EPI_RESID:
       hipLaunchKernelGGL((gemm_bf16_kernel<BM, BN, EPI_RESID>), grid, block, 0, st, A, lda, W, ldw, bias, M, N, K, epi, tn);
+      break;
+    case EPI_SPLIT_VT:
+      hipLaunchKernelGGL((gemm_bf16_kernel<BM, BN, EPI_SPLIT_VT>), grid, block, 0, st, A, lda, W, ldw, bias, M, N, K, epi, tn);
       break;
     default:
       hipLaunchKernelGGL((gemm_bf16_kernel<BM, BN, EPI_RESID_GATED>), grid, block, 0, st, A, lda, W, ldw, bias, M, N, K, epi, tn);
@@ -199,6 +216,100 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(
       if (n < N) epi_apply<float>(epi, KIND, m, n, acc[i][j] + to_f32(bias[n]));
     }
   }
+}
+
+// ---------------------------------------------------------------------------
+// Small-M linear layer (conditioning: timestep MLP and adaLN table, M = number
+// of timesteps).  HBM-bound on the weights: each wave owns 4 output columns,
+// lanes stream 16-byte chunks of the 4 weight rows once, multiply them with up
+// to MT activation rows (fp32, L2-resident), and reduce across the wave.
+// Weight reads are contiguous 1 KB per wave instruction.
+
+template <typename TW, int MT, int KIND>
+__global__ __launch_bounds__(256) void linear_rows_kernel(const float* __restrict__ A, int lda,
+                                                          const TW* __restrict__ W, int ldw,
+                                                          const TW* __restrict__ bias, int M,
+                                                          int N, int K, Epi epi) {
+  constexpr int NC = 4;
+  const int lane = threadIdx.x & 63;
+  const int n0 = (blockIdx.y * 4 + (threadIdx.x >> 6)) * NC;
+  const int m0 = blockIdx.x * MT;
+  if (n0 >= N) return;
+  const int mt = min(MT, M - m0);
+  float acc[MT][NC];
+#pragma unroll
+  for (int m = 0; m < MT; ++m)
+#pragma unroll
+    for (int j = 0; j < NC; ++j) acc[m][j] = 0.f;
+  for (int k = lane * 8; k < K; k += 64 * 8) {
+    float wv[NC][8];
+#pragma unroll
+    for (int j = 0; j < NC; ++j) {
+      const int n = min(n0 + j, N - 1);
+      const TW* wp = W + (size_t)n * ldw + k;
+      if constexpr (sizeof(TW) == 2) {
+        const bf16x8 v = *(const bf16x8*)wp;
+#pragma unroll
+        for (int e = 0; e < 8; ++e) wv[j][e] = (float)v[e];
+      } else {
+        const float4 a = *(const float4*)wp, b = *(const float4*)(wp + 4);
+        wv[j][0] = a.x; wv[j][1] = a.y; wv[j][2] = a.z; wv[j][3] = a.w;
+        wv[j][4] = b.x; wv[j][5] = b.y; wv[j][6] = b.z; wv[j][7] = b.w;
+      }
+    }
+#pragma unroll
+    for (int m = 0; m < MT; ++m) {
+      if (m < mt) {
+        const float* ap = A + (size_t)(m0 + m) * lda + k;
+        const float4 a = *(const float4*)ap, b = *(const float4*)(ap + 4);
+        const float av[8] = {a.x, a.y, a.z, a.w, b.x, b.y, b.z, b.w};
+#pragma unroll
+        for (int j = 0; j < NC; ++j)
+#pragma unroll
+          for (int e = 0; e < 8; ++e) acc[m][j] = fmaf(av[e], wv[j][e], acc[m][j]);
+      }
+    }
+  }
+#pragma unroll
+  for (int m = 0; m < MT; ++m) {
+    if (m >= mt) break;
+#pragma unroll
+    for (int j = 0; j < NC; ++j) {
+      const float v = wave_sum(acc[m][j]);
+      if (lane == 0 && n0 + j < N) epi_apply<float>(epi, KIND, m0 + m, n0 + j, v + to_f32(bias[n0 + j]));
+    }
+  }
+}
+
+template <typename TW, int MT>
+static hipError_t linear_rows_dispatch(const float* A, int lda, const TW* W, int ldw,
+                                       const TW* bias, int M, int N, int K, int kind,
+                                       const Epi& epi, hipStream_t st) {
+  // consecutive workgroups share weight rows (row passes vary fastest)
+  dim3 grid((M + MT - 1) / MT, (N + 15) / 16), block(256);
+  switch (kind) {
+    case EPI_STORE:
+      hipLaunchKernelGGL((linear_rows_kernel<TW, MT, EPI_STORE>), grid, block, 0, st, A, lda, W, ldw, bias, M, N, K, epi);
+      break;
+    case EPI_SILU:
+      hipLaunchKernelGGL((linear_rows_kernel<TW, MT, EPI_SILU>), grid, block, 0, st, A, lda, W, ldw, bias, M, N, K, epi);
+      break;
+    default:
+      return hipErrorInvalidValue;
+  }
+  return hipGetLastError();
+}
+
+hipError_t launch_linear_rows(const float* A, int lda, const void* W, int ldw, bool w_bf16,
+                              const void* bias, int M, int N, int K, int kind, const Epi& epi,
+                              hipStream_t st) {
+  if (M <= 0 || N <= 0) return hipSuccess;
+  if ((kind != EPI_STORE && kind != EPI_SILU) || K % 8 || lda % 4 || ldw % 8 ||
+      ((uintptr_t)A & 15) || ((uintptr_t)W & 15))
+    return hipErrorInvalidValue;
+  if (w_bf16)
+    return linear_rows_dispatch<bf16, 8>(A, lda, (const bf16*)W, ldw, (const bf16*)bias, M, N, K, kind, epi, st);
+  return linear_rows_dispatch<float, 8>(A, lda, (const float*)W, ldw, (const float*)bias, M, N, K, kind, epi, st);
 }
 
 template <typename TW>

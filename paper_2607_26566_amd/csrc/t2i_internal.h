@@ -101,11 +101,15 @@ __device__ __forceinline__ float silu(float v) { return v / (1.0f + __expf(-v));
 // ---------------------------------------------------------------------------
 // Linear-layer epilogue.
 
-enum EpiKind { EPI_STORE = 0, EPI_GELU = 1, EPI_SILU = 2, EPI_RESID = 3, EPI_RESID_GATED = 4 };
+enum EpiKind { EPI_STORE = 0, EPI_GELU = 1, EPI_SILU = 2, EPI_RESID = 3, EPI_RESID_GATED = 4,
+               EPI_SPLIT_VT = 5 };
 
 struct Epi {
-  void* out;          // STORE / GELU / SILU destination
+  void* out;          // STORE / GELU / SILU destination (SPLIT_VT: columns < vcol0)
   int ldo;
+  bf16* vt;           // SPLIT_VT: columns >= vcol0 stored transposed, vt[(n - vcol0) * ldvt + m]
+  int ldvt;
+  int vcol0;
   float* x;           // fp32 residual for RESID kinds
   int ldx;
   bf16* xb;           // optional bf16 copy of the updated residual (stride ldx)
@@ -118,6 +122,9 @@ template <typename OutT>
 __device__ __forceinline__ void epi_apply(const Epi& e, int kind, int m, int n, float y) {
   if (kind == EPI_STORE) {
     ((OutT*)e.out)[(size_t)m * e.ldo + n] = from_f32<OutT>(y);
+  } else if (kind == EPI_SPLIT_VT) {
+    if (n < e.vcol0) ((OutT*)e.out)[(size_t)m * e.ldo + n] = from_f32<OutT>(y);
+    else e.vt[(size_t)(n - e.vcol0) * e.ldvt + m] = (bf16)y;
   } else if (kind == EPI_GELU) {
     ((OutT*)e.out)[(size_t)m * e.ldo + n] = from_f32<OutT>(gelu_tanh(y));
   } else if (kind == EPI_SILU) {
@@ -146,6 +153,11 @@ hipError_t launch_gemm_bf16(const bf16* A, int lda, const bf16* W, int ldw, cons
 hipError_t launch_gemm_f32(const float* A, int lda, const void* W, int ldw, bool w_bf16,
                            const void* bias, int M, int N, int K, int kind, const Epi& epi,
                            hipStream_t st);
+
+// Conditioning GEMMs: A fp32 [M, K], W fp32 or bf16 [N, K]; STORE or SILU.
+hipError_t launch_linear_rows(const float* A, int lda, const void* W, int ldw, bool w_bf16,
+                              const void* bias, int M, int N, int K, int kind, const Epi& epi,
+                              hipStream_t st);
 
 hipError_t launch_attention(bool bf16_io, int heads, int head_dim, const AttnMap& map,
                             const void* q, int ldq, const void* k, int ldk, const void* v,

@@ -97,11 +97,20 @@ def run_attention(dtype, heads, d, seqs, q, k, v):
     n = len(seqs)
     qs, ql, ks, kl = ((C.c_int32 * n)(*[s[i] for s in seqs]) for i in range(4))
     dt = "bf16" if dtype == _lib.T2I_BF16 else "f32"
-    dq, dk, dv = to_dev(q, dt), to_dev(k, dt), to_dev(v, dt)
-    o = torch.zeros(dq.shape, dtype=dq.dtype, device=DEV)
     w = heads * d
+    if dtype == _lib.T2I_BF16:
+        # bf16 kernels read V transposed, token stride padded to 64
+        ldv = (v.shape[0] + 63) // 64 * 64
+        vt = np.zeros((w, ldv), dtype=np.float32)
+        vt[:, :v.shape[0]] = v.T
+        vt[:, v.shape[0]:] = np.nan          # padding must never be read into results
+        v_dev, ldv_arg = to_dev(vt, dt), ldv
+    else:
+        v_dev, ldv_arg = to_dev(v, dt), w
+    dq, dk = to_dev(q, dt), to_dev(k, dt)
+    o = torch.zeros(dq.shape, dtype=dq.dtype, device=DEV)
     st = lib.t2i_op_attention(dtype, heads, d, n, qs, ql, ks, kl, dq.data_ptr(), w, dk.data_ptr(),
-                              w, dv.data_ptr(), w, o.data_ptr(), w, _stream())
+                              w, v_dev.data_ptr(), ldv_arg, o.data_ptr(), w, _stream())
     _lib.check(st)
     torch.cuda.synchronize()
     return to_host(o)
@@ -118,9 +127,10 @@ def attention_ref(seqs, q, k, v, heads):
 
 ATTN_CASES = [
     ("self-ragged", 4, 72, [(0, 333, 0, 333)], 333, 333),
-    ("varlen", 2, 72, [(0, 256, 0, 256), (256, 1024, 256, 1024), (1280, 77, 1280, 77)], 1357, 1357),
+    ("varlen", 2, 72, [(0, 256, 0, 256), (256, 1024, 256, 1024), (1280, 77, 1280, 72)], 1357, 1357),
     ("cross-120", 4, 72, [(0, 500, 0, 120), (500, 300, 120, 120)], 800, 240),
     ("single-key", 2, 72, [(0, 130, 0, 1)], 130, 1),
+    ("ragged-keys", 2, 72, [(0, 70, 0, 77), (70, 300, 80, 13)], 370, 93),
     ("d128", 3, 128, [(0, 200, 0, 260)], 200, 260),
     ("d64", 2, 64, [(0, 129, 0, 64)], 129, 64),
 ]
