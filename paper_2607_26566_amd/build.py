@@ -33,9 +33,14 @@ def sources():
                   if f.endswith((".hip", ".cpp")))
 
 
+# per-source additions: attention never sees NaN scores (masked keys are
+# -inf), so its max reductions need no NaN-quieting canonicalisation
+EXTRA = {"attention.hip": ["-fno-honor-nans"]}
+
+
 def _compile(src: str) -> str:
     obj = os.path.join(BUILD, os.path.basename(src) + ".o")
-    cmd = [HIPCC, *FLAGS, "-c", src, "-o", obj]
+    cmd = [HIPCC, *FLAGS, *EXTRA.get(os.path.basename(src), []), "-c", src, "-o", obj]
     r = subprocess.run(cmd, capture_output=True, text=True)
     if r.returncode != 0:
         raise RuntimeError(f"hipcc failed for {src}:\n{r.stdout}\n{r.stderr}")

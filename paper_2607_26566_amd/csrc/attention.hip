@@ -164,15 +164,19 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(AttnMap map, int head
       // all of them live across tiles (register pressure, not LDS traffic,
       // limits this kernel)
       asm volatile("" ::: "memory");
+      // d-chunk outer, key tile inner: four independent accumulation chains
       f32x4 sc[4];
 #pragma unroll
-      for (int kt = 0; kt < 4; ++kt) {
-        sc[kt] = f32x4{0.f, 0.f, 0.f, 0.f};
+      for (int kt = 0; kt < 4; ++kt) sc[kt] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-        for (int c = 0; c < DC; ++c) {
-          const bf16x8 kf = *(const bf16x8*)&Kb[(kt * 16 + fr) * KP + c * 32 + g * 8];
-          sc[kt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf, qf[qt][c], sc[kt], 0, 0, 0);
-        }
+      for (int c = 0; c < DC; ++c) {
+        bf16x8 kf[4];
+#pragma unroll
+        for (int kt = 0; kt < 4; ++kt)
+          kf[kt] = *(const bf16x8*)&Kb[(kt * 16 + fr) * KP + c * 32 + g * 8];
+#pragma unroll
+        for (int kt = 0; kt < 4; ++kt)
+          sc[kt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf[kt], qf[qt][c], sc[kt], 0, 0, 0);
       }
       if (ragged) {
 #pragma unroll
@@ -212,10 +216,11 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(AttnMap map, int head
         }
       }
       if (!ONES) l_run[qt] += psum;
+      // key chunk outer, d tile inner: DT independent accumulation chains
 #pragma unroll
-      for (int dt = 0; dt < DT; ++dt) {
+      for (int kc = 0; kc < 2; ++kc) {
 #pragma unroll
-        for (int kc = 0; kc < 2; ++kc) {
+        for (int dt = 0; dt < DT; ++dt) {
           const bf16* vrow = &Vb[(dt * 16 + fr) * VP + kc * 32 + g * 4];
           const bf16x4 lo = *(const bf16x4*)vrow;
           const bf16x4 hi = *(const bf16x4*)(vrow + 16);

@@ -24,6 +24,10 @@
 
 namespace t2i {
 
+hipError_t launch_gemm_dma(const bf16* A, int lda, const bf16* W, int ldw, const bf16* bias,
+                           int M, int N, int K, int kind, const Epi& epi, int vec_ok,
+                           hipStream_t st);
+
 // Map launch order -> tile order so XCD x (blocks b with b % 8 == x) owns the
 // contiguous tile range of its share.
 __device__ __forceinline__ int xcd_remap(int b, int nb) {
@@ -32,44 +36,95 @@ __device__ __forceinline__ int xcd_remap(int b, int nb) {
   return (x < r ? x * (q + 1) : r * (q + 1) + (x - r) * q) + j;
 }
 
-template <int BM, int BN, int KIND>
-__global__ __launch_bounds__(256) void gemm_bf16_kernel(
+// Epilogue on four consecutive columns nb..nb+3 of row m (vector path).
+template <int KIND>
+__device__ __forceinline__ void epi_store4(const Epi& e, int m, int nb, const float v[4]) {
+  if (KIND == EPI_STORE || KIND == EPI_GELU || KIND == EPI_SILU) {
+    bf16x4 w;
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      float y = v[r];
+      if (KIND == EPI_GELU) y = gelu_tanh(y);
+      if (KIND == EPI_SILU) y = silu(y);
+      w[r] = (bf16)y;
+    }
+    *(bf16x4*)((bf16*)e.out + (size_t)m * e.ldo + nb) = w;
+  } else {
+    float4 g4 = float4{1.f, 1.f, 1.f, 1.f};
+    if (KIND == EPI_RESID_GATED)
+      g4 = *(const float4*)(e.gate + (size_t)e.map.modrow[seq_of_row(e.map, m)] * e.ld_gate + nb);
+    float4* xp = (float4*)(e.x + (size_t)m * e.ldx + nb);
+    float4 x4 = *xp;
+    x4.x += g4.x * v[0];
+    x4.y += g4.y * v[1];
+    x4.z += g4.z * v[2];
+    x4.w += g4.w * v[3];
+    *xp = x4;
+    if (e.xb) {
+      bf16x4 w{(bf16)x4.x, (bf16)x4.y, (bf16)x4.z, (bf16)x4.w};
+      *(bf16x4*)(e.xb + (size_t)m * e.ldx + nb) = w;
+    }
+  }
+}
+
+// BM x BN tile per workgroup of 4 waves arranged WGM x (4 / WGM).  Except for
+// the split q|k|v store, the MFMA computes C^T fragments (operands swapped),
+// so a lane ends with four consecutive output columns of one row and the
+// epilogue issues one 8-byte (bf16) or 16-byte (fp32) access per lane.
+template <int BM, int BN, int WGM, int KIND>
+__global__ __launch_bounds__(256, 1) void gemm_bf16_kernel(
     const bf16* __restrict__ A, int lda, const bf16* __restrict__ W, int ldw,
-    const bf16* __restrict__ bias, int M, int N, int K, Epi epi, int tiles_n) {
+    const bf16* __restrict__ bias, int M, int N, int K, Epi epi, int tiles_n, int vec_ok) {
   constexpr int BK = 64;
   constexpr int LDK = BK + 8;
-  constexpr int WM = BM / 2, WN = BN / 2;
+  constexpr int WGN = 4 / WGM;
+  constexpr int WM = BM / WGM, WN = BN / WGN;
   constexpr int TM = WM / 16, TN = WN / 16;
-  constexpr int ACH = BM * BK / 8 / 256;   // 16-byte chunks per thread
-  constexpr int BCH = BN * BK / 8 / 256;
+  constexpr int ACH = BM * (BK / 8), BCH = BN * (BK / 8);   // 16-byte chunks per tile
+  constexpr int APT = (ACH + 255) / 256, BPT = (BCH + 255) / 256;
+  constexpr bool CT = KIND != EPI_SPLIT_VT;
+  static_assert(WM % 16 == 0 && WN % 16 == 0, "wave tile");
   __shared__ bf16 As[2][BM * LDK];
   __shared__ bf16 Bs[2][BN * LDK];
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int wm = wave >> 1, wn = wave & 1;
+  const int wm = wave / WGN, wn = wave % WGN;
   const int tile = xcd_remap(blockIdx.x, gridDim.x);
   const int m0 = (tile / tiles_n) * BM, n0 = (tile % tiles_n) * BN;
 
-  const int lrow = tid >> 3, lk = (tid & 7) * 8;
-  const bf16* Ap[ACH];
-  const bf16* Bp[BCH];
+  const bf16* Ap[APT];
+  const bf16* Bp[BPT];
 #pragma unroll
-  for (int i = 0; i < ACH; ++i) Ap[i] = A + (size_t)min(m0 + lrow + 32 * i, M - 1) * lda + lk;
+  for (int i = 0; i < APT; ++i) {
+    const int c = min(tid + 256 * i, ACH - 1);
+    Ap[i] = A + (size_t)min(m0 + (c >> 3), M - 1) * lda + (c & 7) * 8;
+  }
 #pragma unroll
-  for (int i = 0; i < BCH; ++i) Bp[i] = W + (size_t)min(n0 + lrow + 32 * i, N - 1) * ldw + lk;
+  for (int i = 0; i < BPT; ++i) {
+    const int c = min(tid + 256 * i, BCH - 1);
+    Bp[i] = W + (size_t)min(n0 + (c >> 3), N - 1) * ldw + (c & 7) * 8;
+  }
 
-  bf16x8 ra[ACH], rb[BCH];
+  bf16x8 ra[APT], rb[BPT];
   auto gload = [&](int k0) {
 #pragma unroll
-    for (int i = 0; i < ACH; ++i) ra[i] = *(const bf16x8*)(Ap[i] + k0);
+    for (int i = 0; i < APT; ++i)
+      if (ACH % 256 == 0 || tid + 256 * i < ACH) ra[i] = *(const bf16x8*)(Ap[i] + k0);
 #pragma unroll
-    for (int i = 0; i < BCH; ++i) rb[i] = *(const bf16x8*)(Bp[i] + k0);
+    for (int i = 0; i < BPT; ++i)
+      if (BCH % 256 == 0 || tid + 256 * i < BCH) rb[i] = *(const bf16x8*)(Bp[i] + k0);
   };
   auto sstore = [&](int buf) {
 #pragma unroll
-    for (int i = 0; i < ACH; ++i) *(bf16x8*)&As[buf][(lrow + 32 * i) * LDK + lk] = ra[i];
+    for (int i = 0; i < APT; ++i) {
+      const int c = tid + 256 * i;
+      if (ACH % 256 == 0 || c < ACH) *(bf16x8*)&As[buf][(c >> 3) * LDK + (c & 7) * 8] = ra[i];
+    }
 #pragma unroll
-    for (int i = 0; i < BCH; ++i) *(bf16x8*)&Bs[buf][(lrow + 32 * i) * LDK + lk] = rb[i];
+    for (int i = 0; i < BPT; ++i) {
+      const int c = tid + 256 * i;
+      if (BCH % 256 == 0 || c < BCH) *(bf16x8*)&Bs[buf][(c >> 3) * LDK + (c & 7) * 8] = rb[i];
+    }
   };
 
   f32x4 acc[TM][TN];
@@ -99,71 +154,103 @@ __global__ __launch_bounds__(256) void gemm_bf16_kernel(
       for (int i = 0; i < TM; ++i)
 #pragma unroll
         for (int j = 0; j < TN; ++j)
-          acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af[i], bfr[j], acc[i][j], 0, 0, 0);
+          acc[i][j] = CT ? __builtin_amdgcn_mfma_f32_16x16x32_bf16(bfr[j], af[i], acc[i][j], 0, 0, 0)
+                         : __builtin_amdgcn_mfma_f32_16x16x32_bf16(af[i], bfr[j], acc[i][j], 0, 0, 0);
     }
     if (kt + 1 < KT) sstore(buf ^ 1);
     __syncthreads();
   }
 
-  // C fragment layout: lane holds column (lane & 15), rows 4*(lane >> 4) + 0..3.
-#pragma unroll
-  for (int j = 0; j < TN; ++j) {
-    const int n = n0 + wn * WN + j * 16 + fr;
-    if (n >= N) continue;
-    const float b = (float)bias[n];
+  if (CT) {
+    // C^T fragment: lane holds row m = (lane & 15), columns 4*(lane >> 4) + 0..3
 #pragma unroll
     for (int i = 0; i < TM; ++i) {
-      const int mb = m0 + wm * WM + i * 16 + (lane >> 4) * 4;
-      if (KIND == EPI_SPLIT_VT && n >= epi.vcol0 && mb + 3 < M) {
-        // four consecutive tokens of one V column: one 8-byte store into V^T
-        bf16x4 v4;
+      const int m = m0 + wm * WM + i * 16 + fr;
+      if (m >= M) continue;
 #pragma unroll
-        for (int r = 0; r < 4; ++r) v4[r] = (bf16)(acc[i][j][r] + b);
-        *(bf16x4*)(epi.vt + (size_t)(n - epi.vcol0) * epi.ldvt + mb) = v4;
-        continue;
+      for (int j = 0; j < TN; ++j) {
+        const int nb = n0 + wn * WN + j * 16 + (lane >> 4) * 4;
+        if (vec_ok && nb + 3 < N) {
+          const bf16x4 b4 = *(const bf16x4*)(bias + nb);
+          const float v[4] = {acc[i][j][0] + (float)b4[0], acc[i][j][1] + (float)b4[1],
+                              acc[i][j][2] + (float)b4[2], acc[i][j][3] + (float)b4[3]};
+          epi_store4<KIND>(epi, m, nb, v);
+        } else {
+#pragma unroll
+          for (int r = 0; r < 4; ++r)
+            if (nb + r < N) epi_apply<bf16>(epi, KIND, m, nb + r, acc[i][j][r] + (float)bias[nb + r]);
+        }
       }
+    }
+  } else {
+    // C fragment: lane holds column (lane & 15), rows 4*(lane >> 4) + 0..3
 #pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        const int m = mb + r;
-        if (m < M) epi_apply<bf16>(epi, KIND, m, n, acc[i][j][r] + b);
+    for (int j = 0; j < TN; ++j) {
+      const int n = n0 + wn * WN + j * 16 + fr;
+      if (n >= N) continue;
+      const float b = (float)bias[n];
+#pragma unroll
+      for (int i = 0; i < TM; ++i) {
+        const int mb = m0 + wm * WM + i * 16 + (lane >> 4) * 4;
+        if (KIND == EPI_SPLIT_VT && n >= epi.vcol0 && mb + 3 < M) {
+          // four consecutive tokens of one V column: one 8-byte store into V^T
+          bf16x4 v4;
+#pragma unroll
+          for (int r = 0; r < 4; ++r) v4[r] = (bf16)(acc[i][j][r] + b);
+          *(bf16x4*)(epi.vt + (size_t)(n - epi.vcol0) * epi.ldvt + mb) = v4;
+          continue;
+        }
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const int m = mb + r;
+          if (m < M) epi_apply<bf16>(epi, KIND, m, n, acc[i][j][r] + b);
+        }
       }
     }
   }
 }
 
-template <int BM, int BN>
+template <int BM, int BN, int WGM>
 static hipError_t gemm_bf16_dispatch(const bf16* A, int lda, const bf16* W, int ldw,
                                      const bf16* bias, int M, int N, int K, int kind,
-                                     const Epi& epi, hipStream_t st) {
+                                     const Epi& epi, int vec_ok, hipStream_t st) {
   const int tn = (N + BN - 1) / BN, tm = (M + BM - 1) / BM;
   dim3 grid(tm * tn), block(256);
+#define T2I_GEMM_CASE(K_)                                                                       \
+  case K_:                                                                                      \
+    hipLaunchKernelGGL((gemm_bf16_kernel<BM, BN, WGM, K_>), grid, block, 0, st, A, lda, W, ldw, \
+                       bias, M, N, K, epi, tn, vec_ok);                                         \
+    break;
   switch (kind) {
-    case EPI_STORE:
-      hipLaunchKernelGGL((gemm_bf16_kernel<BM, BN, EPI_STORE>), grid, block, 0, st, A, lda, W, ldw, bias, M, N, K, epi, tn);
-      break;
-    case EPI_GELU:
-      hipLaunchKernelGGL((gemm_bf16_kernel<BM, BN, EPI_GELU>), grid, block, 0, st, A, lda, W, ldw, bias, M, N, K, epi, tn);
-      break;
-    case EPI_SILU:
-      hipLaunchKernelGGL((gemm_bf16_kernel<BM, BN, EPI_SILU>), grid, block, 0, st, A, lda, W, ldw, bias, M, N, K, epi, tn);
-      break;
-    case EPI_RESID:
-      hipLaunchKernelGGL((gemm_bf16_kernel<BM, BN, EPI_RESID>), grid, block, 0, st, A, lda, W, ldw, bias, M, N, K, epi, tn);
-      break;
-    case EPI_SPLIT_VT:
-      hipLaunchKernelGGL((gemm_bf16_kernel<BM, BN, EPI_SPLIT_VT>), grid, block, 0, st, A, lda, W, ldw, bias, M, N, K, epi, tn);
-      break;
-    default:
-      hipLaunchKernelGGL((gemm_bf16_kernel<BM, BN, EPI_RESID_GATED>), grid, block, 0, st, A, lda, W, ldw, bias, M, N, K, epi, tn);
-      break;
+    T2I_GEMM_CASE(EPI_STORE)
+    T2I_GEMM_CASE(EPI_GELU)
+    T2I_GEMM_CASE(EPI_SILU)
+    T2I_GEMM_CASE(EPI_RESID)
+    T2I_GEMM_CASE(EPI_RESID_GATED)
+    T2I_GEMM_CASE(EPI_SPLIT_VT)
+    default: return hipErrorInvalidValue;
   }
+#undef T2I_GEMM_CASE
   return hipGetLastError();
 }
 
 hipError_t launch_gemm_bf16(const bf16* A, int lda, const bf16* W, int ldw, const bf16* bias,
                             int M, int N, int K, int kind, const Epi& epi, hipStream_t st) {
   if (M <= 0 || N <= 0) return hipSuccess;
-  return gemm_bf16_dispatch<128, 128>(A, lda, W, ldw, bias, M, N, K, kind, epi, st);
+  auto al = [](const void* p, int a) { return ((uintptr_t)p % a) == 0; };
+  const int vec_ok = (epi.ldo % 4 == 0) && (epi.ldx % 4 == 0) && (epi.ld_gate % 4 == 0) &&
+                     al(bias, 8) && al(epi.out, 8) && al(epi.x, 16) && al(epi.xb, 8) &&
+                     al(epi.gate, 16);
+  // Tile choice.  Large M: 256 x 144 tiles fed by direct HBM->LDS loads
+  // (gemm_dma.hip).  The DiT widths 1152, 2304, 3456 and 4608 are multiples of
+  // 144, so at M = 8192 the layers launch 256 / 512 / 768 / 1024 tiles --
+  // whole rounds on 256 CUs at one workgroup each.  Otherwise 128 x 144 or
+  // 128 x 128 register-staged tiles (the faster ones at M ~ 1000 measured).
+  if (M >= 2048 && N % 144 == 0 && kind != EPI_SILU)
+    return launch_gemm_dma(A, lda, W, ldw, bias, M, N, K, kind, epi, vec_ok, st);
+  if (N % 144 == 0)
+    return gemm_bf16_dispatch<128, 144, 4>(A, lda, W, ldw, bias, M, N, K, kind, epi, vec_ok, st);
+  return gemm_bf16_dispatch<128, 128, 2>(A, lda, W, ldw, bias, M, N, K, kind, epi, vec_ok, st);
 }
 
 // ---------------------------------------------------------------------------

@@ -1,0 +1,254 @@
+// bf16 MFMA GEMM fed by direct HBM->LDS loads (gfx950 global_load_lds_dwordx4).
+//
+// y = A W^T + b for the DiT's projections at large M.  A workgroup owns a
+// BM x BN output tile; its waves (WGM x WGN) each own a (BM/WGM) x (BN/WGN)
+// quadrant of 16x16 MFMA tiles (v_mfma_f32_16x16x32_bf16, fp32 accumulation).
+// K advances 64 at a time through a ring of ST LDS stages:
+//
+//   * each stage holds the A rows (BM x 128 B) then the W rows (BN x 128 B);
+//     every 1 KB of a stage (8 rows) is filled by ONE wave instruction that
+//     moves 16 bytes per lane straight from global memory into LDS -- no
+//     registers, no ds_write;
+//   * rows are not padded: the 16-byte chunk c of row r sits in slot
+//     c ^ ((r >> 1) & 7), so the 16 rows one fragment load touches spread over
+//     all 64 banks (rows alternate bank halves; the swizzle separates the 8
+//     rows of each half);
+//   * ST-1 tiles are in flight while one is consumed: per K step a wave waits
+//     until only its loads of the younger tiles are outstanding (vmcnt),
+//     meets the other waves at one barrier, issues the loads of tile t+ST-1
+//     into the stage everybody finished with, and runs its MFMAs;
+//   * every wave issues the same number of load instructions per tile
+//     (waves with fewer blocks repeat their last one, which rewrites identical
+//     bytes), so the vmcnt thresholds are compile-time constants.
+//
+// The epilogue is the one of gemm.hip: C^T fragments (operands swapped) give a
+// lane four consecutive output columns of one row, stored with one 8-byte
+// (bf16) or 16-byte (fp32 residual) access; the split q|k|v store keeps the C
+// layout and writes V^T four tokens at a time.
+#include "t2i_internal.h"
+
+namespace t2i {
+
+__device__ __forceinline__ int xcd_remap_dma(int b, int nb) {
+  const int q = nb >> 3, r = nb & 7;
+  const int x = b & 7, j = b >> 3;
+  return (x < r ? x * (q + 1) : r * (q + 1) + (x - r) * q) + j;
+}
+
+// s_waitcnt with only vmcnt constrained (gfx9 encoding: vmcnt low bits [3:0],
+// high bits [15:14]; expcnt [6:4] and lgkmcnt [11:8] left at their maximum).
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4) | (15 << 8));
+}
+
+__device__ __forceinline__ void block_barrier() {
+  // this wave's LDS reads are complete (a stage may be refilled right after
+  // the barrier), then a plain s_barrier: no release fence, which would wait
+  // for every outstanding global load, and a compiler barrier for memory ops
+  asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
+}
+
+template <int KIND>
+__device__ __forceinline__ void dma_epi4(const Epi& e, int m, int nb, const float v[4]) {
+  if (KIND == EPI_STORE || KIND == EPI_GELU || KIND == EPI_SILU) {
+    bf16x4 w;
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      float y = v[r];
+      if (KIND == EPI_GELU) y = gelu_tanh(y);
+      if (KIND == EPI_SILU) y = silu(y);
+      w[r] = (bf16)y;
+    }
+    *(bf16x4*)((bf16*)e.out + (size_t)m * e.ldo + nb) = w;
+  } else {
+    float4 g4 = float4{1.f, 1.f, 1.f, 1.f};
+    if (KIND == EPI_RESID_GATED)
+      g4 = *(const float4*)(e.gate + (size_t)e.map.modrow[seq_of_row(e.map, m)] * e.ld_gate + nb);
+    float4* xp = (float4*)(e.x + (size_t)m * e.ldx + nb);
+    float4 x4 = *xp;
+    x4.x += g4.x * v[0];
+    x4.y += g4.y * v[1];
+    x4.z += g4.z * v[2];
+    x4.w += g4.w * v[3];
+    *xp = x4;
+    if (e.xb) {
+      bf16x4 w{(bf16)x4.x, (bf16)x4.y, (bf16)x4.z, (bf16)x4.w};
+      *(bf16x4*)(e.xb + (size_t)m * e.ldx + nb) = w;
+    }
+  }
+}
+
+template <int BM, int BN, int WGM, int WGN, int ST, int KIND>
+__global__ __launch_bounds__(64 * WGM * WGN, 1) void gemm_dma_kernel(
+    const bf16* __restrict__ A, int lda, const bf16* __restrict__ W, int ldw,
+    const bf16* __restrict__ bias, int M, int N, int K, Epi epi, int tiles_n, int vec_ok) {
+  constexpr int NW = WGM * WGN;
+  constexpr int WM = BM / WGM, WN = BN / WGN;
+  constexpr int TM = WM / 16, TN = WN / 16;
+  constexpr int ABLK = BM / 8, BBLK = BN / 8, TBLK = ABLK + BBLK;   // 1-KB blocks per stage
+  constexpr int BPW = (TBLK + NW - 1) / NW;                       // load instructions per wave
+  constexpr int STAGE = (BM + BN) * 64;                            // bf16 elements per stage
+  constexpr bool CT = KIND != EPI_SPLIT_VT;
+  static_assert(BM % 8 == 0 && BN % 8 == 0 && WM % 16 == 0 && WN % 16 == 0, "tile shape");
+  static_assert(ST >= 2 && ST <= 4, "stages");
+  __shared__ __attribute__((aligned(1024))) bf16 smem[ST * STAGE];
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int wm = wave / WGN, wn = wave % WGN;
+  const int tile = xcd_remap_dma(blockIdx.x, gridDim.x);
+  const int m0 = (tile / tiles_n) * BM, n0 = (tile % tiles_n) * BN;
+
+  // this lane's source of every block it loads (k offset added per tile)
+  const bf16* src[BPW];
+  int dst[BPW];   // byte offset of the block inside a stage (wave-uniform)
+#pragma unroll
+  for (int i = 0; i < BPW; ++i) {
+    int b = wave + i * NW;
+    if (b >= TBLK) b -= NW;               // repeat this wave's previous block
+    const int lr = (b < ABLK ? b : b - ABLK) * 8 + (lane >> 3);   // row within A or W tile
+    const int c = (lane & 7) ^ ((lr >> 1) & 7);                   // logical chunk of this slot
+    src[i] = b < ABLK ? A + (size_t)min(m0 + lr, M - 1) * lda + c * 8
+                      : W + (size_t)min(n0 + lr, N - 1) * ldw + c * 8;
+    dst[i] = b * 1024;
+  }
+  auto issue = [&](int t, int stage) {
+    const int k0 = t * 64;
+#pragma unroll
+    for (int i = 0; i < BPW; ++i)
+      __builtin_amdgcn_global_load_lds(
+          (__attribute__((address_space(1))) void*)(src[i] + k0),
+          (__attribute__((address_space(3))) void*)((char*)smem + stage * STAGE * 2 + dst[i]),
+          16, 0, 0);
+  };
+
+  f32x4 acc[TM][TN];
+#pragma unroll
+  for (int i = 0; i < TM; ++i)
+#pragma unroll
+    for (int j = 0; j < TN; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+  const int fr = lane & 15, g = lane >> 4;
+  // byte offset of a fragment row's 16-byte chunk c in the swizzled layout
+  auto frag = [&](const bf16* base, int row, int c) {
+    return *(const bf16x8*)((const char*)base + row * 128 + ((c ^ ((row >> 1) & 7)) << 4));
+  };
+  auto compute = [&](int stage) {
+    const bf16* sA = smem + stage * STAGE;
+    const bf16* sB = sA + BM * 64;
+#pragma unroll
+    for (int kk = 0; kk < 2; ++kk) {
+      bf16x8 af[TM], bfr[TN];
+#pragma unroll
+      for (int i = 0; i < TM; ++i) af[i] = frag(sA, wm * WM + i * 16 + fr, kk * 4 + g);
+#pragma unroll
+      for (int j = 0; j < TN; ++j) bfr[j] = frag(sB, wn * WN + j * 16 + fr, kk * 4 + g);
+#pragma unroll
+      for (int i = 0; i < TM; ++i)
+#pragma unroll
+        for (int j = 0; j < TN; ++j)
+          acc[i][j] = CT ? __builtin_amdgcn_mfma_f32_16x16x32_bf16(bfr[j], af[i], acc[i][j], 0, 0, 0)
+                         : __builtin_amdgcn_mfma_f32_16x16x32_bf16(af[i], bfr[j], acc[i][j], 0, 0, 0);
+    }
+  };
+
+  const int KT = K / 64;
+#pragma unroll
+  for (int s = 0; s < ST - 1; ++s)
+    if (s < KT) issue(s, s);
+  for (int t0 = 0; t0 < KT; t0 += ST) {
+#pragma unroll
+    for (int i = 0; i < ST; ++i) {
+      const int t = t0 + i;
+      if (t >= KT) break;
+      // loads younger than tile t that may stay in flight
+      const int younger = min(ST - 2, KT - 1 - t);
+      if (younger >= 2) wait_vmcnt<2 * BPW>();
+      else if (younger == 1) wait_vmcnt<BPW>();
+      else wait_vmcnt<0>();
+      block_barrier();
+      if (t + ST - 1 < KT) issue(t + ST - 1, (i + ST - 1) % ST);
+      compute(i);
+    }
+  }
+
+  if (CT) {
+#pragma unroll
+    for (int i = 0; i < TM; ++i) {
+      const int m = m0 + wm * WM + i * 16 + fr;
+      if (m >= M) continue;
+#pragma unroll
+      for (int j = 0; j < TN; ++j) {
+        const int nb = n0 + wn * WN + j * 16 + g * 4;
+        if (vec_ok && nb + 3 < N) {
+          const bf16x4 b4 = *(const bf16x4*)(bias + nb);
+          const float v[4] = {acc[i][j][0] + (float)b4[0], acc[i][j][1] + (float)b4[1],
+                              acc[i][j][2] + (float)b4[2], acc[i][j][3] + (float)b4[3]};
+          dma_epi4<KIND>(epi, m, nb, v);
+        } else {
+#pragma unroll
+          for (int r = 0; r < 4; ++r)
+            if (nb + r < N) epi_apply<bf16>(epi, KIND, m, nb + r, acc[i][j][r] + (float)bias[nb + r]);
+        }
+      }
+    }
+  } else {
+#pragma unroll
+    for (int j = 0; j < TN; ++j) {
+      const int n = n0 + wn * WN + j * 16 + fr;
+      if (n >= N) continue;
+      const float b = (float)bias[n];
+#pragma unroll
+      for (int i = 0; i < TM; ++i) {
+        const int mb = m0 + wm * WM + i * 16 + g * 4;
+        if (KIND == EPI_SPLIT_VT && n >= epi.vcol0 && mb + 3 < M) {
+          bf16x4 v4;
+#pragma unroll
+          for (int r = 0; r < 4; ++r) v4[r] = (bf16)(acc[i][j][r] + b);
+          *(bf16x4*)(epi.vt + (size_t)(n - epi.vcol0) * epi.ldvt + mb) = v4;
+          continue;
+        }
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const int m = mb + r;
+          if (m < M) epi_apply<bf16>(epi, KIND, m, n, acc[i][j][r] + b);
+        }
+      }
+    }
+  }
+}
+
+template <int BM, int BN, int WGM, int WGN, int ST>
+hipError_t gemm_dma_dispatch(const bf16* A, int lda, const bf16* W, int ldw, const bf16* bias,
+                             int M, int N, int K, int kind, const Epi& epi, int vec_ok,
+                             hipStream_t st) {
+  const int tn = (N + BN - 1) / BN, tm = (M + BM - 1) / BM;
+  dim3 grid(tm * tn), block(64 * WGM * WGN);
+#define T2I_DMA_CASE(K_)                                                                      \
+  case K_:                                                                                    \
+    hipLaunchKernelGGL((gemm_dma_kernel<BM, BN, WGM, WGN, ST, K_>), grid, block, 0, st, A, lda, \
+                       W, ldw, bias, M, N, K, epi, tn, vec_ok);                               \
+    break;
+  switch (kind) {
+    T2I_DMA_CASE(EPI_STORE)
+    T2I_DMA_CASE(EPI_GELU)
+    T2I_DMA_CASE(EPI_RESID)
+    T2I_DMA_CASE(EPI_RESID_GATED)
+    T2I_DMA_CASE(EPI_SPLIT_VT)
+    default: return hipErrorInvalidValue;
+  }
+#undef T2I_DMA_CASE
+  return hipGetLastError();
+}
+
+// Large-M projections: 256 x 144 tiles, 8 waves of 32 x 144 (two per SIMD),
+// two stages (100 KB of LDS).  Measured on MI355X at M = 8192 this beat
+// 128x144/4-wave, 256x144/4-wave, 256x128/8-wave and 3- or 4-stage variants.
+hipError_t launch_gemm_dma(const bf16* A, int lda, const bf16* W, int ldw, const bf16* bias,
+                           int M, int N, int K, int kind, const Epi& epi, int vec_ok,
+                           hipStream_t st) {
+  return gemm_dma_dispatch<256, 144, 8, 1, 2>(A, lda, W, ldw, bias, M, N, K, kind, epi, vec_ok, st);
+}
+
+}  // namespace t2i

@@ -47,7 +47,8 @@ def run_linear(dtype, epi, A, W, b, resid=None, gate=None, with_copy=False):
 
 
 GEMM_SHAPES = [(300, 192, 128), (1000, 1152, 1152), (64, 3456, 1152), (8192, 1152, 4608),
-               (129, 4608, 1152), (240, 2304, 1152), (1, 128, 64)]
+               (129, 4608, 1152), (240, 2304, 1152), (1, 128, 64), (4096, 3456, 1152),
+               (3000, 1296, 1152), (2100, 200, 128), (2100, 202, 64), (8192, 4608, 1152)]
 
 
 @pytest.mark.parametrize("M,N,K", GEMM_SHAPES)
@@ -61,7 +62,8 @@ def test_linear_bf16_store_and_gelu(M, N, K):
     assert rel_l2(to_host(out), dit.gelu_tanh(ref)) < 3e-3
 
 
-@pytest.mark.parametrize("M,N,K", [(300, 192, 128), (1000, 1152, 4608), (8192, 1152, 1152)])
+@pytest.mark.parametrize("M,N,K", [(300, 192, 128), (1000, 1152, 4608), (8192, 1152, 1152),
+                                   (4096, 2304, 1152), (2050, 1152, 4608)])
 def test_linear_bf16_residual_epilogues(M, N, K):
     say(f"linear bf16 residual {M}x{N}x{K}")
     A, W, b = rnd(4, (M, K)), rnd(5, (N, K), 0.05), rnd(6, (N,), 0.1)
