@@ -15,7 +15,8 @@
 //     again gives lane l query (l & 15) -- so the online-softmax rescale of the
 //     output needs no data exchange between lanes.
 // The row max needs two cross-lane steps per tile (the 4 lanes of a query);
-// row sums are kept per lane and combined once at the end.  The head
+// the row sums ride on a ones row of V^T where the head dimension has padding
+// (else they are kept per lane and combined once at the end).  The head
 // dimension is padded with zeros to a multiple of 32 for Q K^T and to a
 // multiple of 16 for P V (72 -> 96 / 80); the padding never reaches memory.
 //
@@ -29,6 +30,15 @@ __device__ __forceinline__ int xcd_remap_attn(int b, int nb) {
   const int q = nb >> 3, r = nb & 7;
   const int x = b & 7, j = b >> 3;
   return (x < r ? x * (q + 1) : r * (q + 1) + (x - r) * q) + j;
+}
+
+// Position of tile key k (0..63) in a staged V^T row.  Within each 32-key
+// chunk the keys a lane multiplies -- 4g..4g+3 and 16+4g..16+4g+3, the
+// probabilities its S^T fragment holds -- are stored next to each other at
+// 8g..8g+7, so one conflict-free 16-byte LDS read feeds the PV MFMA.
+__device__ __forceinline__ int vpos(int k) {
+  const int kk = k & 31;
+  return (k & 32) + 8 * ((kk & 15) >> 2) + 4 * (kk >> 4) + (kk & 3);
 }
 
 // Flattened tile -> (head, sequence, query tile).  Tiles of one head and one
@@ -57,12 +67,16 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(AttnMap map, int head
   constexpr int DT = (HD + 15) / 16;   // 16-wide tiles of d for P V
   constexpr int HDO = DT * 16;
   constexpr bool ONES = HD < HDO;      // a spare V^T row carries the row sums
-  constexpr int KP = HDP + 8;          // LDS pitch of a K row (bf16)
   constexpr int VP = BKV + 8;          // LDS pitch of a V^T row (bf16)
   constexpr int CPR = HD / 8;          // 16-byte chunks per K row
-  constexpr int KCH = BKV * CPR, VCH = HD * (BKV / 8);
-  constexpr int KPT = (KCH + 255) / 256, VPT = (VCH + 255) / 256;
-  __shared__ bf16 Ks[2][BKV * KP];
+  // K tile, chunk-major: block b (1 KB) holds d = 8b .. 8b+7 of the 64 keys,
+  // key k at byte 16k; block CPR is all zeros (the d padding of Q K^T)
+  constexpr int KBLK = CPR + 1;
+  constexpr int KST = KBLK * 512;      // bf16 elements per K stage
+  constexpr int KBPW = (CPR + 3) / 4;  // K load instructions per wave
+  constexpr int VCH = HD * (BKV / 8);
+  constexpr int VPT = (VCH + 255) / 256;
+  __shared__ __attribute__((aligned(1024))) bf16 Ks[2][KST];
   __shared__ bf16 Vs[2][HDO * VP];
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -73,21 +87,29 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(AttnMap map, int head
   const int qrow0 = q_beg + j * BQ + wave * (QT * 16);
   const int g = lane >> 4, fr = lane & 15;
 
-  // zero both buffers once: K padding columns and V^T padding rows stay zero
-  for (int i = tid; i < 2 * BKV * KP; i += 256) (&Ks[0][0])[i] = (bf16)0.f;
+  // zero both buffers once: the K zero block and the V^T padding rows stay zero
+  for (int i = tid; i < 2 * KST; i += 256) (&Ks[0][0])[i] = (bf16)0.f;
   for (int i = tid; i < 2 * HDO * VP; i += 256) (&Vs[0][0])[i] = (bf16)0.f;
 
-  bf16x8 kr[KPT], vr[VPT];
-  auto gload = [&](int kv0) {
+  // K tiles move HBM -> LDS directly (global_load_lds_dwordx4): instruction
+  // for block b has lane = key and fetches that key's d-chunk b.  Waves with
+  // fewer blocks repeat one (identical bytes).  Key rows past the sequence are
+  // clamped to its last key; their scores are masked.
+  int kblk[KBPW];
 #pragma unroll
-    for (int i = 0; i < KPT; ++i) {
-      const int c = tid + 256 * i;
-      kr[i] = bf16x8{};
-      if (c < KCH) {
-        const int key = c / CPR, dc = (c - key * CPR) * 8, gk = kv0 + key;
-        if (gk < k_end) kr[i] = *(const bf16x8*)(K + (size_t)gk * ldk + h * HD + dc);
-      }
-    }
+  for (int i = 0; i < KBPW; ++i) kblk[i] = min(wave + 4 * i, CPR - 1);
+  auto kload = [&](int kv0, int buf) {
+    const int gk = min(kv0 + lane, k_end - 1);
+    const bf16* src = K + (size_t)gk * ldk + h * HD;
+#pragma unroll
+    for (int i = 0; i < KBPW; ++i)
+      __builtin_amdgcn_global_load_lds(
+          (__attribute__((address_space(1))) void*)(src + kblk[i] * 8),
+          (__attribute__((address_space(3))) void*)(&Ks[buf][kblk[i] * 512]), 16, 0, 0);
+  };
+
+  bf16x8 vr[VPT];
+  auto gload = [&](int kv0) {
 #pragma unroll
     for (int i = 0; i < VPT; ++i) {
       const int c = tid + 256 * i;
@@ -107,19 +129,18 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(AttnMap map, int head
   };
   auto sstore = [&](int buf, int kv0) {
 #pragma unroll
-    for (int i = 0; i < KPT; ++i) {
-      const int c = tid + 256 * i;
-      if (c < KCH) {
-        const int key = c / CPR, dc = (c - key * CPR) * 8;
-        *(bf16x8*)&Ks[buf][key * KP + dc] = kr[i];
-      }
-    }
-#pragma unroll
     for (int i = 0; i < VPT; ++i) {
       const int c = tid + 256 * i;
-      if (c < VCH) *(bf16x8*)&Vs[buf][(c >> 3) * VP + (c & 7) * 8] = vr[i];
+      if (c < VCH) {
+        // keys 8(c&7) .. +7 of row c>>3: two groups of four, each to its
+        // permuted position (see vpos)
+        bf16* row = &Vs[buf][(c >> 3) * VP];
+        const int k = (c & 7) * 8;
+        *(bf16x4*)&row[vpos(k)] = bf16x4{vr[i][0], vr[i][1], vr[i][2], vr[i][3]};
+        *(bf16x4*)&row[vpos(k + 4)] = bf16x4{vr[i][4], vr[i][5], vr[i][6], vr[i][7]};
+      }
     }
-    if (ONES && tid < BKV) Vs[buf][HD * VP + tid] = (bf16)(kv0 + tid < k_end ? 1.f : 0.f);
+    if (ONES && tid < BKV) Vs[buf][HD * VP + vpos(tid)] = (bf16)(kv0 + tid < k_end ? 1.f : 0.f);
   };
 
   // Q fragments (B operand of S^T): query qrow0 + qt*16 + fr, d = c*32 + g*8 .. +7
@@ -147,14 +168,23 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(AttnMap map, int head
     for (int dt = 0; dt < DT; ++dt) o[qt][dt] = f32x4{0.f, 0.f, 0.f, 0.f};
   }
 
+  // K fragment of 32-wide d chunk c: block 4c + g (the zero block past HD)
+  int koff[DC];
+#pragma unroll
+  for (int c = 0; c < DC; ++c) koff[c] = min(4 * c + g, CPR) * 512 + fr * 8;
+
   __syncthreads();          // zero-fill done before the first tile lands
+  kload(k_beg, 0);
   gload(k_beg);
   sstore(0, k_beg);
-  __syncthreads();
+  __syncthreads();          // (waits for the K loads too)
   int buf = 0;
   for (int kv0 = k_beg; kv0 < k_end; kv0 += BKV) {
     const bool next = kv0 + BKV < k_end;
-    if (next) gload(kv0 + BKV);
+    if (next) {
+      kload(kv0 + BKV, buf ^ 1);
+      gload(kv0 + BKV);
+    }
     const bool ragged = kv0 + BKV > k_end;
     const bf16* Kb = Ks[buf];
     const bf16* Vb = Vs[buf];
@@ -172,8 +202,7 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(AttnMap map, int head
       for (int c = 0; c < DC; ++c) {
         bf16x8 kf[4];
 #pragma unroll
-        for (int kt = 0; kt < 4; ++kt)
-          kf[kt] = *(const bf16x8*)&Kb[(kt * 16 + fr) * KP + c * 32 + g * 8];
+        for (int kt = 0; kt < 4; ++kt) kf[kt] = *(const bf16x8*)&Kb[koff[c] + kt * 128];
 #pragma unroll
         for (int kt = 0; kt < 4; ++kt)
           sc[kt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf[kt], qf[qt][c], sc[kt], 0, 0, 0);
@@ -216,15 +245,13 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(AttnMap map, int head
         }
       }
       if (!ONES) l_run[qt] += psum;
-      // key chunk outer, d tile inner: DT independent accumulation chains
+      // key chunk outer, d tile inner: DT independent accumulation chains.
+      // The lane's 8 keys are contiguous in the permuted V^T row: one 16-byte read.
 #pragma unroll
       for (int kc = 0; kc < 2; ++kc) {
 #pragma unroll
         for (int dt = 0; dt < DT; ++dt) {
-          const bf16* vrow = &Vb[(dt * 16 + fr) * VP + kc * 32 + g * 4];
-          const bf16x4 lo = *(const bf16x4*)vrow;
-          const bf16x4 hi = *(const bf16x4*)(vrow + 16);
-          const bf16x8 vf = bf16x8{lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
+          const bf16x8 vf = *(const bf16x8*)&Vb[(dt * 16 + fr) * VP + kc * 32 + g * 8];
           o[qt][dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vf, pf[kc], o[qt][dt], 0, 0, 0);
         }
       }

@@ -3,7 +3,8 @@
 // y = A W^T + b for the DiT's projections at large M.  A workgroup owns a
 // BM x BN output tile; its waves (WGM x WGN) each own a (BM/WGM) x (BN/WGN)
 // quadrant of 16x16 MFMA tiles (v_mfma_f32_16x16x32_bf16, fp32 accumulation).
-// K advances 64 at a time through a ring of ST LDS stages:
+// K advances 64 at a time through a ring of ST LDS stages (see launch_gemm_dma
+// for the tile shapes in use):
 //
 //   * each stage holds the A rows (BM x 128 B) then the W rows (BN x 128 B);
 //     every 1 KB of a stage (8 rows) is filled by ONE wave instruction that
@@ -80,7 +81,7 @@ __device__ __forceinline__ void dma_epi4(const Epi& e, int m, int nb, const floa
   }
 }
 
-template <int BM, int BN, int WGM, int WGN, int ST, int KIND>
+template <int BM, int BN, int WGM, int WGN, int ST, int KIND, int AUX>
 __global__ __launch_bounds__(64 * WGM * WGN, 1) void gemm_dma_kernel(
     const bf16* __restrict__ A, int lda, const bf16* __restrict__ W, int ldw,
     const bf16* __restrict__ bias, int M, int N, int K, Epi epi, int tiles_n, int vec_ok) {
@@ -120,7 +121,7 @@ __global__ __launch_bounds__(64 * WGM * WGN, 1) void gemm_dma_kernel(
       __builtin_amdgcn_global_load_lds(
           (__attribute__((address_space(1))) void*)(src[i] + k0),
           (__attribute__((address_space(3))) void*)((char*)smem + stage * STAGE * 2 + dst[i]),
-          16, 0, 0);
+          16, 0, AUX);
   };
 
   f32x4 acc[TM][TN];
@@ -219,7 +220,7 @@ __global__ __launch_bounds__(64 * WGM * WGN, 1) void gemm_dma_kernel(
   }
 }
 
-template <int BM, int BN, int WGM, int WGN, int ST>
+template <int BM, int BN, int WGM, int WGN, int ST, int AUX>
 hipError_t gemm_dma_dispatch(const bf16* A, int lda, const bf16* W, int ldw, const bf16* bias,
                              int M, int N, int K, int kind, const Epi& epi, int vec_ok,
                              hipStream_t st) {
@@ -227,7 +228,7 @@ hipError_t gemm_dma_dispatch(const bf16* A, int lda, const bf16* W, int ldw, con
   dim3 grid(tm * tn), block(64 * WGM * WGN);
 #define T2I_DMA_CASE(K_)                                                                      \
   case K_:                                                                                    \
-    hipLaunchKernelGGL((gemm_dma_kernel<BM, BN, WGM, WGN, ST, K_>), grid, block, 0, st, A, lda, \
+    hipLaunchKernelGGL((gemm_dma_kernel<BM, BN, WGM, WGN, ST, K_, AUX>), grid, block, 0, st, A, lda, \
                        W, ldw, bias, M, N, K, epi, tn, vec_ok);                               \
     break;
   switch (kind) {
@@ -242,13 +243,19 @@ hipError_t gemm_dma_dispatch(const bf16* A, int lda, const bf16* W, int ldw, con
   return hipGetLastError();
 }
 
-// Large-M projections: 256 x 144 tiles, 8 waves of 32 x 144 (two per SIMD),
-// two stages (100 KB of LDS).  Measured on MI355X at M = 8192 this beat
-// 128x144/4-wave, 256x144/4-wave, 256x128/8-wave and 3- or 4-stage variants.
+// Large-M projections (measured on MI355X at M = 8192).  The tile loads are
+// bounded by how many L1 misses a CU keeps in flight, so bytes per FLOP --
+// (BM + BN) / (BM BN) -- decide: 256 x 288 tiles (8 waves of 64 x 144) where
+// N is a multiple of 288 and leaves whole rounds of tiles (fc1: N = 4608 ->
+// 512 tiles), else 256 x 144 tiles (8 waves of 32 x 144, three stages).  Both
+// load with cache policy bit 0 (sc0) set, which measured faster.
 hipError_t launch_gemm_dma(const bf16* A, int lda, const bf16* W, int ldw, const bf16* bias,
                            int M, int N, int K, int kind, const Epi& epi, int vec_ok,
                            hipStream_t st) {
-  return gemm_dma_dispatch<256, 144, 8, 1, 2>(A, lda, W, ldw, bias, M, N, K, kind, epi, vec_ok, st);
+  const long tiles288 = (long)((M + 255) / 256) * (N / 288);
+  if (N % 288 == 0 && tiles288 % 256 == 0)
+    return gemm_dma_dispatch<256, 288, 4, 2, 2, 1>(A, lda, W, ldw, bias, M, N, K, kind, epi, vec_ok, st);
+  return gemm_dma_dispatch<256, 144, 8, 1, 3, 1>(A, lda, W, ldw, bias, M, N, K, kind, epi, vec_ok, st);
 }
 
 }  // namespace t2i

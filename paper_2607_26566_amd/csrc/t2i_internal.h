@@ -90,13 +90,16 @@ __device__ __forceinline__ double wave_sum(double v) {
 
 // GELU with the tanh approximation, written as u * sigmoid(2z):
 // 0.5 u (1 + tanh z) = u / (1 + exp(-2z)),  z = sqrt(2/pi) (u + 0.044715 u^3).
+// The reciprocal is the hardware v_rcp_f32 (about 1 ulp), not an IEEE
+// division: exp(-2z) -> +inf gives rcp(inf) = 0 and u * 0 = -0 for u -> -inf,
+// matching the limit.
 __device__ __forceinline__ float gelu_tanh(float u) {
   const float k0 = 0.7978845608028654f;   // sqrt(2/pi)
-  float z = k0 * (u + 0.044715f * u * u * u);
-  return u / (1.0f + __expf(-2.0f * z));
+  const float z = k0 * fmaf(0.044715f * u, u * u, u);
+  return u * __builtin_amdgcn_rcpf(1.0f + __expf(-2.0f * z));
 }
 
-__device__ __forceinline__ float silu(float v) { return v / (1.0f + __expf(-v)); }
+__device__ __forceinline__ float silu(float v) { return v * __builtin_amdgcn_rcpf(1.0f + __expf(-v)); }
 
 // ---------------------------------------------------------------------------
 // Linear-layer epilogue.
