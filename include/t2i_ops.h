@@ -45,20 +45,25 @@ t2i_status t2i_op_linear(int32_t dtype, int32_t epilogue, int32_t M, int32_t N,
 
 /*
  * Multi-head attention softmax(Q K^T / sqrt(d)) V over packed variable-length
- * sequences: query sequence s holds rows q_start[s] .. q_start[s]+q_len[s]-1
- * of Q and attends to rows k_start[s] .. +k_len[s]-1 of K and V (host arrays
- * of n_seq <= T2I_MAX_SEQ entries, k_len >= 1).  Head h of a row occupies
- * columns h*d .. h*d+d-1.  Q, K, O are dtype (bf16 or fp32) with row strides
- * ldq, ldk, ldo (multiples of 8).
+ * sequences (the DiT's self- and cross-attention, Sec. 4's model `forward`;
+ * joint text+image attention of the Sec. 8.1 model family): query sequence s
+ * holds rows q_start[s] .. q_start[s]+q_len[s]-1 of Q and attends to rows
+ * k_start[s] .. +k_len[s]-1 of K and V and, when k2_start/k2_len are given
+ * (both or neither), also to rows k2_start[s] .. +k2_len[s]-1 -- the joint
+ * attention's text keys and image keys, wherever each stream's rows sit.
+ * Host arrays of n_seq <= T2I_MAX_SEQ entries; k_len + k2_len >= 1.  Head h of
+ * a row occupies columns h*d .. h*d+d-1.  Q, K, O are dtype (bf16 or fp32)
+ * with row strides ldq, ldk, ldo (multiples of 8).
  *   fp32: V is row-major like K, row stride ldv.
  *   bf16: V is given transposed, V^T [heads*head_dim][ldv] (the key index is
- *         contiguous), the layout the fused qkv projection writes; every
- *         k_start must be a multiple of 8 and k_start + k_len <= ldv.
+ *         contiguous), the layout the fused qkv projection writes; every key
+ *         segment must start at a multiple of 8 and end within ldv.
  */
 t2i_status t2i_op_attention(int32_t dtype, int32_t heads, int32_t head_dim,
                             int32_t n_seq, const int32_t* q_start,
                             const int32_t* q_len, const int32_t* k_start,
-                            const int32_t* k_len, const void* q, int32_t ldq,
+                            const int32_t* k_len, const int32_t* k2_start,
+                            const int32_t* k2_len, const void* q, int32_t ldq,
                             const void* k, int32_t ldk, const void* v,
                             int32_t ldv, void* o, int32_t ldo, void* stream);
 

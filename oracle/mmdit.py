@@ -17,7 +17,11 @@ paper leaves open:
   row, the last d/2 by its column; within a half, dimensions ``(2j, 2j+1)``,
   ``j < d/4``, rotate by ``pos * 10000^(-j/(d/4))``:
   ``(a, b) -> (a cos - b sin, a sin + b cos)``; text tokens are not rotated;
-* the final layer acts on the image stream only.
+* the final layer acts on the image stream only;
+* classifier-free guidance runs the unconditional branch with an all-zero
+  prompt, whose text stream then evolves through the blocks like any other;
+* the step-skip signal is block 0's first modulated input of the image
+  stream, and the cached residual is that of the image stream.
 """
 from __future__ import annotations
 
@@ -118,22 +122,82 @@ def joint_block(W, w, b, x_txt, x_img, c, rows, cols):
     return new["txt"], new["img"]
 
 
+def joint_block_rows(W, w, b, x_txt, x_img, c, rows, cols, sel_txt, sel_img):
+    """:func:`joint_block` evaluated for the selected output rows only.
+
+    Keys and values come from every row of both streams; queries, the output
+    projection and the MLP from the selected rows (``sel_txt`` index text
+    rows, ``sel_img`` image rows).  Returns the selected rows' new values."""
+    D, H = w.hidden, w.heads
+    xs = {"txt": x_txt, "img": x_img}
+    sel = {"txt": np.asarray(sel_txt, dtype=int), "img": np.asarray(sel_img, dtype=int)}
+    mods, q, k, v = {}, {}, {}, {}
+    for s in STREAMS:
+        p = f"blocks.{b}.{s}."
+        mods[s] = stream_modulation(W, w, c, b, s)
+        h = modulate(layer_norm(xs[s], w.ln_eps), mods[s]["shift_msa"], mods[s]["scale_msa"])
+        wq, bq = W[p + "qkv.w"], W[p + "qkv.b"]
+        q[s] = linear(h[sel[s]], wq[:D], bq[:D])
+        k[s] = linear(h, wq[D:2 * D], bq[D:2 * D])
+        v[s] = linear(h, wq[2 * D:], bq[2 * D:])
+    rows, cols = np.asarray(rows), np.asarray(cols)
+    q["img"] = rope_2d(q["img"], rows[sel["img"]], cols[sel["img"]], H)
+    k["img"] = rope_2d(k["img"], rows, cols, H)
+    o = attention(np.concatenate([q["txt"], q["img"]]),
+                  np.concatenate([k["txt"], k["img"]]),
+                  np.concatenate([v["txt"], v["img"]]), H)
+    ns = len(sel["txt"])
+    outs = {"txt": o[:ns], "img": o[ns:]}
+    new = {}
+    for s in STREAMS:
+        p = f"blocks.{b}.{s}."
+        md = mods[s]
+        x = xs[s][sel[s]] + md["gate_msa"] * linear(outs[s], W[p + "o.w"], W[p + "o.b"])
+        h = modulate(layer_norm(x, w.ln_eps), md["shift_mlp"], md["scale_mlp"])
+        u = gelu_tanh(linear(h, W[p + "fc1.w"], W[p + "fc1.b"]))
+        new[s] = x + md["gate_mlp"] * linear(u, W[p + "fc2.w"], W[p + "fc2.b"])
+    return new["txt"], new["img"]
+
+
+def embed_image(W, w, lat):
+    return linear(patchify(np.asarray(lat, dtype=F64), w.patch), W["x_embed.w"], W["x_embed.b"])
+
+
+def embed_text(W, w, text):
+    """Initial text stream; ``None`` is the unconditional (all-zero) prompt."""
+    if text is None:
+        text = np.zeros((w.text_tokens, w.text_dim))
+    return linear(np.asarray(text, dtype=F64), W["y_embed.w"], W["y_embed.b"])
+
+
 def embed(W, w, lat, text):
-    x_img = linear(patchify(np.asarray(lat, dtype=F64), w.patch),
-                   W["x_embed.w"], W["x_embed.b"])
-    x_txt = linear(np.asarray(text, dtype=F64), W["y_embed.w"], W["y_embed.b"])
+    return embed_text(W, w, text), embed_image(W, w, lat)
+
+
+def run_blocks(W, w, x_txt, x_img, c, lat_hw, b0, b1):
+    """Joint blocks ``b0 .. b1-1`` for a latent of spatial size ``lat_hw``."""
+    rows, cols = grid_positions(lat_hw[0] // w.patch, lat_hw[1] // w.patch)
+    for b in range(b0, b1):
+        x_txt, x_img = joint_block(W, w, b, x_txt, x_img, c, rows, cols)
     return x_txt, x_img
 
 
+def cache_signal(W, w, lat, t):
+    """Block 0's first modulated input of the image stream ``[N, D]`` (the
+    quantity the step-skip rule compares between steps)."""
+    c = conditioning(W, w, t)
+    md = stream_modulation(W, w, c, 0, "img")
+    return modulate(layer_norm(embed_image(W, w, lat), w.ln_eps),
+                    md["shift_msa"], md["scale_msa"])
+
+
 def forward(W, w, lat, t, text, n_blocks=None):
-    """Returns ``(v, x_txt, x_img)``; ``v`` is None unless all blocks ran."""
+    """Returns ``(v, x_txt, x_img)``; ``v`` is None unless all blocks ran.
+    ``text`` None is the unconditional prompt."""
     C, h, ww = lat.shape
-    gh, gw = h // w.patch, ww // w.patch
-    rows, cols = grid_positions(gh, gw)
     c = conditioning(W, w, t)
     x_txt, x_img = embed(W, w, lat, text)
     nb = w.depth if n_blocks is None else n_blocks
-    for b in range(nb):
-        x_txt, x_img = joint_block(W, w, b, x_txt, x_img, c, rows, cols)
+    x_txt, x_img = run_blocks(W, w, x_txt, x_img, c, (h, ww), 0, nb)
     v = final_layer(W, w, x_img, c, h, ww) if nb == w.depth else None
     return v, x_txt, x_img

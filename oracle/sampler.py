@@ -28,7 +28,7 @@ from typing import List, Optional, Sequence
 
 import numpy as np
 
-from . import dit
+from . import dit, mmdit
 
 F64 = np.float64
 
@@ -104,8 +104,10 @@ def model_velocity(W, w, lat, t, text, guidance, state: CacheState = None,
     Returns ``(v, v_branches)`` where ``v_branches`` lists the conditional and,
     under guidance, the unconditional velocity."""
     C, h, ww = lat.shape
+    mm = getattr(w, "arch", "cross") == "mmdit"
     c = dit.conditioning(W, w, t)
-    x0 = dit.embed(W, w, lat)
+    x0 = mmdit.embed_image(W, w, lat) if mm else dit.embed(W, w, lat)
+    nb = w.depth if n_blocks is None else n_blocks
     branches = [text] if guidance == 1.0 else [text, None]
     vs, resid = [], []
     for bi, txt in enumerate(branches):
@@ -114,9 +116,11 @@ def model_velocity(W, w, lat, t, text, guidance, state: CacheState = None,
         if skip:
             xl = x0 + state.residual[bi]
         else:
-            y = dit.text_project(W, w, txt)
-            xl = dit.run_blocks(W, w, x0, y, c, 0,
-                                w.depth if n_blocks is None else n_blocks)
+            if mm:   # joint blocks; the residual is the image stream's
+                _, xl = mmdit.run_blocks(W, w, mmdit.embed_text(W, w, txt), x0, c, (h, ww), 0, nb)
+            else:
+                y = dit.text_project(W, w, txt)
+                xl = dit.run_blocks(W, w, x0, y, c, 0, nb)
             resid.append(xl - x0)
         vs.append(dit.final_layer(W, w, xl, c, h, ww))
     if state is not None and not skip:
@@ -136,7 +140,8 @@ def step(W, w, lats, texts, ts, t_nexts, guidance=1.0, states=None, k=0,
         st = None if states is None else states[r]
         skip, d = False, float("nan")
         if st is not None:
-            m = dit.cache_signal(W, w, lat, ts[r])
+            sig = mmdit.cache_signal if getattr(w, "arch", "cross") == "mmdit" else dit.cache_signal
+            m = sig(W, w, lat, ts[r])
             skip, d = cache_decide(st, m, k, n_steps, tau, mode)
         v, vb = model_velocity(W, w, lat, ts[r], texts[r], guidance, st, skip)
         new.append(euler_update(lat, v, ts[r], t_nexts[r]))

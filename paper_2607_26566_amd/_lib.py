@@ -83,8 +83,8 @@ SIGNATURES = {
     "t2i_op_linear": (i32, [i32, i32, i32, i32, i32, vp, i32, vp, i32, vp, vp, i32, vp, i32,
                             vp, vp, vp]),
     "t2i_op_attention": (i32, [i32, i32, i32, i32, C.POINTER(i32), C.POINTER(i32),
-                               C.POINTER(i32), C.POINTER(i32), vp, i32, vp, i32, vp, i32, vp,
-                               i32, vp]),
+                               C.POINTER(i32), C.POINTER(i32), C.POINTER(i32), C.POINTER(i32),
+                               vp, i32, vp, i32, vp, i32, vp, i32, vp]),
     "t2i_op_ln_modulate": (i32, [i32, i32, i32, vp, vp, vp, f32, vp, vp]),
     "t2i_ops_last_error": (C.c_char_p, []),
 }

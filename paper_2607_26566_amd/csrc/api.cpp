@@ -4,6 +4,7 @@
 // produced by the kernels in gemm.hip, attention.hip and pointwise.hip.
 #include <hip/hip_runtime.h>
 
+#include <algorithm>
 #include <cmath>
 #include <cstdio>
 #include <cstring>
@@ -136,7 +137,7 @@ const char* check_config(const t2i_dit_config* c) {
 // workspace layout
 
 struct Layout {
-  size_t x, x0, h, xb, qkv, vt, o, u, ytxt, kv, vtt, tfreq, th1, tsc, mod, partial, total;
+  size_t x, x0, h, xb, qkv, vt, o, u, ytxt, kv, vtt, rope, tfreq, th1, tsc, mod, partial, total;
   int ldvt = 0, ldvt_txt = 0;   // token strides of the transposed V buffers
 };
 
@@ -144,9 +145,12 @@ Layout layout(const t2i_dit_config& c) {
   Layout L{};
   const size_t A = c.dtype == T2I_BF16 ? 2 : 4;
   const size_t D = c.hidden, F = c.mlp_hidden;
-  const size_t txt_rows = (size_t)(c.max_requests + 1) * c.text_tokens;
+  const bool mm = c.arch == T2I_ARCH_MMDIT;
+  // cross-DiT: the prompts plus one shared unconditional prompt; MMDiT: a
+  // text stream per request and guidance branch
+  const size_t txt_rows = (size_t)(mm ? 2 * c.max_requests : c.max_requests + 1) * c.text_tokens;
   size_t rows = c.max_tokens;
-  if (c.arch == T2I_ARCH_MMDIT) rows += (size_t)c.max_requests * c.text_tokens;
+  if (mm) rows += txt_rows;   // residual rows: text stream, then image stream
   const size_t Tt = (size_t)c.max_steps * c.max_requests;
   size_t off = 0;
   auto take = [&](size_t bytes) {
@@ -166,9 +170,10 @@ Layout layout(const t2i_dit_config& c) {
   L.vt = take(bfv ? D * (size_t)L.ldvt * 2 : 0);
   L.o = take(rows * D * A);
   L.u = take(rows * F * A);
-  L.ytxt = take(txt_rows * D * A);
+  L.ytxt = take(txt_rows * D * (mm ? 4 : A));   // MMDiT keeps the projected text in fp32
   L.kv = take(c.arch == T2I_ARCH_CROSS_DIT ? (size_t)c.depth * txt_rows * 2 * D * A : 0);
   L.vtt = take(c.arch == T2I_ARCH_CROSS_DIT && bfv ? (size_t)c.depth * D * L.ldvt_txt * 2 : 0);
+  L.rope = take(mm ? (size_t)(4096 / c.patch) * (c.head_dim / 4) * sizeof(float2) : 0);
   L.tfreq = take(Tt * c.freq_dim * 4);
   L.th1 = take(Tt * D * 4);
   L.tsc = take(Tt * D * 4);
@@ -228,7 +233,11 @@ struct Plan {
   float guidance = 1.f;
   ReqMap rm{};
   SeqMap img{};      // image rows (branch-major) -> sequence -> modulation row
+  SeqMap txt{};      // MMDiT text-stream rows (branch-major), same sequences
   AttnMap self{}, cross{};
+  AttnMap joint{};   // MMDiT: per sequence a text and an image query group,
+                     // keys = the sequence's text rows, then its image rows
+  int rope_pos = 0;  // largest grid side (MMDiT RoPE table length)
   size_t lat_floats = 0;
 };
 
@@ -292,13 +301,47 @@ t2i_status build_plan(t2i_dit* h, int n_req, const int32_t* lat_h, const int32_t
     }
   P.img.start[P.img.n] = P.rows;
   P.self.tile_start[P.self.n] = P.cross.tile_start[P.cross.n] = tiles;
+  if (c.arch == T2I_ARCH_MMDIT) {
+    // residual rows are stream-major: text rows [0, txt_rows) with sequence s
+    // at s*M, then the image rows (offset txt_rows) in the cross-DiT order
+    if (2 * P.img.n > kMaxSeq) return fail(h, T2I_ERR_SHAPE, "too many sequences for MMDiT");
+    P.txt_rows = P.img.n * M;
+    P.txt.n = P.img.n;
+    int jt = 0;
+    for (int s = 0; s < P.img.n; ++s) {
+      P.txt.start[s] = s * M;
+      P.txt.modrow[s] = s % n_req;
+      const int ist = P.txt_rows + P.img.start[s], ilen = P.img.start[s + 1] - P.img.start[s];
+      for (int g = 0; g < 2; ++g) {
+        const int q = 2 * s + g;
+        P.joint.q_start[q] = g ? ist : s * M;
+        P.joint.q_len[q] = g ? ilen : M;
+        P.joint.k_start[q] = s * M;
+        P.joint.k_len[q] = M;
+        P.joint.k2_start[q] = ist;
+        P.joint.k2_len[q] = ilen;
+        P.joint.tile_start[q] = jt;
+        jt += (P.joint.q_len[q] + BQ - 1) / BQ;
+      }
+    }
+    P.txt.start[P.txt.n] = P.txt_rows;
+    P.joint.n = 2 * P.img.n;
+    P.joint.tile_start[P.joint.n] = jt;
+    for (int r = 0; r < n_req; ++r)
+      P.rope_pos = std::max(P.rope_pos, std::max(lat_h[r], lat_w[r]) / c.patch);
+  }
   return T2I_OK;
 }
 
 void set_modrows(Plan& P, int base) {
   for (int r = 0; r < P.n_req; ++r) P.rm.modrow[r] = base + r;
   for (int s = 0; s < P.img.n; ++s) P.img.modrow[s] = base + (s % P.n_req);
+  for (int s = 0; s < P.txt.n; ++s) P.txt.modrow[s] = base + (s % P.n_req);
 }
+
+bool is_mmdit(const t2i_dit* h) { return h->cfg.arch == T2I_ARCH_MMDIT; }
+// first residual row of the image stream
+int img_row0(const t2i_dit* h, const Plan& P) { return is_mmdit(h) ? P.txt_rows : 0; }
 
 Epi make_epi() {
   Epi e;
@@ -365,6 +408,17 @@ t2i_status text_prep(t2i_dit* h, const Plan& P, const void* prompt, hipStream_t 
   Epi e = make_epi();
   e.out = ytxt;
   e.ldo = D;
+  if (is_mmdit(h)) {
+    // fp32 initial text stream of every sequence (unconditional: the bias),
+    // copied into the residual at the start of each step; RoPE table
+    HIP_TRY(h, linear(h, prompt, c.text_dim, W_Y, P.n_req * M, D, c.text_dim, EPI_STORE_F32, e,
+                      st));
+    if (P.branches == 2)
+      HIP_TRY(h, launch_bias_rows_f32(h->w[B_Y], h->bf(), P.n_req * M, D,
+                                      (float*)ytxt + (size_t)P.n_req * M * D, st));
+    HIP_TRY(h, launch_rope_table(h->at<float2>(h->L.rope), P.rope_pos, c.head_dim / 4, st));
+    return T2I_OK;
+  }
   HIP_TRY(h, linear(h, prompt, c.text_dim, W_Y, P.n_req * M, D, c.text_dim, EPI_STORE, e, st));
   if (P.branches == 2)
     HIP_TRY(h, launch_broadcast_rows(h->w[B_Y], h->bf(), M, D,
@@ -494,9 +548,73 @@ t2i_status run_blocks_cross(t2i_dit* h, const Plan& P, int nb, hipStream_t st) {
   return T2I_OK;
 }
 
+// MMDiT joint blocks [0, nb): per stream (text rows, then image rows of the
+// residual) LN-modulate and projections with that stream's weights and
+// modulation; RoPE on the image q, k; one joint attention over both.
+t2i_status run_blocks_mmdit(t2i_dit* h, const Plan& P, int nb, hipStream_t st) {
+  const t2i_dit_config& c = h->cfg;
+  const int D = c.hidden, F = c.mlp_hidden, mw = mod_width(c);
+  float* x = h->at<float>(h->L.x);
+  bf16* hb = h->at<bf16>(h->L.h);
+  bf16* qkv = h->at<bf16>(h->L.qkv);
+  bf16* o = h->at<bf16>(h->L.o);
+  bf16* u = h->at<bf16>(h->L.u);
+  bf16* vt = h->at<bf16>(h->L.vt);
+  const float* mod = h->at<float>(h->L.mod);
+  const float2* rope = h->at<float2>(h->L.rope);
+  const int r0s[2] = {0, P.txt_rows}, ns[2] = {P.txt_rows, P.rows};
+  const SeqMap* maps[2] = {&P.txt, &P.img};
+  for (int b = 0; b < nb; ++b) {
+    for (int s = 0; s < 2; ++s) {
+      const int r0 = r0s[s], R = ns[s], wi = W_BLOCK0 + b * 2 * J_PER_STREAM + s * J_PER_STREAM;
+      const int mo = b * 12 * D + s * 6 * D;
+      TIMED(h, T2I_K_LN, st, launch_ln_modulate(true, R, D, x + (size_t)r0 * D, D, mod, mw, mo,
+                                                 mo + D, *maps[s], hb + (size_t)r0 * D, D,
+                                                 c.ln_eps, st));
+      Epi e = make_epi();   // q|k row-major [rows, 2D], v transposed [D][ldvt]
+      e.out = qkv + (size_t)r0 * 2 * D;
+      e.ldo = 2 * D;
+      e.vt = vt + r0;
+      e.ldvt = h->L.ldvt;
+      e.vcol0 = 2 * D;
+      TIMED(h, T2I_K_GEMM_QKV, st,
+            linear(h, hb + (size_t)r0 * D, D, wi + J_QKV, R, 3 * D, D, EPI_SPLIT_VT, e, st));
+    }
+    HIP_TRY(h, launch_rope_apply(qkv, 2 * D, P.txt_rows, P.rm, c.heads, c.head_dim, c.patch, rope,
+                                 st));
+    TIMED(h, T2I_K_ATTN_SELF, st,
+          launch_attention(true, c.heads, c.head_dim, P.joint, qkv, 2 * D, qkv + D, 2 * D, vt,
+                           h->L.ldvt, o, D, st));
+    for (int s = 0; s < 2; ++s) {
+      const int r0 = r0s[s], R = ns[s], wi = W_BLOCK0 + b * 2 * J_PER_STREAM + s * J_PER_STREAM;
+      const int mo = b * 12 * D + s * 6 * D;
+      Epi e = make_epi();
+      e.x = x + (size_t)r0 * D;
+      e.ldx = D;
+      e.gate = mod + mo + 2 * D;
+      e.ld_gate = mw;
+      e.map = *maps[s];
+      TIMED(h, T2I_K_GEMM_O, st,
+            linear(h, o + (size_t)r0 * D, D, wi + J_O, R, D, D, EPI_RESID_GATED, e, st));
+      TIMED(h, T2I_K_LN, st, launch_ln_modulate(true, R, D, x + (size_t)r0 * D, D, mod, mw,
+                                                 mo + 3 * D, mo + 4 * D, *maps[s],
+                                                 hb + (size_t)r0 * D, D, c.ln_eps, st));
+      Epi f = make_epi();
+      f.out = u + (size_t)r0 * F;
+      f.ldo = F;
+      TIMED(h, T2I_K_GEMM_FC1, st,
+            linear(h, hb + (size_t)r0 * D, D, wi + J_FC1, R, F, D, EPI_GELU, f, st));
+      e.gate = mod + mo + 5 * D;
+      TIMED(h, T2I_K_GEMM_FC2, st,
+            linear(h, u + (size_t)r0 * F, F, wi + J_FC2, R, D, F, EPI_RESID_GATED, e, st));
+    }
+  }
+  return T2I_OK;
+}
+
 t2i_status run_blocks(t2i_dit* h, const Plan& P, int nb, hipStream_t st) {
   if (h->cfg.arch == T2I_ARCH_CROSS_DIT) return run_blocks_cross(h, P, nb, st);
-  return fail(h, T2I_ERR_UNSUPPORTED, "MMDiT blocks are not built yet");
+  return run_blocks_mmdit(h, P, nb, st);
 }
 
 size_t cache_bytes(const t2i_dit_config& c, int n_req, int tokens, int branches) {
@@ -525,9 +643,11 @@ t2i_status cache_check_impl(t2i_dit* h, const Plan& P, int step, int n_steps, do
   const t2i_dit_config& c = h->cfg;
   CachePtrs cp = cache_ptrs(c, state, P.n_req, P.T_img);
   double* partial = h->at<double>(h->L.partial);
+  // block 0's first LN-modulation (MMDiT: of the image stream)
+  const int sh = is_mmdit(h) ? 6 * c.hidden : 0;
   HIP_TRY(h, launch_cache_signal(h->at<float>(h->L.x0), P.rm, h->at<float>(h->L.mod),
-                                 mod_width(c), 0, c.hidden, c.hidden, c.ln_eps, cp.m_prev, cp.hdr,
-                                 step, partial, st));
+                                 mod_width(c), sh, sh + c.hidden, c.hidden, c.ln_eps, cp.m_prev,
+                                 cp.hdr, step, partial, st));
   HIP_TRY(h, launch_cache_decide(P.rm, partial, cp.hdr, step, n_steps, tau, mode, st));
   h->hdr_host.resize(P.n_req);
   HIP_TRY(h, hipMemcpyAsync(h->hdr_host.data(), cp.hdr, sizeof(CacheHeader) * P.n_req,
@@ -550,8 +670,12 @@ t2i_status step_body(t2i_dit* h, Plan& P, const float* latents_in, float* latent
   float* x = h->at<float>(h->L.x);
   float* x0 = h->at<float>(h->L.x0);
   const bool pe = c.arch == T2I_ARCH_CROSS_DIT;
+  float* xi = x + (size_t)img_row0(h, P) * D;   // image stream of the residual
   HIP_TRY(h, launch_embed(latents_in, P.rm, h->w[W_PE], h->w[B_PE], h->bf(), D,
-                          c.latent_channels, c.patch, pe, x0, x, P.branches, st));
+                          c.latent_channels, c.patch, pe, x0, xi, P.branches, st));
+  if (is_mmdit(h))
+    HIP_TRY(h, hipMemcpyAsync(x, h->at<float>(h->L.ytxt), (size_t)P.txt_rows * D * 4,
+                              hipMemcpyDeviceToDevice, st));
   uint32_t skip_mask = 0, compute_mask = 0;
   for (int r = 0; r < P.n_req; ++r) {
     if (skip && skip[r]) skip_mask |= 1u << r;
@@ -563,15 +687,19 @@ t2i_status step_body(t2i_dit* h, Plan& P, const float* latents_in, float* latent
   }
   if (cache_state) {
     CachePtrs cp = cache_ptrs(c, cache_state, P.n_req, P.T_img);
-    if (skip_mask) HIP_TRY(h, launch_apply_residual(x0, cp.R, x, P.rm, skip_mask, D, st));
+    if (skip_mask) HIP_TRY(h, launch_apply_residual(x0, cp.R, xi, P.rm, skip_mask, D, st));
     if (compute_mask)
-      HIP_TRY(h, launch_store_residual(x0, x, cp.R, P.rm, compute_mask, D, cp.hdr, st));
+      HIP_TRY(h, launch_store_residual(x0, xi, cp.R, P.rm, compute_mask, D, cp.hdr, st));
   }
-  if (hidden_out)
-    HIP_TRY(h, hipMemcpyAsync(hidden_out, x, (size_t)P.rows * D * 4, hipMemcpyDeviceToDevice, st));
+  if (hidden_out) {
+    HIP_TRY(h, hipMemcpyAsync(hidden_out, xi, (size_t)P.rows * D * 4, hipMemcpyDeviceToDevice, st));
+    if (is_mmdit(h))
+      HIP_TRY(h, hipMemcpyAsync(hidden_out + (size_t)P.rows * D, x, (size_t)P.txt_rows * D * 4,
+                                hipMemcpyDeviceToDevice, st));
+  }
   const int mw = mod_width(c);
   const int fb = final_base(c);
-  HIP_TRY(h, launch_final_layer(x, P.rm, h->w[fb + 2], h->w[fb + 3], h->bf(), h->at<float>(h->L.mod),
+  HIP_TRY(h, launch_final_layer(xi, P.rm, h->w[fb + 2], h->w[fb + 3], h->bf(), h->at<float>(h->L.mod),
                                 mw, mw - 2 * D, mw - D, D, c.latent_channels, c.patch, c.ln_eps,
                                 P.guidance, latents, noise_pred, st));
   return T2I_OK;
@@ -723,7 +851,7 @@ t2i_status t2i_dit_step(t2i_dit* h, const t2i_step_args* a, void* stream) {
   }
   hipStream_t st = (hipStream_t)stream;
   set_modrows(P, 0);
-  if ((s = conditioning(h, a->t, P.n_req, c.depth, st)) != T2I_OK) return s;
+  if ((s = conditioning(h, a->t, P.n_req, std::max(nb, 1), st)) != T2I_OK) return s;
   if ((s = text_prep(h, P, a->prompt_embeds, st)) != T2I_OK) return s;
   return step_body(h, P, a->latents, a->latents, a->noise_pred, nb, a->hidden_out, a->skip,
                    a->cache_state, st);
@@ -860,9 +988,9 @@ t2i_status t2i_op_linear(int32_t dtype, int32_t epilogue, int32_t M, int32_t N, 
 
 t2i_status t2i_op_attention(int32_t dtype, int32_t heads, int32_t head_dim, int32_t n_seq,
                             const int32_t* q_start, const int32_t* q_len, const int32_t* k_start,
-                            const int32_t* k_len, const void* q, int32_t ldq, const void* k,
-                            int32_t ldk, const void* v, int32_t ldv, void* o, int32_t ldo,
-                            void* stream) {
+                            const int32_t* k_len, const int32_t* k2_start, const int32_t* k2_len,
+                            const void* q, int32_t ldq, const void* k, int32_t ldk, const void* v,
+                            int32_t ldv, void* o, int32_t ldo, void* stream) {
   if (dtype != T2I_F32 && dtype != T2I_BF16) return ops_fail(T2I_ERR_INVALID_ARG, "bad dtype");
   if (heads < 1 || (head_dim != 8 && head_dim != 32 && head_dim != 64 && head_dim != 72 &&
                     head_dim != 128))
@@ -870,24 +998,30 @@ t2i_status t2i_op_attention(int32_t dtype, int32_t heads, int32_t head_dim, int3
   if (n_seq < 1 || n_seq > kMaxSeq) return ops_fail(T2I_ERR_SHAPE, "bad n_seq");
   if (!q_start || !q_len || !k_start || !k_len || !q || !k || !v || !o)
     return ops_fail(T2I_ERR_INVALID_ARG, "NULL pointer");
+  if (!k2_start != !k2_len) return ops_fail(T2I_ERR_INVALID_ARG, "k2_start and k2_len go together");
   const int w = heads * head_dim;
   if (ldq < w || ldk < w || ldo < w || ldq % 8 || ldk % 8 || ldv % 8 || ldo % 8 ||
       (dtype == T2I_F32 && ldv < w))
     return ops_fail(T2I_ERR_SHAPE, "bad leading dimension");
   AttnMap m;
-  std::memset(&m, 0, sizeof(m));
+  std::memset(&m, 0, sizeof(m));   // no second key segment
   m.n = n_seq;
   const int BQ = attention_query_tile(dtype == T2I_BF16, head_dim);
   int tiles = 0;
   for (int s = 0; s < n_seq; ++s) {
-    if (q_start[s] < 0 || q_len[s] < 0 || k_start[s] < 0 || k_len[s] < 1)
+    const int s2 = k2_start ? k2_start[s] : 0, n2 = k2_len ? k2_len[s] : 0;
+    if (q_start[s] < 0 || q_len[s] < 0 || k_start[s] < 0 || k_len[s] < 0 || s2 < 0 || n2 < 0 ||
+        k_len[s] + n2 < 1)
       return ops_fail(T2I_ERR_SHAPE, "bad sequence bounds");
-    if (dtype == T2I_BF16 && (k_start[s] % 8 || (long)k_start[s] + k_len[s] > ldv))
-      return ops_fail(T2I_ERR_SHAPE, "bf16 attention needs k_start % 8 == 0 and keys within ldv");
+    if (dtype == T2I_BF16 && (k_start[s] % 8 || (long)k_start[s] + k_len[s] > ldv || s2 % 8 ||
+                              (long)s2 + n2 > ldv))
+      return ops_fail(T2I_ERR_SHAPE, "bf16 attention needs key starts % 8 == 0 and keys within ldv");
     m.q_start[s] = q_start[s];
     m.q_len[s] = q_len[s];
     m.k_start[s] = k_start[s];
     m.k_len[s] = k_len[s];
+    m.k2_start[s] = s2;
+    m.k2_len[s] = n2;
     m.tile_start[s] = tiles;
     tiles += (q_len[s] + BQ - 1) / BQ;
   }

@@ -83,7 +83,19 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(AttnMap map, int head
   int h, s, j;
   decode_tile(map, heads, xcd_remap_attn(blockIdx.x, gridDim.x), h, s, j);
   const int q_beg = map.q_start[s], q_end = q_beg + map.q_len[s];
-  const int k_beg = map.k_start[s], k_end = k_beg + map.k_len[s];
+  // key tiles: those of segment 1, then those of segment 2
+  const int k1 = map.k_start[s], n1 = map.k_len[s];
+  const int k2 = map.k2_start[s], n2 = map.k2_len[s];
+  const int t1 = (n1 + BKV - 1) / BKV, nt = t1 + (n2 + BKV - 1) / BKV;
+  auto tile_keys = [&](int ti, int& kv0, int& kend) {
+    if (ti < t1) {
+      kv0 = k1 + ti * BKV;
+      kend = k1 + n1;
+    } else {
+      kv0 = k2 + (ti - t1) * BKV;
+      kend = k2 + n2;
+    }
+  };
   const int qrow0 = q_beg + j * BQ + wave * (QT * 16);
   const int g = lane >> 4, fr = lane & 15;
 
@@ -98,7 +110,7 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(AttnMap map, int head
   int kblk[KBPW];
 #pragma unroll
   for (int i = 0; i < KBPW; ++i) kblk[i] = min(wave + 4 * i, CPR - 1);
-  auto kload = [&](int kv0, int buf) {
+  auto kload = [&](int kv0, int k_end, int buf) {
     const int gk = min(kv0 + lane, k_end - 1);
     const bf16* src = K + (size_t)gk * ldk + h * HD;
 #pragma unroll
@@ -109,7 +121,7 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(AttnMap map, int head
   };
 
   bf16x8 vr[VPT];
-  auto gload = [&](int kv0) {
+  auto gload = [&](int kv0, int k_end) {
 #pragma unroll
     for (int i = 0; i < VPT; ++i) {
       const int c = tid + 256 * i;
@@ -127,7 +139,7 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(AttnMap map, int head
       }
     }
   };
-  auto sstore = [&](int buf, int kv0) {
+  auto sstore = [&](int buf, int kv0, int k_end) {
 #pragma unroll
     for (int i = 0; i < VPT; ++i) {
       const int c = tid + 256 * i;
@@ -174,16 +186,23 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(AttnMap map, int head
   for (int c = 0; c < DC; ++c) koff[c] = min(4 * c + g, CPR) * 512 + fr * 8;
 
   __syncthreads();          // zero-fill done before the first tile lands
-  kload(k_beg, 0);
-  gload(k_beg);
-  sstore(0, k_beg);
+  {
+    int kv0, kend;
+    tile_keys(0, kv0, kend);
+    kload(kv0, kend, 0);
+    gload(kv0, kend);
+    sstore(0, kv0, kend);
+  }
   __syncthreads();          // (waits for the K loads too)
   int buf = 0;
-  for (int kv0 = k_beg; kv0 < k_end; kv0 += BKV) {
-    const bool next = kv0 + BKV < k_end;
+  for (int ti = 0; ti < nt; ++ti) {
+    int kv0, k_end, nkv0 = 0, nkend = 0;
+    tile_keys(ti, kv0, k_end);
+    const bool next = ti + 1 < nt;
     if (next) {
-      kload(kv0 + BKV, buf ^ 1);
-      gload(kv0 + BKV);
+      tile_keys(ti + 1, nkv0, nkend);
+      kload(nkv0, nkend, buf ^ 1);
+      gload(nkv0, nkend);
     }
     const bool ragged = kv0 + BKV > k_end;
     const bf16* Kb = Ks[buf];
@@ -256,7 +275,7 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(AttnMap map, int head
         }
       }
     }
-    if (next) sstore(buf ^ 1, kv0 + BKV);
+    if (next) sstore(buf ^ 1, nkv0, nkend);
     __syncthreads();
     buf ^= 1;
   }
@@ -304,7 +323,6 @@ __global__ __launch_bounds__(64) void attn_f32_kernel(AttnMap map, int heads,
   int h, s, j;
   decode_tile(map, heads, blockIdx.x, h, s, j);
   const int q_beg = map.q_start[s], q_end = q_beg + map.q_len[s];
-  const int k_beg = map.k_start[s], k_end = k_beg + map.k_len[s];
   const int qr = q_beg + j * BQ + threadIdx.x;
   const bool active = qr < q_end;
   float q[HD], acc[HD];
@@ -314,27 +332,31 @@ __global__ __launch_bounds__(64) void attn_f32_kernel(AttnMap map, int heads,
     acc[d] = 0.f;
   }
   float m = -INFINITY, l = 0.f;
-  for (int kv0 = k_beg; kv0 < k_end; kv0 += BKV) {
-    __syncthreads();
-    for (int i = threadIdx.x; i < BKV * HD; i += 64) {
-      const int key = i / HD, d = i - key * HD, gk = kv0 + key;
-      Ks[key][d] = gk < k_end ? K[(size_t)gk * ldk + h * HD + d] : 0.f;
-      Vs[key][d] = gk < k_end ? V[(size_t)gk * ldv + h * HD + d] : 0.f;
-    }
-    __syncthreads();
-    const int nk = min(BKV, k_end - kv0);
-    for (int key = 0; key < nk; ++key) {
-      float sdot = 0.f;
+  for (int seg = 0; seg < 2; ++seg) {
+    const int k_beg = seg ? map.k2_start[s] : map.k_start[s];
+    const int k_end = k_beg + (seg ? map.k2_len[s] : map.k_len[s]);
+    for (int kv0 = k_beg; kv0 < k_end; kv0 += BKV) {
+      __syncthreads();
+      for (int i = threadIdx.x; i < BKV * HD; i += 64) {
+        const int key = i / HD, d = i - key * HD, gk = kv0 + key;
+        Ks[key][d] = gk < k_end ? K[(size_t)gk * ldk + h * HD + d] : 0.f;
+        Vs[key][d] = gk < k_end ? V[(size_t)gk * ldv + h * HD + d] : 0.f;
+      }
+      __syncthreads();
+      const int nk = min(BKV, k_end - kv0);
+      for (int key = 0; key < nk; ++key) {
+        float sdot = 0.f;
 #pragma unroll
-      for (int d = 0; d < HD; ++d) sdot = fmaf(q[d], Ks[key][d], sdot);
-      sdot *= scale;
-      const float m_new = fmaxf(m, sdot);
-      const float corr = expf(m - m_new);
-      const float p = expf(sdot - m_new);
-      l = l * corr + p;
+        for (int d = 0; d < HD; ++d) sdot = fmaf(q[d], Ks[key][d], sdot);
+        sdot *= scale;
+        const float m_new = fmaxf(m, sdot);
+        const float corr = expf(m - m_new);
+        const float p = expf(sdot - m_new);
+        l = l * corr + p;
 #pragma unroll
-      for (int d = 0; d < HD; ++d) acc[d] = acc[d] * corr + p * Vs[key][d];
-      m = m_new;
+        for (int d = 0; d < HD; ++d) acc[d] = acc[d] * corr + p * Vs[key][d];
+        m = m_new;
+      }
     }
   }
   if (active) {

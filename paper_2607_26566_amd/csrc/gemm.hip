@@ -39,7 +39,9 @@ __device__ __forceinline__ int xcd_remap(int b, int nb) {
 // Epilogue on four consecutive columns nb..nb+3 of row m (vector path).
 template <int KIND>
 __device__ __forceinline__ void epi_store4(const Epi& e, int m, int nb, const float v[4]) {
-  if (KIND == EPI_STORE || KIND == EPI_GELU || KIND == EPI_SILU) {
+  if (KIND == EPI_STORE_F32) {
+    *(float4*)((float*)e.out + (size_t)m * e.ldo + nb) = float4{v[0], v[1], v[2], v[3]};
+  } else if (KIND == EPI_STORE || KIND == EPI_GELU || KIND == EPI_SILU) {
     bf16x4 w;
 #pragma unroll
     for (int r = 0; r < 4; ++r) {
@@ -228,6 +230,7 @@ static hipError_t gemm_bf16_dispatch(const bf16* A, int lda, const bf16* W, int 
     T2I_GEMM_CASE(EPI_RESID)
     T2I_GEMM_CASE(EPI_RESID_GATED)
     T2I_GEMM_CASE(EPI_SPLIT_VT)
+    T2I_GEMM_CASE(EPI_STORE_F32)
     default: return hipErrorInvalidValue;
   }
 #undef T2I_GEMM_CASE
@@ -239,14 +242,15 @@ hipError_t launch_gemm_bf16(const bf16* A, int lda, const bf16* W, int ldw, cons
   if (M <= 0 || N <= 0) return hipSuccess;
   auto al = [](const void* p, int a) { return ((uintptr_t)p % a) == 0; };
   const int vec_ok = (epi.ldo % 4 == 0) && (epi.ldx % 4 == 0) && (epi.ld_gate % 4 == 0) &&
-                     al(bias, 8) && al(epi.out, 8) && al(epi.x, 16) && al(epi.xb, 8) &&
-                     al(epi.gate, 16);
-  // Tile choice.  Large M: 256 x 144 tiles fed by direct HBM->LDS loads
+                     al(bias, 8) && al(epi.out, kind == EPI_STORE_F32 ? 16 : 8) &&
+                     al(epi.x, 16) && al(epi.xb, 8) && al(epi.gate, 16);
+  // Tile choice.  Large M: 256-row tiles fed by direct HBM->LDS loads
   // (gemm_dma.hip).  The DiT widths 1152, 2304, 3456 and 4608 are multiples of
   // 144, so at M = 8192 the layers launch 256 / 512 / 768 / 1024 tiles --
-  // whole rounds on 256 CUs at one workgroup each.  Otherwise 128 x 144 or
-  // 128 x 128 register-staged tiles (the faster ones at M ~ 1000 measured).
-  if (M >= 2048 && N % 144 == 0 && kind != EPI_SILU)
+  // whole rounds on 256 CUs at one workgroup each; widths that are multiples
+  // of 128 take 192- or 128-wide tiles.  Otherwise 128 x 144 or 128 x 128
+  // register-staged tiles (the faster ones at M ~ 1000 measured).
+  if (M >= 2048 && (N % 144 == 0 || N % 128 == 0) && kind != EPI_SILU)
     return launch_gemm_dma(A, lda, W, ldw, bias, M, N, K, kind, epi, vec_ok, st);
   if (N % 144 == 0)
     return gemm_bf16_dispatch<128, 144, 4>(A, lda, W, ldw, bias, M, N, K, kind, epi, vec_ok, st);

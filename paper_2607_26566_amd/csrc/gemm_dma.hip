@@ -53,7 +53,9 @@ __device__ __forceinline__ void block_barrier() {
 
 template <int KIND>
 __device__ __forceinline__ void dma_epi4(const Epi& e, int m, int nb, const float v[4]) {
-  if (KIND == EPI_STORE || KIND == EPI_GELU || KIND == EPI_SILU) {
+  if (KIND == EPI_STORE_F32) {
+    *(float4*)((float*)e.out + (size_t)m * e.ldo + nb) = float4{v[0], v[1], v[2], v[3]};
+  } else if (KIND == EPI_STORE || KIND == EPI_GELU || KIND == EPI_SILU) {
     bf16x4 w;
 #pragma unroll
     for (int r = 0; r < 4; ++r) {
@@ -237,6 +239,7 @@ hipError_t gemm_dma_dispatch(const bf16* A, int lda, const bf16* W, int ldw, con
     T2I_DMA_CASE(EPI_RESID)
     T2I_DMA_CASE(EPI_RESID_GATED)
     T2I_DMA_CASE(EPI_SPLIT_VT)
+    T2I_DMA_CASE(EPI_STORE_F32)
     default: return hipErrorInvalidValue;
   }
 #undef T2I_DMA_CASE
@@ -247,15 +250,21 @@ hipError_t gemm_dma_dispatch(const bf16* A, int lda, const bf16* W, int ldw, con
 // bounded by how many L1 misses a CU keeps in flight, so bytes per FLOP --
 // (BM + BN) / (BM BN) -- decide: 256 x 288 tiles (8 waves of 64 x 144) where
 // N is a multiple of 288 and leaves whole rounds of tiles (fc1: N = 4608 ->
-// 512 tiles), else 256 x 144 tiles (8 waves of 32 x 144, three stages).  Both
-// load with cache policy bit 0 (sc0) set, which measured faster.
+// 512 tiles), else 256 x 144 tiles (8 waves of 32 x 144, three stages).  The
+// widths of the 3072-wide joint-attention model (3072, 12288) take 256 x 192
+// tiles (8 waves of 64 x 96; 4096 rows -> 256 or 1024 tiles), else 256 x 128.
+// All load with cache policy bit 0 (sc0) set, which measured faster.
 hipError_t launch_gemm_dma(const bf16* A, int lda, const bf16* W, int ldw, const bf16* bias,
                            int M, int N, int K, int kind, const Epi& epi, int vec_ok,
                            hipStream_t st) {
-  const long tiles288 = (long)((M + 255) / 256) * (N / 288);
-  if (N % 288 == 0 && tiles288 % 256 == 0)
+  const long mt = (M + 255) / 256;
+  if (N % 288 == 0 && (mt * (N / 288)) % 256 == 0)
     return gemm_dma_dispatch<256, 288, 4, 2, 2, 1>(A, lda, W, ldw, bias, M, N, K, kind, epi, vec_ok, st);
-  return gemm_dma_dispatch<256, 144, 8, 1, 3, 1>(A, lda, W, ldw, bias, M, N, K, kind, epi, vec_ok, st);
+  if (N % 144 == 0)
+    return gemm_dma_dispatch<256, 144, 8, 1, 3, 1>(A, lda, W, ldw, bias, M, N, K, kind, epi, vec_ok, st);
+  if (N % 192 == 0 && (mt * (N / 192)) % 256 == 0)
+    return gemm_dma_dispatch<256, 192, 4, 2, 2, 1>(A, lda, W, ldw, bias, M, N, K, kind, epi, vec_ok, st);
+  return gemm_dma_dispatch<256, 128, 4, 2, 3, 1>(A, lda, W, ldw, bias, M, N, K, kind, epi, vec_ok, st);
 }
 
 }  // namespace t2i

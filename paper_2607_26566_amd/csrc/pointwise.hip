@@ -195,6 +195,84 @@ hipError_t launch_broadcast_rows(const void* src, bool bf16_io, int rows, int D,
 }
 
 // ---------------------------------------------------------------------------
+// 2D rotary position embedding of the image tokens (joint-attention model).
+
+__global__ void rope_table_kernel(float2* __restrict__ tab, int npos, int q) {
+  const int i = blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= npos * q) return;
+  const int pos = i / q, j = i - pos * q;
+  const double ang = (double)pos * pow(10000.0, -(double)j / (double)q);
+  tab[i] = float2{(float)cos(ang), (float)sin(ang)};
+}
+
+hipError_t launch_rope_table(float2* table, int npos, int q, hipStream_t st) {
+  const int n = npos * q;
+  if (n <= 0) return hipSuccess;
+  hipLaunchKernelGGL(rope_table_kernel, dim3((n + 255) / 256), dim3(256), 0, st, table, npos, q);
+  return hipGetLastError();
+}
+
+// one thread per (row, head, half, pair): rotates the q pair and the k pair
+__global__ void rope_apply_kernel(bf16* __restrict__ qk, int ld, int row0, ReqMap rm, int heads,
+                                  int hd, int patch, const float2* __restrict__ tab) {
+  const int q = hd / 4;
+  const long per_row = (long)heads * 2 * q;
+  const long total = (long)rm.tokens_total * rm.branches * per_row;
+  const int D = heads * hd;
+  for (long i = blockIdx.x * 256L + threadIdx.x; i < total; i += (long)gridDim.x * 256) {
+    const long row = i / per_row;
+    int rem = (int)(i - row * per_row);
+    const int h = rem / (2 * q);
+    rem -= h * 2 * q;
+    const int half = rem / q, j = rem - half * q;
+    const int tok = (int)(row % rm.tokens_total);
+    const int r = req_of_token(rm, tok);
+    const int lt = tok - rm.tok_off[r];
+    const int gw = rm.w[r] / patch;
+    const int pos = half ? lt % gw : lt / gw;
+    const float2 cs = tab[pos * q + j];
+    bf16* base = qk + (size_t)(row0 + row) * ld + h * hd + half * (hd / 2) + 2 * j;
+#pragma unroll
+    for (int part = 0; part < 2; ++part) {   // q, then k (D columns further)
+      bf16* pp = base + part * D;
+      const float a = (float)pp[0], b = (float)pp[1];
+      pp[0] = (bf16)(a * cs.x - b * cs.y);
+      pp[1] = (bf16)(a * cs.y + b * cs.x);
+    }
+  }
+}
+
+hipError_t launch_rope_apply(bf16* qk, int ld, int row0, const ReqMap& rm, int heads, int head_dim,
+                             int patch, const float2* table, hipStream_t st) {
+  const long total = (long)rm.tokens_total * rm.branches * heads * (head_dim / 2);
+  if (total == 0) return hipSuccess;
+  const int grid = (int)std::min<long>((total + 255) / 256, 16384);
+  hipLaunchKernelGGL(rope_apply_kernel, dim3(grid), dim3(256), 0, st, qk, ld, row0, rm, heads,
+                     head_dim, patch, table);
+  return hipGetLastError();
+}
+
+__global__ void bias_rows_f32_kernel(const bf16* __restrict__ b16, const float* __restrict__ b32,
+                                     int rows, int D, float* __restrict__ dst) {
+  const long n = (long)rows * D;
+  for (long i = blockIdx.x * 256L + threadIdx.x; i < n; i += (long)gridDim.x * 256) {
+    const int d = (int)(i % D);
+    dst[i] = b16 ? (float)b16[d] : b32[d];
+  }
+}
+
+hipError_t launch_bias_rows_f32(const void* bias, bool bias_bf16, int rows, int D, float* dst,
+                                hipStream_t st) {
+  const long n = (long)rows * D;
+  if (n == 0) return hipSuccess;
+  const int grid = (int)std::min<long>((n + 255) / 256, 8192);
+  hipLaunchKernelGGL(bias_rows_f32_kernel, dim3(grid), dim3(256), 0, st,
+                     bias_bf16 ? (const bf16*)bias : nullptr,
+                     bias_bf16 ? nullptr : (const float*)bias, rows, D, dst);
+  return hipGetLastError();
+}
+
+// ---------------------------------------------------------------------------
 // Final layer: per image token and guidance branch,
 //   out = LNmod(x; shift, scale) W_out^T + b_out     (P = p*p*C outputs)
 // then v = v_u + g (v_c - v_u), unpatchify, noise_pred = v, latent += dt v.

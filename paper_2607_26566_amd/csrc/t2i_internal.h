@@ -27,11 +27,15 @@ struct SeqMap {
 };
 
 // Variable-length attention: query sequence s reads Q rows [q_start, +q_len)
-// and K/V rows [k_start, +k_len).  tile_start[s] is the first query tile of s
-// in the flattened tile space of one head (prefix sum of ceil(q_len/BQ)).
+// and attends to the K/V rows [k_start, +k_len) followed by the optional
+// second segment [k2_start, +k2_len) (joint attention: a request's text rows
+// and its image rows live in different parts of the buffers).  tile_start[s]
+// is the first query tile of s in the flattened tile space of one head
+// (prefix sum of ceil(q_len/BQ)).
 struct AttnMap {
   int n;
   int q_start[kMaxSeq], q_len[kMaxSeq], k_start[kMaxSeq], k_len[kMaxSeq];
+  int k2_start[kMaxSeq], k2_len[kMaxSeq];
   int tile_start[kMaxSeq + 1];
 };
 
@@ -105,7 +109,7 @@ __device__ __forceinline__ float silu(float v) { return v * __builtin_amdgcn_rcp
 // Linear-layer epilogue.
 
 enum EpiKind { EPI_STORE = 0, EPI_GELU = 1, EPI_SILU = 2, EPI_RESID = 3, EPI_RESID_GATED = 4,
-               EPI_SPLIT_VT = 5 };
+               EPI_SPLIT_VT = 5, EPI_STORE_F32 = 6 };
 
 struct Epi {
   void* out;          // STORE / GELU / SILU destination (SPLIT_VT: columns < vcol0)
@@ -125,6 +129,8 @@ template <typename OutT>
 __device__ __forceinline__ void epi_apply(const Epi& e, int kind, int m, int n, float y) {
   if (kind == EPI_STORE) {
     ((OutT*)e.out)[(size_t)m * e.ldo + n] = from_f32<OutT>(y);
+  } else if (kind == EPI_STORE_F32) {
+    ((float*)e.out)[(size_t)m * e.ldo + n] = y;
   } else if (kind == EPI_SPLIT_VT) {
     if (n < e.vcol0) ((OutT*)e.out)[(size_t)m * e.ldo + n] = from_f32<OutT>(y);
     else e.vt[(size_t)(n - e.vcol0) * e.ldvt + m] = (bf16)y;
@@ -186,6 +192,18 @@ hipError_t launch_final_layer(const float* x, const ReqMap& rm, const void* w_ou
                               const void* b_out, bool w_bf16, const float* mod, int ld_mod,
                               int shift_off, int scale_off, int D, int C, int p, float eps,
                               float guidance, float* latents, float* noise_pred, hipStream_t st);
+
+// 2D RoPE.  table[pos * q + j] = (cos, sin)(pos * 10000^(-j/q)), q = head_dim/4,
+// pos < npos; rope_apply rotates, in place, the q (columns [0, D)) and k
+// (columns [D, 2D)) of the image rows [row0, row0 + branches * tokens) of a
+// bf16 buffer with row stride ld: the first head_dim/2 dims of each head by
+// the token's grid row, the last head_dim/2 by its grid column, pairs (2j, 2j+1).
+hipError_t launch_rope_table(float2* table, int npos, int q, hipStream_t st);
+hipError_t launch_rope_apply(bf16* qk, int ld, int row0, const ReqMap& rm, int heads, int head_dim,
+                             int patch, const float2* table, hipStream_t st);
+// dst[r][:] = float(bias[:]) for r < rows (bf16 or fp32 bias)
+hipError_t launch_bias_rows_f32(const void* bias, bool bias_bf16, int rows, int D, float* dst,
+                                hipStream_t st);
 
 // Cache-skip support.
 struct CacheHeader {      // one per request, in the caller's cache-state buffer

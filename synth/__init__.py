@@ -164,15 +164,17 @@ def texts(w: Workload, seed: int | None = None) -> List[np.ndarray]:
 
 
 def weights(w: Workload, layout: Sequence[Tuple[str, Tuple[int, ...]]],
-            seed: int | None = None, only: int | None = None) -> List[np.ndarray]:
+            seed: int | None = None, only: int | None = None,
+            pick: Sequence[int] | None = None) -> List[np.ndarray]:
     """Weight tensors for a weight table given as (name, shape) pairs.
 
     Tensor ``i`` depends only on (seed, i, shape), so a caller may generate a
-    prefix of the table (``only`` = number of leading tensors)."""
+    prefix of the table (``only`` = number of leading tensors) or the tensors
+    at chosen indices (``pick``, returned in that order)."""
     s = w.seed if seed is None else seed
-    n = len(layout) if only is None else only
+    idx = list(pick) if pick is not None else range(len(layout) if only is None else only)
     out = []
-    for i in range(n):
+    for i in idx:
         a = normal(s, (2, i), tuple(layout[i][1]), std=0.02)
         out.append(round_bf16(a) if w.dtype == "bf16" else a)
     return out

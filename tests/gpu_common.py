@@ -7,7 +7,7 @@ import torch
 
 import synth
 import paper_2607_26566_amd as t2i
-from oracle import dit
+from oracle import dit, mmdit
 
 DEV = "cuda"
 
@@ -40,8 +40,9 @@ class Model:
         t0 = time.time()
         self.w = w
         self.cfg = t2i.Config.from_shape(w, max_tokens, max_requests, max_steps)
+        self.om = mmdit if w.arch == "mmdit" else dit   # the oracle module of this family
         table = t2i.weight_table(self.cfg)
-        assert table == [(n, tuple(s)) for n, s in dit.weight_layout(w)]
+        assert table == [(n, tuple(s)) for n, s in self.om.weight_layout(w)]
         self.host = weights if weights is not None else synth.weights(w, table)
         self.dev = [to_dev(a, w.dtype) for a in self.host]
         self.m = t2i.t2i_dit_init(self.cfg, self.dev)
@@ -51,7 +52,7 @@ class Model:
     @property
     def W(self):
         if self._W is None:
-            self._W = dit.as_dict(self.w, self.host)
+            self._W = self.om.as_dict(self.w, self.host)
         return self._W
 
     def latents_dev(self, lats):

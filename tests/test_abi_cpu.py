@@ -181,7 +181,15 @@ def test_op_argument_errors():
     qs = (C.c_int32 * 1)(0)
     ql = (C.c_int32 * 1)(4)
     kl = (C.c_int32 * 1)(0)                              # no keys
-    assert lib.t2i_op_attention(1, 2, 72, 1, qs, ql, qs, kl, 0x1000, 144, 0x2000, 144,
-                                0x3000, 144, 0x4000, 144, None) == 2
-    assert lib.t2i_op_attention(1, 2, 48, 1, qs, ql, qs, ql, 0x1000, 96, 0x2000, 96,
+    assert lib.t2i_op_attention(1, 2, 72, 1, qs, ql, qs, kl, None, None, 0x1000, 144, 0x2000,
+                                144, 0x3000, 144, 0x4000, 144, None) == 2
+    assert lib.t2i_op_attention(1, 2, 48, 1, qs, ql, qs, ql, None, None, 0x1000, 96, 0x2000, 96,
                                 0x3000, 96, 0x4000, 96, None) == 2
+    # no keys in either segment; a second segment given by halves; misaligned segment
+    assert lib.t2i_op_attention(1, 2, 72, 1, qs, ql, qs, kl, qs, kl, 0x1000, 144, 0x2000,
+                                144, 0x3000, 144, 0x4000, 144, None) == 2
+    assert lib.t2i_op_attention(1, 2, 72, 1, qs, ql, qs, ql, qs, None, 0x1000, 144, 0x2000,
+                                144, 0x3000, 144, 0x4000, 144, None) == 1
+    k2 = (C.c_int32 * 1)(4)
+    assert lib.t2i_op_attention(1, 2, 72, 1, qs, ql, qs, ql, k2, ql, 0x1000, 144, 0x2000,
+                                144, 0x3000, 144, 0x4000, 144, None) == 2

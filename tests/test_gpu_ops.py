@@ -94,10 +94,14 @@ def test_linear_f32(M, N, K, epi):
         assert rel_l2(x.cpu().numpy().astype(np.float64) - x0, gate * ref) < 1e-6
 
 
-def run_attention(dtype, heads, d, seqs, q, k, v):
+def run_attention(dtype, heads, d, seqs, q, k, v, seg2=None):
+    """seqs: (q_start, q_len, k_start, k_len); seg2: (k2_start, k2_len) per sequence."""
     lib = t2i.load()
     n = len(seqs)
     qs, ql, ks, kl = ((C.c_int32 * n)(*[s[i] for s in seqs]) for i in range(4))
+    k2s = k2l = None
+    if seg2 is not None:
+        k2s, k2l = ((C.c_int32 * n)(*[s[i] for s in seg2]) for i in range(2))
     dt = "bf16" if dtype == _lib.T2I_BF16 else "f32"
     w = heads * d
     if dtype == _lib.T2I_BF16:
@@ -111,8 +115,9 @@ def run_attention(dtype, heads, d, seqs, q, k, v):
         v_dev, ldv_arg = to_dev(v, dt), w
     dq, dk = to_dev(q, dt), to_dev(k, dt)
     o = torch.zeros(dq.shape, dtype=dq.dtype, device=DEV)
-    st = lib.t2i_op_attention(dtype, heads, d, n, qs, ql, ks, kl, dq.data_ptr(), w, dk.data_ptr(),
-                              w, v_dev.data_ptr(), ldv_arg, o.data_ptr(), w, _stream())
+    st = lib.t2i_op_attention(dtype, heads, d, n, qs, ql, ks, kl, k2s, k2l, dq.data_ptr(), w,
+                              dk.data_ptr(), w, v_dev.data_ptr(), ldv_arg, o.data_ptr(), w,
+                              _stream())
     _lib.check(st)
     torch.cuda.synchronize()
     return to_host(o)
@@ -172,6 +177,34 @@ def test_attention_bf16_full_size_sampled_rows():
         ref[i] = dit.attention(q[r:r + 1].astype(np.float64), k[s0:s0 + n].astype(np.float64),
                                v[s0:s0 + n].astype(np.float64), H)[0]
     assert rel_l2(got[rows], ref) < 6e-3
+
+
+JOINT_CASES = [
+    # (name, H, d, [(q_start, q_len, k_start, k_len)], [(k2_start, k2_len)], nq, nk)
+    ("txt+img", 2, 128, [(0, 64, 0, 64), (64, 256, 0, 64)], [(64, 256), (64, 256)], 320, 320),
+    ("ragged-two-seqs", 3, 128, [(0, 77, 0, 40), (77, 130, 48, 23)],
+     [(80, 130), (216, 77)], 207, 296),
+    ("second-only", 2, 72, [(0, 100, 0, 0)], [(8, 93)], 100, 101),
+    ("first-only", 2, 64, [(0, 70, 16, 50)], [(0, 0)], 70, 66),
+]
+
+
+@pytest.mark.parametrize("name,H,d,seqs,seg2,nq,nk", JOINT_CASES, ids=[c[0] for c in JOINT_CASES])
+@pytest.mark.parametrize("dtype", [_lib.T2I_BF16, _lib.T2I_F32], ids=["bf16", "f32"])
+def test_attention_two_key_segments(dtype, name, H, d, seqs, seg2, nq, nk):
+    """Keys of a sequence in two separate row ranges == attention over their concatenation."""
+    say(f"attention two segments {name} dtype {dtype}")
+    bf = dtype == _lib.T2I_BF16
+    q, k, v = rnd(50, (nq, H * d), bf=bf), rnd(51, (nk, H * d), bf=bf), rnd(52, (nk, H * d), bf=bf)
+    got = run_attention(dtype, H, d, seqs, q, k, v, seg2)
+    ref = np.zeros(q.shape)
+    for (q0, n_q, k0, n_k), (k20, n_k2) in zip(seqs, seg2):
+        idx = np.r_[np.arange(k0, k0 + n_k), np.arange(k20, k20 + n_k2)]
+        ref[q0:q0 + n_q] = dit.attention(q[q0:q0 + n_q].astype(np.float64),
+                                         k[idx].astype(np.float64), v[idx].astype(np.float64), H)
+    err = rel_l2(got, ref)
+    say(f"  rel_l2 {err:.2e}")
+    assert err < (6e-3 if bf else 1e-6)
 
 
 @pytest.mark.parametrize("H,d,seqs,nq,nk", [(2, 64, [(0, 64, 0, 64)], 64, 64),

@@ -133,3 +133,56 @@ def test_layout_sizes():
     per_block = 2 * (6 * D * D + 6 * D + 3 * D * D + 3 * D + D * D + D + F * D + F + D * F + D)
     assert n == per_block * 19 + (D * 64 + D) + (D * 256 + D + D * D + D) + (D * 4096 + D) \
         + (2 * D * D + 2 * D) + (64 * D + 64)
+
+
+def _stream_inputs(seed=5):
+    rng = np.random.default_rng(seed)
+    D = TINY.hidden
+    return rng.standard_normal((3, D)), rng.standard_normal((6, D)), rng.standard_normal(D)
+
+
+def test_joint_block_rows_matches_full_block():
+    W = weights()
+    xt, xi, c = _stream_inputs()
+    rows, cols = mmdit.grid_positions(2, 3)
+    nt, ni = mmdit.joint_block(W, TINY, 1, xt, xi, c, rows, cols)
+    at, ai = mmdit.joint_block_rows(W, TINY, 1, xt, xi, c, rows, cols, range(3), range(6))
+    assert np.allclose(at, nt, atol=1e-12) and np.allclose(ai, ni, atol=1e-12)
+    st, si = [2, 0], [5, 1, 3]
+    bt, bi = mmdit.joint_block_rows(W, TINY, 1, xt, xi, c, rows, cols, st, si)
+    assert np.allclose(bt, nt[st], atol=1e-12) and np.allclose(bi, ni[si], atol=1e-12)
+
+
+def test_cache_signal_is_image_block0_modulated_input():
+    import torch
+    import torch.nn.functional as TF
+    W = weights()
+    lat = np.random.default_rng(6).standard_normal((2, 4, 6))
+    m = mmdit.cache_signal(W, TINY, lat, 0.3)
+    c = dit.conditioning(W, TINY, 0.3)
+    a = dit.silu(c) @ W["blocks.0.img.ada.w"].T + W["blocks.0.img.ada.b"]
+    D = TINY.hidden
+    x = torch.from_numpy(dit.patchify(lat, 2) @ W["x_embed.w"].T + W["x_embed.b"])
+    ln = TF.layer_norm(x, (D,), eps=TINY.ln_eps).numpy()
+    assert np.allclose(m, ln * (1 + a[D:2 * D]) + a[:D], atol=1e-12)
+
+
+def test_sampler_runs_mmdit_velocity_guidance_and_cached_residual():
+    from oracle import sampler
+    W = weights()
+    rng = np.random.default_rng(7)
+    lat = rng.standard_normal((2, 4, 6))
+    text = rng.standard_normal((3, 6))
+    vc = mmdit.forward(W, TINY, lat, 0.8, text)[0]
+    vu = mmdit.forward(W, TINY, lat, 0.8, None)[0]
+    v1, _ = sampler.model_velocity(W, TINY, lat, 0.8, text, 1.0)
+    assert np.allclose(v1, vc, atol=1e-12)
+    st = sampler.CacheState()
+    v2, vb = sampler.model_velocity(W, TINY, lat, 0.8, text, 3.0, st)
+    assert np.allclose(vb[0], vc, atol=1e-12) and np.allclose(vb[1], vu, atol=1e-12)
+    assert np.allclose(v2, vu + 3.0 * (vc - vu), atol=1e-12)
+    # a skipped step reuses the image-stream residual: same velocity here
+    v3, _ = sampler.model_velocity(W, TINY, lat, 0.8, text, 3.0, st, skip=True)
+    assert np.allclose(v3, v2, atol=1e-10)
+    # the unconditional text stream starts from the bias alone
+    assert np.allclose(mmdit.embed_text(W, TINY, None), np.tile(W["y_embed.b"], (3, 1)))
