@@ -11,6 +11,10 @@ update -- on synthetic inputs already resident in HBM.
 Prints ONE JSON line.  ``roofline`` is for the kernel with the largest share of
 step time, timed with HIP events on the library's stream during the timed
 steps; ``cpu_baseline`` is the oracle on the host cores on a bounded sample.
+
+``--workload`` selects one of the other synthetic workloads instead (the
+512-px DiT, the 3072-wide joint-attention model, the packed multi-request
+batch) to report their achieved fractions the same way.
 """
 from __future__ import annotations
 
@@ -30,58 +34,94 @@ WORKLOAD = "dit1024_cfg"
 
 
 def class_work(w):
-    """Algorithmic work of one launch of each kernel class at workload ``w``
+    """Algorithmic work of each kernel class in ONE block at workload ``w``
     (FLOPs = 2MNK per GEMM and 4 Nq Nk d per attention head; bytes for the
-    HBM-bound LN-mod: read fp32 x, write bf16 h)."""
+    HBM-bound LN-mod: read fp32 x, write bf16 h), and its launches per block."""
     R = w.image_tokens * w.branches
     D, F = w.hidden, w.mlp_hidden
     seq = [w.tokens(r) for r in range(w.n_req)] * w.branches
     dh = w.heads * w.head_dim
+    if w.arch == "mmdit":
+        T = w.text_tokens
+        Rt = R + len(seq) * T                       # text and image rows
+        return {
+            "gemm_qkv": ("flop", 2.0 * Rt * 3 * D * D, 2),
+            "attn_self": ("flop", sum(4.0 * (n + T) ** 2 * dh for n in seq), 1),
+            "gemm_o": ("flop", 2.0 * Rt * D * D, 2),
+            "ln_mod": ("byte", 2 * Rt * D * (4.0 + 2.0), 4),
+            "gemm_fc1": ("flop", 2.0 * Rt * F * D, 2),
+            "gemm_fc2": ("flop", 2.0 * Rt * F * D, 2),
+        }
     return {
-        "gemm_qkv": ("flop", 2.0 * R * 3 * D * D),
-        "attn_self": ("flop", sum(4.0 * n * n * dh for n in seq)),
-        "gemm_o": ("flop", 2.0 * R * D * D),
-        "gemm_xq": ("flop", 2.0 * R * D * D),
-        "attn_cross": ("flop", sum(4.0 * n * w.text_tokens * dh for n in seq)),
-        "gemm_xo": ("flop", 2.0 * R * D * D),
-        "ln_mod": ("byte", R * D * (4.0 + 2.0)),
-        "gemm_fc1": ("flop", 2.0 * R * F * D),
-        "gemm_fc2": ("flop", 2.0 * R * F * D),
+        "gemm_qkv": ("flop", 2.0 * R * 3 * D * D, 1),
+        "attn_self": ("flop", sum(4.0 * n * n * dh for n in seq), 1),
+        "gemm_o": ("flop", 2.0 * R * D * D, 1),
+        "gemm_xq": ("flop", 2.0 * R * D * D, 1),
+        "attn_cross": ("flop", sum(4.0 * n * w.text_tokens * dh for n in seq), 1),
+        "gemm_xo": ("flop", 2.0 * R * D * D, 1),
+        "ln_mod": ("byte", 2 * R * D * (4.0 + 2.0), 2),
+        "gemm_fc1": ("flop", 2.0 * R * F * D, 1),
+        "gemm_fc2": ("flop", 2.0 * R * F * D, 1),
     }
 
 
 def step_flops(w):
     cw = class_work(w)
-    per_block = sum(v for k, (kind, v) in cw.items() if kind == "flop")
-    return per_block * w.depth
+    return w.depth * sum(v for kind, v, _ in cw.values() if kind == "flop")
 
 
-def cpu_baseline(w, host_prefix, n_blocks=1):
-    """The oracle on a bounded sample: blocks 0..n_blocks-1 of one 1024-px
-    step for both guidance branches, scaled to a whole step."""
+def cpu_baseline(w, W_host):
+    """The oracle on a bounded sample: block 0 of one step (every request and
+    guidance branch), scaled to a whole step's blocks."""
     import numpy as np
     import synth
-    from oracle import dit
+    from oracle import dit, mmdit
     try:
         from threadpoolctl import threadpool_info
         cores = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
     except Exception:
         cores = os.cpu_count()
-    wp = synth.reduced(w, depth=n_blocks)
-    W = dit.as_dict(wp, host_prefix)
-    lat, text = synth.latents(w)[0], synth.texts(w)[0]
+    wp = synth.reduced(w, depth=1)
+    mm = w.arch == "mmdit"
+    W = (mmdit if mm else dit).as_dict(wp, W_host)
+    lats, texts = synth.latents(w), synth.texts(w)
     t0 = time.perf_counter()
-    c = dit.conditioning(W, wp, 1.0)
-    x0 = dit.embed(W, wp, lat)
-    for txt in (text, np.zeros((w.text_tokens, w.text_dim))):
-        y = dit.text_project(W, wp, txt)
-        dit.run_blocks(W, wp, x0, y, c)
+    for r, lat in enumerate(lats):
+        c = dit.conditioning(W, wp, 1.0)
+        for txt in (texts[r], None)[:w.branches]:
+            if mm:
+                xt, xi = mmdit.embed(W, wp, lat, txt)
+                mmdit.run_blocks(W, wp, xt, xi, c, lat.shape[1:], 0, 1)
+            else:
+                y = dit.text_project(W, wp, txt if txt is not None
+                                     else np.zeros((w.text_tokens, w.text_dim)))
+                dit.run_blocks(W, wp, dit.embed(W, wp, lat), y, c)
     dt = time.perf_counter() - t0
-    per_step = dt * w.depth / n_blocks
-    return {"value": 1.0 / per_step, "unit": "steps/s", "cores": int(cores), "kind": "oracle",
-            "sample": f"float64 numpy oracle, blocks 0-{n_blocks - 1} of one 1024px step for both "
-                      f"guidance branches (2x4096 tokens) in {dt:.1f} s, scaled x{w.depth / n_blocks:g} "
-                      f"to all {w.depth} blocks"}
+    per_step = dt * w.depth
+    return {"value": round(1.0 / per_step, 6), "unit": "steps/s", "cores": int(cores),
+            "kind": "oracle",
+            "sample": f"float64 numpy oracle, block 0 of one {w.name} step for all "
+                      f"{w.n_req} request(s) x {w.branches} guidance branch(es) in {dt:.1f} s, "
+                      f"scaled x{w.depth} to all blocks"}
+
+
+WORKLOADS = {
+    "dit1024_cfg": ("denoising steps/s at 1024px DiT; MFMA TFLOP/s as fraction of MI355X bf16 peak",
+                    "dit1024_cfg: 1024px image, latent 4x128x128, patch 2 -> 4096 tokens x 2 "
+                    "guidance branches (g=4.5), hidden 1152, 28 blocks, 16 heads x 72, MLP 4608, "
+                    "120 text tokens x 4096, seed 2"),
+    "dit512": ("denoising steps/s at 512px DiT (1024 tokens)",
+               "dit512: 512px image, latent 4x64x64, patch 2 -> 1024 tokens, hidden 1152, "
+               "28 blocks, 16 heads x 72, MLP 4608, 120 text tokens x 4096, seed 1"),
+    "mmdit1024": ("denoising steps/s at 1024px joint-attention DiT (4096 image + 512 text tokens)",
+                  "mmdit1024: latent 16x128x128, patch 2 -> 4096 image tokens + 512 text tokens "
+                  "(4096 -> 3072), hidden 3072, 19 joint blocks, 24 heads x 128, MLP 12288, "
+                  "2D RoPE, seed 3"),
+    "packed8": ("denoising steps/s of a packed 8-request batch (12032 tokens)",
+                "packed8: 3x256px + 3x512px + 2x1024px requests packed (256/1024/4096 tokens "
+                "each, 12032 total), own timestep each, hidden 1152, 28 blocks, 16 heads x 72, "
+                "cache skip off, seed 4"),
+}
 
 
 def main():
@@ -90,6 +130,7 @@ def main():
     ap.add_argument("--steps", type=int, default=10)
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--workload", default=WORKLOAD, choices=sorted(WORKLOADS))
     ap.add_argument("--copy-calibration", action="store_true",
                     help="run only a plain 1 GiB device copy (HBM counter calibration)")
     args = ap.parse_args()
@@ -114,22 +155,38 @@ def main():
         print(json.dumps({"copy_bytes_read": 4 * n, "copy_bytes_written": 4 * n, "launches": 5}))
         return
 
-    w = synth.workload(WORKLOAD)
+    w = synth.workload(args.workload)
+    metric, desc = WORKLOADS[args.workload]
     cfg = t2i.Config.from_shape(w)
     table = t2i.weight_table(cfg)
-    host = synth.weights(w, table)
-    dev = t2i.upload(host, w.dtype)
+    # weights generated and uploaded one tensor at a time (the 3072-wide model
+    # has 6.5e9 parameters); the host keeps block 0 and the final layer for
+    # the oracle baseline
+    per_block = 16 if w.arch == "cross" else 20
+    keep = set(range(8 + per_block)) | set(range(len(table) - 4, len(table)))
+    dev, kept = [], {}
+    t_w = time.time()
+    for i in range(len(table)):
+        a = synth.weights(w, table, pick=[i])[0]
+        dev.append(t2i.upload([a], w.dtype)[0])
+        if i in keep:
+            kept[i] = a
+        if time.time() - t_w > 20:
+            print(f"[bench] weights {i + 1}/{len(table)}", file=sys.stderr, flush=True)
+            t_w = time.time()
+    W_host = [kept[i] for i in sorted(kept)]
     m = t2i.t2i_dit_init(cfg, dev)
     lats, texts = synth.latents(w), synth.texts(w)
     hw = list(w.requests)
     x = torch.from_numpy(np.concatenate([l.ravel() for l in lats])).cuda()
     tx = torch.from_numpy(np.stack(texts)).to("cuda", torch.bfloat16)
     n = w.steps
-    sched = [1.0 - k / n for k in range(n + 1)]
+    t0s = synth.start_times(w)
+    sched = [[t0 * (1.0 - k / n) for t0 in t0s] for k in range(n + 1)]
 
     def run(i):
         k = i % n
-        t2i.t2i_dit_step(m, x, hw, [sched[k]], tx, guidance=w.guidance, t_next=[sched[k + 1]])
+        t2i.t2i_dit_step(m, x, hw, sched[k], tx, guidance=w.guidance, t_next=sched[k + 1])
 
     lib = t2i.load()
     # warmup; the last warmup pass times every kernel class to find the dominant one
@@ -162,35 +219,45 @@ def main():
     sps = args.steps / elapsed
     flops = step_flops(w)
     cw = class_work(w)
-    kind, work = cw[dominant]
+    kind, work_block, per_blk = cw[dominant]
+    blocks = w.depth * args.steps                      # blocks executed in the timed region
+    dom_s = tot.value / 1e3
     if kind == "flop":
-        ach = work / dom_avg_s / 1e12
+        ach = work_block * blocks / dom_s / 1e12
         roof = {"bound": "mfma", "achieved": round(ach, 1), "peak": PEAK_BF16_TFLOPS,
                 "unit": "TFLOP/s", "frac": round(ach / PEAK_BF16_TFLOPS, 4), "traffic": None}
     else:
-        ach = work / dom_avg_s / 1e9
+        ach = work_block * blocks / dom_s / 1e9
         roof = {"bound": "hbm", "achieved": round(ach, 1), "peak": PEAK_HBM_GBS,
                 "unit": "GB/s", "frac": round(ach / PEAK_HBM_GBS, 4), "traffic": None}
     roof["kernel"] = dominant
     roof["avg_launch_ms"] = round(dom_avg_s * 1e3, 4)
     roof["launches"] = int(cnt.value)
-    roof["work_per_launch"] = work
+    roof["work_per_launch"] = work_block / per_blk
 
-    kernel_ms = {k: round(v[0] / max(v[1], 1), 4) for k, v in per_class.items()}
-    ln_bytes = cw["ln_mod"][1]
-    ln_ms = kernel_ms["ln_mod"]
-    gemm_attn_ms = sum(v[0] for k, v in per_class.items() if cw[k][0] == "flop")
+    # per class: average launch time, and achieved rate over the profiled step
+    kernel_ms = {k: round(v[0] / max(v[1], 1), 4) for k, v in per_class.items() if v[1]}
+    class_rate = {}
+    for k, (tms, c) in per_class.items():
+        if not c or k not in cw:
+            continue
+        kd, wb, _ = cw[k]
+        r = wb * w.depth / (tms / 1e3)
+        class_rate[k] = (f"{r / 1e12:.1f} TFLOP/s" if kd == "flop" else f"{r / 1e9:.1f} GB/s")
+    gemm_attn_ms = sum(v[0] for k, v in per_class.items() if k in cw and cw[k][0] == "flop")
+    ln_ms = per_class["ln_mod"][0]
+    ln_bytes = cw["ln_mod"][1] * w.depth
 
-    # a whole 20-step sample (conditioning and text computed once per sample)
+    # a whole sample (conditioning and text computed once per sample)
     x.copy_(torch.from_numpy(np.concatenate([l.ravel() for l in lats])).cuda())
     torch.cuda.synchronize()
     ts = time.perf_counter()
-    t2i.t2i_dit_sample(m, x, hw, tx, n, guidance=w.guidance)
+    t2i.t2i_dit_sample(m, x, hw, tx, n, guidance=w.guidance, timesteps=np.array(sched))
     torch.cuda.synchronize()
     sample_s = time.perf_counter() - ts
 
     out = {
-        "metric": "denoising steps/s at 1024px DiT (CFG, 2x4096 tokens)",
+        "metric": metric,
         "value": round(sps, 3),
         "unit": "steps/s",
         "n_gpus": 1,
@@ -200,24 +267,25 @@ def main():
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
-        "dtype": "bf16",
+        "dtype": "bf16" if w.dtype == "bf16" else "f32",
         "data": "synthetic",
-        "config": {"workload": "dit1024_cfg: 1024px image, latent 4x128x128, patch 2 -> 4096 "
-                               "tokens x 2 guidance branches (g=4.5), hidden 1152, 28 blocks, "
-                               "16 heads x 72, MLP 4608, 120 text tokens x 4096, seed 2",
-                   "global_batch": 2, "seq_len": 4096, "parallelism": "none (1 GPU)"},
+        "config": {"workload": desc, "global_batch": w.n_req * w.branches,
+                   "seq_len": max(w.tokens(r) for r in range(w.n_req)),
+                   "parallelism": "none (1 GPU)"},
         "roofline": roof,
         "gemm_attn_tflops_step": round(flops * sps / 1e12, 1),
         "gemm_attn_frac_of_peak_step": round(flops * sps / 1e12 / PEAK_BF16_TFLOPS, 4),
         "gemm_attn_tflops_kernels": round(flops / (gemm_attn_ms / 1e3) / 1e12, 1),
+        "gemm_attn_frac_of_peak_kernels": round(flops / (gemm_attn_ms / 1e3) / 1e12 / PEAK_BF16_TFLOPS, 4),
         "ln_mod_gbs": round(ln_bytes / (ln_ms / 1e3) / 1e9, 1) if ln_ms > 0 else None,
-        "images_per_s": round(1.0 / sample_s, 3),
+        "images_per_s": round(w.n_req / sample_s, 3),
         "sample_steps_per_s": round(n / sample_s, 3),
         "kernel_avg_ms": kernel_ms,
+        "kernel_class_rate": class_rate,
         "flops_per_step": flops,
     }
     if not args.no_cpu_baseline:
-        out["cpu_baseline"] = cpu_baseline(w, host[:8 + 16] + host[-4:])
+        out["cpu_baseline"] = cpu_baseline(w, W_host)
     print(json.dumps(out), flush=True)
 
 

@@ -66,7 +66,9 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(AttnMap map, int head
   constexpr int HDP = DC * 32;
   constexpr int DT = (HD + 15) / 16;   // 16-wide tiles of d for P V
   constexpr int HDO = DT * 16;
-  constexpr bool ONES = HD < HDO;      // a spare V^T row carries the row sums
+  // row sums: a spare V^T row of ones where the head dimension has padding,
+  // else one more P V MFMA against a ones fragment held in registers
+  constexpr bool ONES = HD < HDO;
   constexpr int VP = BKV + 8;          // LDS pitch of a V^T row (bf16)
   constexpr int CPR = HD / 8;          // 16-byte chunks per K row
   // K tile, chunk-major: block b (1 KB) holds d = 8b .. 8b+7 of the 64 keys,
@@ -155,7 +157,8 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(AttnMap map, int head
     if (ONES && tid < BKV) Vs[buf][HD * VP + vpos(tid)] = (bf16)(kv0 + tid < k_end ? 1.f : 0.f);
   };
 
-  // Q fragments (B operand of S^T): query qrow0 + qt*16 + fr, d = c*32 + g*8 .. +7
+  // Q fragments (B operand of S^T): query qrow0 + qt*16 + fr, d = c*32 + g*8 .. +7,
+  // pre-multiplied by log2(e)/sqrt(d) so that scores come out in log2 units
   bf16x8 qf[QT][DC];
 #pragma unroll
   for (int qt = 0; qt < QT; ++qt) {
@@ -163,22 +166,32 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(AttnMap map, int head
 #pragma unroll
     for (int c = 0; c < DC; ++c) {
       const int d = c * 32 + g * 8;
-      if (qr < q_end && d < HD)
-        qf[qt][c] = *(const bf16x8*)(Q + (size_t)qr * ldq + h * HD + d);
-      else
-        qf[qt][c] = bf16x8{};
+      qf[qt][c] = bf16x8{};
+      if (qr < q_end && d < HD) {
+        const bf16x8 raw = *(const bf16x8*)(Q + (size_t)qr * ldq + h * HD + d);
+#pragma unroll
+        for (int e = 0; e < 8; ++e) qf[qt][c][e] = (bf16)((float)raw[e] * scale_log2);
+      }
     }
   }
 
-  f32x4 o[QT][DT];
-  float m_run[QT], l_run[QT];
+  // Online softmax with a lazily updated maximum: every score accumulator
+  // starts at -m_run (the MFMA's C operand), so S' = s - m_run arrives ready
+  // for exp2.  While no S' exceeds 8 the stale maximum is kept: probabilities
+  // stay <= 256 and the common scale cancels between numerator and row sum.
+  f32x4 o[QT][DT], osum[QT];
+  float m_run[QT];
 #pragma unroll
   for (int qt = 0; qt < QT; ++qt) {
     m_run[qt] = -INFINITY;
-    l_run[qt] = 0.f;
+    osum[qt] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
     for (int dt = 0; dt < DT; ++dt) o[qt][dt] = f32x4{0.f, 0.f, 0.f, 0.f};
   }
+  // A fragment of a [16 x 32] tile whose row 0 is all ones (lane fr == 0)
+  bf16x8 ones_frag;
+#pragma unroll
+  for (int e = 0; e < 8; ++e) ones_frag[e] = (bf16)(fr == 0 ? 1.f : 0.f);
 
   // K fragment of 32-wide d chunk c: block 4c + g (the zero block past HD)
   int koff[DC];
@@ -213,10 +226,11 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(AttnMap map, int head
       // all of them live across tiles (register pressure, not LDS traffic,
       // limits this kernel)
       asm volatile("" ::: "memory");
-      // d-chunk outer, key tile inner: four independent accumulation chains
+      // d-chunk outer, key tile inner: four independent accumulation chains,
+      // each started from -m_run
+      const float negm = m_run[qt] == -INFINITY ? 0.f : -m_run[qt];
+      const f32x4 cinit = f32x4{negm, negm, negm, negm};
       f32x4 sc[4];
-#pragma unroll
-      for (int kt = 0; kt < 4; ++kt) sc[kt] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
       for (int c = 0; c < DC; ++c) {
         bf16x8 kf[4];
@@ -224,7 +238,8 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(AttnMap map, int head
         for (int kt = 0; kt < 4; ++kt) kf[kt] = *(const bf16x8*)&Kb[koff[c] + kt * 128];
 #pragma unroll
         for (int kt = 0; kt < 4; ++kt)
-          sc[kt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf[kt], qf[qt][c], sc[kt], 0, 0, 0);
+          sc[kt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf[kt], qf[qt][c],
+                                                           c == 0 ? cinit : sc[kt], 0, 0, 0);
       }
       if (ragged) {
 #pragma unroll
@@ -233,37 +248,32 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(AttnMap map, int head
           for (int r = 0; r < 4; ++r)
             if (kv0 + kt * 16 + g * 4 + r >= k_end) sc[kt][r] = -INFINITY;
       }
-      float mx = -INFINITY;
+      float lm = -INFINITY;
 #pragma unroll
       for (int kt = 0; kt < 4; ++kt)
-        mx = fmaxf(fmaxf(mx, fmaxf(sc[kt][0], sc[kt][1])), fmaxf(sc[kt][2], sc[kt][3]));
-      mx = fmaxf(mx, __shfl_xor(mx, 16, 64));
-      mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
-      const float mt = mx * scale_log2;
-      // keep a stale maximum while the tile's stays within 2^8 of it: the
-      // probabilities stay <= 256 and the result is unchanged (the same
-      // maximum scales numerator and denominator)
-      if (__any(mt > m_run[qt] + 8.0f)) {
-        const float m_new = fmaxf(m_run[qt], mt);
+        lm = fmaxf(fmaxf(lm, fmaxf(sc[kt][0], sc[kt][1])), fmaxf(sc[kt][2], sc[kt][3]));
+      if (ti == 0 || __any(lm > 8.0f)) {
+        // new maximum: the query's 64 scores sit in the 4 lanes fr, fr+16, ..
+        float mx = fmaxf(lm, __shfl_xor(lm, 16, 64));
+        mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
+        const float m_new = fmaxf(m_run[qt], mx - negm);
+        const float delta = m_new + negm;          // shift of the subtracted value
         const float alpha = __builtin_amdgcn_exp2f(m_run[qt] - m_new);
         m_run[qt] = m_new;
-        l_run[qt] *= alpha;
+#pragma unroll
+        for (int kt = 0; kt < 4; ++kt)
+#pragma unroll
+          for (int r = 0; r < 4; ++r) sc[kt][r] -= delta;
 #pragma unroll
         for (int dt = 0; dt < DT; ++dt) o[qt][dt] *= alpha;
+        osum[qt] *= alpha;
       }
-      const float mr = m_run[qt];
-      float psum = 0.f;
       bf16x8 pf[2];
 #pragma unroll
-      for (int kt = 0; kt < 4; ++kt) {
+      for (int kt = 0; kt < 4; ++kt)
 #pragma unroll
-        for (int r = 0; r < 4; ++r) {
-          const float p = __builtin_amdgcn_exp2f(fmaf(sc[kt][r], scale_log2, -mr));
-          if (!ONES) psum += p;
-          pf[kt >> 1][(kt & 1) * 4 + r] = (bf16)p;
-        }
-      }
-      if (!ONES) l_run[qt] += psum;
+        for (int r = 0; r < 4; ++r)
+          pf[kt >> 1][(kt & 1) * 4 + r] = (bf16)__builtin_amdgcn_exp2f(sc[kt][r]);
       // key chunk outer, d tile inner: DT independent accumulation chains.
       // The lane's 8 keys are contiguous in the permuted V^T row: one 16-byte read.
 #pragma unroll
@@ -273,6 +283,8 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(AttnMap map, int head
           const bf16x8 vf = *(const bf16x8*)&Vb[(dt * 16 + fr) * VP + kc * 32 + g * 8];
           o[qt][dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vf, pf[kc], o[qt][dt], 0, 0, 0);
         }
+        if (!ONES)
+          osum[qt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ones_frag, pf[kc], osum[qt], 0, 0, 0);
       }
     }
     if (next) sstore(buf ^ 1, nkv0, nkend);
@@ -289,9 +301,7 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(AttnMap map, int head
       constexpr int LT = HD / 16, LR = HD % 16;
       l = __shfl(o[qt][LT][LR % 4], (LR / 4) * 16 + fr, 64);
     } else {
-      l = l_run[qt];
-      l += __shfl_xor(l, 16, 64);
-      l += __shfl_xor(l, 32, 64);
+      l = __shfl(osum[qt][0], fr, 64);   // row 0 of the ones product
     }
     const float inv = 1.0f / l;
     const int qr = qrow0 + qt * 16 + fr;
