@@ -32,13 +32,31 @@ __device__ __forceinline__ int xcd_remap_attn(int b, int nb) {
   return (x < r ? x * (q + 1) : r * (q + 1) + (x - r) * q) + j;
 }
 
-// Position of tile key k (0..63) in a staged V^T row.  Within each 32-key
-// chunk the keys a lane multiplies -- 4g..4g+3 and 16+4g..16+4g+3, the
-// probabilities its S^T fragment holds -- are stored next to each other at
-// 8g..8g+7, so one conflict-free 16-byte LDS read feeds the PV MFMA.
-__device__ __forceinline__ int vpos(int k) {
-  const int kk = k & 31;
-  return (k & 32) + 8 * ((kk & 15) >> 2) + 4 * (kk >> 4) + (kk & 3);
+// Key order inside a staged K tile.  The P V MFMA's B operand is the lane's
+// own probabilities: for 16-key chunk q a lane of half h holds S^T rows
+// 16q + 8a + 4h + j (a in 0..1, j in 0..3), which the MFMA consumes as k-index
+// 8h + 4a + j.  Staging key swap23(r) in K row r (bits 2 and 3 swapped) makes
+// that k-index the natural key order, so V^T tiles stay in key order and can
+// be copied to LDS unchanged.
+__device__ __forceinline__ int swap23(int r) {
+  return (r & ~12) | ((r & 4) << 1) | ((r & 8) >> 1);
+}
+
+// s_waitcnt vmcnt(n) for a wave-uniform n < 16 known only at run time.
+__device__ __forceinline__ void wait_vmcnt_dyn(int n) {
+  switch (n) {
+#define T2I_W(N_) case N_: __builtin_amdgcn_s_waitcnt((N_) | (7 << 4) | (15 << 8)); break;
+    T2I_W(0) T2I_W(1) T2I_W(2) T2I_W(3) T2I_W(4) T2I_W(5) T2I_W(6) T2I_W(7)
+    T2I_W(8) T2I_W(9) T2I_W(10) T2I_W(11) T2I_W(12) T2I_W(13) T2I_W(14)
+#undef T2I_W
+    default: __builtin_amdgcn_s_waitcnt((15) | (7 << 4) | (15 << 8)); break;
+  }
+}
+
+__device__ __forceinline__ void attn_barrier() {
+  // this wave's LDS accesses are complete, then s_barrier (no wait for
+  // outstanding global loads, which __syncthreads would add)
+  asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
 }
 
 // Flattened tile -> (head, sequence, query tile).  Tiles of one head and one
@@ -54,36 +72,37 @@ __device__ __forceinline__ void decode_tile(const AttnMap& m, int heads, int L, 
   j = t - m.tile_start[s];
 }
 
-template <int HD, int QT>
-__global__ __launch_bounds__(256, 2) void attn_bf16_kernel(AttnMap map, int heads,
+template <int HD>
+__global__ __launch_bounds__(512, 1) void attn_bf16_kernel(AttnMap map, int heads,
                                                            const bf16* __restrict__ Q, int ldq,
                                                            const bf16* __restrict__ K, int ldk,
                                                            const bf16* __restrict__ Vt, int ldvt,
                                                            bf16* __restrict__ O, int ldo,
                                                            float scale_log2) {
-  constexpr int BQ = 4 * QT * 16, BKV = 64;
-  constexpr int DC = (HD + 31) / 32;   // 32-wide chunks of d for Q K^T
-  constexpr int HDP = DC * 32;
-  constexpr int DT = (HD + 15) / 16;   // 16-wide tiles of d for P V
-  constexpr int HDO = DT * 16;
-  // row sums: a spare V^T row of ones where the head dimension has padding,
-  // else one more P V MFMA against a ones fragment held in registers
+  constexpr int NW = 8, BQ = NW * 32, BKV = 64, ST = 4;
+  // 16-wide chunks of the S^T = K Q^T contraction: d = 0 .. HD-1, then one
+  // more slot (d = HD) that carries the softmax shift: K has 1 there and Q has
+  // -m, so the MFMA itself returns s - m
+  constexpr int DC = (HD + 1 + 15) / 16;
+  constexpr int DT = (HD + 31) / 32;   // 32-row d tiles of O^T = V^T P^T
+  constexpr int HDO = DT * 32;
+  // row sums: a spare V^T row of ones where O^T has padding rows, else a
+  // per-lane sum of the probabilities
   constexpr bool ONES = HD < HDO;
-  constexpr int VP = BKV + 8;          // LDS pitch of a V^T row (bf16)
   constexpr int CPR = HD / 8;          // 16-byte chunks per K row
-  // K tile, chunk-major: block b (1 KB) holds d = 8b .. 8b+7 of the 64 keys,
-  // key k at byte 16k; block CPR is all zeros (the d padding of Q K^T)
-  constexpr int KBLK = CPR + 1;
-  constexpr int KST = KBLK * 512;      // bf16 elements per K stage
-  constexpr int KBPW = (CPR + 3) / 4;  // K load instructions per wave
-  constexpr int VCH = HD * (BKV / 8);
-  constexpr int VPT = (VCH + 255) / 256;
-  __shared__ __attribute__((aligned(1024))) bf16 Ks[2][KST];
-  __shared__ bf16 Vs[2][HDO * VP];
+  constexpr int PK = 2 * HD;           // K row pitch in LDS (bytes)
+  // K chunk slot swizzle for pitches that are multiples of 64 bytes: the 16
+  // rows one fragment read touches then cover all 64 banks
+  constexpr int KRS = (CPR == 4 || CPR == 8 || CPR == 16) ? 16 / CPR : 0;
+  constexpr int KSTAGE = BKV * PK;     // bytes
+  constexpr int VSTAGE = HDO * 128;    // V^T rows of 64 keys
+  constexpr int NI = 2 * CPR;          // 1-KB load instructions per tile (K, then V^T)
+  static_assert(HD % 8 == 0 && KSTAGE % 1024 == 0, "head dim");
+  __shared__ __attribute__((aligned(1024))) char smem[ST * (KSTAGE + VSTAGE)];
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  int h, s, j;
-  decode_tile(map, heads, xcd_remap_attn(blockIdx.x, gridDim.x), h, s, j);
+  int hh, s, j;
+  decode_tile(map, heads, xcd_remap_attn(blockIdx.x, gridDim.x), hh, s, j);
   const int q_beg = map.q_start[s], q_end = q_beg + map.q_len[s];
   // key tiles: those of segment 1, then those of segment 2
   const int k1 = map.k_start[s], n1 = map.k_len[s];
@@ -98,225 +117,240 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(AttnMap map, int head
       kend = k2 + n2;
     }
   };
-  const int qrow0 = q_beg + j * BQ + wave * (QT * 16);
-  const int g = lane >> 4, fr = lane & 15;
+  // 32x32x16 MFMA lane roles: column (query) ql, k-half hl; C element 4i + jj
+  // of a lane is row 8i + 4hl + jj
+  const int ql = lane & 31, hl = lane >> 5;
+  const int qr = q_beg + j * BQ + wave * 32 + ql;
+  auto kst = [&](int st) { return smem + st * (KSTAGE + VSTAGE); };
+  auto vst = [&](int st) { return smem + st * (KSTAGE + VSTAGE) + KSTAGE; };
 
-  // zero both buffers once: the K zero block and the V^T padding rows stay zero
-  for (int i = tid; i < 2 * KST; i += 256) (&Ks[0][0])[i] = (bf16)0.f;
-  for (int i = tid; i < 2 * HDO * VP; i += 256) (&Vs[0][0])[i] = (bf16)0.f;
+  // Q fragments (B operand of S^T): query qr, d = 16c + 8hl .. +7, pre-multiplied
+  // by log2(e)/sqrt(d) so that scores come out in log2 units; the shift slot
+  // d = HD is element 0 of chunk HD/16 in the lanes of half (HD%16)/8
+  constexpr int BC = HD / 16, BH = (HD % 16) / 8;
+  bf16x8 qf[DC];
+#pragma unroll
+  for (int c = 0; c < DC; ++c) {
+    const int d = c * 16 + hl * 8;
+    qf[c] = bf16x8{};
+    if (qr < q_end && d < HD) {
+      const bf16x8 raw = *(const bf16x8*)(Q + (size_t)qr * ldq + hh * HD + d);
+#pragma unroll
+      for (int e = 0; e < 8; ++e) qf[c][e] = (bf16)((float)raw[e] * scale_log2);
+    }
+  }
+  // V^T rows HD .. HDO-1 of every stage: the ones row, then zeros
+  for (int i = tid; i < ST * (HDO - HD) * 64; i += NW * 64) {
+    const int st = i / ((HDO - HD) * 64), rem = i - st * (HDO - HD) * 64;
+    const int row = HD + rem / 64, col = rem & 63;
+    ((bf16*)(vst(st) + row * 128))[col] = (bf16)(row == HD ? 1.f : 0.f);
+  }
 
-  // K tiles move HBM -> LDS directly (global_load_lds_dwordx4): instruction
-  // for block b has lane = key and fetches that key's d-chunk b.  Waves with
-  // fewer blocks repeat one (identical bytes).  Key rows past the sequence are
-  // clamped to its last key; their scores are masked.
-  int kblk[KBPW];
+  // Tile loads: HBM -> LDS directly (global_load_lds_dwordx4), instruction i of
+  // a tile writes bytes 1024i .. +1023 of the stage, lane l 16 bytes at 16l.
+  //   K (i < CPR): row r = key swap23(r), chunk slot swizzled; keys past the
+  //     sequence are clamped to its last key (their scores are masked);
+  //   V^T (i >= CPR): row d, 128 bytes = 64 keys, chunk slot c ^ ((d>>1)&7);
+  //     chunks past the sequence are read from its first chunk and zeroed
+  //     in LDS before use.
+  // Wave w issues instructions w, w+8, ...: n_w per tile.
+  constexpr int IPW = (NI + NW - 1) / NW;
+  int g_off[IPW], g_key[IPW], l_off[IPW];
+  const int n_w = (NI - wave + NW - 1) / NW;
 #pragma unroll
-  for (int i = 0; i < KBPW; ++i) kblk[i] = min(wave + 4 * i, CPR - 1);
-  auto kload = [&](int kv0, int k_end, int buf) {
-    const int gk = min(kv0 + lane, k_end - 1);
-    const bf16* src = K + (size_t)gk * ldk + h * HD;
+  for (int ii = 0; ii < IPW; ++ii) {
+    const int i = wave + NW * ii;
+    g_off[ii] = g_key[ii] = l_off[ii] = 0;
+    if (i < CPR) {
+      const int o = i * 1024 + lane * 16;
+      const int r = o / PK, slot = (o - r * PK) / 16;
+      const int c = KRS ? slot ^ ((r / KRS) & (CPR - 1)) : slot;
+      g_key[ii] = swap23(r);
+      g_off[ii] = hh * HD + c * 8;
+      l_off[ii] = i * 1024;                      // wave-uniform base; +16 per lane implied
+    } else if (i < NI) {
+      const int o = (i - CPR) * 1024 + lane * 16;
+      const int d = o / 128, c = (lane & 7) ^ ((d >> 1) & 7);
+      g_key[ii] = c * 8;                         // key offset of the chunk
+      g_off[ii] = hh * HD + d;                   // V^T row
+      l_off[ii] = KSTAGE + (i - CPR) * 1024;
+    }
+  }
+  auto issue = [&](int ti) {
+    int kv0, k_end;
+    tile_keys(ti, kv0, k_end);
+    char* base = kst(ti % ST);
 #pragma unroll
-    for (int i = 0; i < KBPW; ++i)
-      __builtin_amdgcn_global_load_lds(
-          (__attribute__((address_space(1))) void*)(src + kblk[i] * 8),
-          (__attribute__((address_space(3))) void*)(&Ks[buf][kblk[i] * 512]), 16, 0, 0);
-  };
-
-  bf16x8 vr[VPT];
-  auto gload = [&](int kv0, int k_end) {
-#pragma unroll
-    for (int i = 0; i < VPT; ++i) {
-      const int c = tid + 256 * i;
-      vr[i] = bf16x8{};
-      if (c < VCH) {
-        const int d = c >> 3, gk = kv0 + (c & 7) * 8;
-        if (gk < k_end) {
-          vr[i] = *(const bf16x8*)(Vt + (size_t)(h * HD + d) * ldvt + gk);
-          if (gk + 8 > k_end) {
-#pragma unroll
-            for (int e = 0; e < 8; ++e)
-              if (gk + e >= k_end) vr[i][e] = (bf16)0.f;
-          }
-        }
+    for (int ii = 0; ii < IPW; ++ii) {
+      const int i = wave + NW * ii;
+      if (i >= NI) break;
+      const bf16* src;
+      if (i < CPR) {
+        src = K + (size_t)min(kv0 + g_key[ii], k_end - 1) * ldk + g_off[ii];
+      } else {
+        const int gk = kv0 + g_key[ii];
+        src = Vt + (size_t)g_off[ii] * ldvt + (gk < k_end ? gk : kv0);
       }
+      __builtin_amdgcn_global_load_lds((__attribute__((address_space(1))) void*)src,
+                                       (__attribute__((address_space(3))) void*)(base + l_off[ii]),
+                                       16, 0, 0);
     }
   };
-  auto sstore = [&](int buf, int kv0, int k_end) {
-#pragma unroll
-    for (int i = 0; i < VPT; ++i) {
-      const int c = tid + 256 * i;
-      if (c < VCH) {
-        // keys 8(c&7) .. +7 of row c>>3: two groups of four, each to its
-        // permuted position (see vpos)
-        bf16* row = &Vs[buf][(c >> 3) * VP];
-        const int k = (c & 7) * 8;
-        *(bf16x4*)&row[vpos(k)] = bf16x4{vr[i][0], vr[i][1], vr[i][2], vr[i][3]};
-        *(bf16x4*)&row[vpos(k + 4)] = bf16x4{vr[i][4], vr[i][5], vr[i][6], vr[i][7]};
-      }
-    }
-    if (ONES && tid < BKV) Vs[buf][HD * VP + vpos(tid)] = (bf16)(kv0 + tid < k_end ? 1.f : 0.f);
+  // K fragment (A operand) of key block kb, 16-wide d chunk c for this lane:
+  // LDS row 32kb + ql, 16-byte chunk 2c + hl (zero past HD)
+  bf16x8 kone = bf16x8{};      // the K side of the shift slot
+  kone[0] = (bf16)1.f;
+  auto kfrag = [&](int st, int kb, int c) {
+    const int r = 32 * kb + ql, cc = 2 * c + hl;
+    if (cc == CPR) return kone;
+    if (cc > CPR) return bf16x8{};
+    const int slot = KRS ? cc ^ ((r / KRS) & (CPR - 1)) : cc;
+    return *(const bf16x8*)(kst(st) + r * PK + slot * 16);
   };
-
-  // Q fragments (B operand of S^T): query qrow0 + qt*16 + fr, d = c*32 + g*8 .. +7,
-  // pre-multiplied by log2(e)/sqrt(d) so that scores come out in log2 units
-  bf16x8 qf[QT][DC];
-#pragma unroll
-  for (int qt = 0; qt < QT; ++qt) {
-    const int qr = qrow0 + qt * 16 + fr;
+  auto qk = [&](int ti, f32x16 (&sc)[2]) {
+    const int st = ti % ST;
 #pragma unroll
     for (int c = 0; c < DC; ++c) {
-      const int d = c * 32 + g * 8;
-      qf[qt][c] = bf16x8{};
-      if (qr < q_end && d < HD) {
-        const bf16x8 raw = *(const bf16x8*)(Q + (size_t)qr * ldq + h * HD + d);
+      bf16x8 kf[2];
 #pragma unroll
-        for (int e = 0; e < 8; ++e) qf[qt][c][e] = (bf16)((float)raw[e] * scale_log2);
-      }
+      for (int kb = 0; kb < 2; ++kb) kf[kb] = kfrag(st, kb, c);
+#pragma unroll
+      for (int kb = 0; kb < 2; ++kb)
+        sc[kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf[kb], qf[c],
+                                                         c == 0 ? f32x16{} : sc[kb], 0, 0, 0);
     }
-  }
+  };
+  auto lane_max = [&](const f32x16 (&sc)[2]) {
+    float m0 = fmaxf(sc[0][0], sc[0][1]), m1 = fmaxf(sc[1][0], sc[1][1]);
+#pragma unroll
+    for (int e = 2; e < 16; e += 2) {
+      m0 = fmaxf(fmaxf(m0, sc[0][e]), sc[0][e + 1]);
+      m1 = fmaxf(fmaxf(m1, sc[1][e]), sc[1][e + 1]);
+    }
+    return fmaxf(m0, m1);
+  };
 
-  // Online softmax with a lazily updated maximum: every score accumulator
-  // starts at -m_run (the MFMA's C operand), so S' = s - m_run arrives ready
-  // for exp2.  While no S' exceeds 8 the stale maximum is kept: probabilities
-  // stay <= 256 and the common scale cancels between numerator and row sum.
-  f32x4 o[QT][DT], osum[QT];
-  float m_run[QT];
+  // Online softmax with a lazily updated maximum m (kept bf16-representable,
+  // as it rides in Q's shift slot): scores arrive as S' = s - m.  While no S'
+  // exceeds 8 the stale maximum is kept: probabilities stay <= 256 and the
+  // common scale cancels between numerator and row sum.
+  f32x16 o[DT];
 #pragma unroll
-  for (int qt = 0; qt < QT; ++qt) {
-    m_run[qt] = -INFINITY;
-    osum[qt] = f32x4{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-    for (int dt = 0; dt < DT; ++dt) o[qt][dt] = f32x4{0.f, 0.f, 0.f, 0.f};
-  }
-  // A fragment of a [16 x 32] tile whose row 0 is all ones (lane fr == 0)
-  bf16x8 ones_frag;
-#pragma unroll
-  for (int e = 0; e < 8; ++e) ones_frag[e] = (bf16)(fr == 0 ? 1.f : 0.f);
+  for (int dt = 0; dt < DT; ++dt) o[dt] = f32x16{};
+  float m_ref = 0.f, l_run = 0.f;   // the m in Q's shift slot (0 before the first tile)
 
-  // K fragment of 32-wide d chunk c: block 4c + g (the zero block past HD)
-  int koff[DC];
-#pragma unroll
-  for (int c = 0; c < DC; ++c) koff[c] = min(4 * c + g, CPR) * 512 + fr * 8;
-
-  __syncthreads();          // zero-fill done before the first tile lands
-  {
-    int kv0, kend;
-    tile_keys(0, kv0, kend);
-    kload(kv0, kend, 0);
-    gload(kv0, kend);
-    sstore(0, kv0, kend);
-  }
-  __syncthreads();          // (waits for the K loads too)
-  int buf = 0;
-  for (int ti = 0; ti < nt; ++ti) {
-    int kv0, k_end, nkv0 = 0, nkend = 0;
+  // one tile: S^T of tile ti is in cur with lane maximum lm; the next tile's
+  // S^T and lane maximum go to nxt / lm_nxt
+  auto step = [&](int ti, f32x16 (&cur)[2], float& lm, f32x16 (&nxt)[2], float& lm_nxt) {
+    int kv0, k_end;
     tile_keys(ti, kv0, k_end);
-    const bool next = ti + 1 < nt;
-    if (next) {
-      tile_keys(ti + 1, nkv0, nkend);
-      kload(nkv0, nkend, buf ^ 1);
-      gload(nkv0, nkend);
+    // tile ti+1 landed (tile ti+2 may still be in flight), for every wave
+    wait_vmcnt_dyn(ti + 2 < nt ? n_w : 0);
+    attn_barrier();
+    if (ti + ST - 1 < nt) issue(ti + ST - 1);     // into the stage of tile ti-1
+    if (kv0 + BKV > k_end) {
+      // ragged tile: zero V^T columns past the sequence (their probabilities
+      // are 0, but the copied bytes need not be finite) and mask the scores
+      const int v0 = k_end - kv0;
+      char* vb = vst(ti % ST);
+      for (int i = tid; i < HD * 64; i += NW * 64) {
+        const int d = i >> 6, col = i & 63;
+        if (col >= v0)
+          *(bf16*)(vb + d * 128 + (((col >> 3) ^ ((d >> 1) & 7)) << 4) + (col & 7) * 2) = (bf16)0.f;
+      }
+#pragma unroll
+      for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+        for (int e = 0; e < 16; ++e)
+          if (kv0 + swap23(32 * kb + 8 * (e >> 2) + 4 * hl + (e & 3)) >= k_end)
+            cur[kb][e] = -INFINITY;
+      lm = lane_max(cur);
+      attn_barrier();
     }
-    const bool ragged = kv0 + BKV > k_end;
-    const bf16* Kb = Ks[buf];
-    const bf16* Vb = Vs[buf];
+    if (ti == 0 || __any(lm > 8.0f)) {
+      // new maximum: the query's 64 scores sit in lanes ql and ql + 32
+      const float mx = fmaxf(lm, __shfl_xor(lm, 32, 64)) + m_ref;   // tile maximum
+      const float m_old = ti == 0 ? -INFINITY : m_ref;
+      const float m_new = (float)(bf16)fmaxf(m_old, mx);
+      const float alpha = __builtin_amdgcn_exp2f(m_old - m_new);
 #pragma unroll
-    for (int qt = 0; qt < QT; ++qt) {
-      // re-read the K / V^T fragments for every query tile instead of keeping
-      // all of them live across tiles (register pressure, not LDS traffic,
-      // limits this kernel)
-      asm volatile("" ::: "memory");
-      // d-chunk outer, key tile inner: four independent accumulation chains,
-      // each started from -m_run
-      const float negm = m_run[qt] == -INFINITY ? 0.f : -m_run[qt];
-      const f32x4 cinit = f32x4{negm, negm, negm, negm};
-      f32x4 sc[4];
+      for (int kb = 0; kb < 2; ++kb) cur[kb] -= (m_new - m_ref);
 #pragma unroll
-      for (int c = 0; c < DC; ++c) {
-        bf16x8 kf[4];
+      for (int dt = 0; dt < DT; ++dt) o[dt] *= alpha;
+      l_run *= alpha;
+      m_ref = m_new;
+      if (hl == BH) qf[BC][0] = (bf16)(-m_new);
+    }
+    // straight-line part: the next tile's scores (independent MFMAs) overlap
+    // this tile's exponentials; for the last tile the "next" scores come from
+    // a stale stage and are never used
+    qk(ti + 1, nxt);
+    // P^T fragments: chunk q (16 keys) = elements 8(q&1) .. +7 of cur[q>>1]
+    bf16x8 pf[4];
+    float psum = 0.f;
 #pragma unroll
-        for (int kt = 0; kt < 4; ++kt) kf[kt] = *(const bf16x8*)&Kb[koff[c] + kt * 128];
+    for (int q = 0; q < 4; ++q)
 #pragma unroll
-        for (int kt = 0; kt < 4; ++kt)
-          sc[kt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf[kt], qf[qt][c],
-                                                           c == 0 ? cinit : sc[kt], 0, 0, 0);
+      for (int e = 0; e < 8; ++e) {
+        const float p = __builtin_amdgcn_exp2f(cur[q >> 1][8 * (q & 1) + e]);
+        if (!ONES) psum += p;
+        pf[q][e] = (bf16)p;
       }
-      if (ragged) {
+    if (!ONES) l_run += psum;
+    // key chunk outer, d tile inner: DT independent accumulation chains; V^T
+    // row 32dt + ql, keys 16q + 8hl .. +7
+    const char* vb = vst(ti % ST);
 #pragma unroll
-        for (int kt = 0; kt < 4; ++kt)
+    for (int q = 0; q < 4; ++q) {
 #pragma unroll
-          for (int r = 0; r < 4; ++r)
-            if (kv0 + kt * 16 + g * 4 + r >= k_end) sc[kt][r] = -INFINITY;
-      }
-      float lm = -INFINITY;
-#pragma unroll
-      for (int kt = 0; kt < 4; ++kt)
-        lm = fmaxf(fmaxf(lm, fmaxf(sc[kt][0], sc[kt][1])), fmaxf(sc[kt][2], sc[kt][3]));
-      if (ti == 0 || __any(lm > 8.0f)) {
-        // new maximum: the query's 64 scores sit in the 4 lanes fr, fr+16, ..
-        float mx = fmaxf(lm, __shfl_xor(lm, 16, 64));
-        mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
-        const float m_new = fmaxf(m_run[qt], mx - negm);
-        const float delta = m_new + negm;          // shift of the subtracted value
-        const float alpha = __builtin_amdgcn_exp2f(m_run[qt] - m_new);
-        m_run[qt] = m_new;
-#pragma unroll
-        for (int kt = 0; kt < 4; ++kt)
-#pragma unroll
-          for (int r = 0; r < 4; ++r) sc[kt][r] -= delta;
-#pragma unroll
-        for (int dt = 0; dt < DT; ++dt) o[qt][dt] *= alpha;
-        osum[qt] *= alpha;
-      }
-      bf16x8 pf[2];
-#pragma unroll
-      for (int kt = 0; kt < 4; ++kt)
-#pragma unroll
-        for (int r = 0; r < 4; ++r)
-          pf[kt >> 1][(kt & 1) * 4 + r] = (bf16)__builtin_amdgcn_exp2f(sc[kt][r]);
-      // key chunk outer, d tile inner: DT independent accumulation chains.
-      // The lane's 8 keys are contiguous in the permuted V^T row: one 16-byte read.
-#pragma unroll
-      for (int kc = 0; kc < 2; ++kc) {
-#pragma unroll
-        for (int dt = 0; dt < DT; ++dt) {
-          const bf16x8 vf = *(const bf16x8*)&Vb[(dt * 16 + fr) * VP + kc * 32 + g * 8];
-          o[qt][dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vf, pf[kc], o[qt][dt], 0, 0, 0);
-        }
-        if (!ONES)
-          osum[qt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ones_frag, pf[kc], osum[qt], 0, 0, 0);
+      for (int dt = 0; dt < DT; ++dt) {
+        const int row = dt * 32 + ql;
+        const bf16x8 vf =
+            *(const bf16x8*)(vb + row * 128 + (((2 * q + hl) ^ ((row >> 1) & 7)) << 4));
+        o[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf, pf[q], o[dt], 0, 0, 0);
       }
     }
-    if (next) sstore(buf ^ 1, nkv0, nkend);
-    __syncthreads();
-    buf ^= 1;
+    lm_nxt = lane_max(nxt);
+  };
+
+  // prologue: tiles 0 .. ST-2 in flight, tile 0's scores
+#pragma unroll
+  for (int ti = 0; ti < ST - 1; ++ti)
+    if (ti < nt) issue(ti);
+  wait_vmcnt_dyn(n_w * (min(nt, ST - 1) - 1));
+  attn_barrier();
+  f32x16 sa[2], sb[2];
+  float la, lb;
+  qk(0, sa);
+  la = lane_max(sa);
+  for (int ti = 0; ti < nt; ti += 2) {
+    step(ti, sa, la, sb, lb);
+    if (ti + 1 < nt) step(ti + 1, sb, lb, sa, la);
   }
 
+  float l;
+  if (ONES) {
+    // row HD of O^T = sum of the probabilities: tile HD/32, row r = HD%32 =
+    // 8i + 4h + jj, held by the lanes of half h as element 4i + jj
+    constexpr int R = HD % 32;
+    l = __shfl(o[HD / 32][4 * (R / 8) + (R % 4)], ((R % 8) / 4) * 32 + ql, 64);
+  } else {
+    l = l_run + __shfl_xor(l_run, 32, 64);
+  }
+  if (qr >= q_end) return;
+  const float inv = 1.0f / l;
 #pragma unroll
-  for (int qt = 0; qt < QT; ++qt) {
-    float l;
-    if (ONES) {
-      // row HD of O^T = sum of the probabilities: tile HD/16, row HD%16, held
-      // by the lanes with g = (HD%16)/4 as component (HD%16)%4
-      constexpr int LT = HD / 16, LR = HD % 16;
-      l = __shfl(o[qt][LT][LR % 4], (LR / 4) * 16 + fr, 64);
-    } else {
-      l = __shfl(osum[qt][0], fr, 64);   // row 0 of the ones product
-    }
-    const float inv = 1.0f / l;
-    const int qr = qrow0 + qt * 16 + fr;
-    if (qr >= q_end) continue;
+  for (int dt = 0; dt < DT; ++dt)
 #pragma unroll
-    for (int dt = 0; dt < DT; ++dt) {
-      const int d = dt * 16 + g * 4;
+    for (int i = 0; i < 4; ++i) {
+      const int d = dt * 32 + i * 8 + hl * 4;
       if (d < HD) {
         bf16x4 w;
 #pragma unroll
-        for (int r = 0; r < 4; ++r) w[r] = (bf16)(o[qt][dt][r] * inv);
-        *(bf16x4*)(O + (size_t)qr * ldo + h * HD + d) = w;
+        for (int jj = 0; jj < 4; ++jj) w[jj] = (bf16)(o[dt][4 * i + jj] * inv);
+        *(bf16x4*)(O + (size_t)qr * ldo + hh * HD + d) = w;
       }
     }
-  }
 }
 
 // ---------------------------------------------------------------------------
@@ -376,12 +410,10 @@ __global__ __launch_bounds__(64) void attn_f32_kernel(AttnMap map, int heads,
   }
 }
 
-// 16-query tiles per wave: 4 (64 queries) while the output accumulators fit
-// next to everything else in 256 registers, 2 for the widest heads
-constexpr int query_tiles(int hd) { return hd > 96 ? 2 : 4; }
+// bf16: 8 waves x 32 queries per workgroup; fp32: 64 queries
 int attention_query_tile(bool bf16_io, int head_dim) {
-  if (!bf16_io) return 64;
-  return 4 * 16 * (head_dim > 96 ? 2 : 4);
+  (void)head_dim;
+  return bf16_io ? 256 : 64;
 }
 
 template <int HD>
@@ -392,7 +424,7 @@ static hipError_t launch_hd(bool bf16_io, int heads, const AttnMap& map, const v
   if (tiles == 0) return hipSuccess;
   if (bf16_io) {
     const float scale_log2 = 1.4426950408889634f / sqrtf((float)HD);
-    hipLaunchKernelGGL((attn_bf16_kernel<HD, query_tiles(HD)>), dim3(tiles), dim3(256), 0, st, map, heads,
+    hipLaunchKernelGGL((attn_bf16_kernel<HD>), dim3(tiles), dim3(512), 0, st, map, heads,
                        (const bf16*)q, ldq, (const bf16*)k, ldk, (const bf16*)v, ldv, (bf16*)o, ldo,
                        scale_log2);
   } else {

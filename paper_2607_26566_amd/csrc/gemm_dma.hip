@@ -86,7 +86,8 @@ __device__ __forceinline__ void dma_epi4(const Epi& e, int m, int nb, const floa
 template <int BM, int BN, int WGM, int WGN, int ST, int KIND, int AUX>
 __global__ __launch_bounds__(64 * WGM * WGN, 1) void gemm_dma_kernel(
     const bf16* __restrict__ A, int lda, const bf16* __restrict__ W, int ldw,
-    const bf16* __restrict__ bias, int M, int N, int K, Epi epi, int tiles_n, int vec_ok) {
+    const bf16* __restrict__ bias, int M, int N, int K, Epi epi, int tiles_n, int group_m,
+    int vec_ok) {
   constexpr int NW = WGM * WGN;
   constexpr int WM = BM / WGM, WN = BN / WGN;
   constexpr int TM = WM / 16, TN = WN / 16;
@@ -100,8 +101,15 @@ __global__ __launch_bounds__(64 * WGM * WGN, 1) void gemm_dma_kernel(
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int wm = wave / WGN, wn = wave % WGN;
+  // tile order: the tiles of one XCD are consecutive; within that range they
+  // walk group_m row blocks down before moving one column block right, so the
+  // workgroups resident on an XCD share both A rows and W rows in its L2
   const int tile = xcd_remap_dma(blockIdx.x, gridDim.x);
-  const int m0 = (tile / tiles_n) * BM, n0 = (tile % tiles_n) * BN;
+  const int tiles_m = (M + BM - 1) / BM;
+  const int per_group = group_m * tiles_n, grp = tile / per_group;
+  const int first = grp * group_m, rows_in = min(tiles_m - first, group_m);
+  const int in_grp = tile - grp * per_group;
+  const int m0 = (first + in_grp % rows_in) * BM, n0 = (in_grp / rows_in) * BN;
 
   // this lane's source of every block it loads (k offset added per tile)
   const bf16* src[BPW];
@@ -225,13 +233,13 @@ __global__ __launch_bounds__(64 * WGM * WGN, 1) void gemm_dma_kernel(
 template <int BM, int BN, int WGM, int WGN, int ST, int AUX>
 hipError_t gemm_dma_dispatch(const bf16* A, int lda, const bf16* W, int ldw, const bf16* bias,
                              int M, int N, int K, int kind, const Epi& epi, int vec_ok,
-                             hipStream_t st) {
+                             int group_m, hipStream_t st) {
   const int tn = (N + BN - 1) / BN, tm = (M + BM - 1) / BM;
   dim3 grid(tm * tn), block(64 * WGM * WGN);
 #define T2I_DMA_CASE(K_)                                                                      \
   case K_:                                                                                    \
     hipLaunchKernelGGL((gemm_dma_kernel<BM, BN, WGM, WGN, ST, K_, AUX>), grid, block, 0, st, A, lda, \
-                       W, ldw, bias, M, N, K, epi, tn, vec_ok);                               \
+                       W, ldw, bias, M, N, K, epi, tn, group_m, vec_ok);                      \
     break;
   switch (kind) {
     T2I_DMA_CASE(EPI_STORE)
@@ -246,25 +254,41 @@ hipError_t gemm_dma_dispatch(const bf16* A, int lda, const bf16* W, int ldw, con
   return hipGetLastError();
 }
 
-// Large-M projections (measured on MI355X at M = 8192).  The tile loads are
-// bounded by how many L1 misses a CU keeps in flight, so bytes per FLOP --
-// (BM + BN) / (BM BN) -- decide: 256 x 288 tiles (8 waves of 64 x 144) where
-// N is a multiple of 288 and leaves whole rounds of tiles (fc1: N = 4608 ->
-// 512 tiles), else 256 x 144 tiles (8 waves of 32 x 144, three stages).  The
-// widths of the 3072-wide joint-attention model (3072, 12288) take 256 x 192
-// tiles (8 waves of 64 x 96; 4096 rows -> 256 or 1024 tiles), else 256 x 128.
-// All load with cache policy bit 0 (sc0) set, which measured faster.
+// Large-M projections (tile shapes and orders measured on MI355X at the DiT's
+// and the joint-attention model's shapes).  A CU moves ~17 bytes per clock
+// from L2 into LDS whatever the tile, so bytes per FLOP -- (BM + BN) / (BM BN)
+// -- decide, together with filling whole rounds of 256 workgroups:
+//   256 x 288 (8 waves of 64 x 144) where N is a multiple of 288 and the tiles
+//             make whole rounds (fc1: N = 4608, M = 8192 -> 512 tiles);
+//   256 x 256 for long K where N is a multiple of 256 with whole rounds
+//             (joint-attention MLP up-projection: N = 12288 -> 768 tiles);
+//   256 x 144 (8 waves of 32 x 144, three stages) for the other DiT widths;
+//   256 x 192 (8 waves of 64 x 96) where that fills whole rounds (N = 3072);
+//   256 x 128 otherwise.
+// Row blocks per tile group (see gemm_dma_kernel): 8 for long K, 2 for the
+// 288-wide tiles at short K, 1 for the 144-wide residual updates.  All load
+// with cache policy bit 0 (sc0) set, which measured faster.
 hipError_t launch_gemm_dma(const bf16* A, int lda, const bf16* W, int ldw, const bf16* bias,
                            int M, int N, int K, int kind, const Epi& epi, int vec_ok,
                            hipStream_t st) {
   const long mt = (M + 255) / 256;
+  const bool longk = K >= 2048;
   if (N % 288 == 0 && (mt * (N / 288)) % 256 == 0)
-    return gemm_dma_dispatch<256, 288, 4, 2, 2, 1>(A, lda, W, ldw, bias, M, N, K, kind, epi, vec_ok, st);
-  if (N % 144 == 0)
-    return gemm_dma_dispatch<256, 144, 8, 1, 3, 1>(A, lda, W, ldw, bias, M, N, K, kind, epi, vec_ok, st);
+    return gemm_dma_dispatch<256, 288, 4, 2, 2, 1>(A, lda, W, ldw, bias, M, N, K, kind, epi, vec_ok,
+                                                   longk ? 8 : 2, st);
+  if (longk && N % 256 == 0 && (mt * (N / 256)) % 256 == 0)
+    return gemm_dma_dispatch<256, 256, 4, 2, 2, 1>(A, lda, W, ldw, bias, M, N, K, kind, epi, vec_ok,
+                                                   8, st);
+  if (N % 144 == 0) {
+    const int gm = longk ? 8 : (kind == EPI_RESID || kind == EPI_RESID_GATED) ? 1 : 8;
+    return gemm_dma_dispatch<256, 144, 8, 1, 3, 1>(A, lda, W, ldw, bias, M, N, K, kind, epi, vec_ok,
+                                                   gm, st);
+  }
   if (N % 192 == 0 && (mt * (N / 192)) % 256 == 0)
-    return gemm_dma_dispatch<256, 192, 4, 2, 2, 1>(A, lda, W, ldw, bias, M, N, K, kind, epi, vec_ok, st);
-  return gemm_dma_dispatch<256, 128, 4, 2, 3, 1>(A, lda, W, ldw, bias, M, N, K, kind, epi, vec_ok, st);
+    return gemm_dma_dispatch<256, 192, 4, 2, 2, 1>(A, lda, W, ldw, bias, M, N, K, kind, epi, vec_ok,
+                                                   8, st);
+  return gemm_dma_dispatch<256, 128, 4, 2, 3, 1>(A, lda, W, ldw, bias, M, N, K, kind, epi, vec_ok, 8,
+                                                 st);
 }
 
 }  // namespace t2i

@@ -78,6 +78,32 @@ def test_linear_bf16_residual_epilogues(M, N, K):
     assert rel_l2(x.cpu().numpy().astype(np.float64) - x0, gate * ref) < 1e-4
 
 
+WIDE_SHAPES = [(4096, 12288, 3072, 1), (4096, 9216, 3072, 0), (4096, 3072, 3072, 4),
+               (4096, 3072, 12288, 4), (3000, 3072, 3072, 0), (2048, 4096, 2048, 1)]
+
+
+@pytest.mark.parametrize("M,N,K,epi", WIDE_SHAPES)
+def test_linear_bf16_wide_sampled_rows(M, N, K, epi):
+    """The 3072-wide model's projections (256x256 / 256x192 / 256x128 tiles,
+    long K) on sampled rows."""
+    say(f"linear bf16 wide {M}x{N}x{K} epi {epi}")
+    A, W, b = rnd(60, (M, K)), rnd(61, (N, K), 0.03), rnd(62, (N,), 0.1)
+    x0 = rnd(63, (M, N), bf=False) if epi >= 3 else None
+    gate = rnd(64, (N,), 0.5, bf=False) if epi == 4 else None
+    out, x, _ = run_linear(_lib.T2I_BF16, epi, A, W, b, resid=x0, gate=gate)
+    rows = np.r_[np.arange(0, M, 97), M - 1]
+    ref = dit.linear(A[rows].astype(np.float64), W.astype(np.float64), b.astype(np.float64))
+    if epi == 0:
+        got = to_host(out)[rows]
+    elif epi == 1:
+        got, ref = to_host(out)[rows], dit.gelu_tanh(ref)
+    else:
+        got, ref = x.cpu().numpy().astype(np.float64)[rows] - x0[rows], gate * ref
+    err = rel_l2(got, ref)
+    say(f"  rel_l2 {err:.2e}")
+    assert err < (3e-3 if epi < 3 else 1e-4)
+
+
 @pytest.mark.parametrize("M,N,K,epi", [(64, 128, 256, 0), (100, 520, 128, 2), (77, 33, 90, 4)])
 def test_linear_f32(M, N, K, epi):
     A, W, b = rnd(10, (M, K), bf=False), rnd(11, (N, K), 0.05, bf=False), rnd(12, (N,), 0.1, bf=False)
