@@ -72,14 +72,14 @@ __device__ __forceinline__ void decode_tile(const AttnMap& m, int heads, int L, 
   j = t - m.tile_start[s];
 }
 
-template <int HD>
-__global__ __launch_bounds__(512, 1) void attn_bf16_kernel(AttnMap map, int heads,
+template <int HD, int NW, int ST>
+__global__ __launch_bounds__(NW * 64, 8 / NW) void attn_bf16_kernel(AttnMap map, int heads,
                                                            const bf16* __restrict__ Q, int ldq,
                                                            const bf16* __restrict__ K, int ldk,
                                                            const bf16* __restrict__ Vt, int ldvt,
                                                            bf16* __restrict__ O, int ldo,
                                                            float scale_log2) {
-  constexpr int NW = 8, BQ = NW * 32, BKV = 64, ST = 4;
+  constexpr int BQ = NW * 32, BKV = 64;
   // 16-wide chunks of the S^T = K Q^T contraction: d = 0 .. HD-1, then one
   // more slot (d = HD) that carries the softmax shift: K has 1 there and Q has
   // -m, so the MFMA itself returns s - m
@@ -151,8 +151,8 @@ __global__ __launch_bounds__(512, 1) void attn_bf16_kernel(AttnMap map, int head
   //   K (i < CPR): row r = key swap23(r), chunk slot swizzled; keys past the
   //     sequence are clamped to its last key (their scores are masked);
   //   V^T (i >= CPR): row d, 128 bytes = 64 keys, chunk slot c ^ ((d>>1)&7);
-  //     chunks past the sequence are read from its first chunk and zeroed
-  //     in LDS before use.
+  //     chunks wholly past the sequence are read from the tile's first chunk
+  //     (their probabilities are 0).
   // Wave w issues instructions w, w+8, ...: n_w per tile.
   constexpr int IPW = (NI + NW - 1) / NW;
   int g_off[IPW], g_key[IPW], l_off[IPW];
@@ -249,14 +249,21 @@ __global__ __launch_bounds__(512, 1) void attn_bf16_kernel(AttnMap map, int head
     attn_barrier();
     if (ti + ST - 1 < nt) issue(ti + ST - 1);     // into the stage of tile ti-1
     if (kv0 + BKV > k_end) {
-      // ragged tile: zero V^T columns past the sequence (their probabilities
-      // are 0, but the copied bytes need not be finite) and mask the scores
-      const int v0 = k_end - kv0;
-      char* vb = vst(ti % ST);
-      for (int i = tid; i < HD * 64; i += NW * 64) {
-        const int d = i >> 6, col = i & 63;
-        if (col >= v0)
-          *(bf16*)(vb + d * 128 + (((col >> 3) ^ ((d >> 1) & 7)) << 4) + (col & 7) * 2) = (bf16)0.f;
+      // ragged tile: mask the scores past the sequence.  V^T chunks wholly
+      // past it were copied from the tile's first chunk, finite when the
+      // sequence length is a multiple of 8.  Otherwise a chunk the sequence
+      // ends inside holds bytes from beyond it (and may have been copied):
+      // zero every column past the sequence (their probabilities are 0)
+      if (k_end & 7) {
+        const int c0 = k_end - kv0;
+        char* vb = vst(ti % ST);
+        for (int i = tid; i < HD * 64; i += NW * 64) {
+          const int d = i >> 6, col = i & 63;
+          if (col >= c0)
+            *(bf16*)(vb + d * 128 + (((col >> 3) ^ ((d >> 1) & 7)) << 4) + (col & 7) * 2) =
+                (bf16)0.f;
+        }
+        attn_barrier();
       }
 #pragma unroll
       for (int kb = 0; kb < 2; ++kb)
@@ -265,7 +272,6 @@ __global__ __launch_bounds__(512, 1) void attn_bf16_kernel(AttnMap map, int head
           if (kv0 + swap23(32 * kb + 8 * (e >> 2) + 4 * hl + (e & 3)) >= k_end)
             cur[kb][e] = -INFINITY;
       lm = lane_max(cur);
-      attn_barrier();
     }
     if (ti == 0 || __any(lm > 8.0f)) {
       // new maximum: the query's 64 scores sit in lanes ql and ql + 32
@@ -411,9 +417,10 @@ __global__ __launch_bounds__(64) void attn_f32_kernel(AttnMap map, int heads,
 }
 
 // bf16: 8 waves x 32 queries per workgroup; fp32: 64 queries
+constexpr int kAttnWaves = 8, kAttnStages = 4;
 int attention_query_tile(bool bf16_io, int head_dim) {
   (void)head_dim;
-  return bf16_io ? 256 : 64;
+  return bf16_io ? kAttnWaves * 32 : 64;
 }
 
 template <int HD>
@@ -424,7 +431,8 @@ static hipError_t launch_hd(bool bf16_io, int heads, const AttnMap& map, const v
   if (tiles == 0) return hipSuccess;
   if (bf16_io) {
     const float scale_log2 = 1.4426950408889634f / sqrtf((float)HD);
-    hipLaunchKernelGGL((attn_bf16_kernel<HD>), dim3(tiles), dim3(512), 0, st, map, heads,
+    hipLaunchKernelGGL((attn_bf16_kernel<HD, kAttnWaves, kAttnStages>), dim3(tiles),
+                       dim3(kAttnWaves * 64), 0, st, map, heads,
                        (const bf16*)q, ldq, (const bf16*)k, ldk, (const bf16*)v, ldv, (bf16*)o, ldo,
                        scale_log2);
   } else {
