@@ -71,6 +71,8 @@ t2i_status t2i_op_attention(int32_t dtype, int32_t heads, int32_t head_dim,
  * LayerNorm (no affine, biased variance) fused with adaLN modulation:
  * out = (x - mean) / sqrt(var + eps) * (1 + scale) + shift per row of
  * x [rows, D] fp32; shift, scale fp32 [D]; out dtype (bf16 or fp32) [rows, D].
+ * D % 4 == 0, D <= 3072; x and shift 16-byte aligned, out 8-byte (bf16) or
+ * 16-byte (fp32) aligned.
  */
 t2i_status t2i_op_ln_modulate(int32_t dtype, int32_t rows, int32_t D,
                               const float* x, const float* shift,

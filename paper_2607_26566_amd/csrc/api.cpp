@@ -137,7 +137,7 @@ const char* check_config(const t2i_dit_config* c) {
 // workspace layout
 
 struct Layout {
-  size_t x, x0, h, xb, qkv, vt, o, u, ytxt, kv, vtt, rope, tfreq, th1, tsc, mod, partial, total;
+  size_t x, x0, h, xb, qkv, vt, o, u, ytxt, kv, vtt, rope, pe, tfreq, th1, tsc, mod, partial, total;
   int ldvt = 0, ldvt_txt = 0;   // token strides of the transposed V buffers
 };
 
@@ -174,6 +174,7 @@ Layout layout(const t2i_dit_config& c) {
   L.kv = take(c.arch == T2I_ARCH_CROSS_DIT ? (size_t)c.depth * txt_rows * 2 * D * A : 0);
   L.vtt = take(c.arch == T2I_ARCH_CROSS_DIT && bfv ? (size_t)c.depth * D * L.ldvt_txt * 2 : 0);
   L.rope = take(mm ? (size_t)(4096 / c.patch) * (c.head_dim / 4) * sizeof(float2) : 0);
+  L.pe = take(mm ? 0 : (size_t)(4096 / c.patch) * (c.hidden / 4) * sizeof(float2));
   L.tfreq = take(Tt * c.freq_dim * 4);
   L.th1 = take(Tt * D * 4);
   L.tsc = take(Tt * D * 4);
@@ -237,7 +238,7 @@ struct Plan {
   AttnMap self{}, cross{};
   AttnMap joint{};   // MMDiT: per sequence a text and an image query group,
                      // keys = the sequence's text rows, then its image rows
-  int rope_pos = 0;  // largest grid side (MMDiT RoPE table length)
+  int grid_max = 0;  // largest grid side (length of the position tables)
   size_t lat_floats = 0;
 };
 
@@ -327,9 +328,9 @@ t2i_status build_plan(t2i_dit* h, int n_req, const int32_t* lat_h, const int32_t
     P.txt.start[P.txt.n] = P.txt_rows;
     P.joint.n = 2 * P.img.n;
     P.joint.tile_start[P.joint.n] = jt;
-    for (int r = 0; r < n_req; ++r)
-      P.rope_pos = std::max(P.rope_pos, std::max(lat_h[r], lat_w[r]) / c.patch);
   }
+  for (int r = 0; r < n_req; ++r)
+    P.grid_max = std::max(P.grid_max, std::max(lat_h[r], lat_w[r]) / c.patch);
   return T2I_OK;
 }
 
@@ -340,6 +341,16 @@ void set_modrows(Plan& P, int base) {
 }
 
 bool is_mmdit(const t2i_dit* h) { return h->cfg.arch == T2I_ARCH_MMDIT; }
+
+// Patch embedding of the call's latents into x0 (and `copies` copies into xi);
+// the cross-attention DiT adds its 2D sin-cos position embedding.
+hipError_t embed(t2i_dit* h, const Plan& P, const float* lat, float* x0, float* xi, int copies,
+                 hipStream_t st) {
+  const t2i_dit_config& c = h->cfg;
+  float2* pe = is_mmdit(h) ? nullptr : h->at<float2>(h->L.pe);
+  return launch_embed(lat, P.rm, h->w[W_PE], h->w[B_PE], h->bf(), c.hidden, c.latent_channels,
+                      c.patch, pe, P.grid_max, x0, xi, copies, st);
+}
 // first residual row of the image stream
 int img_row0(const t2i_dit* h, const Plan& P) { return is_mmdit(h) ? P.txt_rows : 0; }
 
@@ -416,7 +427,7 @@ t2i_status text_prep(t2i_dit* h, const Plan& P, const void* prompt, hipStream_t 
     if (P.branches == 2)
       HIP_TRY(h, launch_bias_rows_f32(h->w[B_Y], h->bf(), P.n_req * M, D,
                                       (float*)ytxt + (size_t)P.n_req * M * D, st));
-    HIP_TRY(h, launch_rope_table(h->at<float2>(h->L.rope), P.rope_pos, c.head_dim / 4, st));
+    HIP_TRY(h, launch_rope_table(h->at<float2>(h->L.rope), P.grid_max, c.head_dim / 4, st));
     return T2I_OK;
   }
   HIP_TRY(h, linear(h, prompt, c.text_dim, W_Y, P.n_req * M, D, c.text_dim, EPI_STORE, e, st));
@@ -493,13 +504,13 @@ t2i_status run_blocks_cross(t2i_dit* h, const Plan& P, int nb, hipStream_t st) {
       e.vcol0 = 2 * D;
       TIMED(h, T2I_K_GEMM_QKV, st, linear(h, hb, D, wb + X_QKV, R, 3 * D, D, EPI_SPLIT_VT, e, st));
       TIMED(h, T2I_K_ATTN_SELF, st,
-            launch_attention(bf, c.heads, c.head_dim, P.self, qkv, 2 * D, qkv + D * A, 2 * D, vt,
+            launch_attention(bf, 0, c.heads, c.head_dim, P.self, qkv, 2 * D, qkv + D * A, 2 * D, vt,
                              h->L.ldvt, o, D, st));
     } else {
       e.ldo = 3 * D;
       TIMED(h, T2I_K_GEMM_QKV, st, linear(h, hb, D, wb + X_QKV, R, 3 * D, D, EPI_STORE, e, st));
       TIMED(h, T2I_K_ATTN_SELF, st,
-            launch_attention(bf, c.heads, c.head_dim, P.self, qkv, 3 * D, qkv + D * A, 3 * D,
+            launch_attention(bf, 0, c.heads, c.head_dim, P.self, qkv, 3 * D, qkv + D * A, 3 * D,
                              qkv + 2 * D * A, 3 * D, o, D, st));
     }
     e = make_epi();
@@ -519,12 +530,12 @@ t2i_status run_blocks_cross(t2i_dit* h, const Plan& P, int nb, hipStream_t st) {
     const char* kv = h->at<char>(h->L.kv) + (size_t)b * txt_rows_max * 2 * D * A;
     if (bf)
       TIMED(h, T2I_K_ATTN_CROSS, st,
-            launch_attention(bf, c.heads, c.head_dim, P.cross, qkv, D, kv, D,
+            launch_attention(bf, 1, c.heads, c.head_dim, P.cross, qkv, D, kv, D,
                              h->at<bf16>(h->L.vtt) + (size_t)b * D * h->L.ldvt_txt,
                              h->L.ldvt_txt, o, D, st));
     else
       TIMED(h, T2I_K_ATTN_CROSS, st,
-            launch_attention(bf, c.heads, c.head_dim, P.cross, qkv, D, kv, 2 * D, kv + D * A,
+            launch_attention(bf, 1, c.heads, c.head_dim, P.cross, qkv, D, kv, 2 * D, kv + D * A,
                              2 * D, o, D, st));
     e = make_epi();
     e.x = x;
@@ -583,7 +594,7 @@ t2i_status run_blocks_mmdit(t2i_dit* h, const Plan& P, int nb, hipStream_t st) {
     HIP_TRY(h, launch_rope_apply(qkv, 2 * D, P.txt_rows, P.rm, c.heads, c.head_dim, c.patch, rope,
                                  st));
     TIMED(h, T2I_K_ATTN_SELF, st,
-          launch_attention(true, c.heads, c.head_dim, P.joint, qkv, 2 * D, qkv + D, 2 * D, vt,
+          launch_attention(true, 0, c.heads, c.head_dim, P.joint, qkv, 2 * D, qkv + D, 2 * D, vt,
                            h->L.ldvt, o, D, st));
     for (int s = 0; s < 2; ++s) {
       const int r0 = r0s[s], R = ns[s], wi = W_BLOCK0 + b * 2 * J_PER_STREAM + s * J_PER_STREAM;
@@ -669,10 +680,8 @@ t2i_status step_body(t2i_dit* h, Plan& P, const float* latents_in, float* latent
   const int D = c.hidden;
   float* x = h->at<float>(h->L.x);
   float* x0 = h->at<float>(h->L.x0);
-  const bool pe = c.arch == T2I_ARCH_CROSS_DIT;
   float* xi = x + (size_t)img_row0(h, P) * D;   // image stream of the residual
-  HIP_TRY(h, launch_embed(latents_in, P.rm, h->w[W_PE], h->w[B_PE], h->bf(), D,
-                          c.latent_channels, c.patch, pe, x0, xi, P.branches, st));
+  HIP_TRY(h, embed(h, P, latents_in, x0, xi, P.branches, st));
   if (is_mmdit(h))
     HIP_TRY(h, hipMemcpyAsync(x, h->at<float>(h->L.ytxt), (size_t)P.txt_rows * D * 4,
                               hipMemcpyDeviceToDevice, st));
@@ -876,9 +885,7 @@ t2i_status t2i_cache_check(t2i_dit* h, const t2i_cache_args* a, void* stream) {
   hipStream_t st = (hipStream_t)stream;
   set_modrows(P, 0);
   if ((s = conditioning(h, a->t, P.n_req, 1, st)) != T2I_OK) return s;
-  HIP_TRY(h, launch_embed(a->latents, P.rm, h->w[W_PE], h->w[B_PE], h->bf(), c.hidden,
-                          c.latent_channels, c.patch, c.arch == T2I_ARCH_CROSS_DIT,
-                          h->at<float>(h->L.x0), h->at<float>(h->L.x), 0, st));
+  HIP_TRY(h, embed(h, P, a->latents, h->at<float>(h->L.x0), h->at<float>(h->L.x), 0, st));
   return cache_check_impl(h, P, a->step, a->n_steps, a->tau, a->mode, a->cache_state, a->rel_l1,
                           a->skip, st);
 }
@@ -919,9 +926,7 @@ t2i_status t2i_dit_sample(t2i_dit* h, const t2i_sample_args* a, void* stream) {
     for (int r = 0; r < R; ++r)
       P.rm.dt[r] = (float)(ts[(size_t)(k + 1) * R + r] - ts[(size_t)k * R + r]);
     if (use_cache) {
-      HIP_TRY(h, launch_embed(a->latents, P.rm, h->w[W_PE], h->w[B_PE], h->bf(), c.hidden,
-                              c.latent_channels, c.patch, c.arch == T2I_ARCH_CROSS_DIT,
-                              h->at<float>(h->L.x0), h->at<float>(h->L.x), 0, st));
+      HIP_TRY(h, embed(h, P, a->latents, h->at<float>(h->L.x0), h->at<float>(h->L.x), 0, st));
       if ((s = cache_check_impl(h, P, k, n, a->cache_tau, a->cache_mode, a->cache_state,
                                 rel.data(), skip.data(), st)) != T2I_OK)
         return s;
@@ -1026,7 +1031,7 @@ t2i_status t2i_op_attention(int32_t dtype, int32_t heads, int32_t head_dim, int3
     tiles += (q_len[s] + BQ - 1) / BQ;
   }
   m.tile_start[n_seq] = tiles;
-  hipError_t err = launch_attention(dtype == T2I_BF16, heads, head_dim, m, q, ldq, k, ldk, v, ldv,
+  hipError_t err = launch_attention(dtype == T2I_BF16, 0, heads, head_dim, m, q, ldq, k, ldk, v, ldv,
                                     o, ldo, (hipStream_t)stream);
   if (err != hipSuccess) return ops_fail(T2I_ERR_DEVICE, hipGetErrorString(err));
   return T2I_OK;
@@ -1039,6 +1044,8 @@ t2i_status t2i_op_ln_modulate(int32_t dtype, int32_t rows, int32_t D, const floa
   if (rows < 1 || D < 4 || D % 4 || D > 3072) return ops_fail(T2I_ERR_SHAPE, "bad shape");
   if (!x || !shift || !scale || !out) return ops_fail(T2I_ERR_INVALID_ARG, "NULL pointer");
   if (scale != shift + D) return ops_fail(T2I_ERR_INVALID_ARG, "scale must follow shift (scale == shift + D)");
+  if ((uintptr_t)x % 16 || (uintptr_t)shift % 16 || (uintptr_t)out % (dtype == T2I_BF16 ? 8 : 16))
+    return ops_fail(T2I_ERR_INVALID_ARG, "x, shift need 16-byte and out 8 (bf16) / 16-byte alignment");
   SeqMap m;
   std::memset(&m, 0, sizeof(m));
   m.n = 1;

@@ -72,7 +72,9 @@ __device__ __forceinline__ void decode_tile(const AttnMap& m, int heads, int L, 
   j = t - m.tile_start[s];
 }
 
-template <int HD, int NW, int ST>
+// ROLE: 0 = self / joint attention, 1 = cross-attention to text (separate
+// instances, so that profiles tell them apart)
+template <int HD, int NW, int ST, int ROLE>
 __global__ __launch_bounds__(NW * 64, 8 / NW) void attn_bf16_kernel(AttnMap map, int heads,
                                                            const bf16* __restrict__ Q, int ldq,
                                                            const bf16* __restrict__ K, int ldk,
@@ -424,17 +426,21 @@ int attention_query_tile(bool bf16_io, int head_dim) {
 }
 
 template <int HD>
-static hipError_t launch_hd(bool bf16_io, int heads, const AttnMap& map, const void* q, int ldq,
-                            const void* k, int ldk, const void* v, int ldv, void* o, int ldo,
-                            hipStream_t st) {
+static hipError_t launch_hd(bool bf16_io, int role, int heads, const AttnMap& map, const void* q,
+                            int ldq, const void* k, int ldk, const void* v, int ldv, void* o,
+                            int ldo, hipStream_t st) {
   const int tiles = map.tile_start[map.n] * heads;
   if (tiles == 0) return hipSuccess;
   if (bf16_io) {
     const float scale_log2 = 1.4426950408889634f / sqrtf((float)HD);
-    hipLaunchKernelGGL((attn_bf16_kernel<HD, kAttnWaves, kAttnStages>), dim3(tiles),
-                       dim3(kAttnWaves * 64), 0, st, map, heads,
-                       (const bf16*)q, ldq, (const bf16*)k, ldk, (const bf16*)v, ldv, (bf16*)o, ldo,
-                       scale_log2);
+    if (role == 1)
+      hipLaunchKernelGGL((attn_bf16_kernel<HD, kAttnWaves, kAttnStages, 1>), dim3(tiles),
+                         dim3(kAttnWaves * 64), 0, st, map, heads, (const bf16*)q, ldq,
+                         (const bf16*)k, ldk, (const bf16*)v, ldv, (bf16*)o, ldo, scale_log2);
+    else
+      hipLaunchKernelGGL((attn_bf16_kernel<HD, kAttnWaves, kAttnStages, 0>), dim3(tiles),
+                         dim3(kAttnWaves * 64), 0, st, map, heads, (const bf16*)q, ldq,
+                         (const bf16*)k, ldk, (const bf16*)v, ldv, (bf16*)o, ldo, scale_log2);
   } else {
     const float scale = 1.0f / sqrtf((float)HD);
     hipLaunchKernelGGL(attn_f32_kernel<HD>, dim3(tiles), dim3(64), 0, st, map, heads,
@@ -444,15 +450,15 @@ static hipError_t launch_hd(bool bf16_io, int heads, const AttnMap& map, const v
   return hipGetLastError();
 }
 
-hipError_t launch_attention(bool bf16_io, int heads, int head_dim, const AttnMap& map,
+hipError_t launch_attention(bool bf16_io, int role, int heads, int head_dim, const AttnMap& map,
                             const void* q, int ldq, const void* k, int ldk, const void* v, int ldv,
                             void* o, int ldo, hipStream_t st) {
   switch (head_dim) {
-    case 8: return launch_hd<8>(bf16_io, heads, map, q, ldq, k, ldk, v, ldv, o, ldo, st);
-    case 32: return launch_hd<32>(bf16_io, heads, map, q, ldq, k, ldk, v, ldv, o, ldo, st);
-    case 64: return launch_hd<64>(bf16_io, heads, map, q, ldq, k, ldk, v, ldv, o, ldo, st);
-    case 72: return launch_hd<72>(bf16_io, heads, map, q, ldq, k, ldk, v, ldv, o, ldo, st);
-    case 128: return launch_hd<128>(bf16_io, heads, map, q, ldq, k, ldk, v, ldv, o, ldo, st);
+    case 8: return launch_hd<8>(bf16_io, role, heads, map, q, ldq, k, ldk, v, ldv, o, ldo, st);
+    case 32: return launch_hd<32>(bf16_io, role, heads, map, q, ldq, k, ldk, v, ldv, o, ldo, st);
+    case 64: return launch_hd<64>(bf16_io, role, heads, map, q, ldq, k, ldk, v, ldv, o, ldo, st);
+    case 72: return launch_hd<72>(bf16_io, role, heads, map, q, ldq, k, ldk, v, ldv, o, ldo, st);
+    case 128: return launch_hd<128>(bf16_io, role, heads, map, q, ldq, k, ldk, v, ldv, o, ldo, st);
     default: return hipErrorInvalidValue;
   }
 }

@@ -18,6 +18,25 @@ constexpr int kMaxV4 = 12;   // float4 per lane: rows up to 3072 wide
 // ---------------------------------------------------------------------------
 // LayerNorm (biased variance, no affine) + modulation.
 
+// Sum over the 64 lanes of a wave, the same value in every lane: DPP steps
+// inside each 16-lane row, then the four row sums read out in a fixed order.
+__device__ __forceinline__ float wave_sum_dpp(float v) {
+  auto add_dpp = [](float x, int y) { return x + __int_as_float(y); };
+  v = add_dpp(v, __builtin_amdgcn_update_dpp(0, __float_as_int(v), 0xB1, 0xF, 0xF, false));  // quad_perm 1,0,3,2
+  v = add_dpp(v, __builtin_amdgcn_update_dpp(0, __float_as_int(v), 0x4E, 0xF, 0xF, false));  // quad_perm 2,3,0,1
+  v = add_dpp(v, __builtin_amdgcn_update_dpp(0, __float_as_int(v), 0x124, 0xF, 0xF, false)); // row_ror 4
+  v = add_dpp(v, __builtin_amdgcn_update_dpp(0, __float_as_int(v), 0x128, 0xF, 0xF, false)); // row_ror 8
+  const int b = __float_as_int(v);
+  return (__int_as_float(__builtin_amdgcn_readlane(b, 0)) +
+          __int_as_float(__builtin_amdgcn_readlane(b, 16))) +
+         (__int_as_float(__builtin_amdgcn_readlane(b, 32)) +
+          __int_as_float(__builtin_amdgcn_readlane(b, 48)));
+}
+
+// One wave per row, four rows per workgroup: many small independent waves
+// keep enough loads in flight (the kernel is bound by memory latency).
+constexpr int kLnRows = 4;
+
 template <typename OutT>
 __global__ __launch_bounds__(256) void ln_mod_kernel(const float* __restrict__ x, int ldx, int rows,
                                                      int D, const float* __restrict__ mod,
@@ -25,10 +44,10 @@ __global__ __launch_bounds__(256) void ln_mod_kernel(const float* __restrict__ x
                                                      SeqMap map, OutT* __restrict__ out, int ldo,
                                                      float eps) {
   const int lane = threadIdx.x & 63;
-  const int row = blockIdx.x * 4 + (threadIdx.x >> 6);
+  const int row = blockIdx.x * kLnRows + (threadIdx.x >> 6);
   if (row >= rows) return;
-  const float4* xr = (const float4*)(x + (size_t)row * ldx);
   const int nv = D >> 2;
+  const float4* xr = (const float4*)(x + (size_t)row * ldx);
   float4 v[kMaxV4];
   float s = 0.f;
 #pragma unroll
@@ -39,7 +58,7 @@ __global__ __launch_bounds__(256) void ln_mod_kernel(const float* __restrict__ x
       s += (v[i].x + v[i].y) + (v[i].z + v[i].w);
     }
   }
-  const float mean = wave_sum(s) / (float)D;
+  const float mean = wave_sum_dpp(s) / (float)D;
   float q = 0.f;
 #pragma unroll
   for (int i = 0; i < kMaxV4; ++i) {
@@ -49,7 +68,7 @@ __global__ __launch_bounds__(256) void ln_mod_kernel(const float* __restrict__ x
       q += (a * a + b * b) + (cc * cc + d * d);
     }
   }
-  const float rstd = 1.0f / sqrtf(wave_sum(q) / (float)D + eps);
+  const float rstd = 1.0f / sqrtf(wave_sum_dpp(q) / (float)D + eps);
   const float* md = mod + (size_t)map.modrow[seq_of_row(map, row)] * ld_mod;
   const float4* sh = (const float4*)(md + shift_off);
   const float4* sc = (const float4*)(md + scale_off);
@@ -59,10 +78,14 @@ __global__ __launch_bounds__(256) void ln_mod_kernel(const float* __restrict__ x
     const int c = lane + 64 * i;
     if (c < nv) {
       const float4 a = sh[c], b = sc[c];
-      orow[4 * c + 0] = from_f32<OutT>((v[i].x - mean) * rstd * (1.f + b.x) + a.x);
-      orow[4 * c + 1] = from_f32<OutT>((v[i].y - mean) * rstd * (1.f + b.y) + a.y);
-      orow[4 * c + 2] = from_f32<OutT>((v[i].z - mean) * rstd * (1.f + b.z) + a.z);
-      orow[4 * c + 3] = from_f32<OutT>((v[i].w - mean) * rstd * (1.f + b.w) + a.w);
+      const float y0 = (v[i].x - mean) * rstd * (1.f + b.x) + a.x;
+      const float y1 = (v[i].y - mean) * rstd * (1.f + b.y) + a.y;
+      const float y2 = (v[i].z - mean) * rstd * (1.f + b.z) + a.z;
+      const float y3 = (v[i].w - mean) * rstd * (1.f + b.w) + a.w;
+      if constexpr (sizeof(OutT) == 2)     // one 8-byte store of four bf16
+        *(bf16x4*)(orow + 4 * c) = bf16x4{(bf16)y0, (bf16)y1, (bf16)y2, (bf16)y3};
+      else
+        *(float4*)(orow + 4 * c) = float4{y0, y1, y2, y3};
     }
   }
 }
@@ -71,7 +94,7 @@ hipError_t launch_ln_modulate(bool bf16_out, int rows, int D, const float* x, in
                               const float* mod, int ld_mod, int shift_off, int scale_off,
                               const SeqMap& map, void* out, int ldo, float eps, hipStream_t st) {
   if (rows <= 0) return hipSuccess;
-  dim3 grid((rows + 3) / 4), block(256);
+  dim3 grid((rows + kLnRows - 1) / kLnRows), block(256);
   if (bf16_out)
     hipLaunchKernelGGL(ln_mod_kernel<bf16>, grid, block, 0, st, x, ldx, rows, D, mod, ld_mod,
                        shift_off, scale_off, map, (bf16*)out, ldo, eps);
@@ -86,57 +109,92 @@ hipError_t launch_ln_modulate(bool bf16_out, int rows, int D, const float* x, in
 // Token i*(w/p)+j of a request reads latent [c, i*p+a, j*p+b] as feature
 // (a*p+b)*C+c.  Writes x0 (one copy) and `copies` copies into x (one per
 // guidance branch, branch-major).
+//
+// pe_table_kernel: tab[pos * qd + f] = (sin, cos)(pos * 10000^(-f/qd)) in fp64,
+// qd = D/4.  embed_kernel: a workgroup takes kEmbTok tokens x 256 channels;
+// the tokens' patches are staged in LDS, each thread keeps its channel's
+// weight row in registers.  The first D/2 channels add the row's sin-cos
+// embedding, the last D/2 the column's; within a half the first D/4 are sin,
+// the next D/4 cos.
+
+__global__ void pe_table_kernel(float2* __restrict__ tab, int npos, int qd) {
+  const int i = blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= npos * qd) return;
+  const int pos = i / qd, f = i - pos * qd;
+  const double ang = (double)pos * pow(10000.0, -(double)f / (double)qd);
+  tab[i] = float2{(float)sin(ang), (float)cos(ang)};
+}
+
+constexpr int kEmbTok = 32;
 
 template <typename TW>
 __global__ __launch_bounds__(256) void embed_kernel(const float* __restrict__ lat, ReqMap rm,
                                                     const TW* __restrict__ w_pe,
                                                     const TW* __restrict__ b_pe, int D, int C,
-                                                    int p, int pos_embed, float* __restrict__ x0,
-                                                    float* __restrict__ x, int copies) {
+                                                    int p, const float2* __restrict__ pe,
+                                                    float* __restrict__ x0, float* __restrict__ x,
+                                                    int copies) {
+  __shared__ float patch[kEmbTok][64];
+  __shared__ int grid_pos[kEmbTok][2];
   const int P = p * p * C;
-  const long total = (long)rm.tokens_total * D;
-  for (long idx = blockIdx.x * 256L + threadIdx.x; idx < total; idx += (long)gridDim.x * 256) {
-    const int tok = (int)(idx / D), d = (int)(idx - (long)tok * D);
-    const int r = req_of_token(rm, tok);
-    const int lt = tok - rm.tok_off[r];
-    const int W = rm.w[r], H = rm.h[r], gw = W / p;
-    const int gi = lt / gw, gj = lt - gi * gw;
-    const float* L = lat + rm.lat_off[r];
-    float acc = to_f32(b_pe[d]);
-    const TW* wr = w_pe + (size_t)d * P;
-    for (int a = 0; a < p; ++a)
-      for (int b = 0; b < p; ++b)
-        for (int c = 0; c < C; ++c)
-          acc = fmaf(to_f32(wr[(a * p + b) * C + c]),
-                     L[(size_t)c * H * W + (size_t)(gi * p + a) * W + gj * p + b], acc);
-    if (pos_embed) {
-      // first D/2 channels: row gi, last D/2: column gj; within a half the
-      // first D/4 are sin(pos w_k), the next D/4 cos(pos w_k), w_k = 10000^(-k/(D/4))
-      const int half = D / 2, qd = D / 4;
-      const int k = d % half;
-      const int pos = d < half ? gi : gj;
-      const int f = k % qd;
-      const double ang = (double)pos * pow(10000.0, -(double)f / (double)qd);
-      acc += (float)(k < qd ? sin(ang) : cos(ang));
+  const int T = rm.tokens_total;
+  const int t0 = blockIdx.x * kEmbTok, d = blockIdx.y * 256 + threadIdx.x;
+  for (int i = threadIdx.x; i < kEmbTok * P; i += 256) {
+    const int t = i / P, k = i - t * P, tok = t0 + t;
+    float v = 0.f;
+    if (tok < T) {
+      const int r = req_of_token(rm, tok);
+      const int lt = tok - rm.tok_off[r];
+      const int W = rm.w[r], H = rm.h[r], gw = W / p;
+      const int gi = lt / gw, gj = lt - gi * gw;
+      const int c = k % C, ab = k / C, a = ab / p, b = ab - a * p;
+      v = lat[rm.lat_off[r] + (size_t)c * H * W + (size_t)(gi * p + a) * W + gj * p + b];
+      if (k == 0) {
+        grid_pos[t][0] = gi;
+        grid_pos[t][1] = gj;
+      }
+    }
+    patch[t][k] = v;
+  }
+  __syncthreads();
+  if (d >= D) return;
+  float w[64];
+#pragma unroll
+  for (int k = 0; k < 64; ++k) w[k] = k < P ? to_f32(w_pe[(size_t)d * P + k]) : 0.f;
+  const float bias = to_f32(b_pe[d]);
+  const int half = D / 2, qd = D / 4, kk = d % half, f = kk % qd;
+  for (int t = 0; t < kEmbTok; ++t) {
+    const int tok = t0 + t;
+    if (tok >= T) break;
+    float acc = bias;
+#pragma unroll
+    for (int k = 0; k < 64; ++k)
+      if (k < P) acc = fmaf(w[k], patch[t][k], acc);
+    if (pe) {
+      const float2 sc = pe[grid_pos[t][d < half ? 0 : 1] * qd + f];
+      acc += kk < qd ? sc.x : sc.y;
     }
     x0[(size_t)tok * D + d] = acc;
-    for (int cp = 0; cp < copies; ++cp) x[((size_t)cp * rm.tokens_total + tok) * D + d] = acc;
+    for (int cp = 0; cp < copies; ++cp) x[((size_t)cp * T + tok) * D + d] = acc;
   }
 }
 
 hipError_t launch_embed(const float* lat, const ReqMap& rm, const void* w_pe, const void* b_pe,
-                        bool w_bf16, int D, int C, int p, bool pos_embed, float* x0, float* x,
-                        int copies, hipStream_t st) {
-  const long total = (long)rm.tokens_total * D;
-  if (total == 0) return hipSuccess;
-  const int grid = (int)std::min<long>((total + 255) / 256, 8192);
+                        bool w_bf16, int D, int C, int p, float2* pe_table, int pe_npos,
+                        float* x0, float* x, int copies, hipStream_t st) {
+  if (rm.tokens_total == 0) return hipSuccess;
+  if (pe_table) {
+    const int n = pe_npos * (D / 4);
+    hipLaunchKernelGGL(pe_table_kernel, dim3((n + 255) / 256), dim3(256), 0, st, pe_table, pe_npos,
+                       D / 4);
+  }
+  dim3 grid((rm.tokens_total + kEmbTok - 1) / kEmbTok, (D + 255) / 256);
   if (w_bf16)
-    hipLaunchKernelGGL(embed_kernel<bf16>, dim3(grid), dim3(256), 0, st, lat, rm, (const bf16*)w_pe,
-                       (const bf16*)b_pe, D, C, p, pos_embed ? 1 : 0, x0, x, copies);
+    hipLaunchKernelGGL(embed_kernel<bf16>, grid, dim3(256), 0, st, lat, rm, (const bf16*)w_pe,
+                       (const bf16*)b_pe, D, C, p, pe_table, x0, x, copies);
   else
-    hipLaunchKernelGGL(embed_kernel<float>, dim3(grid), dim3(256), 0, st, lat, rm,
-                       (const float*)w_pe, (const float*)b_pe, D, C, p, pos_embed ? 1 : 0, x0, x,
-                       copies);
+    hipLaunchKernelGGL(embed_kernel<float>, grid, dim3(256), 0, st, lat, rm, (const float*)w_pe,
+                       (const float*)b_pe, D, C, p, pe_table, x0, x, copies);
   return hipGetLastError();
 }
 

@@ -169,7 +169,8 @@ hipError_t launch_linear_rows(const float* A, int lda, const void* W, int ldw, b
                               const void* bias, int M, int N, int K, int kind, const Epi& epi,
                               hipStream_t st);
 
-hipError_t launch_attention(bool bf16_io, int heads, int head_dim, const AttnMap& map,
+// role: 0 self / joint attention, 1 cross-attention (same kernel, own instance)
+hipError_t launch_attention(bool bf16_io, int role, int heads, int head_dim, const AttnMap& map,
                             const void* q, int ldq, const void* k, int ldk, const void* v,
                             int ldv, void* o, int ldo, hipStream_t st);
 int attention_query_tile(bool bf16_io, int head_dim);
@@ -178,9 +179,11 @@ hipError_t launch_ln_modulate(bool bf16_out, int rows, int D, const float* x, in
                               const float* mod, int ld_mod, int shift_off, int scale_off,
                               const SeqMap& map, void* out, int ldo, float eps, hipStream_t st);
 
+// pe_table: workspace for the 2D sin-cos table (pe_npos x D/4 float2), NULL
+// for no position embedding; pe_npos = largest grid side of the call
 hipError_t launch_embed(const float* lat, const ReqMap& rm, const void* w_pe, const void* b_pe,
-                        bool w_bf16, int D, int C, int p, bool pos_embed, float* x0, float* x,
-                        int copies, hipStream_t st);
+                        bool w_bf16, int D, int C, int p, float2* pe_table, int pe_npos,
+                        float* x0, float* x, int copies, hipStream_t st);
 
 // t: HOST array of `rows` timesteps (launched in chunks of kTValsChunk).
 hipError_t launch_timestep_freq(const double* t, int rows, int freq_dim, double t_scale,
