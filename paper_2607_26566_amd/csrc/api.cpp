@@ -137,7 +137,9 @@ const char* check_config(const t2i_dit_config* c) {
 // workspace layout
 
 struct Layout {
-  size_t x, x0, h, xb, qkv, vt, o, u, ytxt, kv, vtt, rope, pe, tfreq, th1, tsc, mod, partial, total;
+  size_t x, x0, h, xb, qkv, vt, o, u, ytxt, kv, vtt, rope, pe, splitk, tfreq, th1, tsc, mod, partial,
+      total;
+  size_t splitk_floats = 0;
   int ldvt = 0, ldvt_txt = 0;   // token strides of the transposed V buffers
 };
 
@@ -175,6 +177,10 @@ Layout layout(const t2i_dit_config& c) {
   L.vtt = take(c.arch == T2I_ARCH_CROSS_DIT && bfv ? (size_t)c.depth * D * L.ldvt_txt * 2 : 0);
   L.rope = take(mm ? (size_t)(4096 / c.patch) * (c.head_dim / 4) * sizeof(float2) : 0);
   L.pe = take(mm ? 0 : (size_t)(4096 / c.patch) * (c.hidden / 4) * sizeof(float2));
+  // split-K partial sums of the text stream's narrow projections (at most 4
+  // slices of up to 2047 rows)
+  L.splitk_floats = mm ? (size_t)4 * std::min<size_t>(txt_rows, 2047) * D : 0;
+  L.splitk = take(L.splitk_floats * 4);
   L.tfreq = take(Tt * c.freq_dim * 4);
   L.th1 = take(Tt * D * 4);
   L.tsc = take(Tt * D * 4);
@@ -360,14 +366,16 @@ Epi make_epi() {
   return e;
 }
 
-// y = A W^T + b with the config's operand type.
+// y = A W^T + b with the config's operand type.  allow_split lets a
+// short-M, long-K layer split K (MMDiT text stream).
 hipError_t linear(t2i_dit* h, const void* A, int lda, int wi, int M, int N, int K, int kind,
-                  Epi epi, hipStream_t st) {
+                  Epi epi, hipStream_t st, bool allow_split = false) {
   const void* W = h->w[wi];
   const void* B = h->w[wi + 1];
   if (h->bf())
     return launch_gemm_bf16((const bf16*)A, lda, (const bf16*)W, K, (const bf16*)B, M, N, K, kind,
-                            epi, st);
+                            epi, allow_split ? h->at<float>(h->L.splitk) : nullptr,
+                            allow_split ? h->L.splitk_floats : 0, st);
   return launch_gemm_f32((const float*)A, lda, W, K, false, B, M, N, K, kind, epi, st);
 }
 
@@ -606,7 +614,7 @@ t2i_status run_blocks_mmdit(t2i_dit* h, const Plan& P, int nb, hipStream_t st) {
       e.ld_gate = mw;
       e.map = *maps[s];
       TIMED(h, T2I_K_GEMM_O, st,
-            linear(h, o + (size_t)r0 * D, D, wi + J_O, R, D, D, EPI_RESID_GATED, e, st));
+            linear(h, o + (size_t)r0 * D, D, wi + J_O, R, D, D, EPI_RESID_GATED, e, st, s == 0));
       TIMED(h, T2I_K_LN, st, launch_ln_modulate(true, R, D, x + (size_t)r0 * D, D, mod, mw,
                                                  mo + 3 * D, mo + 4 * D, *maps[s],
                                                  hb + (size_t)r0 * D, D, c.ln_eps, st));
@@ -617,7 +625,7 @@ t2i_status run_blocks_mmdit(t2i_dit* h, const Plan& P, int nb, hipStream_t st) {
             linear(h, hb + (size_t)r0 * D, D, wi + J_FC1, R, F, D, EPI_GELU, f, st));
       e.gate = mod + mo + 5 * D;
       TIMED(h, T2I_K_GEMM_FC2, st,
-            linear(h, u + (size_t)r0 * F, F, wi + J_FC2, R, D, F, EPI_RESID_GATED, e, st));
+            linear(h, u + (size_t)r0 * F, F, wi + J_FC2, R, D, F, EPI_RESID_GATED, e, st, s == 0));
     }
   }
   return T2I_OK;
@@ -984,7 +992,7 @@ t2i_status t2i_op_linear(int32_t dtype, int32_t epilogue, int32_t M, int32_t N, 
   hipStream_t st = (hipStream_t)stream;
   hipError_t err = dtype == T2I_BF16
                        ? launch_gemm_bf16((const bf16*)A, lda, (const bf16*)W, ldw, (const bf16*)bias,
-                                          M, N, K, epilogue, e, st)
+                                          M, N, K, epilogue, e, nullptr, 0, st)
                        : launch_gemm_f32((const float*)A, lda, W, ldw, false, bias, M, N, K,
                                          epilogue, e, st);
   if (err != hipSuccess) return ops_fail(T2I_ERR_DEVICE, hipGetErrorString(err));

@@ -20,6 +20,9 @@
 // gated residual add (gate row chosen by the row's sequence), and split-store
 // for fused q|k|v projections: q and k row-major, v transposed (V^T[d][token],
 // four tokens per 8-byte store) so attention can stage V^T tiles directly.
+#include <algorithm>
+#include <cstring>
+
 #include "t2i_internal.h"
 
 namespace t2i {
@@ -77,6 +80,15 @@ template <int BM, int BN, int WGM, int KIND>
 __global__ __launch_bounds__(256, 1) void gemm_bf16_kernel(
     const bf16* __restrict__ A, int lda, const bf16* __restrict__ W, int ldw,
     const bf16* __restrict__ bias, int M, int N, int K, Epi epi, int tiles_n, int vec_ok) {
+  // split-K: workgroup row blockIdx.y takes K columns [y K, (y+1) K) and
+  // writes its partial sums to slice y of the fp32 output
+  constexpr bool PART = KIND == EPI_PARTIAL;
+  constexpr int EK = PART ? EPI_STORE_F32 : KIND;
+  if (PART) {
+    A += (size_t)blockIdx.y * K;
+    W += (size_t)blockIdx.y * K;
+    epi.out = (float*)epi.out + (size_t)blockIdx.y * M * epi.ldo;
+  }
   constexpr int BK = 64;
   constexpr int LDK = BK + 8;
   constexpr int WGN = 4 / WGM;
@@ -173,14 +185,15 @@ __global__ __launch_bounds__(256, 1) void gemm_bf16_kernel(
       for (int j = 0; j < TN; ++j) {
         const int nb = n0 + wn * WN + j * 16 + (lane >> 4) * 4;
         if (vec_ok && nb + 3 < N) {
-          const bf16x4 b4 = *(const bf16x4*)(bias + nb);
+          const bf16x4 b4 = PART ? bf16x4{} : *(const bf16x4*)(bias + nb);
           const float v[4] = {acc[i][j][0] + (float)b4[0], acc[i][j][1] + (float)b4[1],
                               acc[i][j][2] + (float)b4[2], acc[i][j][3] + (float)b4[3]};
-          epi_store4<KIND>(epi, m, nb, v);
+          epi_store4<EK>(epi, m, nb, v);
         } else {
 #pragma unroll
           for (int r = 0; r < 4; ++r)
-            if (nb + r < N) epi_apply<bf16>(epi, KIND, m, nb + r, acc[i][j][r] + (float)bias[nb + r]);
+            if (nb + r < N)
+              epi_apply<bf16>(epi, EK, m, nb + r, acc[i][j][r] + (PART ? 0.f : (float)bias[nb + r]));
         }
       }
     }
@@ -215,9 +228,9 @@ __global__ __launch_bounds__(256, 1) void gemm_bf16_kernel(
 template <int BM, int BN, int WGM>
 static hipError_t gemm_bf16_dispatch(const bf16* A, int lda, const bf16* W, int ldw,
                                      const bf16* bias, int M, int N, int K, int kind,
-                                     const Epi& epi, int vec_ok, hipStream_t st) {
+                                     const Epi& epi, int vec_ok, hipStream_t st, int splits = 1) {
   const int tn = (N + BN - 1) / BN, tm = (M + BM - 1) / BM;
-  dim3 grid(tm * tn), block(256);
+  dim3 grid(tm * tn, splits), block(256);
 #define T2I_GEMM_CASE(K_)                                                                       \
   case K_:                                                                                      \
     hipLaunchKernelGGL((gemm_bf16_kernel<BM, BN, WGM, K_>), grid, block, 0, st, A, lda, W, ldw, \
@@ -231,14 +244,60 @@ static hipError_t gemm_bf16_dispatch(const bf16* A, int lda, const bf16* W, int 
     T2I_GEMM_CASE(EPI_RESID_GATED)
     T2I_GEMM_CASE(EPI_SPLIT_VT)
     T2I_GEMM_CASE(EPI_STORE_F32)
+    T2I_GEMM_CASE(EPI_PARTIAL)
     default: return hipErrorInvalidValue;
   }
 #undef T2I_GEMM_CASE
   return hipGetLastError();
 }
 
+// Split-K reduction: y = bias + sum over slices (fixed order), then the
+// epilogue; four consecutive columns per thread.
+template <int KIND>
+__global__ __launch_bounds__(256) void splitk_reduce_kernel(const float* __restrict__ part,
+                                                            int splits, const bf16* __restrict__ bias,
+                                                            int M, int N, Epi epi, int vec_ok) {
+  const int nq = (N + 3) / 4;
+  const long total = (long)M * nq;
+  const size_t slice = (size_t)M * N;
+  for (long i = blockIdx.x * 256L + threadIdx.x; i < total; i += (long)gridDim.x * 256) {
+    const int m = (int)(i / nq), nb = (int)(i - (long)m * nq) * 4;
+    const float* p = part + (size_t)m * N + nb;
+    if (vec_ok && nb + 3 < N && KIND != EPI_SPLIT_VT) {
+      const bf16x4 b4 = *(const bf16x4*)(bias + nb);
+      float v[4] = {(float)b4[0], (float)b4[1], (float)b4[2], (float)b4[3]};
+      for (int z = 0; z < splits; ++z) {
+        const float4 q = *(const float4*)(p + z * slice);
+        v[0] += q.x;
+        v[1] += q.y;
+        v[2] += q.z;
+        v[3] += q.w;
+      }
+      epi_store4<KIND>(epi, m, nb, v);
+    } else {
+      for (int r = 0; r < 4 && nb + r < N; ++r) {
+        float v = (float)bias[nb + r];
+        for (int z = 0; z < splits; ++z) v += p[z * slice + r];
+        epi_apply<bf16>(epi, KIND, m, nb + r, v);
+      }
+    }
+  }
+}
+
+// Number of K slices (1 = no split) for a layer whose caller allows
+// splitting: narrow outputs (N <= 4096) against K >= 2048, one slice per
+// 1024 columns, at most 4.  It depends on the layer's shape only, never on
+// M, so a row's result does not depend on how many rows share the launch.
+static int splitk_factor(int N, int K) {
+  if (N > 4096 || K < 2048) return 1;
+  int s = std::min(4, K / 1024);
+  while (s > 1 && K % (64 * s) != 0) --s;
+  return s;
+}
+
 hipError_t launch_gemm_bf16(const bf16* A, int lda, const bf16* W, int ldw, const bf16* bias,
-                            int M, int N, int K, int kind, const Epi& epi, hipStream_t st) {
+                            int M, int N, int K, int kind, const Epi& epi, float* splitk_ws,
+                            size_t splitk_floats, hipStream_t st) {
   if (M <= 0 || N <= 0) return hipSuccess;
   auto al = [](const void* p, int a) { return ((uintptr_t)p % a) == 0; };
   const int vec_ok = (epi.ldo % 4 == 0) && (epi.ldx % 4 == 0) && (epi.ld_gate % 4 == 0) &&
@@ -249,9 +308,44 @@ hipError_t launch_gemm_bf16(const bf16* A, int lda, const bf16* W, int ldw, cons
   // 144, so at M = 8192 the layers launch 256 / 512 / 768 / 1024 tiles --
   // whole rounds on 256 CUs at one workgroup each; widths that are multiples
   // of 128 take 192- or 128-wide tiles.  Otherwise 128 x 144 or 128 x 128
-  // register-staged tiles (the faster ones at M ~ 1000 measured).
+  // register-staged tiles (the faster ones at M ~ 1000 measured), with K
+  // split over several workgroups when there are too few tiles to fill the
+  // chip (e.g. the 512-row text stream against K = 3072 or 12288).
   if (M >= 2048 && (N % 144 == 0 || N % 128 == 0) && kind != EPI_SILU)
     return launch_gemm_dma(A, lda, W, ldw, bias, M, N, K, kind, epi, vec_ok, st);
+  const int splits = splitk_ws ? splitk_factor(N, K) : 1;
+  if (splits > 1 && (size_t)splits * M * N <= splitk_floats && kind != EPI_SILU) {
+    Epi pe;
+    std::memset(&pe, 0, sizeof(pe));
+    pe.out = splitk_ws;
+    pe.ldo = N;
+    const int pvec = N % 4 == 0;
+    hipError_t err =
+        N % 144 == 0
+            ? gemm_bf16_dispatch<128, 144, 4>(A, lda, W, ldw, bias, M, N, K / splits, EPI_PARTIAL,
+                                              pe, pvec, st, splits)
+            : gemm_bf16_dispatch<128, 128, 2>(A, lda, W, ldw, bias, M, N, K / splits, EPI_PARTIAL,
+                                              pe, pvec, st, splits);
+    if (err != hipSuccess) return err;
+    const long work = (long)M * ((N + 3) / 4);
+    const int grid = (int)std::min<long>((work + 255) / 256, 4096);
+#define T2I_RED_CASE(K_)                                                                   \
+  case K_:                                                                                 \
+    hipLaunchKernelGGL(splitk_reduce_kernel<K_>, dim3(grid), dim3(256), 0, st, splitk_ws, \
+                       splits, bias, M, N, epi, vec_ok && pvec);                           \
+    break;
+    switch (kind) {
+      T2I_RED_CASE(EPI_STORE)
+      T2I_RED_CASE(EPI_GELU)
+      T2I_RED_CASE(EPI_RESID)
+      T2I_RED_CASE(EPI_RESID_GATED)
+      T2I_RED_CASE(EPI_SPLIT_VT)
+      T2I_RED_CASE(EPI_STORE_F32)
+      default: return hipErrorInvalidValue;
+    }
+#undef T2I_RED_CASE
+    return hipGetLastError();
+  }
   if (N % 144 == 0)
     return gemm_bf16_dispatch<128, 144, 4>(A, lda, W, ldw, bias, M, N, K, kind, epi, vec_ok, st);
   return gemm_bf16_dispatch<128, 128, 2>(A, lda, W, ldw, bias, M, N, K, kind, epi, vec_ok, st);

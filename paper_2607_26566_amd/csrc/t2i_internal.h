@@ -110,7 +110,8 @@ __device__ __forceinline__ float silu(float v) { return v * __builtin_amdgcn_rcp
 // Linear-layer epilogue.
 
 enum EpiKind { EPI_STORE = 0, EPI_GELU = 1, EPI_SILU = 2, EPI_RESID = 3, EPI_RESID_GATED = 4,
-               EPI_SPLIT_VT = 5, EPI_STORE_F32 = 6 };
+               EPI_SPLIT_VT = 5, EPI_STORE_F32 = 6,
+               EPI_PARTIAL = 7 /* split-K partial sums, fp32, no bias */ };
 
 struct Epi {
   void* out;          // STORE / GELU / SILU destination (SPLIT_VT: columns < vcol0)
@@ -155,8 +156,12 @@ __device__ __forceinline__ void epi_apply(const Epi& e, int kind, int m, int n, 
 // ---------------------------------------------------------------------------
 // Launchers (defined in the kernel files; all asynchronous on `st`).
 
+// splitk_ws (fp32, splitk_floats of room, or NULL): lets a short-M, long-K
+// layer split K over several workgroups (partial sums there, then a
+// fixed-order reduction that applies the epilogue)
 hipError_t launch_gemm_bf16(const bf16* A, int lda, const bf16* W, int ldw, const bf16* bias,
-                            int M, int N, int K, int kind, const Epi& epi, hipStream_t st);
+                            int M, int N, int K, int kind, const Epi& epi, float* splitk_ws,
+                            size_t splitk_floats, hipStream_t st);
 
 // SIMT fp32-accumulating GEMM: A fp32, W fp32 or bf16 (w_bf16), bias like W,
 // output fp32 for STORE kinds.

@@ -29,8 +29,10 @@ from gpu_common import DEV, Model, rel_l2, say, to_dev
 
 pytestmark = pytest.mark.gpu
 
+# MLP width 2048: the text stream's down-projection (64 rows, K = 2048) takes
+# the split-K path
 SMALL = synth.reduced(synth.workload("mmdit1024"), name="mmdit_small", hidden=256, heads=2,
-                      head_dim=128, depth=3, mlp_hidden=512, text_dim=128, text_tokens=64,
+                      head_dim=128, depth=3, mlp_hidden=2048, text_dim=128, text_tokens=64,
                       requests=((32, 32), (16, 48)), guidance=4.5, steps=8)
 
 
