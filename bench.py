@@ -32,6 +32,29 @@ PEAK_BF16_TFLOPS = 2500.0      # MI355X dense bf16 MFMA
 PEAK_HBM_GBS = 8000.0          # MI355X HBM3E
 WORKLOAD = "dit1024_cfg"
 
+# HBM bytes per launch measured with rocprofv3 (FETCH_SIZE x 2.00 + WRITE_SIZE
+# x 1.00, factors from a 1 GiB copy; profiles/attn_self_dit1024_hbm_traffic.md),
+# keyed by (workload, kernel class) with the source file it was measured on
+# and the first 16 hex digits of that file's sha256: reported only while the
+# source is unchanged.
+MEASURED_TRAFFIC = {
+    ("dit1024_cfg", "attn_self"): (107.1e6, "paper_2607_26566_amd/csrc/attention.hip", "bcf7220d226ea2a6"),
+}
+
+
+def measured_traffic(workload, kernel):
+    import hashlib
+    rec = MEASURED_TRAFFIC.get((workload, kernel))
+    if rec is None:
+        return None
+    nbytes, src, digest = rec
+    try:
+        with open(os.path.join(ROOT, src), "rb") as f:
+            ok = hashlib.sha256(f.read()).hexdigest()[:16] == digest
+    except OSError:
+        ok = False
+    return nbytes if ok else None
+
 
 def class_work(w):
     """Algorithmic work of each kernel class in ONE block at workload ``w``
@@ -230,6 +253,7 @@ def main():
         ach = work_block * blocks / dom_s / 1e9
         roof = {"bound": "hbm", "achieved": round(ach, 1), "peak": PEAK_HBM_GBS,
                 "unit": "GB/s", "frac": round(ach / PEAK_HBM_GBS, 4), "traffic": None}
+    roof["traffic"] = measured_traffic(args.workload, dominant)
     roof["kernel"] = dominant
     roof["avg_launch_ms"] = round(dom_avg_s * 1e3, 4)
     roof["launches"] = int(cnt.value)
