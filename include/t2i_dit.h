@@ -43,7 +43,7 @@ typedef enum {
   T2I_OK = 0,
   T2I_ERR_INVALID_ARG = 1,   /* NULL pointer, bad enum, struct_size mismatch */
   T2I_ERR_SHAPE = 2,         /* sizes inconsistent with the config or limits */
-  T2I_ERR_UNSUPPORTED = 3,   /* valid but not implemented (e.g. control_outputs) */
+  T2I_ERR_UNSUPPORTED = 3,   /* valid but not implemented for this configuration */
   T2I_ERR_WORKSPACE = 4,     /* workspace or cache state too small */
   T2I_ERR_OUT_OF_MEMORY = 5, /* host allocation failed */
   T2I_ERR_DEVICE = 6         /* a HIP call failed; t2i_last_error has its text */
@@ -57,6 +57,7 @@ typedef enum { T2I_CACHE_ACCUMULATE = 0, T2I_CACHE_PER_STEP = 1 } t2i_cache_mode
 #define T2I_MAX_SEQ 64
 /* Most requests one call may carry. */
 #define T2I_MAX_REQ 32
+#define T2I_MAX_CONTROL 64     /* entries of one t2i_control */
 
 /*
  * Model shape.  `dtype` is the type of weights, text embeddings and of the
@@ -137,6 +138,29 @@ t2i_status t2i_dit_rebind_weights(t2i_dit* h, const void* const* weights,
                                   void* stream);
 
 /*
+ * Callback input of a step: the `control_outputs` input the paper's model
+ * function declares with callback=True (Sec. 4, Fig. "Flux function";
+ * Sec. 5, "Efficient and flexible data fetching"), consumed partway through
+ * the forward pass -- the single-GPU half of ControlNet parallelization.
+ * Entry i adds residuals[i], an fp32 [rows, hidden] device tensor in the
+ * image-stream row order of hidden_out (branch-major, then request), to the
+ * residual stream right after block blocks[i].  When ready != NULL and
+ * ready[i] != NULL (a hipEvent_t recorded by the producer, possibly on
+ * another stream), the step's stream waits on that event only at that point,
+ * so the producer overlaps with the blocks before it.  blocks[] is strictly
+ * increasing; entries at or past the last block that runs are rejected.
+ * Requests whose blocks are skipped by the cache reuse their residual and get
+ * no control input.  All pointers are borrowed for the duration of the call.
+ */
+typedef struct t2i_control {
+  uint32_t struct_size;           /* = sizeof(t2i_control) */
+  int32_t n;                      /* 1 .. T2I_MAX_CONTROL */
+  const int32_t* blocks;          /* host [n] */
+  const float* const* residuals;  /* host [n] of device pointers */
+  void* const* ready;             /* host [n] of hipEvent_t (entries may be NULL), or NULL */
+} t2i_control;
+
+/*
  * One model evaluation for a batch of requests (the model function's
  * `execute`), with classifier-free guidance and an optional Euler update.
  *
@@ -170,7 +194,7 @@ typedef struct t2i_step_args {
   void* cache_state;           /* device or NULL: when given, computed requests
                                   store their residual for later skips */
   size_t cache_state_bytes;
-  const void* control_outputs; /* reserved, must be NULL */
+  const t2i_control* control_outputs; /* callback input (see t2i_control), or NULL */
 } t2i_step_args;
 
 t2i_status t2i_dit_step(t2i_dit* h, const t2i_step_args* args, void* stream);

@@ -233,11 +233,17 @@ def block_rows(W, w, b, x, y, mod, rows):
     return xr + mod["gate_mlp"] * linear(u, W[p + "mlp.fc2.w"], W[p + "mlp.fc2.b"])
 
 
-def run_blocks(W, w, x, y, c, first=0, last=None):
-    """Blocks ``first ... last-1`` on the residual stream."""
+def run_blocks(W, w, x, y, c, first=0, last=None, control=None):
+    """Blocks ``first ... last-1`` on the residual stream.
+
+    ``control`` maps a block index to a residual added to the stream right
+    after that block: the model function's callback input ``control_outputs``
+    (Sec. 4), the per-layer outputs a ControlNet feeds into the base model."""
     last = w.depth if last is None else last
     for b in range(first, last):
         x = block(W, w, b, x, y, block_modulation(W, w, c, b))
+        if control is not None and b in control:
+            x = x + control[b]
     return x
 
 
@@ -248,17 +254,18 @@ def final_layer(W, w, x, c, h, ww):
     return unpatchify(out, w.patch, w.latent_channels, h, ww)
 
 
-def forward(W, w, lat, t, text, n_blocks=None, return_hidden=False):
+def forward(W, w, lat, t, text, n_blocks=None, return_hidden=False, control=None):
     """Velocity of one request: ``[C, h, w]`` latent at time ``t``.
 
-    ``text`` ``None`` means the unconditional (all-zero) text."""
+    ``text`` ``None`` means the unconditional (all-zero) text; ``control`` as
+    in :func:`run_blocks`."""
     C, h, ww = lat.shape
     if text is None:
         text = np.zeros((w.text_tokens, w.text_dim))
     c = conditioning(W, w, t)
     x = embed(W, w, lat)
     y = text_project(W, w, text)
-    x = run_blocks(W, w, x, y, c, 0, w.depth if n_blocks is None else n_blocks)
+    x = run_blocks(W, w, x, y, c, 0, w.depth if n_blocks is None else n_blocks, control)
     v = final_layer(W, w, x, c, h, ww)
     return (v, x) if return_hidden else v
 

@@ -174,11 +174,14 @@ def embed(W, w, lat, text):
     return embed_text(W, w, text), embed_image(W, w, lat)
 
 
-def run_blocks(W, w, x_txt, x_img, c, lat_hw, b0, b1):
-    """Joint blocks ``b0 .. b1-1`` for a latent of spatial size ``lat_hw``."""
+def run_blocks(W, w, x_txt, x_img, c, lat_hw, b0, b1, control=None):
+    """Joint blocks ``b0 .. b1-1`` for a latent of spatial size ``lat_hw``;
+    ``control`` residuals (block -> array) are added to the image stream."""
     rows, cols = grid_positions(lat_hw[0] // w.patch, lat_hw[1] // w.patch)
     for b in range(b0, b1):
         x_txt, x_img = joint_block(W, w, b, x_txt, x_img, c, rows, cols)
+        if control is not None and b in control:
+            x_img = x_img + control[b]
     return x_txt, x_img
 
 
@@ -191,13 +194,13 @@ def cache_signal(W, w, lat, t):
                     md["shift_msa"], md["scale_msa"])
 
 
-def forward(W, w, lat, t, text, n_blocks=None):
+def forward(W, w, lat, t, text, n_blocks=None, control=None):
     """Returns ``(v, x_txt, x_img)``; ``v`` is None unless all blocks ran.
     ``text`` None is the unconditional prompt."""
     C, h, ww = lat.shape
     c = conditioning(W, w, t)
     x_txt, x_img = embed(W, w, lat, text)
     nb = w.depth if n_blocks is None else n_blocks
-    x_txt, x_img = run_blocks(W, w, x_txt, x_img, c, (h, ww), 0, nb)
+    x_txt, x_img = run_blocks(W, w, x_txt, x_img, c, (h, ww), 0, nb, control)
     v = final_layer(W, w, x_img, c, h, ww) if nb == w.depth else None
     return v, x_txt, x_img

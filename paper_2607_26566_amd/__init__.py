@@ -159,9 +159,15 @@ def t2i_dit_step(m: DiT, latents: torch.Tensor, lat_hw: Sequence[tuple], t: Sequ
                  noise_pred: Optional[torch.Tensor] = None, n_blocks: int = -1,
                  hidden_out: Optional[torch.Tensor] = None,
                  skip: Optional[Sequence[int]] = None,
-                 cache_state: Optional[torch.Tensor] = None, stream=None):
+                 cache_state: Optional[torch.Tensor] = None, stream=None,
+                 control: Optional[Sequence[tuple]] = None):
     """One model evaluation on packed fp32 ``latents`` (updated in place when
-    ``t_next`` is given).  ``prompt_embeds`` is ``[n_req, text_tokens, text_dim]``."""
+    ``t_next`` is given).  ``prompt_embeds`` is ``[n_req, text_tokens, text_dim]``.
+
+    ``control``: the callback input, a list of ``(block, residual, event)``:
+    ``residual`` (fp32 device tensor ``[rows, hidden]``) is added after block
+    ``block``; ``event`` (a recorded ``torch.cuda.Event`` or None) is waited for
+    on the step's stream only at that point."""
     _check_lat(latents)
     n = len(lat_hw)
     a = _lib.t2i_step_args()
@@ -180,7 +186,19 @@ def t2i_dit_step(m: DiT, latents: torch.Tensor, lat_hw: Sequence[tuple], t: Sequ
     a.skip = _arr(C.c_uint8, list(skip)) if skip is not None else None
     a.cache_state = cache_state.data_ptr() if cache_state is not None else None
     a.cache_state_bytes = cache_state.numel() if cache_state is not None else 0
-    a.control_outputs = None
+    ctl = None
+    if control:
+        for _, r, _ in control:
+            if r.dtype != torch.float32 or not r.is_cuda or not r.is_contiguous():
+                raise T2IError(1, "control residuals must be contiguous fp32 device tensors")
+        ctl = _lib.t2i_control()
+        ctl.struct_size = C.sizeof(ctl)
+        ctl.n = len(control)
+        ctl.blocks = _arr(C.c_int32, [int(b) for b, _, _ in control])
+        ctl.residuals = _arr(C.c_void_p, [r.data_ptr() for _, r, _ in control])
+        ctl.ready = _arr(C.c_void_p, [int(ev.cuda_event) if ev is not None else None
+                                      for _, _, ev in control])
+    a.control_outputs = C.cast(C.byref(ctl), C.c_void_p) if ctl is not None else None
     check(m.lib.t2i_dit_step(m.h, C.byref(a), C.c_void_p(_stream(stream))), m.h)
 
 

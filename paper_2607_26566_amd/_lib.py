@@ -37,6 +37,11 @@ class t2i_dit_config(C.Structure):
                 ("max_requests", i32), ("max_steps", i32), ("ln_eps", f32), ("t_scale", f32)]
 
 
+class t2i_control(C.Structure):
+    _fields_ = [("struct_size", u32), ("n", i32), ("blocks", C.POINTER(i32)),
+                ("residuals", C.POINTER(vp)), ("ready", C.POINTER(vp))]
+
+
 class t2i_step_args(C.Structure):
     _fields_ = [("struct_size", u32), ("n_req", i32), ("lat_h", C.POINTER(i32)),
                 ("lat_w", C.POINTER(i32)), ("t", C.POINTER(f64)), ("t_next", C.POINTER(f64)),

@@ -245,6 +245,7 @@ struct Plan {
   AttnMap joint{};   // MMDiT: per sequence a text and an image query group,
                      // keys = the sequence's text rows, then its image rows
   int grid_max = 0;  // largest grid side (length of the position tables)
+  const t2i_control* ctl = nullptr;   // validated callback input, or NULL
   size_t lat_floats = 0;
 };
 
@@ -359,6 +360,23 @@ hipError_t embed(t2i_dit* h, const Plan& P, const float* lat, float* x0, float* 
 }
 // first residual row of the image stream
 int img_row0(const t2i_dit* h, const Plan& P) { return is_mmdit(h) ? P.txt_rows : 0; }
+
+// Callback input after block b: wait for its producer's event (if any) at this
+// point only, then add the residual to the image stream.
+hipError_t inject_control(t2i_dit* h, const Plan& P, int b, hipStream_t st) {
+  const t2i_control* c = P.ctl;
+  if (!c) return hipSuccess;
+  for (int i = 0; i < c->n; ++i) {
+    if (c->blocks[i] != b) continue;
+    if (c->ready && c->ready[i]) {
+      hipError_t e = hipStreamWaitEvent(st, (hipEvent_t)c->ready[i], 0);
+      if (e != hipSuccess) return e;
+    }
+    float* xi = h->at<float>(h->L.x) + (size_t)img_row0(h, P) * h->cfg.hidden;
+    return launch_add_inplace(xi, c->residuals[i], (size_t)P.rows * h->cfg.hidden, st);
+  }
+  return hipSuccess;
+}
 
 Epi make_epi() {
   Epi e;
@@ -563,6 +581,7 @@ t2i_status run_blocks_cross(t2i_dit* h, const Plan& P, int nb, hipStream_t st) {
     e.ld_gate = mw;
     e.map = P.img;
     TIMED(h, T2I_K_GEMM_FC2, st, linear(h, u, F, wb + X_FC2, R, D, F, EPI_RESID_GATED, e, st));
+    HIP_TRY(h, inject_control(h, P, b, st));
   }
   return T2I_OK;
 }
@@ -627,6 +646,7 @@ t2i_status run_blocks_mmdit(t2i_dit* h, const Plan& P, int nb, hipStream_t st) {
       TIMED(h, T2I_K_GEMM_FC2, st,
             linear(h, u + (size_t)r0 * F, F, wi + J_FC2, R, D, F, EPI_RESID_GATED, e, st, s == 0));
     }
+    HIP_TRY(h, inject_control(h, P, b, st));
   }
   return T2I_OK;
 }
@@ -845,7 +865,6 @@ t2i_status t2i_dit_step(t2i_dit* h, const t2i_step_args* a, void* stream) {
   if (!h) return T2I_ERR_INVALID_ARG;
   if (!a || a->struct_size != sizeof(t2i_step_args))
     return fail(h, T2I_ERR_INVALID_ARG, "step args NULL or struct_size mismatch");
-  if (a->control_outputs) return fail(h, T2I_ERR_UNSUPPORTED, "control_outputs is reserved");
   if (!a->t || !a->latents || !a->prompt_embeds)
     return fail(h, T2I_ERR_INVALID_ARG, "t, latents and prompt_embeds are required");
   const t2i_dit_config& c = h->cfg;
@@ -854,6 +873,21 @@ t2i_status t2i_dit_step(t2i_dit* h, const t2i_step_args* a, void* stream) {
   if (s != T2I_OK) return s;
   const int nb = a->n_blocks < 0 ? c.depth : a->n_blocks;
   if (nb > c.depth) return fail(h, T2I_ERR_SHAPE, "n_blocks > depth");
+  if (const t2i_control* ctl = a->control_outputs) {
+    if (ctl->struct_size != sizeof(t2i_control))
+      return fail(h, T2I_ERR_INVALID_ARG, "control_outputs struct_size mismatch");
+    if (ctl->n < 1 || ctl->n > T2I_MAX_CONTROL)
+      return fail(h, T2I_ERR_SHAPE, "control_outputs: n out of range");
+    if (!ctl->blocks || !ctl->residuals)
+      return fail(h, T2I_ERR_INVALID_ARG, "control_outputs: blocks / residuals is NULL");
+    for (int i = 0; i < ctl->n; ++i) {
+      if (ctl->blocks[i] < 0 || ctl->blocks[i] >= nb || (i && ctl->blocks[i] <= ctl->blocks[i - 1]))
+        return fail(h, T2I_ERR_SHAPE,
+                    "control_outputs: blocks must increase strictly and lie below the blocks run");
+      if (!ctl->residuals[i]) return fail(h, T2I_ERR_INVALID_ARG, "control_outputs: NULL residual");
+    }
+    P.ctl = ctl;
+  }
   if (a->skip && !a->cache_state)
     return fail(h, T2I_ERR_INVALID_ARG, "skip decisions need cache_state");
   if (a->cache_state &&

@@ -310,6 +310,17 @@ hipError_t launch_rope_apply(bf16* qk, int ld, int row0, const ReqMap& rm, int h
   return hipGetLastError();
 }
 
+__global__ void add_inplace_kernel(float* __restrict__ x, const float* __restrict__ r, size_t n) {
+  for (size_t i = blockIdx.x * 256ul + threadIdx.x; i < n; i += (size_t)gridDim.x * 256) x[i] += r[i];
+}
+
+hipError_t launch_add_inplace(float* x, const float* r, size_t n, hipStream_t st) {
+  if (n == 0) return hipSuccess;
+  const int grid = (int)std::min<size_t>((n + 255) / 256, 8192);
+  hipLaunchKernelGGL(add_inplace_kernel, dim3(grid), dim3(256), 0, st, x, r, n);
+  return hipGetLastError();
+}
+
 __global__ void bias_rows_f32_kernel(const bf16* __restrict__ b16, const float* __restrict__ b32,
                                      int rows, int D, float* __restrict__ dst) {
   const long n = (long)rows * D;

@@ -210,6 +210,8 @@ hipError_t launch_final_layer(const float* x, const ReqMap& rm, const void* w_ou
 hipError_t launch_rope_table(float2* table, int npos, int q, hipStream_t st);
 hipError_t launch_rope_apply(bf16* qk, int ld, int row0, const ReqMap& rm, int heads, int head_dim,
                              int patch, const float2* table, hipStream_t st);
+// x[i] += r[i] for i < n (fp32)
+hipError_t launch_add_inplace(float* x, const float* r, size_t n, hipStream_t st);
 // dst[r][:] = float(bias[:]) for r < rows (bf16 or fp32 bias)
 hipError_t launch_bias_rows_f32(const void* bias, bool bias_bf16, int rows, int D, float* dst,
                                 hipStream_t st);

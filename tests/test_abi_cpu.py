@@ -125,8 +125,25 @@ def test_step_argument_errors_return_status():
         a.n_blocks = 29
         assert lib.t2i_dit_step(h, C.byref(a), None) == 2
         a.n_blocks = -1
-        a.control_outputs = 0x4000
-        assert lib.t2i_dit_step(h, C.byref(a), None) == 3
+        # callback input: struct size, block order / range, NULL residual
+        ctl = _lib.t2i_control()
+        ctl.struct_size = C.sizeof(ctl) + 8
+        ctl.n = 2
+        blocks = (C.c_int32 * 2)(3, 1)
+        res = (C.c_void_p * 2)(0x5000, 0x6000)
+        ctl.blocks, ctl.residuals, ctl.ready = blocks, res, None
+        a.control_outputs = C.cast(C.byref(ctl), C.c_void_p)
+        assert lib.t2i_dit_step(h, C.byref(a), None) == 1
+        ctl.struct_size = C.sizeof(ctl)
+        assert lib.t2i_dit_step(h, C.byref(a), None) == 2          # not increasing
+        assert b"increase" in lib.t2i_last_error(h)
+        blocks[0], blocks[1] = 1, 28                               # block 28 never runs
+        assert lib.t2i_dit_step(h, C.byref(a), None) == 2
+        blocks[1] = 3
+        res[1] = None
+        assert lib.t2i_dit_step(h, C.byref(a), None) == 1
+        ctl.n = 0
+        assert lib.t2i_dit_step(h, C.byref(a), None) == 2
         a.control_outputs = None
         hh[0] = 128                                     # 4096 tokens > max_tokens 1024
         assert lib.t2i_dit_step(h, C.byref(a), None) == 2

@@ -293,6 +293,35 @@ def test_zero_gates_make_block_identity():
     assert np.array_equal(dit.run_blocks(W, TINY, x, y, c), x)
 
 
+def test_control_residuals_through_identity_blocks():
+    """Callback input: with identity blocks (zero gates, zero ungated
+    cross-attention output) the stream after the blocks is x0 plus the sum of
+    the injected residuals; injection after the last block that runs shows in
+    the output, injection past it does not."""
+    W = tiny_weights()
+    D = TINY.hidden
+    for b in range(TINY.depth):
+        p = f"blocks.{b}."
+        for chunk in (2, 5):
+            W[p + "ada.w"][chunk * D:(chunk + 1) * D] = 0
+            W[p + "ada.b"][chunk * D:(chunk + 1) * D] = 0
+        W[p + "xattn.o.w"][:] = 0
+        W[p + "xattn.o.b"][:] = 0
+    rng = np.random.default_rng(19)
+    x = rng.standard_normal((6, D))
+    y = rng.standard_normal((3, D))
+    c = rng.standard_normal(D)
+    r0, r1 = rng.standard_normal((6, D)), rng.standard_normal((6, D))
+    out = dit.run_blocks(W, TINY, x, y, c, control={0: r0, TINY.depth - 1: r1})
+    assert np.allclose(out, x + r0 + r1, rtol=0, atol=1e-14)
+    out = dit.run_blocks(W, TINY, x, y, c, 0, 1, control={0: r0, 1: r1})
+    assert np.allclose(out, x + r0, rtol=0, atol=1e-14)
+    # a zero residual changes nothing in a real (non-identity) model
+    W2 = tiny_weights()
+    assert np.array_equal(dit.run_blocks(W2, TINY, x, y, c, control={1: np.zeros((6, D))}),
+                          dit.run_blocks(W2, TINY, x, y, c))
+
+
 def test_unconditional_cross_attention_closed_form():
     """All-zero text makes every key equal, so each query gets the value row."""
     W = tiny_weights()
