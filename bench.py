@@ -128,6 +128,37 @@ def cpu_baseline(w, W_host):
                       f"scaled x{w.depth} to all blocks"}
 
 
+def lora_cost(t2i, table, dev, rank):
+    """Time merging one rank-``rank`` LoRA (alpha 1) into every 2-D weight of
+    the blocks, as done once before sampling with an adapter."""
+    import torch
+    idx = [i for i, (n, shp) in enumerate(table) if n.startswith("blocks.") and len(shp) == 2]
+    g = torch.Generator(device="cuda").manual_seed(0)
+    ad = {}
+    for i in idx:
+        n_out, n_in = table[i][1]
+        key = (n_out, n_in)
+        if key not in ad:
+            ad[key] = (torch.randn(rank, n_in, generator=g, device="cuda").to(dev[i].dtype) * 0.01,
+                       torch.randn(n_out, rank, generator=g, device="cuda").to(dev[i].dtype) * 0.01)
+    torch.cuda.synchronize()
+    # GPU time of each merge (events around each launch), summed
+    evs = []
+    nbytes = 0
+    for i in idx:
+        a, b = ad[table[i][1]]
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        t2i.lora_merge(dev[i], a, b, 1.0)
+        e1.record()
+        evs.append((e0, e1))
+        nbytes += 2 * dev[i].numel() * dev[i].element_size() + (a.numel() + b.numel()) * a.element_size()
+    torch.cuda.synchronize()
+    ms = sum(e0.elapsed_time(e1) for e0, e1 in evs)
+    return {"rank": rank, "layers": len(idx), "gpu_ms": round(ms, 3),
+            "hbm_gbs": round(nbytes / (ms / 1e3) / 1e9, 1)}
+
+
 WORKLOADS = {
     "dit1024_cfg": ("denoising steps/s at 1024px DiT; MFMA TFLOP/s as fraction of MI355X bf16 peak",
                     "dit1024_cfg: 1024px image, latent 4x128x128, patch 2 -> 4096 tokens x 2 "
@@ -154,6 +185,8 @@ def main():
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--workload", default=WORKLOAD, choices=sorted(WORKLOADS))
+    ap.add_argument("--lora-rank", type=int, default=0,
+                    help="also time merging a rank-R LoRA into every 2-D block weight")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="run only a plain 1 GiB device copy (HBM counter calibration)")
     args = ap.parse_args()
@@ -308,6 +341,8 @@ def main():
         "kernel_class_rate": class_rate,
         "flops_per_step": flops,
     }
+    if args.lora_rank:
+        out["lora_merge"] = lora_cost(t2i, table, dev, args.lora_rank)
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(w, W_host)
     print(json.dumps(out), flush=True)

@@ -79,6 +79,21 @@ t2i_status t2i_op_ln_modulate(int32_t dtype, int32_t rows, int32_t D,
                               const float* scale, float eps, void* out,
                               void* stream);
 
+/*
+ * LoRA weight update merged on the device before sampling (the paper's
+ * weight-update adapters, Sec. 2.2 / Sec. 3, which modify base-model weights
+ * before inference): W <- W + alpha * B A for one linear layer, in place.
+ *   W [n_out, n_in] with row stride ldw, A [rank, n_in] (row stride n_in),
+ *   B [n_out, rank] (row stride rank), all of dtype (bf16 or fp32);
+ *   1 <= rank <= 128.  The product is accumulated in fp32 over rank, added to
+ *   W in fp32 and rounded once to W's dtype (round-to-nearest-even).
+ * W is caller-owned memory (e.g. a tensor bound to a t2i_dit handle: merge
+ * between calls, not during one).
+ */
+t2i_status t2i_op_lora_merge(int32_t dtype, int32_t n_out, int32_t n_in, int32_t rank,
+                             float alpha, void* W, int32_t ldw, const void* A,
+                             const void* B, void* stream);
+
 const char* t2i_ops_last_error(void);
 
 #ifdef __cplusplus

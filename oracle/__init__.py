@@ -23,5 +23,6 @@ Modules:
   mmdit    joint-attention (MMDiT-style) blocks with 2D RoPE
   sampler  classifier-free guidance, Euler update, schedules, cache rule and
            the sampling loop
+  lora     weight-update adapter merge W + alpha B A
 """
-from . import dit, sampler, mmdit  # noqa: F401
+from . import dit, sampler, mmdit, lora  # noqa: F401

@@ -202,6 +202,24 @@ def t2i_dit_step(m: DiT, latents: torch.Tensor, lat_hw: Sequence[tuple], t: Sequ
     check(m.lib.t2i_dit_step(m.h, C.byref(a), C.c_void_p(_stream(stream))), m.h)
 
 
+def lora_merge(W: torch.Tensor, A: torch.Tensor, B: torch.Tensor, alpha: float, stream=None):
+    """``W += alpha * B @ A`` in place on the device (``t2i_op_lora_merge``):
+    ``W [out, in]``, ``A [rank, in]``, ``B [out, rank]``, one dtype (bf16 or fp32)."""
+    for t in (W, A, B):
+        if not t.is_cuda or not t.is_contiguous() or t.dtype != W.dtype:
+            raise T2IError(1, "W, A, B must be contiguous device tensors of one dtype")
+    n_out, n_in = W.shape
+    rank = A.shape[0]
+    if A.shape != (rank, n_in) or B.shape != (n_out, rank):
+        raise T2IError(2, "A must be [rank, in] and B [out, rank]")
+    lib = load()
+    dt = T2I_BF16 if W.dtype == torch.bfloat16 else T2I_F32
+    st = lib.t2i_op_lora_merge(dt, n_out, n_in, rank, float(alpha), W.data_ptr(), n_in,
+                               A.data_ptr(), B.data_ptr(), C.c_void_p(_stream(stream)))
+    if st != 0:
+        raise T2IError(st, lib.t2i_ops_last_error().decode())
+
+
 def t2i_cache_check(m: DiT, latents: torch.Tensor, lat_hw, t, step: int, n_steps: int,
                     tau: float, cache_state: torch.Tensor, branches: int = 1,
                     mode: int = T2I_CACHE_ACCUMULATE, stream=None):

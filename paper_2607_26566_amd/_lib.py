@@ -91,6 +91,7 @@ SIGNATURES = {
                                C.POINTER(i32), C.POINTER(i32), C.POINTER(i32), C.POINTER(i32),
                                vp, i32, vp, i32, vp, i32, vp, i32, vp]),
     "t2i_op_ln_modulate": (i32, [i32, i32, i32, vp, vp, vp, f32, vp, vp]),
+    "t2i_op_lora_merge": (i32, [i32, i32, i32, i32, f32, vp, i32, vp, vp, vp]),
     "t2i_ops_last_error": (C.c_char_p, []),
 }
 

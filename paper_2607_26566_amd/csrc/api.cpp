@@ -1098,4 +1098,18 @@ t2i_status t2i_op_ln_modulate(int32_t dtype, int32_t rows, int32_t D, const floa
   return T2I_OK;
 }
 
+t2i_status t2i_op_lora_merge(int32_t dtype, int32_t n_out, int32_t n_in, int32_t rank,
+                             float alpha, void* W, int32_t ldw, const void* A, const void* B,
+                             void* stream) {
+  if (dtype != T2I_F32 && dtype != T2I_BF16) return ops_fail(T2I_ERR_INVALID_ARG, "bad dtype");
+  if (n_out < 1 || n_in < 1 || ldw < n_in) return ops_fail(T2I_ERR_SHAPE, "bad weight shape");
+  if (rank < 1 || rank > 128) return ops_fail(T2I_ERR_SHAPE, "rank must be in 1 .. 128");
+  if (!W || !A || !B) return ops_fail(T2I_ERR_INVALID_ARG, "NULL pointer");
+  if (!std::isfinite(alpha)) return ops_fail(T2I_ERR_INVALID_ARG, "alpha not finite");
+  hipError_t err = launch_lora_merge(dtype == T2I_BF16, n_out, n_in, rank, alpha, W, ldw, A, B,
+                                     (hipStream_t)stream);
+  if (err != hipSuccess) return ops_fail(T2I_ERR_DEVICE, hipGetErrorString(err));
+  return T2I_OK;
+}
+
 }  // extern "C"

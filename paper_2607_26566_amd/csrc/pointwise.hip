@@ -310,6 +310,69 @@ hipError_t launch_rope_apply(bf16* qk, int ld, int row0, const ReqMap& rm, int h
   return hipGetLastError();
 }
 
+// LoRA merge: a thread owns one input column i and keeps A[:, i] in
+// registers; the workgroup walks kLoraRows output rows, B's rows staged in LDS.
+// RK (16 / 32 / 64 / 128) is the rank rounded up; the padding is zero.
+constexpr int kLoraRows = 64, kLoraMaxRank = 128;
+
+template <typename T, int RK>
+__global__ __launch_bounds__(256) void lora_merge_kernel(int n_out, int n_in, int rank, float alpha,
+                                                         T* __restrict__ W, int ldw,
+                                                         const T* __restrict__ A,
+                                                         const T* __restrict__ B) {
+  __shared__ float brow[kLoraRows][RK];
+  const int i = blockIdx.x * 256 + threadIdx.x;
+  const int o0 = blockIdx.y * kLoraRows;
+  for (int e = threadIdx.x; e < kLoraRows * RK; e += 256) {
+    const int r = e / RK, k = e - r * RK;
+    brow[r][k] = (o0 + r < n_out && k < rank) ? to_f32(B[(size_t)(o0 + r) * rank + k]) : 0.f;
+  }
+  __syncthreads();
+  if (i >= n_in) return;
+  float a[RK];
+#pragma unroll
+  for (int k = 0; k < RK; ++k) a[k] = k < rank ? to_f32(A[(size_t)k * n_in + i]) : 0.f;
+  const int rows = min(kLoraRows, n_out - o0);
+  // 16 rows at a time: their W elements are loaded together (independent
+  // loads in flight), updated, stored
+  for (int r0 = 0; r0 < rows; r0 += 16) {
+    float wv[16];
+#pragma unroll
+    for (int j = 0; j < 16; ++j)
+      wv[j] = r0 + j < rows ? to_f32(W[(size_t)(o0 + r0 + j) * ldw + i]) : 0.f;
+#pragma unroll
+    for (int j = 0; j < 16; ++j) {
+      float acc = 0.f;
+#pragma unroll
+      for (int k = 0; k < RK; ++k) acc = fmaf(brow[r0 + j][k], a[k], acc);
+      if (r0 + j < rows) W[(size_t)(o0 + r0 + j) * ldw + i] = from_f32<T>(fmaf(alpha, acc, wv[j]));
+    }
+  }
+}
+
+template <typename T>
+static hipError_t lora_dispatch(int n_out, int n_in, int rank, float alpha, void* W, int ldw,
+                                const void* A, const void* B, hipStream_t st) {
+  dim3 grid((n_in + 255) / 256, (n_out + kLoraRows - 1) / kLoraRows);
+#define T2I_LORA(RK_)                                                                        \
+  hipLaunchKernelGGL((lora_merge_kernel<T, RK_>), grid, dim3(256), 0, st, n_out, n_in, rank, \
+                     alpha, (T*)W, ldw, (const T*)A, (const T*)B)
+  if (rank <= 16) T2I_LORA(16);
+  else if (rank <= 32) T2I_LORA(32);
+  else if (rank <= 64) T2I_LORA(64);
+  else T2I_LORA(128);
+#undef T2I_LORA
+  return hipGetLastError();
+}
+
+hipError_t launch_lora_merge(bool bf16_io, int n_out, int n_in, int rank, float alpha, void* W,
+                             int ldw, const void* A, const void* B, hipStream_t st) {
+  if (n_out <= 0 || n_in <= 0) return hipSuccess;
+  if (rank < 1 || rank > kLoraMaxRank) return hipErrorInvalidValue;
+  return bf16_io ? lora_dispatch<bf16>(n_out, n_in, rank, alpha, W, ldw, A, B, st)
+                 : lora_dispatch<float>(n_out, n_in, rank, alpha, W, ldw, A, B, st);
+}
+
 __global__ void add_inplace_kernel(float* __restrict__ x, const float* __restrict__ r, size_t n) {
   for (size_t i = blockIdx.x * 256ul + threadIdx.x; i < n; i += (size_t)gridDim.x * 256) x[i] += r[i];
 }

@@ -210,6 +210,9 @@ hipError_t launch_final_layer(const float* x, const ReqMap& rm, const void* w_ou
 hipError_t launch_rope_table(float2* table, int npos, int q, hipStream_t st);
 hipError_t launch_rope_apply(bf16* qk, int ld, int row0, const ReqMap& rm, int heads, int head_dim,
                              int patch, const float2* table, hipStream_t st);
+// W <- W + alpha B A (LoRA merge), W [n_out, n_in] stride ldw, rank <= 128
+hipError_t launch_lora_merge(bool bf16_io, int n_out, int n_in, int rank, float alpha, void* W,
+                             int ldw, const void* A, const void* B, hipStream_t st);
 // x[i] += r[i] for i < n (fp32)
 hipError_t launch_add_inplace(float* x, const float* r, size_t n, hipStream_t st);
 // dst[r][:] = float(bias[:]) for r < rows (bf16 or fp32 bias)

@@ -198,6 +198,12 @@ def test_op_argument_errors():
     qs = (C.c_int32 * 1)(0)
     ql = (C.c_int32 * 1)(4)
     kl = (C.c_int32 * 1)(0)                              # no keys
+    # LoRA merge: rank range, NULL operand, non-finite alpha
+    assert lib.t2i_op_lora_merge(1, 64, 64, 0, 1.0, 0x1000, 64, 0x2000, 0x3000, None) == 2
+    assert lib.t2i_op_lora_merge(1, 64, 64, 129, 1.0, 0x1000, 64, 0x2000, 0x3000, None) == 2
+    assert lib.t2i_op_lora_merge(1, 64, 64, 8, 1.0, None, 64, 0x2000, 0x3000, None) == 1
+    assert lib.t2i_op_lora_merge(1, 64, 64, 8, float("nan"), 0x1000, 64, 0x2000, 0x3000, None) == 1
+    assert lib.t2i_op_lora_merge(1, 64, 64, 8, 1.0, 0x1000, 32, 0x2000, 0x3000, None) == 2
     assert lib.t2i_op_attention(1, 2, 72, 1, qs, ql, qs, kl, None, None, 0x1000, 144, 0x2000,
                                 144, 0x3000, 144, 0x4000, 144, None) == 2
     assert lib.t2i_op_attention(1, 2, 48, 1, qs, ql, qs, ql, None, None, 0x1000, 96, 0x2000, 96,

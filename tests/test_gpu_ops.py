@@ -254,3 +254,35 @@ def test_ln_modulate(dtype, rows, D):
     torch.cuda.synchronize()
     ref = dit.modulate(dit.layer_norm(x.astype(np.float64), 1e-6), mod[0], mod[1])
     assert rel_l2(to_host(out), ref) < (3e-3 if dtype == 1 else 1e-6)
+
+
+@pytest.mark.parametrize("dtype,n_out,n_in,rank", [(1, 3072, 3072, 64), (1, 1152, 4608, 16),
+                                                    (1, 77, 300, 128), (0, 200, 130, 8)])
+def test_lora_merge(dtype, n_out, n_in, rank):
+    """W + alpha B A against the oracle: fp32 to 1e-6; bf16 equal to the oracle
+    rounded to bf16 except where the fp32 sum lands on the other side of a
+    rounding boundary (at most one bf16 step, on a tiny fraction)."""
+    bf = dtype == 1
+    W = rnd(70, (n_out, n_in), 0.05, bf=bf)
+    A = rnd(71, (rank, n_in), 0.05, bf=bf)
+    B = rnd(72, (n_out, rank), 0.05, bf=bf)
+    alpha = 0.8
+    dt = "bf16" if bf else "f32"
+    dW, dA, dB = to_dev(W, dt), to_dev(A, dt), to_dev(B, dt)
+    t2i.lora_merge(dW, dA, dB, alpha)
+    torch.cuda.synchronize()
+    from oracle import lora
+    ref = lora.merge(W, A, B, alpha)
+    got = to_host(dW)
+    if not bf:
+        assert rel_l2(got, ref) < 1e-6
+        return
+    ref_b = synth.round_bf16(ref.astype(np.float32)).astype(np.float64)
+    diff = got != ref_b
+    frac = diff.mean()
+    say(f"lora {n_out}x{n_in} r{rank}: {frac:.2e} of elements one rounding step off")
+    assert frac < 1e-3
+    # a mismatch is one bf16 step of the larger of the two values (plus fp32
+    # accumulation slack where W and alpha B A nearly cancel)
+    d = np.abs(got[diff] - ref[diff])
+    assert np.all(d <= np.maximum(np.abs(ref[diff]), np.abs(got[diff])) * 2.0 ** -7 + 1e-6)
