@@ -159,6 +159,42 @@ def lora_cost(t2i, table, dev, rank):
             "hbm_gbs": round(nbytes / (ms / 1e3) / 1e9, 1)}
 
 
+def sched_bench(tenants=64, ready_per_tenant=4, decisions=20000):
+    """Decisions per second of the vTime scheduler (submit + schedule +
+    complete per decision) with `tenants` x `ready_per_tenant` ready
+    invocations, on the host."""
+    import numpy as np
+    from paper_2607_26566_amd.scheduler import Scheduler
+
+    def run(s, n):
+        rng = np.random.default_rng(0)
+        nid = 0
+        for u in range(tenants):
+            for _ in range(ready_per_tenant):
+                s.submit(u, nid, float(rng.uniform(0.5, 10.0)), float(rng.uniform(0, 50)), 0.0)
+                nid += 1
+        t = 0.0
+        t0 = time.perf_counter()
+        for i in range(n):
+            fn, u, est = s.schedule(t)
+            s.complete(fn, est)
+            t += est
+            s.submit(u, nid, float(rng.uniform(0.5, 10.0)), float(rng.uniform(0, 50)), t)
+            nid += 1
+        return n / (time.perf_counter() - t0)
+
+    rate = run(Scheduler(5.0), decisions)
+    from oracle.sched import VTimeScheduler
+    orate = run(VTimeScheduler(5.0), decisions // 20)
+    return {"metric": "vTime scheduler decisions/s (host, via the Python binding)",
+            "value": round(rate, 1), "unit": "decisions/s",
+            "us_per_decision": round(1e6 / rate, 2),
+            "config": {"tenants": tenants, "ready_invocations": tenants * ready_per_tenant},
+            "cpu_baseline": {"value": round(orate, 1), "unit": "decisions/s", "cores": 1,
+                             "kind": "oracle",
+                             "sample": f"{decisions // 20} decisions of the Python oracle"}}
+
+
 WORKLOADS = {
     "dit1024_cfg": ("denoising steps/s at 1024px DiT; MFMA TFLOP/s as fraction of MI355X bf16 peak",
                     "dit1024_cfg: 1024px image, latent 4x128x128, patch 2 -> 4096 tokens x 2 "
@@ -185,6 +221,8 @@ def main():
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--workload", default=WORKLOAD, choices=sorted(WORKLOADS))
+    ap.add_argument("--sched", action="store_true",
+                    help="time only the vTime scheduler library (host CPU, no GPU)")
     ap.add_argument("--lora-rank", type=int, default=0,
                     help="also time merging a rank-R LoRA into every 2-D block weight")
     ap.add_argument("--copy-calibration", action="store_true",
@@ -194,6 +232,10 @@ def main():
         print(f"bench.py runs on one GPU only (got --gpus {args.gpus}); the denoising step "
               "is not sharded across GPUs in this build", file=sys.stderr)
         sys.exit(2)
+
+    if args.sched:
+        print(json.dumps(sched_bench()), flush=True)
+        return
 
     import numpy as np
     import torch

@@ -24,5 +24,6 @@ Modules:
   sampler  classifier-free guidance, Euler update, schedules, cache rule and
            the sampling loop
   lora     weight-update adapter merge W + alpha B A
+  sched    the vTime two-layer fair scheduler (control plane)
 """
-from . import dit, sampler, mmdit, lora  # noqa: F401
+from . import dit, sampler, mmdit, lora, sched  # noqa: F401

@@ -92,6 +92,13 @@ SIGNATURES = {
                                vp, i32, vp, i32, vp, i32, vp, i32, vp]),
     "t2i_op_ln_modulate": (i32, [i32, i32, i32, vp, vp, vp, f32, vp, vp]),
     "t2i_op_lora_merge": (i32, [i32, i32, i32, i32, f32, vp, i32, vp, vp, vp]),
+    "t2i_sched_create": (i32, [f64, C.POINTER(vp)]),
+    "t2i_sched_destroy": (None, [vp]),
+    "t2i_sched_submit": (i32, [vp, i32, C.c_int64, f64, f64, f64]),
+    "t2i_sched_schedule": (i32, [vp, f64, C.POINTER(i32), C.POINTER(C.c_int64), C.POINTER(i32),
+                                 C.POINTER(f64)]),
+    "t2i_sched_complete": (i32, [vp, C.c_int64, f64]),
+    "t2i_sched_vtime": (i32, [vp, i32, C.POINTER(f64)]),
     "t2i_ops_last_error": (C.c_char_p, []),
 }
 
