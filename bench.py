@@ -195,6 +195,88 @@ def sched_bench(tenants=64, ready_per_tenant=4, decisions=20000):
                              "sample": f"{decisions // 20} decisions of the Python oracle"}}
 
 
+PCIE5_X16_GBS = 63.0   # PCIe 5.0 x16, one direction: 32 GT/s x 16 lanes x 128/130
+
+
+def loading_bench(t2i, m, cfg, w, dev, step, reps=3):
+    """First-layers caching (Eq. 1-2) on this model: per-block copy time from
+    pinned host memory, per-block compute time, and the end-to-end latency of
+    one step started while the evicted blocks [L_e, L) are copied on a second
+    stream, for every prefix L_e, next to Eq. 1 with the measured times."""
+    import torch
+    L = w.depth
+    t0 = time.time()
+    host = t2i.pack_blocks(cfg, dev)
+    t2i.t2i_dit_host_tier(m, host)
+    first, n, offs, bb = t2i.t2i_dit_block_layout(cfg)
+    print(f"[bench] host tier packed: {L} x {bb / 1e6:.1f} MB in {time.time() - t0:.1f} s",
+          file=sys.stderr, flush=True)
+    comp = torch.cuda.current_stream()
+    copy = torch.cuda.Stream()
+    g = torch.randn(4096, 4096, device="cuda") * 1e-2
+
+    def timed(fn):
+        # a few ms of matmuls ahead of the timed region, so that every launch and
+        # copy of it is queued before its first one can start
+        a = g
+        for _ in range(16):
+            a = a @ g
+        s, e = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        s.record(comp)
+        fn()
+        e.record(comp)
+        torch.cuda.synchronize()
+        return s.elapsed_time(e)
+
+    def median(fn, before=None):
+        xs = []
+        for _ in range(reps):
+            if before:
+                before()
+            xs.append(timed(fn))
+        return sorted(xs)[len(xs) // 2]
+
+    def load_on(stream):
+        copy.wait_stream(comp)
+        t2i.t2i_dit_load_async(m, stream)
+
+    def load_only():
+        load_on(copy)
+        comp.wait_stream(copy)
+
+    step()
+    torch.cuda.synchronize()
+    evict0 = lambda: t2i.t2i_dit_evict(m, 0)
+    t_load_all = median(load_only, evict0)
+    t_step = median(step)
+    t_step0 = median(lambda: step(n_blocks=0))
+    t_serial = median(lambda: (t2i.t2i_dit_load_async(m, comp), step()), evict0)
+    tl, tc = t_load_all / L, (t_step - t_step0) / L
+    e2e = []
+    for le in range(L + 1):
+        e2e.append(round(median(lambda: (load_on(copy), step()),
+                                lambda: t2i.t2i_dit_evict(m, le)), 3))
+        print(f"[bench] L_e={le}: {e2e[-1]:.2f} ms", file=sys.stderr, flush=True)
+    t2i.t2i_dit_evict(m, L)
+    eq1 = [round(t_step0 + max(L * tc, (L - le) * tl + tc), 3) for le in range(L + 1)]
+    lp = t2i.t2i_first_layers(L, tl, tc)
+    return {
+        "metric": "first-layers caching: latency of one step that starts while blocks "
+                  "[L_e, L) load from pinned host memory",
+        "unit": "ms", "higher_is_better": False, "data": "synthetic",
+        "config": {"workload": w.name, "blocks": L, "block_bytes": bb},
+        "t_load_ms_per_block": round(tl, 4), "t_comp_ms_per_block": round(tc, 4),
+        "t_rest_ms": round(t_step0, 3),
+        "h2d_roofline": {"bound": "pcie", "achieved": round(bb * L / (t_load_all / 1e3) / 1e9, 1),
+                         "peak": PCIE5_X16_GBS, "unit": "GB/s",
+                         "frac": round(bb * L / (t_load_all / 1e3) / 1e9 / PCIE5_X16_GBS, 3)},
+        "prefix_eq2": lp,
+        "resident_ms": round(t_step, 3), "serial_ms": round(t_serial, 3),
+        "ppl_0_ms": e2e[0], "ppl_prefix_ms": e2e[lp], "ppl_half_prefix_ms": e2e[lp // 2],
+        "e2e_ms_by_prefix": e2e, "eq1_ms_by_prefix": eq1,
+    }
+
+
 WORKLOADS = {
     "dit1024_cfg": ("denoising steps/s at 1024px DiT; MFMA TFLOP/s as fraction of MI355X bf16 peak",
                     "dit1024_cfg: 1024px image, latent 4x128x128, patch 2 -> 4096 tokens x 2 "
@@ -225,6 +307,8 @@ def main():
                     help="time only the vTime scheduler library (host CPU, no GPU)")
     ap.add_argument("--lora-rank", type=int, default=0,
                     help="also time merging a rank-R LoRA into every 2-D block weight")
+    ap.add_argument("--loading", action="store_true",
+                    help="time first-layers caching with progressive loading instead")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="run only a plain 1 GiB device copy (HBM counter calibration)")
     args = ap.parse_args()
@@ -285,6 +369,12 @@ def main():
     def run(i):
         k = i % n
         t2i.t2i_dit_step(m, x, hw, sched[k], tx, guidance=w.guidance, t_next=sched[k + 1])
+
+    if args.loading:
+        def one_step(n_blocks=-1):
+            t2i.t2i_dit_step(m, x, hw, sched[0], tx, guidance=w.guidance, n_blocks=n_blocks)
+        print(json.dumps(loading_bench(t2i, m, cfg, w, dev, one_step)), flush=True)
+        return
 
     lib = t2i.load()
     # warmup; the last warmup pass times every kernel class to find the dominant one

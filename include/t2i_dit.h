@@ -133,7 +133,8 @@ t2i_status t2i_dit_init(const t2i_dit_config* cfg, const void* const* weights,
                         void* workspace, size_t ws_bytes, void* stream,
                         t2i_dit** out);
 
-/* Replace the weight pointers (same shapes and dtypes) of a live handle. */
+/* Replace the weight pointers (same shapes and dtypes) of a live handle;
+ * every block becomes resident (queued loads are waited for first). */
 t2i_status t2i_dit_rebind_weights(t2i_dit* h, const void* const* weights,
                                   void* stream);
 
@@ -256,6 +257,82 @@ typedef struct t2i_sample_args {
 
 /* Synchronises `stream` once per step when cache_tau > 0, else never. */
 t2i_status t2i_dit_sample(t2i_dit* h, const t2i_sample_args* args, void* stream);
+
+/*
+ * Layer residency: first-layers caching with progressive loading (Sec. 5.1,
+ * "Caching the first layers", Eq. 1-2) over the weight table as a layer
+ * lookup table (Sec. 5.3, "model weight virtualization").
+ *
+ * A block's weights are its t2i_dit_weight_desc entries [first_index + b *
+ * n_tensors, first_index + (b + 1) * n_tensors).  Packed, tensor j of a block
+ * sits at byte offsets[j] (256-byte aligned) of a block_bytes record.  The
+ * host tier is the caller's page-locked host copy of every block, packed
+ * [depth][block_bytes]; the arena is a device buffer of the same shape that
+ * the library loads evicted blocks into (block b at b * block_bytes).
+ *
+ * A block is resident (its table entries point at device weights: the
+ * caller's from init / rebind, or its arena record after a load), loading
+ * (a copy into its arena record is queued, with an event recorded after it)
+ * or evicted (its entries are unbound).  Eviction goes in reverse layer
+ * order and loading in layer order, so the resident and loading blocks
+ * always form a prefix.  A step or sample whose blocks include an evicted one
+ * fails with T2I_ERR_INVALID_ARG before launching anything.  A loading block
+ * is waited for on the call's stream only right before its first use: its
+ * modulation rows and (cross-DiT) text K/V are then computed there instead of
+ * up front, with the same kernels and arguments, so results are bitwise
+ * those of a resident model.
+ */
+
+/* Bytes of one packed block; fills *first_index, *n_tensors and, when
+ * offsets != NULL, offsets[n_tensors].  Returns 0 on a bad config. */
+size_t t2i_dit_block_layout(const t2i_dit_config* cfg, int32_t* first_index,
+                            int32_t* n_tensors, size_t* offsets);
+
+/*
+ * Register the host tier.  host_blocks: page-locked host memory (hipHostMalloc)
+ * of depth * block_bytes bytes; arena: device memory, 256-byte aligned, of
+ * arena_bytes >= depth * block_bytes.  Both are borrowed for the handle's life
+ * (or until the next t2i_dit_host_tier).  Pageable host memory is rejected
+ * (T2I_ERR_INVALID_ARG): copies from it would not overlap with compute.
+ * Waits for loads still queued from an earlier registration.
+ */
+t2i_status t2i_dit_host_tier(t2i_dit* h, const void* host_blocks, void* arena,
+                             size_t arena_bytes);
+
+/*
+ * Evict blocks [keep, depth), last block first (Sec. 5.3, elastic weight
+ * eviction: reverse layer order keeps the first layers that let loading
+ * overlap inference).  Needs a host tier.  Waits for queued loads of those
+ * blocks to finish.  Frees nothing: the device memory the evicted blocks
+ * were bound to goes back to its owner, who may reuse it once the work
+ * queued on it (earlier steps) has completed.
+ */
+t2i_status t2i_dit_evict(t2i_dit* h, int32_t keep);
+
+/*
+ * Queue the load of every evicted block, in layer order, on copy_stream (a
+ * hipStream_t as void*; use a stream other than the compute stream to
+ * overlap): one host-to-device copy of block_bytes into the block's arena
+ * record, then an event.  The blocks' table entries are rebound to the arena
+ * at once, and later calls wait on the events.  *n_loaded (may be NULL)
+ * receives the number of blocks queued.
+ */
+t2i_status t2i_dit_load_async(t2i_dit* h, void* copy_stream, int32_t* n_loaded);
+
+/*
+ * Prefix length to keep resident (Eq. 2): the fewest first layers of L
+ * uniform layers (copy time t_load and inference time t_comp per layer, any
+ * one unit) whose resident copy lets the copies of the others finish while
+ * inference runs, so that the latency is L * t_comp.  Equals Eq. 2 when
+ * t_load >= t_comp (the case the paper considers); otherwise 1, since with
+ * nothing resident the first layer's copy always delays inference.  Returns
+ * -1 when L < 1 or a time is not finite and positive.
+ */
+int32_t t2i_first_layers(int32_t L, double t_load, double t_comp);
+
+/* Per-block state, host [depth]: 0 resident, 1 loading, 2 evicted.  A loading
+ * block whose copy has finished is reported (and kept) as resident. */
+t2i_status t2i_dit_block_state(t2i_dit* h, int32_t* state);
 
 /*
  * Kernel timing (tracing aid).  When a class's bit is set in `class_mask`,

@@ -25,5 +25,6 @@ Modules:
            the sampling loop
   lora     weight-update adapter merge W + alpha B A
   sched    the vTime two-layer fair scheduler (control plane)
+  loading  the load/compute pipeline of first-layers caching (Eq. 1-2)
 """
-from . import dit, sampler, mmdit, lora, sched  # noqa: F401
+from . import dit, sampler, mmdit, lora, sched, loading  # noqa: F401

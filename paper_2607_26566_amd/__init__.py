@@ -8,6 +8,8 @@ kernels.  The functions below carry the C ABI's names:
 * :func:`t2i_dit_step`   one model evaluation (+ guidance, + Euler update)
 * :func:`t2i_dit_sample` the whole denoising loop with the optional cache skip
 * :func:`t2i_cache_check` the cache-skip decision of one step
+* :func:`t2i_dit_host_tier`, :func:`t2i_dit_evict`, :func:`t2i_dit_load_async`,
+  :func:`t2i_dit_block_state`: first-layers caching with progressive loading
 """
 from __future__ import annotations
 
@@ -22,7 +24,9 @@ from ._lib import (T2I_F32, T2I_BF16, T2I_ARCH_CROSS_DIT, T2I_ARCH_MMDIT,
                    T2I_CACHE_ACCUMULATE, T2I_CACHE_PER_STEP, T2IError, check, load)
 
 __all__ = ["Config", "DiT", "t2i_dit_init", "t2i_dit_step", "t2i_dit_sample",
-           "t2i_cache_check", "weight_table", "upload", "T2IError", "load"]
+           "t2i_cache_check", "weight_table", "upload", "T2IError", "load",
+           "t2i_dit_block_layout", "pack_blocks", "t2i_dit_host_tier", "t2i_dit_evict",
+           "t2i_dit_load_async", "t2i_dit_block_state", "t2i_first_layers"]
 
 
 def _stream(stream=None) -> int:
@@ -146,6 +150,71 @@ class DiT:
 
 def t2i_dit_init(cfg: Config, weights: Sequence[torch.Tensor], device="cuda", stream=None) -> DiT:
     return DiT(cfg, weights, device, stream)
+
+
+# ---------------------------------------------------------------- layer residency
+
+def t2i_dit_block_layout(cfg: Config):
+    """(first_index, n_tensors, offsets, block_bytes) of the packed per-block
+    weight record (``t2i_dit_block_layout``)."""
+    lib = load()
+    first, n = C.c_int32(), C.c_int32()
+    bb = lib.t2i_dit_block_layout(cfg.ref(), C.byref(first), C.byref(n), None)
+    if bb == 0:
+        raise T2IError(1, "invalid config")
+    offs = (C.c_size_t * n.value)()
+    lib.t2i_dit_block_layout(cfg.ref(), C.byref(first), C.byref(n), offs)
+    return first.value, n.value, list(offs), int(bb)
+
+
+def pack_blocks(cfg: Config, weights: Sequence[torch.Tensor]) -> torch.Tensor:
+    """The host tier: every block's tensors (weight-table order) copied into a
+    page-locked uint8 [depth, block_bytes] buffer at the packed offsets."""
+    first, n, offs, bb = t2i_dit_block_layout(cfg)
+    depth = cfg.c.depth
+    out = torch.zeros((depth, bb), dtype=torch.uint8, pin_memory=True)
+    for b in range(depth):
+        for j in range(n):
+            t = weights[first + b * n + j].contiguous().reshape(-1).view(torch.uint8)
+            out[b, offs[j]:offs[j] + t.numel()].copy_(t)
+    return out
+
+
+def t2i_dit_host_tier(m: DiT, host_blocks: torch.Tensor, arena: Optional[torch.Tensor] = None):
+    """Register the host tier (pinned, from :func:`pack_blocks`) and the device
+    arena blocks load into (allocated here when not given)."""
+    if not host_blocks.is_pinned():
+        raise T2IError(1, "host_blocks must be page-locked (pin_memory)")
+    if arena is None:
+        arena = torch.empty(host_blocks.numel(), dtype=torch.uint8, device="cuda")
+    check(m.lib.t2i_dit_host_tier(m.h, C.c_void_p(host_blocks.data_ptr()),
+                                  C.c_void_p(arena.data_ptr()), arena.numel()), m.h)
+    m.host_blocks, m.arena = host_blocks, arena
+    return arena
+
+
+def t2i_dit_evict(m: DiT, keep: int):
+    """Evict blocks [keep, depth), last first."""
+    check(m.lib.t2i_dit_evict(m.h, int(keep)), m.h)
+
+
+def t2i_dit_load_async(m: DiT, stream=None) -> int:
+    """Queue the loads of every evicted block on ``stream``; returns how many."""
+    n = C.c_int32()
+    check(m.lib.t2i_dit_load_async(m.h, C.c_void_p(_stream(stream)), C.byref(n)), m.h)
+    return n.value
+
+
+def t2i_first_layers(L: int, t_load: float, t_comp: float) -> int:
+    """Resident prefix that hides loading (Eq. 2; see the header)."""
+    return int(load().t2i_first_layers(int(L), float(t_load), float(t_comp)))
+
+
+def t2i_dit_block_state(m: DiT) -> List[int]:
+    """Per block: 0 resident, 1 loading, 2 evicted."""
+    st = (C.c_int32 * m.cfg.c.depth)()
+    check(m.lib.t2i_dit_block_state(m.h, st), m.h)
+    return list(st)
 
 
 def _check_lat(latents: torch.Tensor):

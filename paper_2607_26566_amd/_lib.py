@@ -77,6 +77,13 @@ SIGNATURES = {
     "t2i_dit_init": (i32, [C.POINTER(t2i_dit_config), C.POINTER(vp), vp, sz, vp,
                            C.POINTER(vp)]),
     "t2i_dit_rebind_weights": (i32, [vp, C.POINTER(vp), vp]),
+    "t2i_dit_block_layout": (sz, [C.POINTER(t2i_dit_config), C.POINTER(i32), C.POINTER(i32),
+                                  C.POINTER(sz)]),
+    "t2i_dit_host_tier": (i32, [vp, vp, vp, sz]),
+    "t2i_dit_evict": (i32, [vp, i32]),
+    "t2i_dit_load_async": (i32, [vp, vp, C.POINTER(i32)]),
+    "t2i_dit_block_state": (i32, [vp, C.POINTER(i32)]),
+    "t2i_first_layers": (i32, [i32, f64, f64]),
     "t2i_dit_step": (i32, [vp, C.POINTER(t2i_step_args), vp]),
     "t2i_cache_check": (i32, [vp, C.POINTER(t2i_cache_args), vp]),
     "t2i_dit_sample": (i32, [vp, C.POINTER(t2i_sample_args), vp]),

@@ -5,6 +5,8 @@
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
+#include <bitset>
+#include <climits>
 #include <cmath>
 #include <cstdio>
 #include <cstring>
@@ -207,8 +209,22 @@ struct t2i_dit {
   std::vector<hipEvent_t> ev_pool;               // created on demand, reused
   size_t ev_used = 0;
   std::vector<std::pair<int, size_t>> ev_pairs;  // (class, index of start event)
+  // layer residency: per block resident / loading / evicted, the event after
+  // each block's queued copy, and the host tier the copies read
+  enum : uint8_t { BLK_RESIDENT = 0, BLK_LOADING = 1, BLK_EVICTED = 2 };
+  std::vector<uint8_t> blk;
+  std::vector<hipEvent_t> blk_ev;
+  const char* host_blocks = nullptr;
+  char* arena = nullptr;
+  size_t blk_bytes = 0;
+  std::vector<size_t> blk_off;   // packed offset of each tensor of a block
 
   ~t2i_dit() {
+    for (size_t b = 0; b < blk_ev.size(); ++b)
+      if (blk_ev[b]) {
+        if (blk[b] == BLK_LOADING) (void)hipEventSynchronize(blk_ev[b]);
+        (void)hipEventDestroy(blk_ev[b]);
+      }
     for (hipEvent_t e : ev_pool) (void)hipEventDestroy(e);
   }
 
@@ -247,6 +263,12 @@ struct Plan {
   int grid_max = 0;  // largest grid side (length of the position tables)
   const t2i_control* ctl = nullptr;   // validated callback input, or NULL
   size_t lat_floats = 0;
+  // blocks >= defer_from are still loading: their modulation rows (cond_rows
+  // of them) and text K/V are computed right before the block, after its load
+  // event; `done` marks the deferred blocks already prepared in this call
+  int defer_from = INT_MAX;
+  int cond_rows = 0;
+  mutable std::bitset<256> done;
 };
 
 t2i_status build_plan(t2i_dit* h, int n_req, const int32_t* lat_h, const int32_t* lat_w,
@@ -397,10 +419,42 @@ hipError_t linear(t2i_dit* h, const void* A, int lda, int wi, int M, int N, int 
   return launch_gemm_f32((const float*)A, lda, W, K, false, B, M, N, K, kind, epi, st);
 }
 
+// Block b's adaLN chunks of `rows` conditioning rows (silu(c) in tsc) into
+// the modulation table.
+hipError_t block_modulation(t2i_dit* h, int b, int rows, hipStream_t st) {
+  const t2i_dit_config& c = h->cfg;
+  const int D = c.hidden, pb = per_block(c);
+  const float* tsc = h->at<float>(h->L.tsc);
+  float* mod = h->at<float>(h->L.mod);
+  Epi e = make_epi();
+  e.ldo = mod_width(c);
+  if (c.arch == T2I_ARCH_CROSS_DIT) {
+    e.out = mod + (size_t)b * 6 * D;
+    const int wi = W_BLOCK0 + b * pb + X_ADA;
+    return launch_linear_rows(tsc, D, h->w[wi], D, h->bf(), h->w[wi + 1], rows, 6 * D, D,
+                              EPI_STORE, e, st);
+  }
+  for (int s = 0; s < 2; ++s) {
+    e.out = mod + (size_t)b * 12 * D + (size_t)s * 6 * D;
+    const int wi = W_BLOCK0 + b * pb + s * J_PER_STREAM + J_ADA;
+    hipError_t err = launch_linear_rows(tsc, D, h->w[wi], D, h->bf(), h->w[wi + 1], rows, 6 * D,
+                                        D, EPI_STORE, e, st);
+    if (err != hipSuccess) return err;
+  }
+  return hipSuccess;
+}
+
+// The call's stream waits for block b's queued load, if any.
+hipError_t wait_block(t2i_dit* h, int b, hipStream_t st) {
+  if (h->blk[b] != t2i_dit::BLK_LOADING) return hipSuccess;
+  return hipStreamWaitEvent(st, h->blk_ev[b], 0);
+}
+
 // Conditioning of `rows` timesteps (rows <= max_steps * max_requests):
-// silu(c) into tsc and every block's adaLN chunks into the modulation table.
+// silu(c) into tsc and the adaLN chunks of blocks [0, min(n_blocks_mod,
+// defer_from)) into the modulation table.
 t2i_status conditioning(t2i_dit* h, const double* t_host, int rows, int n_blocks_mod,
-                        hipStream_t st) {
+                        int defer_from, hipStream_t st) {
   const t2i_dit_config& c = h->cfg;
   const int D = c.hidden, fd = c.freq_dim;
   float* tfreq = h->at<float>(h->L.tfreq);
@@ -416,20 +470,10 @@ t2i_status conditioning(t2i_dit* h, const double* t_host, int rows, int n_blocks
   e.out = tsc;
   HIP_TRY(h, launch_linear_rows(th1, D, h->w[W_T2], D, wb, h->w[B_T2], rows, D, D, EPI_SILU, e, st));
   const int mw = mod_width(c);
-  const int pb = per_block(c);
   e.ldo = mw;
-  for (int b = 0; b < n_blocks_mod; ++b) {
-    if (c.arch == T2I_ARCH_CROSS_DIT) {
-      e.out = mod + (size_t)b * 6 * D;
-      const int wi = W_BLOCK0 + b * pb + X_ADA;
-      HIP_TRY(h, launch_linear_rows(tsc, D, h->w[wi], D, wb, h->w[wi + 1], rows, 6 * D, D, EPI_STORE, e, st));
-    } else {
-      for (int s = 0; s < 2; ++s) {
-        e.out = mod + (size_t)b * 12 * D + (size_t)s * 6 * D;
-        const int wi = W_BLOCK0 + b * pb + s * J_PER_STREAM + J_ADA;
-        HIP_TRY(h, launch_linear_rows(tsc, D, h->w[wi], D, wb, h->w[wi + 1], rows, 6 * D, D, EPI_STORE, e, st));
-      }
-    }
+  for (int b = 0; b < std::min(n_blocks_mod, defer_from); ++b) {
+    HIP_TRY(h, wait_block(h, b, st));
+    HIP_TRY(h, block_modulation(h, b, rows, st));
   }
   e.out = mod + (size_t)(mw - 2 * D);
   const int fb = final_base(c);
@@ -437,8 +481,29 @@ t2i_status conditioning(t2i_dit* h, const double* t_host, int rows, int n_blocks
   return T2I_OK;
 }
 
-// Text projection and (cross-DiT) every block's text K/V.
-t2i_status text_prep(t2i_dit* h, const Plan& P, const void* prompt, hipStream_t st) {
+// Cross-DiT block b's text K/V from the projected text in ytxt.
+hipError_t block_text_kv(t2i_dit* h, const Plan& P, int b, hipStream_t st) {
+  const t2i_dit_config& c = h->cfg;
+  const int D = c.hidden;
+  const size_t txt_rows_max = (size_t)(c.max_requests + 1) * c.text_tokens;
+  Epi e = make_epi();
+  e.out = h->at<char>(h->L.kv) + (size_t)b * txt_rows_max * 2 * D * h->act();
+  e.ldo = 2 * D;
+  int kind = EPI_STORE;
+  if (h->bf()) {   // k row-major [rows, D], v transposed [D][ldvt_txt]
+    kind = EPI_SPLIT_VT;
+    e.ldo = D;
+    e.vt = h->at<bf16>(h->L.vtt) + (size_t)b * D * h->L.ldvt_txt;
+    e.ldvt = h->L.ldvt_txt;
+    e.vcol0 = D;
+  }
+  return linear(h, h->at<char>(h->L.ytxt), D, W_BLOCK0 + b * X_PER_BLOCK + X_XKV, P.txt_rows,
+                2 * D, D, kind, e, st);
+}
+
+// Text projection and (cross-DiT) the text K/V of blocks [0, min(nb,
+// P.defer_from)).
+t2i_status text_prep(t2i_dit* h, const Plan& P, const void* prompt, int nb, hipStream_t st) {
   const t2i_dit_config& c = h->cfg;
   const int D = c.hidden, M = c.text_tokens;
   char* ytxt = h->at<char>(h->L.ytxt);
@@ -461,21 +526,19 @@ t2i_status text_prep(t2i_dit* h, const Plan& P, const void* prompt, hipStream_t 
     HIP_TRY(h, launch_broadcast_rows(h->w[B_Y], h->bf(), M, D,
                                      ytxt + (size_t)P.n_req * M * D * h->act(), st));
   if (c.arch != T2I_ARCH_CROSS_DIT) return T2I_OK;
-  const size_t txt_rows_max = (size_t)(c.max_requests + 1) * M;
-  for (int b = 0; b < c.depth; ++b) {
-    e.out = h->at<char>(h->L.kv) + (size_t)b * txt_rows_max * 2 * D * h->act();
-    e.ldo = 2 * D;
-    int kind = EPI_STORE;
-    if (h->bf()) {   // k row-major [rows, D], v transposed [D][ldvt_txt]
-      kind = EPI_SPLIT_VT;
-      e.ldo = D;
-      e.vt = h->at<bf16>(h->L.vtt) + (size_t)b * D * h->L.ldvt_txt;
-      e.ldvt = h->L.ldvt_txt;
-      e.vcol0 = D;
-    }
-    HIP_TRY(h, linear(h, ytxt, D, W_BLOCK0 + b * X_PER_BLOCK + X_XKV, P.txt_rows, 2 * D, D,
-                      kind, e, st));
-  }
+  for (int b = 0; b < std::min(nb, P.defer_from); ++b) HIP_TRY(h, block_text_kv(h, P, b, st));
+  return T2I_OK;
+}
+
+// Before the first use of block b's weights in a call: when the block is
+// still loading, wait for its copy and compute its deferred modulation rows
+// and text K/V.
+t2i_status ensure_block(t2i_dit* h, const Plan& P, int b, hipStream_t st) {
+  if (b < P.defer_from || P.done[b]) return T2I_OK;
+  HIP_TRY(h, wait_block(h, b, st));
+  HIP_TRY(h, block_modulation(h, b, P.cond_rows, st));
+  if (h->cfg.arch == T2I_ARCH_CROSS_DIT) HIP_TRY(h, block_text_kv(h, P, b, st));
+  P.done[b] = true;
   return T2I_OK;
 }
 
@@ -516,6 +579,7 @@ t2i_status run_blocks_cross(t2i_dit* h, const Plan& P, int nb, hipStream_t st) {
   const size_t A = h->act();
   const size_t txt_rows_max = (size_t)(c.max_requests + 1) * c.text_tokens;
   for (int b = 0; b < nb; ++b) {
+    if (t2i_status s = ensure_block(h, P, b, st)) return s;
     const int wb = W_BLOCK0 + b * X_PER_BLOCK;
     const int mo = b * 6 * D;
     // self-attention
@@ -603,6 +667,7 @@ t2i_status run_blocks_mmdit(t2i_dit* h, const Plan& P, int nb, hipStream_t st) {
   const int r0s[2] = {0, P.txt_rows}, ns[2] = {P.txt_rows, P.rows};
   const SeqMap* maps[2] = {&P.txt, &P.img};
   for (int b = 0; b < nb; ++b) {
+    if (t2i_status s = ensure_block(h, P, b, st)) return s;
     for (int s = 0; s < 2; ++s) {
       const int r0 = r0s[s], R = ns[s], wi = W_BLOCK0 + b * 2 * J_PER_STREAM + s * J_PER_STREAM;
       const int mo = b * 12 * D + s * 6 * D;
@@ -696,6 +761,58 @@ t2i_status cache_check_impl(t2i_dit* h, const Plan& P, int step, int n_steps, do
     if (rel_l1) rel_l1[r] = h->hdr_host[r].d;
     if (skip) skip[r] = (uint8_t)(h->hdr_host[r].skip ? 1 : 0);
   }
+  return T2I_OK;
+}
+
+// Packed byte offsets of one block's tensors (every block has the same
+// shapes); returns the record size.
+size_t block_layout(const t2i_dit_config& c, std::vector<size_t>* offs) {
+  const std::vector<WDesc> t = weight_table(c);
+  const size_t A = c.dtype == T2I_BF16 ? 2 : 4;
+  size_t off = 0;
+  for (int j = 0; j < per_block(c); ++j) {
+    const WDesc& d = t[W_BLOCK0 + j];
+    size_t n = 1;
+    for (int k = 0; k < d.nd; ++k) n *= (size_t)d.shape[k];
+    if (offs) offs->push_back(off);
+    off = align_up(off + n * A);
+  }
+  return off;
+}
+
+// Loading blocks whose copy has finished become resident.
+t2i_status refresh_loads(t2i_dit* h) {
+  for (size_t b = 0; b < h->blk.size(); ++b) {
+    if (h->blk[b] != t2i_dit::BLK_LOADING) continue;
+    hipError_t e = hipEventQuery(h->blk_ev[b]);
+    if (e == hipSuccess) h->blk[b] = t2i_dit::BLK_RESIDENT;
+    else if (e != hipErrorNotReady)
+      return fail(h, T2I_ERR_DEVICE, std::string("hipEventQuery: ") + hipGetErrorString(e));
+  }
+  return T2I_OK;
+}
+
+// Blocks [0, nb) must be resident or loading; the first still loading
+// becomes P.defer_from.
+t2i_status check_residency(t2i_dit* h, Plan& P, int nb) {
+  if (t2i_status s = refresh_loads(h)) return s;
+  P.defer_from = INT_MAX;
+  for (int b = 0; b < nb; ++b) {
+    if (h->blk[b] == t2i_dit::BLK_EVICTED)
+      return fail(h, T2I_ERR_INVALID_ARG,
+                  "block " + std::to_string(b) + " is evicted: queue its load first");
+    if (h->blk[b] == t2i_dit::BLK_LOADING && P.defer_from == INT_MAX) P.defer_from = b;
+  }
+  return T2I_OK;
+}
+
+// Wait for every queued load (before the host tier or the bindings change).
+t2i_status drain_loads(t2i_dit* h) {
+  for (size_t b = 0; b < h->blk.size(); ++b)
+    if (h->blk[b] == t2i_dit::BLK_LOADING) {
+      HIP_TRY(h, hipEventSynchronize(h->blk_ev[b]));
+      h->blk[b] = t2i_dit::BLK_RESIDENT;
+    }
   return T2I_OK;
 }
 
@@ -819,6 +936,7 @@ t2i_status t2i_dit_init(const t2i_dit_config* cfg, const void* const* weights, v
   h->ws = (char*)workspace;
   h->ws_bytes = ws_bytes;
   h->L = layout(*cfg);
+  h->blk.assign(cfg->depth, t2i_dit::BLK_RESIDENT);
   *out = h;
   return T2I_OK;
 }
@@ -828,7 +946,112 @@ t2i_status t2i_dit_rebind_weights(t2i_dit* h, const void* const* weights, void* 
   if (!h || !weights) return T2I_ERR_INVALID_ARG;
   for (size_t i = 0; i < h->w.size(); ++i)
     if (!weights[i]) return fail(h, T2I_ERR_INVALID_ARG, "NULL weight pointer");
+  if (t2i_status s = drain_loads(h)) return s;
   h->w.assign(weights, weights + h->w.size());
+  h->blk.assign(h->cfg.depth, t2i_dit::BLK_RESIDENT);
+  return T2I_OK;
+}
+
+size_t t2i_dit_block_layout(const t2i_dit_config* cfg, int32_t* first_index, int32_t* n_tensors,
+                            size_t* offsets) {
+  if (check_config(cfg) || !first_index || !n_tensors) return 0;
+  std::vector<size_t> o;
+  const size_t bytes = block_layout(*cfg, &o);
+  *first_index = W_BLOCK0;
+  *n_tensors = per_block(*cfg);
+  if (offsets) std::copy(o.begin(), o.end(), offsets);
+  return bytes;
+}
+
+t2i_status t2i_dit_host_tier(t2i_dit* h, const void* host_blocks, void* arena,
+                             size_t arena_bytes) {
+  if (!h) return T2I_ERR_INVALID_ARG;
+  if (!host_blocks || !arena) return fail(h, T2I_ERR_INVALID_ARG, "host_blocks and arena are required");
+  if ((uintptr_t)arena % kAlign) return fail(h, T2I_ERR_INVALID_ARG, "arena must be 256-byte aligned");
+  std::vector<size_t> offs;
+  const size_t bb = block_layout(h->cfg, &offs);
+  const size_t need = bb * (size_t)h->cfg.depth;
+  if (arena_bytes < need) return fail(h, T2I_ERR_WORKSPACE, "arena smaller than depth * block_bytes");
+  // both ends of each range must lie in memory of the right kind
+  const char* hb = (const char*)host_blocks;
+  const char* ab = (const char*)arena;
+  const struct { const char* p; hipMemoryType want; const char* msg; } probes[] = {
+      {hb, hipMemoryTypeHost, "host_blocks is not page-locked host memory"},
+      {hb + need - 1, hipMemoryTypeHost, "host_blocks is not page-locked host memory"},
+      {ab, hipMemoryTypeDevice, "arena is not device memory"},
+      {ab + need - 1, hipMemoryTypeDevice, "arena is not device memory"}};
+  for (const auto& pr : probes) {
+    hipPointerAttribute_t at;
+    std::memset(&at, 0, sizeof(at));
+    hipError_t e = hipPointerGetAttributes(&at, pr.p);
+    if (e != hipSuccess || at.type != pr.want) {
+      (void)hipGetLastError();
+      return fail(h, T2I_ERR_INVALID_ARG, pr.msg);
+    }
+  }
+  if (t2i_status s = drain_loads(h)) return s;
+  h->host_blocks = hb;
+  h->arena = (char*)arena;
+  h->blk_bytes = bb;
+  h->blk_off = offs;
+  return T2I_OK;
+}
+
+t2i_status t2i_dit_evict(t2i_dit* h, int32_t keep) {
+  if (!h) return T2I_ERR_INVALID_ARG;
+  if (!h->host_blocks) return fail(h, T2I_ERR_INVALID_ARG, "evict needs a host tier");
+  const int depth = h->cfg.depth, pb = per_block(h->cfg);
+  if (keep < 0 || keep > depth) return fail(h, T2I_ERR_SHAPE, "keep out of [0, depth]");
+  for (int b = depth - 1; b >= keep; --b) {
+    if (h->blk[b] == t2i_dit::BLK_LOADING) HIP_TRY(h, hipEventSynchronize(h->blk_ev[b]));
+    h->blk[b] = t2i_dit::BLK_EVICTED;
+    for (int j = 0; j < pb; ++j) h->w[W_BLOCK0 + (size_t)b * pb + j] = nullptr;
+  }
+  return T2I_OK;
+}
+
+t2i_status t2i_dit_load_async(t2i_dit* h, void* copy_stream, int32_t* n_loaded) {
+  if (!h) return T2I_ERR_INVALID_ARG;
+  if (n_loaded) *n_loaded = 0;
+  if (!h->host_blocks) return fail(h, T2I_ERR_INVALID_ARG, "load needs a host tier");
+  const int depth = h->cfg.depth, pb = per_block(h->cfg);
+  hipStream_t cs = (hipStream_t)copy_stream;
+  if (h->blk_ev.empty()) h->blk_ev.assign(depth, nullptr);
+  int n = 0;
+  for (int b = 0; b < depth; ++b) {
+    if (h->blk[b] != t2i_dit::BLK_EVICTED) continue;
+    if (!h->blk_ev[b])
+      HIP_TRY(h, hipEventCreateWithFlags(&h->blk_ev[b], hipEventDisableTiming));
+    char* dst = h->arena + (size_t)b * h->blk_bytes;
+    HIP_TRY(h, hipMemcpyAsync(dst, h->host_blocks + (size_t)b * h->blk_bytes, h->blk_bytes,
+                              hipMemcpyHostToDevice, cs));
+    HIP_TRY(h, hipEventRecord(h->blk_ev[b], cs));
+    for (int j = 0; j < pb; ++j) h->w[W_BLOCK0 + (size_t)b * pb + j] = dst + h->blk_off[j];
+    h->blk[b] = t2i_dit::BLK_LOADING;
+    ++n;
+  }
+  if (n_loaded) *n_loaded = n;
+  return T2I_OK;
+}
+
+int32_t t2i_first_layers(int32_t L, double t_load, double t_comp) {
+  if (L < 1 || !std::isfinite(t_load) || !std::isfinite(t_comp) || !(t_load > 0.0) ||
+      !(t_comp > 0.0))
+    return -1;
+  // loading is hidden when the last copy, finished at (L - Le) t_load, still
+  // leaves the last layer's compute as the only exposed time
+  auto hides = [&](long le) { return (double)(L - le) * t_load + t_comp <= (double)L * t_comp; };
+  const double v = std::ceil(((double)L * (t_load - t_comp) + t_comp) / t_load);
+  long k = v < 1.0 ? 1 : v > (double)L ? L : (long)v;
+  while (k > 1 && hides(k - 1)) --k;   // rounding of the quotient
+  while (k < L && !hides(k)) ++k;
+  return (int32_t)k;
+}
+
+t2i_status t2i_dit_block_state(t2i_dit* h, int32_t* state) {
+  if (!h || !state) return T2I_ERR_INVALID_ARG;
+  if (t2i_status s = refresh_loads(h)) return s;
+  for (size_t b = 0; b < h->blk.size(); ++b) state[b] = h->blk[b];
   return T2I_OK;
 }
 
@@ -900,10 +1123,12 @@ t2i_status t2i_dit_step(t2i_dit* h, const t2i_step_args* a, void* stream) {
       P.rm.dt[r] = (float)(a->t_next[r] - a->t[r]);
     }
   }
+  if ((s = check_residency(h, P, std::max(nb, 1))) != T2I_OK) return s;
   hipStream_t st = (hipStream_t)stream;
   set_modrows(P, 0);
-  if ((s = conditioning(h, a->t, P.n_req, std::max(nb, 1), st)) != T2I_OK) return s;
-  if ((s = text_prep(h, P, a->prompt_embeds, st)) != T2I_OK) return s;
+  P.cond_rows = P.n_req;
+  if ((s = conditioning(h, a->t, P.n_req, std::max(nb, 1), P.defer_from, st)) != T2I_OK) return s;
+  if ((s = text_prep(h, P, a->prompt_embeds, nb, st)) != T2I_OK) return s;
   return step_body(h, P, a->latents, a->latents, a->noise_pred, nb, a->hidden_out, a->skip,
                    a->cache_state, st);
 }
@@ -924,9 +1149,11 @@ t2i_status t2i_cache_check(t2i_dit* h, const t2i_cache_args* a, void* stream) {
   const t2i_dit_config& c = h->cfg;
   if (a->cache_state_bytes < cache_bytes(c, P.n_req, P.T_img, P.branches))
     return fail(h, T2I_ERR_WORKSPACE, "cache_state too small");
+  if ((s = check_residency(h, P, 1)) != T2I_OK) return s;
   hipStream_t st = (hipStream_t)stream;
   set_modrows(P, 0);
-  if ((s = conditioning(h, a->t, P.n_req, 1, st)) != T2I_OK) return s;
+  // block 0's modulation only: a loading block 0 is waited for in place
+  if ((s = conditioning(h, a->t, P.n_req, 1, INT_MAX, st)) != T2I_OK) return s;
   HIP_TRY(h, embed(h, P, a->latents, h->at<float>(h->L.x0), h->at<float>(h->L.x), 0, st));
   return cache_check_impl(h, P, a->step, a->n_steps, a->tau, a->mode, a->cache_state, a->rel_l1,
                           a->skip, st);
@@ -957,10 +1184,12 @@ t2i_status t2i_dit_sample(t2i_dit* h, const t2i_sample_args* a, void* stream) {
       if (!std::isfinite(v)) return fail(h, T2I_ERR_INVALID_ARG, "timestep not finite");
       ts[(size_t)k * R + r] = v;
     }
+  if ((s = check_residency(h, P, c.depth)) != T2I_OK) return s;
   hipStream_t st = (hipStream_t)stream;
   // conditioning rows k*R + r for every step k < n
-  if ((s = conditioning(h, ts.data(), n * R, c.depth, st)) != T2I_OK) return s;
-  if ((s = text_prep(h, P, a->prompt_embeds, st)) != T2I_OK) return s;
+  P.cond_rows = n * R;
+  if ((s = conditioning(h, ts.data(), n * R, c.depth, P.defer_from, st)) != T2I_OK) return s;
+  if ((s = text_prep(h, P, a->prompt_embeds, c.depth, st)) != T2I_OK) return s;
   std::vector<uint8_t> skip(R, 0);
   std::vector<double> rel(R, 0.0);
   for (int k = a->start_step; k < n; ++k) {
@@ -969,6 +1198,7 @@ t2i_status t2i_dit_sample(t2i_dit* h, const t2i_sample_args* a, void* stream) {
       P.rm.dt[r] = (float)(ts[(size_t)(k + 1) * R + r] - ts[(size_t)k * R + r]);
     if (use_cache) {
       HIP_TRY(h, embed(h, P, a->latents, h->at<float>(h->L.x0), h->at<float>(h->L.x), 0, st));
+      if ((s = ensure_block(h, P, 0, st)) != T2I_OK) return s;   // block 0's modulation
       if ((s = cache_check_impl(h, P, k, n, a->cache_tau, a->cache_mode, a->cache_state,
                                 rel.data(), skip.data(), st)) != T2I_OK)
         return s;

@@ -5,6 +5,7 @@ import ctypes as C
 import os
 import re
 
+import numpy as np
 import pytest
 
 import synth
@@ -216,3 +217,45 @@ def test_op_argument_errors():
     k2 = (C.c_int32 * 1)(4)
     assert lib.t2i_op_attention(1, 2, 72, 1, qs, ql, qs, ql, k2, ql, 0x1000, 144, 0x2000,
                                 144, 0x3000, 144, 0x4000, 144, None) == 2
+
+
+@pytest.mark.parametrize("name", ["dit1024_cfg", "mmdit1024", "tiny_f32"])
+def test_block_layout_matches_weight_table(name):
+    w = synth.workload(name)
+    cfg = t2i.Config.from_shape(w)
+    first, n, offs, bb = t2i.t2i_dit_block_layout(cfg)
+    table = t2i.weight_table(cfg)
+    elt = 2 if w.dtype == "bf16" else 4
+    assert table[first][0] == "blocks.0.ada.w" or table[first][0] == "blocks.0.txt.ada.w"
+    assert table[first + n][0].startswith("blocks.1.")
+    end = 0
+    for j in range(n):
+        size = int(np.prod(table[first + j][1])) * elt
+        assert offs[j] % 256 == 0 and offs[j] >= end      # aligned, no overlap
+        end = offs[j] + size
+        # every block has the same shapes
+        assert table[first + (w.depth - 1) * n + j][1] == table[first + j][1]
+    assert bb == (end + 255) // 256 * 256
+    assert table[first + w.depth * n][0] == "final.ada.w"
+
+
+def test_residency_argument_errors():
+    w = synth.workload("dit512")
+    lib, cfg, h = _fake_handle(w)
+    try:
+        st = (C.c_int32 * w.depth)()
+        assert lib.t2i_dit_block_state(h, st) == 0 and list(st) == [0] * w.depth
+        # nothing to evict from / load into before a host tier is registered
+        assert lib.t2i_dit_evict(h, 3) == 1
+        assert b"host tier" in lib.t2i_last_error(h)
+        n = C.c_int32(-1)
+        assert lib.t2i_dit_load_async(h, None, C.byref(n)) == 1 and n.value == 0
+        _, _, _, bb = t2i.t2i_dit_block_layout(cfg)
+        need = bb * w.depth
+        assert lib.t2i_dit_host_tier(h, None, C.c_void_p(1 << 20), need) == 1
+        assert lib.t2i_dit_host_tier(h, C.c_void_p(0x1000), C.c_void_p((1 << 20) + 16), need) == 1
+        assert b"aligned" in lib.t2i_last_error(h)
+        assert lib.t2i_dit_host_tier(h, C.c_void_p(0x1000), C.c_void_p(1 << 20), need - 1) == 4
+        assert lib.t2i_dit_block_state(h, None) == 1
+    finally:
+        lib.t2i_dit_destroy(h)
