@@ -87,7 +87,7 @@ def test_progressive_step_bitwise_dit512():
 
 def test_progressive_sample_with_cache():
     w = synth.reduced(synth.workload("dit512"), name="dit512_d6", depth=6,
-                      requests=((32, 32), (24, 40)))
+                      requests=((32, 32), (24, 40)), guidance=4.5)
     M = Model(w, max_steps=8)
     lats, texts = synth.latents(w), synth.texts(w)
     hw, tx = list(w.requests), M.text_dev(texts)
@@ -97,7 +97,7 @@ def test_progressive_sample_with_cache():
     def run():
         x = M.latents_dev(lats)
         state = M.m.new_cache_state(toks, 2)
-        log, rel = t2i.t2i_dit_sample(M.m, x, hw, tx, n, guidance=w.guidance, cache_tau=0.08,
+        log, rel = t2i.t2i_dit_sample(M.m, x, hw, tx, n, guidance=w.guidance, cache_tau=0.3,
                                       cache_state=state)
         torch.cuda.synchronize()
         return x.cpu(), np.asarray(log)
