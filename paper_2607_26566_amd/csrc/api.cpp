@@ -444,6 +444,38 @@ hipError_t block_modulation(t2i_dit* h, int b, int rows, hipStream_t st) {
   return hipSuccess;
 }
 
+// The adaLN chunks of blocks [b0, b1) in grouped launches (one group per
+// block, per stream for MMDiT); bitwise the per-block block_modulation.
+hipError_t blocks_modulation(t2i_dit* h, int b0, int b1, int rows, hipStream_t st) {
+  const t2i_dit_config& c = h->cfg;
+  const int D = c.hidden, pb = per_block(c);
+  const bool mm = c.arch != T2I_ARCH_CROSS_DIT;
+  const float* tsc = h->at<float>(h->L.tsc);
+  float* mod = h->at<float>(h->L.mod);
+  Epi e = make_epi();
+  e.ldo = mod_width(c);
+  PtrGroup g;
+  int n = 0;
+  auto flush = [&]() {
+    hipError_t err = launch_linear_rows_group(tsc, D, g, n, D, h->bf(), rows, 6 * D, D, e, st);
+    n = 0;
+    return err;
+  };
+  for (int b = b0; b < b1; ++b)
+    for (int s = 0; s < (mm ? 2 : 1); ++s) {
+      const int wi = mm ? W_BLOCK0 + b * pb + s * J_PER_STREAM + J_ADA : W_BLOCK0 + b * pb + X_ADA;
+      g.W[n] = h->w[wi];
+      g.bias[n] = h->w[wi + 1];
+      g.out[n] = mod + (size_t)b * (mm ? 12 : 6) * D + (size_t)s * 6 * D;
+      g.vt[n] = nullptr;
+      if (++n == kMaxGroups) {
+        hipError_t err = flush();
+        if (err != hipSuccess) return err;
+      }
+    }
+  return flush();
+}
+
 // The call's stream waits for block b's queued load, if any.
 hipError_t wait_block(t2i_dit* h, int b, hipStream_t st) {
   if (h->blk[b] != t2i_dit::BLK_LOADING) return hipSuccess;
@@ -471,10 +503,9 @@ t2i_status conditioning(t2i_dit* h, const double* t_host, int rows, int n_blocks
   HIP_TRY(h, launch_linear_rows(th1, D, h->w[W_T2], D, wb, h->w[B_T2], rows, D, D, EPI_SILU, e, st));
   const int mw = mod_width(c);
   e.ldo = mw;
-  for (int b = 0; b < std::min(n_blocks_mod, defer_from); ++b) {
-    HIP_TRY(h, wait_block(h, b, st));
-    HIP_TRY(h, block_modulation(h, b, rows, st));
-  }
+  const int nbm = std::min(n_blocks_mod, defer_from);
+  for (int b = 0; b < nbm; ++b) HIP_TRY(h, wait_block(h, b, st));
+  HIP_TRY(h, blocks_modulation(h, 0, nbm, rows, st));
   e.out = mod + (size_t)(mw - 2 * D);
   const int fb = final_base(c);
   HIP_TRY(h, launch_linear_rows(tsc, D, h->w[fb], D, wb, h->w[fb + 1], rows, 2 * D, D, EPI_STORE, e, st));
@@ -526,7 +557,30 @@ t2i_status text_prep(t2i_dit* h, const Plan& P, const void* prompt, int nb, hipS
     HIP_TRY(h, launch_broadcast_rows(h->w[B_Y], h->bf(), M, D,
                                      ytxt + (size_t)P.n_req * M * D * h->act(), st));
   if (c.arch != T2I_ARCH_CROSS_DIT) return T2I_OK;
-  for (int b = 0; b < std::min(nb, P.defer_from); ++b) HIP_TRY(h, block_text_kv(h, P, b, st));
+  const int nkv = std::min(nb, P.defer_from);
+  if (!h->bf() || !gemm_bf16_groupable(P.txt_rows, 2 * D, EPI_SPLIT_VT)) {
+    for (int b = 0; b < nkv; ++b) HIP_TRY(h, block_text_kv(h, P, b, st));
+    return T2I_OK;
+  }
+  // every block's K / V from one grouped launch (per 64 blocks)
+  const size_t txt_rows_max = (size_t)(c.max_requests + 1) * M;
+  Epi g_epi = make_epi();
+  g_epi.ldo = D;
+  g_epi.ldvt = h->L.ldvt_txt;
+  g_epi.vcol0 = D;
+  PtrGroup g;
+  for (int b0 = 0; b0 < nkv; b0 += kMaxGroups) {
+    const int n = std::min(kMaxGroups, nkv - b0);
+    for (int i = 0; i < n; ++i) {
+      const int b = b0 + i, wi = W_BLOCK0 + b * X_PER_BLOCK + X_XKV;
+      g.W[i] = h->w[wi];
+      g.bias[i] = h->w[wi + 1];
+      g.out[i] = h->at<char>(h->L.kv) + (size_t)b * txt_rows_max * 2 * D * h->act();
+      g.vt[i] = h->at<bf16>(h->L.vtt) + (size_t)b * D * h->L.ldvt_txt;
+    }
+    HIP_TRY(h, launch_gemm_bf16_group(h->at<bf16>(h->L.ytxt), D, g, n, D, P.txt_rows, 2 * D, D,
+                                      EPI_SPLIT_VT, g_epi, st));
+  }
   return T2I_OK;
 }
 

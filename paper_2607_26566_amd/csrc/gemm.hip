@@ -77,18 +77,12 @@ __device__ __forceinline__ void epi_store4(const Epi& e, int m, int nb, const fl
 // so a lane ends with four consecutive output columns of one row and the
 // epilogue issues one 8-byte (bf16) or 16-byte (fp32) access per lane.
 template <int BM, int BN, int WGM, int KIND>
-__global__ __launch_bounds__(256, 1) void gemm_bf16_kernel(
-    const bf16* __restrict__ A, int lda, const bf16* __restrict__ W, int ldw,
-    const bf16* __restrict__ bias, int M, int N, int K, Epi epi, int tiles_n, int vec_ok) {
-  // split-K: workgroup row blockIdx.y takes K columns [y K, (y+1) K) and
-  // writes its partial sums to slice y of the fp32 output
+__device__ __forceinline__ void gemm_bf16_body(const bf16* __restrict__ A, int lda,
+                                               const bf16* __restrict__ W, int ldw,
+                                               const bf16* __restrict__ bias, int M, int N, int K,
+                                               const Epi& epi, int tiles_n, int vec_ok, int tile) {
   constexpr bool PART = KIND == EPI_PARTIAL;
   constexpr int EK = PART ? EPI_STORE_F32 : KIND;
-  if (PART) {
-    A += (size_t)blockIdx.y * K;
-    W += (size_t)blockIdx.y * K;
-    epi.out = (float*)epi.out + (size_t)blockIdx.y * M * epi.ldo;
-  }
   constexpr int BK = 64;
   constexpr int LDK = BK + 8;
   constexpr int WGN = 4 / WGM;
@@ -103,7 +97,6 @@ __global__ __launch_bounds__(256, 1) void gemm_bf16_kernel(
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int wm = wave / WGN, wn = wave % WGN;
-  const int tile = xcd_remap(blockIdx.x, gridDim.x);
   const int m0 = (tile / tiles_n) * BM, n0 = (tile % tiles_n) * BN;
 
   const bf16* Ap[APT];
@@ -223,6 +216,36 @@ __global__ __launch_bounds__(256, 1) void gemm_bf16_kernel(
       }
     }
   }
+}
+
+template <int BM, int BN, int WGM, int KIND>
+__global__ __launch_bounds__(256, 1) void gemm_bf16_kernel(
+    const bf16* __restrict__ A, int lda, const bf16* __restrict__ W, int ldw,
+    const bf16* __restrict__ bias, int M, int N, int K, Epi epi, int tiles_n, int vec_ok) {
+  // split-K: workgroup row blockIdx.y takes K columns [y K, (y+1) K) and
+  // writes its partial sums to slice y of the fp32 output
+  if (KIND == EPI_PARTIAL) {
+    A += (size_t)blockIdx.y * K;
+    W += (size_t)blockIdx.y * K;
+    epi.out = (float*)epi.out + (size_t)blockIdx.y * M * epi.ldo;
+  }
+  gemm_bf16_body<BM, BN, WGM, KIND>(A, lda, W, ldw, bias, M, N, K, epi, tiles_n, vec_ok,
+                                    xcd_remap(blockIdx.x, gridDim.x));
+}
+
+// One launch for several GEMMs that share A and the shape: group blockIdx.y
+// takes its weight, bias and output pointers from the table.  Each tile is
+// computed exactly as by gemm_bf16_kernel.
+template <int BM, int BN, int WGM, int KIND>
+__global__ __launch_bounds__(256, 1) void gemm_bf16_group_kernel(
+    const bf16* __restrict__ A, int lda, PtrGroup g, int ldw, int M, int N, int K, Epi epi,
+    int tiles_n, int vec_ok) {
+  const int grp = blockIdx.y;
+  epi.out = g.out[grp];
+  epi.vt = g.vt[grp];
+  gemm_bf16_body<BM, BN, WGM, KIND>(A, lda, (const bf16*)g.W[grp], ldw, (const bf16*)g.bias[grp],
+                                    M, N, K, epi, tiles_n, vec_ok,
+                                    xcd_remap(blockIdx.x, gridDim.x));
 }
 
 template <int BM, int BN, int WGM>
@@ -351,6 +374,36 @@ hipError_t launch_gemm_bf16(const bf16* A, int lda, const bf16* W, int ldw, cons
   return gemm_bf16_dispatch<128, 128, 2>(A, lda, W, ldw, bias, M, N, K, kind, epi, vec_ok, st);
 }
 
+bool gemm_bf16_groupable(int M, int N, int kind) {
+  // the shapes launch_gemm_bf16 runs on register-staged tiles without split-K
+  return M > 0 && N > 0 && !(M >= 2048 && (N % 144 == 0 || N % 128 == 0) && kind != EPI_SILU) &&
+         (kind == EPI_STORE || kind == EPI_SPLIT_VT);
+}
+
+hipError_t launch_gemm_bf16_group(const bf16* A, int lda, const PtrGroup& g, int groups, int ldw,
+                                  int M, int N, int K, int kind, const Epi& epi, hipStream_t st) {
+  if (groups <= 0) return hipSuccess;
+  if (groups > kMaxGroups || !gemm_bf16_groupable(M, N, kind)) return hipErrorInvalidValue;
+  auto al = [](const void* p, int a) { return ((uintptr_t)p % a) == 0; };
+  int vec_ok = (epi.ldo % 4 == 0) && (epi.ldx % 4 == 0) && (epi.ld_gate % 4 == 0);
+  for (int i = 0; i < groups; ++i)
+    vec_ok = vec_ok && al(g.bias[i], 8) && al(g.out[i], 8);
+  dim3 block(256);
+#define T2I_GRP(BM_, BN_, WGM_, K_)                                                          \
+  {                                                                                          \
+    const int tn = (N + BN_ - 1) / BN_, tm = (M + BM_ - 1) / BM_;                            \
+    hipLaunchKernelGGL((gemm_bf16_group_kernel<BM_, BN_, WGM_, K_>), dim3(tm * tn, groups),  \
+                       block, 0, st, A, lda, g, ldw, M, N, K, epi, tn, vec_ok);              \
+  }
+  if (N % 144 == 0) {
+    if (kind == EPI_STORE) T2I_GRP(128, 144, 4, EPI_STORE) else T2I_GRP(128, 144, 4, EPI_SPLIT_VT)
+  } else {
+    if (kind == EPI_STORE) T2I_GRP(128, 128, 2, EPI_STORE) else T2I_GRP(128, 128, 2, EPI_SPLIT_VT)
+  }
+#undef T2I_GRP
+  return hipGetLastError();
+}
+
 // ---------------------------------------------------------------------------
 
 template <typename TW, int KIND>
@@ -411,10 +464,10 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(
 // Weight reads are contiguous 1 KB per wave instruction.
 
 template <typename TW, int MT, int KIND>
-__global__ __launch_bounds__(256) void linear_rows_kernel(const float* __restrict__ A, int lda,
-                                                          const TW* __restrict__ W, int ldw,
-                                                          const TW* __restrict__ bias, int M,
-                                                          int N, int K, Epi epi) {
+__device__ __forceinline__ void linear_rows_body(const float* __restrict__ A, int lda,
+                                                 const TW* __restrict__ W, int ldw,
+                                                 const TW* __restrict__ bias, int M, int N, int K,
+                                                 const Epi& epi) {
   constexpr int NC = 4;
   const int lane = threadIdx.x & 63;
   const int n0 = (blockIdx.y * 4 + (threadIdx.x >> 6)) * NC;
@@ -466,6 +519,26 @@ __global__ __launch_bounds__(256) void linear_rows_kernel(const float* __restric
   }
 }
 
+template <typename TW, int MT, int KIND>
+__global__ __launch_bounds__(256) void linear_rows_kernel(const float* __restrict__ A, int lda,
+                                                          const TW* __restrict__ W, int ldw,
+                                                          const TW* __restrict__ bias, int M,
+                                                          int N, int K, Epi epi) {
+  linear_rows_body<TW, MT, KIND>(A, lda, W, ldw, bias, M, N, K, epi);
+}
+
+// Several weight matrices against the same rows in one launch: group
+// blockIdx.z takes its weight, bias and output from the table.
+template <typename TW, int MT, int KIND>
+__global__ __launch_bounds__(256) void linear_rows_group_kernel(const float* __restrict__ A,
+                                                                int lda, PtrGroup g, int ldw,
+                                                                int M, int N, int K, Epi epi) {
+  const int grp = blockIdx.z;
+  epi.out = g.out[grp];
+  linear_rows_body<TW, MT, KIND>(A, lda, (const TW*)g.W[grp], ldw, (const TW*)g.bias[grp], M, N,
+                                 K, epi);
+}
+
 template <typename TW, int MT>
 static hipError_t linear_rows_dispatch(const float* A, int lda, const TW* W, int ldw,
                                        const TW* bias, int M, int N, int K, int kind,
@@ -482,6 +555,24 @@ static hipError_t linear_rows_dispatch(const float* A, int lda, const TW* W, int
     default:
       return hipErrorInvalidValue;
   }
+  return hipGetLastError();
+}
+
+hipError_t launch_linear_rows_group(const float* A, int lda, const PtrGroup& g, int groups,
+                                    int ldw, bool w_bf16, int M, int N, int K, const Epi& epi,
+                                    hipStream_t st) {
+  if (groups <= 0 || M <= 0 || N <= 0) return hipSuccess;
+  if (groups > kMaxGroups || K % 8 || lda % 4 || ldw % 8 || ((uintptr_t)A & 15))
+    return hipErrorInvalidValue;
+  for (int i = 0; i < groups; ++i)
+    if ((uintptr_t)g.W[i] & 15) return hipErrorInvalidValue;
+  dim3 grid((M + 7) / 8, (N + 15) / 16, groups), block(256);
+  if (w_bf16)
+    hipLaunchKernelGGL((linear_rows_group_kernel<bf16, 8, EPI_STORE>), grid, block, 0, st, A, lda,
+                       g, ldw, M, N, K, epi);
+  else
+    hipLaunchKernelGGL((linear_rows_group_kernel<float, 8, EPI_STORE>), grid, block, 0, st, A, lda,
+                       g, ldw, M, N, K, epi);
   return hipGetLastError();
 }
 

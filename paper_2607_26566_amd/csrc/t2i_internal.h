@@ -170,6 +170,27 @@ hipError_t launch_gemm_f32(const float* A, int lda, const void* W, int ldw, bool
                            hipStream_t st);
 
 // Conditioning GEMMs: A fp32 [M, K], W fp32 or bf16 [N, K]; STORE or SILU.
+// Per-group operand table of a grouped launch (by value in the kernel
+// arguments): group i uses W[i], bias[i] and writes out[i] (vt[i]).
+constexpr int kMaxGroups = 64;
+struct PtrGroup {
+  const void* W[kMaxGroups];
+  const void* bias[kMaxGroups];
+  void* out[kMaxGroups];
+  bf16* vt[kMaxGroups];
+};
+
+// Grouped bf16 GEMM over shapes that launch_gemm_bf16 runs on its
+// register-staged tiles without split-K (gemm_bf16_groupable); STORE or
+// SPLIT_VT epilogue; bitwise the per-group launch_gemm_bf16 results.
+bool gemm_bf16_groupable(int M, int N, int kind);
+hipError_t launch_gemm_bf16_group(const bf16* A, int lda, const PtrGroup& g, int groups, int ldw,
+                                  int M, int N, int K, int kind, const Epi& epi, hipStream_t st);
+// Grouped conditioning GEMV (EPI_STORE), bitwise the per-group
+// launch_linear_rows results.
+hipError_t launch_linear_rows_group(const float* A, int lda, const PtrGroup& g, int groups,
+                                    int ldw, bool w_bf16, int M, int N, int K, const Epi& epi,
+                                    hipStream_t st);
 hipError_t launch_linear_rows(const float* A, int lda, const void* W, int ldw, bool w_bf16,
                               const void* bias, int M, int N, int K, int kind, const Epi& epi,
                               hipStream_t st);
