@@ -1,24 +1,27 @@
 // Multi-head attention over packed variable-length sequences (self-attention,
 // cross-attention to text, joint attention) on gfx950.
 //
-// attn_bf16_kernel: flash-style, one workgroup = 4 waves = 128 queries of one
-// head of one sequence; each wave owns 32 queries (two 16-query MFMA tiles).
-// Keys/values stream through LDS 64 at a time.  Everything is arranged so that
-// a lane always holds data of ONE query:
-//   * scores are computed transposed, S^T = K Q^T, with v_mfma_f32_16x16x32_bf16
-//     (A = K fragment, B = Q fragment kept in registers for the whole loop):
-//     the C fragment gives lane l the scores of query (l & 15) against keys
-//     4*(l >> 4) + 0..3 of each 16-key tile;
+// attn_bf16_kernel: flash-style, one workgroup = 8 waves = 256 queries of one
+// head of one sequence; each wave owns 32 queries.  Keys and values stream
+// through a 4-stage LDS ring, 64 keys per tile, filled by direct HBM->LDS
+// loads three tiles ahead.  Everything is arranged so that a lane always holds
+// data of ONE query:
+//   * scores are computed transposed, S^T = K Q^T, with
+//     v_mfma_f32_32x32x16_bf16 (A = K fragment from LDS, B = the query's Q
+//     fragment, kept in registers for the whole loop): lane l gets query
+//     (l & 31) against 16 keys of each 32-key block;
 //   * the output is accumulated transposed, O^T = V^T P^T: the B operand is
-//     exactly the lane's own probabilities (8 keys of two adjacent 16-key
-//     tiles), the A operand is read from a V^T tile in LDS, and the C fragment
-//     again gives lane l query (l & 15) -- so the online-softmax rescale of the
-//     output needs no data exchange between lanes.
-// The row max needs two cross-lane steps per tile (the 4 lanes of a query);
-// the row sums ride on a ones row of V^T where the head dimension has padding
-// (else they are kept per lane and combined once at the end).  The head
-// dimension is padded with zeros to a multiple of 32 for Q K^T and to a
-// multiple of 16 for P V (72 -> 96 / 80); the padding never reaches memory.
+//     exactly the lane's own probabilities, the A operand a V^T fragment from
+//     LDS, and the C fragment again belongs to query (l & 31) -- so the
+//     online-softmax rescale of the output needs no data exchange between
+//     lanes;
+//   * the softmax shift rides in a spare slot of the Q K^T contraction (Q
+//     carries -m, K a 1), so scores leave the MFMA as s - m; the maximum is
+//     updated lazily (only when a score exceeds it by 2^8);
+//   * row sums come from a ones row of V^T where the head dimension has
+//     padding (72 -> 96), else from a per-lane sum combined once at the end;
+//   * the next tile's scores are issued before this tile's exponentials, so
+//     the two overlap.
 //
 // attn_f32_kernel: plain fp32 online softmax, one thread per query, for the
 // fp32 model.
@@ -74,7 +77,7 @@ __device__ __forceinline__ void decode_tile(const AttnMap& m, int heads, int L, 
 
 // ROLE: 0 = self / joint attention, 1 = cross-attention to text (separate
 // instances, so that profiles tell them apart)
-template <int HD, int NW, int ST, int ROLE, int PF = 0>
+template <int HD, int NW, int ST, int ROLE>
 __global__ __launch_bounds__(NW * 64, 8 / NW) void attn_bf16_kernel(AttnMap map, int heads,
                                                            const bf16* __restrict__ Q, int ldq,
                                                            const bf16* __restrict__ K, int ldk,
@@ -209,41 +212,17 @@ __global__ __launch_bounds__(NW * 64, 8 / NW) void attn_bf16_kernel(AttnMap map,
     const int slot = KRS ? cc ^ ((r / KRS) & (CPR - 1)) : cc;
     return *(const bf16x8*)(kst(st) + r * PK + slot * 16);
   };
-  // branch-free fragment read: every lane reads a valid chunk, lanes past the
-  // head dimension then take the shift-slot ones or zeros
-  auto kfrag_nb = [&](int st, int kb, int c) {
-    const int r = 32 * kb + ql, cc = 2 * c + hl;
-    const int ccl = cc < CPR ? cc : CPR - 1;
-    const int slot = KRS ? ccl ^ ((r / KRS) & (CPR - 1)) : ccl;
-    const bf16x8 v = *(const bf16x8*)(kst(st) + r * PK + slot * 16);
-    return cc < CPR ? v : (cc == CPR ? kone : bf16x8{});
-  };
   auto qk = [&](int ti, f32x16 (&sc)[2]) {
     const int st = ti % ST;
-    if constexpr (PF == 0) {
 #pragma unroll
-      for (int c = 0; c < DC; ++c) {
-        bf16x8 kf[2];
+    for (int c = 0; c < DC; ++c) {
+      bf16x8 kf[2];
 #pragma unroll
-        for (int kb = 0; kb < 2; ++kb) kf[kb] = kfrag(st, kb, c);
+      for (int kb = 0; kb < 2; ++kb) kf[kb] = kfrag(st, kb, c);
 #pragma unroll
-        for (int kb = 0; kb < 2; ++kb)
-          sc[kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf[kb], qf[c],
-                                                           c == 0 ? f32x16{} : sc[kb], 0, 0, 0);
-      }
-    } else {
-      // all K fragments of the tile first, then the MFMAs
-      bf16x8 kf[DC][2];
-#pragma unroll
-      for (int c = 0; c < DC; ++c)
-#pragma unroll
-        for (int kb = 0; kb < 2; ++kb) kf[c][kb] = kfrag_nb(st, kb, c);
-#pragma unroll
-      for (int c = 0; c < DC; ++c)
-#pragma unroll
-        for (int kb = 0; kb < 2; ++kb)
-          sc[kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf[c][kb], qf[c],
-                                                           c == 0 ? f32x16{} : sc[kb], 0, 0, 0);
+      for (int kb = 0; kb < 2; ++kb)
+        sc[kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf[kb], qf[c],
+                                                         c == 0 ? f32x16{} : sc[kb], 0, 0, 0);
     }
   };
   auto lane_max = [&](const f32x16 (&sc)[2]) {
@@ -332,32 +311,15 @@ __global__ __launch_bounds__(NW * 64, 8 / NW) void attn_bf16_kernel(AttnMap map,
     // key chunk outer, d tile inner: DT independent accumulation chains; V^T
     // row 32dt + ql, keys 16q + 8hl .. +7
     const char* vb = vst(ti % ST);
-    if constexpr (PF < 2) {
 #pragma unroll
-      for (int q = 0; q < 4; ++q) {
+    for (int q = 0; q < 4; ++q) {
 #pragma unroll
-        for (int dt = 0; dt < DT; ++dt) {
-          const int row = dt * 32 + ql;
-          const bf16x8 vf =
-              *(const bf16x8*)(vb + row * 128 + (((2 * q + hl) ^ ((row >> 1) & 7)) << 4));
-          o[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf, pf[q], o[dt], 0, 0, 0);
-        }
+      for (int dt = 0; dt < DT; ++dt) {
+        const int row = dt * 32 + ql;
+        const bf16x8 vf =
+            *(const bf16x8*)(vb + row * 128 + (((2 * q + hl) ^ ((row >> 1) & 7)) << 4));
+        o[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf, pf[q], o[dt], 0, 0, 0);
       }
-    } else {
-      // V^T fragments of two key chunks ahead of their MFMAs
-      bf16x8 vf[4][DT];
-#pragma unroll
-      for (int q = 0; q < 4; ++q)
-#pragma unroll
-        for (int dt = 0; dt < DT; ++dt) {
-          const int row = dt * 32 + ql;
-          vf[q][dt] = *(const bf16x8*)(vb + row * 128 + (((2 * q + hl) ^ ((row >> 1) & 7)) << 4));
-        }
-#pragma unroll
-      for (int q = 0; q < 4; ++q)
-#pragma unroll
-        for (int dt = 0; dt < DT; ++dt)
-          o[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf[q][dt], pf[q], o[dt], 0, 0, 0);
     }
     lm_nxt = lane_max(nxt);
   };
@@ -400,295 +362,6 @@ __global__ __launch_bounds__(NW * 64, 8 / NW) void attn_bf16_kernel(AttnMap map,
         *(bf16x4*)(O + (size_t)qr * ldo + hh * HD + d) = w;
       }
     }
-}
-
-// O^T += V^T P^T with the accumulator held in AGPRs (the score and probability
-// tiles then keep the VGPRs to themselves)
-__device__ __forceinline__ void mfma32_acc_agpr(f32x16& acc, const bf16x8& a, const bf16x8& b) {
-  asm volatile("v_mfma_f32_32x32x16_bf16 %0, %1, %2, %0" : "+a"(acc) : "v"(a), "v"(b));
-}
-
-// ---------------------------------------------------------------------------
-// Two query tiles per wave: 4 waves (one per SIMD) x 64 queries.  Same tile
-// ring, layouts and arithmetic as attn_bf16_kernel, but every K / V^T
-// fragment read from LDS feeds the MFMAs of both 32-query tiles (half the LDS
-// traffic per FLOP), and within one wave the exponentials of one tile are
-// independent of the other tile's MFMAs, so the two overlap.  Each query's
-// arithmetic (operands, summation order, roundings) is exactly that of
-// attn_bf16_kernel, so the two kernels give bitwise-identical outputs.
-template <int HD, int ST, int ROLE, bool AO = false>
-__global__ __launch_bounds__(256, 1) void attn_q64_kernel(AttnMap map, int heads,
-                                                         const bf16* __restrict__ Q, int ldq,
-                                                         const bf16* __restrict__ K, int ldk,
-                                                         const bf16* __restrict__ Vt, int ldvt,
-                                                         bf16* __restrict__ O, int ldo,
-                                                         float scale_log2) {
-  constexpr int NW = 4, NQ = 2, BKV = 64;
-  constexpr int DC = (HD + 1 + 15) / 16;
-  constexpr int DT = (HD + 31) / 32;
-  constexpr int HDO = DT * 32;
-  constexpr bool ONES = HD < HDO;
-  constexpr int CPR = HD / 8;
-  constexpr int PK = 2 * HD;
-  constexpr int KRS = (CPR == 4 || CPR == 8 || CPR == 16) ? 16 / CPR : 0;
-  constexpr int KSTAGE = BKV * PK;
-  constexpr int VSTAGE = HDO * 128;
-  constexpr int NI = 2 * CPR;
-  static_assert(HD % 8 == 0 && KSTAGE % 1024 == 0, "head dim");
-  __shared__ __attribute__((aligned(1024))) char smem[ST * (KSTAGE + VSTAGE)];
-
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  int hh, s, j;
-  decode_tile(map, heads, xcd_remap_attn(blockIdx.x, gridDim.x), hh, s, j);
-  const int q_beg = map.q_start[s], q_end = q_beg + map.q_len[s];
-  const int k1 = map.k_start[s], n1 = map.k_len[s];
-  const int k2 = map.k2_start[s], n2 = map.k2_len[s];
-  const int t1 = (n1 + BKV - 1) / BKV, nt = t1 + (n2 + BKV - 1) / BKV;
-  auto tile_keys = [&](int ti, int& kv0, int& kend) {
-    if (ti < t1) {
-      kv0 = k1 + ti * BKV;
-      kend = k1 + n1;
-    } else {
-      kv0 = k2 + (ti - t1) * BKV;
-      kend = k2 + n2;
-    }
-  };
-  const int ql = lane & 31, hl = lane >> 5;
-  // query tile t of this wave: queries wave*64 + 32t + ql of the workgroup
-  int qr[NQ];
-#pragma unroll
-  for (int t = 0; t < NQ; ++t) qr[t] = q_beg + j * (NW * 64) + wave * 64 + t * 32 + ql;
-  auto kst = [&](int st) { return smem + st * (KSTAGE + VSTAGE); };
-  auto vst = [&](int st) { return smem + st * (KSTAGE + VSTAGE) + KSTAGE; };
-
-  constexpr int BC = HD / 16, BH = (HD % 16) / 8;
-  bf16x8 qf[NQ][DC];
-#pragma unroll
-  for (int t = 0; t < NQ; ++t)
-#pragma unroll
-    for (int c = 0; c < DC; ++c) {
-      const int d = c * 16 + hl * 8;
-      qf[t][c] = bf16x8{};
-      if (qr[t] < q_end && d < HD) {
-        const bf16x8 raw = *(const bf16x8*)(Q + (size_t)qr[t] * ldq + hh * HD + d);
-#pragma unroll
-        for (int e = 0; e < 8; ++e) qf[t][c][e] = (bf16)((float)raw[e] * scale_log2);
-      }
-    }
-  for (int i = tid; i < ST * (HDO - HD) * 64; i += NW * 64) {
-    const int st = i / ((HDO - HD) * 64), rem = i - st * (HDO - HD) * 64;
-    const int row = HD + rem / 64, col = rem & 63;
-    ((bf16*)(vst(st) + row * 128))[col] = (bf16)(row == HD ? 1.f : 0.f);
-  }
-
-  constexpr int IPW = (NI + NW - 1) / NW;
-  int g_off[IPW], g_key[IPW], l_off[IPW];
-  const int n_w = (NI - wave + NW - 1) / NW;
-#pragma unroll
-  for (int ii = 0; ii < IPW; ++ii) {
-    const int i = wave + NW * ii;
-    g_off[ii] = g_key[ii] = l_off[ii] = 0;
-    if (i < CPR) {
-      const int o = i * 1024 + lane * 16;
-      const int r = o / PK, slot = (o - r * PK) / 16;
-      const int c = KRS ? slot ^ ((r / KRS) & (CPR - 1)) : slot;
-      g_key[ii] = swap23(r);
-      g_off[ii] = hh * HD + c * 8;
-      l_off[ii] = i * 1024;
-    } else if (i < NI) {
-      const int o = (i - CPR) * 1024 + lane * 16;
-      const int d = o / 128, c = (lane & 7) ^ ((d >> 1) & 7);
-      g_key[ii] = c * 8;
-      g_off[ii] = hh * HD + d;
-      l_off[ii] = KSTAGE + (i - CPR) * 1024;
-    }
-  }
-  auto issue = [&](int ti) {
-    int kv0, k_end;
-    tile_keys(ti, kv0, k_end);
-    char* base = kst(ti % ST);
-#pragma unroll
-    for (int ii = 0; ii < IPW; ++ii) {
-      const int i = wave + NW * ii;
-      if (i >= NI) break;
-      const bf16* src;
-      if (i < CPR) {
-        src = K + (size_t)min(kv0 + g_key[ii], k_end - 1) * ldk + g_off[ii];
-      } else {
-        const int gk = kv0 + g_key[ii];
-        src = Vt + (size_t)g_off[ii] * ldvt + (gk < k_end ? gk : kv0);
-      }
-      __builtin_amdgcn_global_load_lds((__attribute__((address_space(1))) void*)src,
-                                       (__attribute__((address_space(3))) void*)(base + l_off[ii]),
-                                       16, 0, 0);
-    }
-  };
-  bf16x8 kone = bf16x8{};
-  kone[0] = (bf16)1.f;
-  auto kfrag = [&](int st, int kb, int c) {
-    const int r = 32 * kb + ql, cc = 2 * c + hl;
-    if (cc == CPR) return kone;
-    if (cc > CPR) return bf16x8{};
-    const int slot = KRS ? cc ^ ((r / KRS) & (CPR - 1)) : cc;
-    return *(const bf16x8*)(kst(st) + r * PK + slot * 16);
-  };
-  // S^T of both query tiles for tile ti: each K fragment feeds two MFMAs
-  auto qk2 = [&](int ti, f32x16 (&sc)[NQ][2]) {
-    const int st = ti % ST;
-#pragma unroll
-    for (int c = 0; c < DC; ++c) {
-      bf16x8 kf[2];
-#pragma unroll
-      for (int kb = 0; kb < 2; ++kb) kf[kb] = kfrag(st, kb, c);
-#pragma unroll
-      for (int t = 0; t < NQ; ++t)
-#pragma unroll
-        for (int kb = 0; kb < 2; ++kb)
-          sc[t][kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
-              kf[kb], qf[t][c], c == 0 ? f32x16{} : sc[t][kb], 0, 0, 0);
-    }
-  };
-  auto lane_max = [&](const f32x16 (&sc)[2]) {
-    float m0 = fmaxf(sc[0][0], sc[0][1]), m1 = fmaxf(sc[1][0], sc[1][1]);
-#pragma unroll
-    for (int e = 2; e < 16; e += 2) {
-      m0 = fmaxf(fmaxf(m0, sc[0][e]), sc[0][e + 1]);
-      m1 = fmaxf(fmaxf(m1, sc[1][e]), sc[1][e + 1]);
-    }
-    return fmaxf(m0, m1);
-  };
-
-  f32x16 o[NQ][DT];
-#pragma unroll
-  for (int t = 0; t < NQ; ++t)
-#pragma unroll
-    for (int dt = 0; dt < DT; ++dt) o[t][dt] = f32x16{};
-  float m_ref[NQ] = {0.f, 0.f}, l_run[NQ] = {0.f, 0.f};
-
-  auto step = [&](int ti, f32x16 (&cur)[NQ][2], float (&lm)[NQ], f32x16 (&nxt)[NQ][2],
-                  float (&lm_nxt)[NQ]) {
-    int kv0, k_end;
-    tile_keys(ti, kv0, k_end);
-    wait_vmcnt_dyn(ti + 2 < nt ? n_w : 0);
-    attn_barrier();
-    if (ti + ST - 1 < nt) issue(ti + ST - 1);
-    if (kv0 + BKV > k_end) {
-      if (k_end & 7) {
-        const int c0 = k_end - kv0;
-        char* vb = vst(ti % ST);
-        for (int i = tid; i < HD * 64; i += NW * 64) {
-          const int d = i >> 6, col = i & 63;
-          if (col >= c0)
-            *(bf16*)(vb + d * 128 + (((col >> 3) ^ ((d >> 1) & 7)) << 4) + (col & 7) * 2) =
-                (bf16)0.f;
-        }
-        attn_barrier();
-      }
-#pragma unroll
-      for (int t = 0; t < NQ; ++t) {
-#pragma unroll
-        for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-          for (int e = 0; e < 16; ++e)
-            if (kv0 + swap23(32 * kb + 8 * (e >> 2) + 4 * hl + (e & 3)) >= k_end)
-              cur[t][kb][e] = -INFINITY;
-        lm[t] = lane_max(cur[t]);
-      }
-    }
-#pragma unroll
-    for (int t = 0; t < NQ; ++t) {
-      if (ti == 0 || __any(lm[t] > 8.0f)) {
-        const float mx = fmaxf(lm[t], __shfl_xor(lm[t], 32, 64)) + m_ref[t];
-        const float m_old = ti == 0 ? -INFINITY : m_ref[t];
-        const float m_new = (float)(bf16)fmaxf(m_old, mx);
-        const float alpha = __builtin_amdgcn_exp2f(m_old - m_new);
-#pragma unroll
-        for (int kb = 0; kb < 2; ++kb) cur[t][kb] -= (m_new - m_ref[t]);
-#pragma unroll
-        for (int dt = 0; dt < DT; ++dt) o[t][dt] *= alpha;
-        l_run[t] *= alpha;
-        m_ref[t] = m_new;
-        if (hl == BH) qf[t][BC][0] = (bf16)(-m_new);
-      }
-    }
-    // the next tile's scores of both query tiles (independent MFMAs) overlap
-    // this tile's exponentials
-    qk2(ti + 1, nxt);
-    bf16x8 pf[NQ][4];
-#pragma unroll
-    for (int t = 0; t < NQ; ++t) {
-      float psum = 0.f;
-#pragma unroll
-      for (int q = 0; q < 4; ++q)
-#pragma unroll
-        for (int e = 0; e < 8; ++e) {
-          const float p = __builtin_amdgcn_exp2f(cur[t][q >> 1][8 * (q & 1) + e]);
-          if (!ONES) psum += p;
-          pf[t][q][e] = (bf16)p;
-        }
-      if (!ONES) l_run[t] += psum;
-    }
-    const char* vb = vst(ti % ST);
-#pragma unroll
-    for (int q = 0; q < 4; ++q) {
-#pragma unroll
-      for (int dt = 0; dt < DT; ++dt) {
-        const int row = dt * 32 + ql;
-        const bf16x8 vf =
-            *(const bf16x8*)(vb + row * 128 + (((2 * q + hl) ^ ((row >> 1) & 7)) << 4));
-#pragma unroll
-        for (int t = 0; t < NQ; ++t) {
-          if constexpr (AO)
-            mfma32_acc_agpr(o[t][dt], vf, pf[t][q]);
-          else
-            o[t][dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf, pf[t][q], o[t][dt], 0, 0, 0);
-        }
-      }
-    }
-#pragma unroll
-    for (int t = 0; t < NQ; ++t) lm_nxt[t] = lane_max(nxt[t]);
-  };
-
-#pragma unroll
-  for (int ti = 0; ti < ST - 1; ++ti)
-    if (ti < nt) issue(ti);
-  wait_vmcnt_dyn(n_w * (min(nt, ST - 1) - 1));
-  attn_barrier();
-  f32x16 sa[NQ][2], sb[NQ][2];
-  float la[NQ], lb[NQ];
-  qk2(0, sa);
-#pragma unroll
-  for (int t = 0; t < NQ; ++t) la[t] = lane_max(sa[t]);
-  for (int ti = 0; ti < nt; ti += 2) {
-    step(ti, sa, la, sb, lb);
-    if (ti + 1 < nt) step(ti + 1, sb, lb, sa, la);
-  }
-
-#pragma unroll
-  for (int t = 0; t < NQ; ++t) {
-    float l;
-    if (ONES) {
-      constexpr int R = HD % 32;
-      l = __shfl(o[t][HD / 32][4 * (R / 8) + (R % 4)], ((R % 8) / 4) * 32 + ql, 64);
-    } else {
-      l = l_run[t] + __shfl_xor(l_run[t], 32, 64);
-    }
-    if (qr[t] < q_end) {
-      const float inv = 1.0f / l;
-#pragma unroll
-      for (int dt = 0; dt < DT; ++dt)
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          const int d = dt * 32 + i * 8 + hl * 4;
-          if (d < HD) {
-            bf16x4 w;
-#pragma unroll
-            for (int jj = 0; jj < 4; ++jj) w[jj] = (bf16)(o[t][dt][4 * i + jj] * inv);
-            *(bf16x4*)(O + (size_t)qr[t] * ldo + hh * HD + d) = w;
-          }
-        }
-    }
-  }
 }
 
 // ---------------------------------------------------------------------------
