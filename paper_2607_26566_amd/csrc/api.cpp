@@ -309,10 +309,11 @@ t2i_status build_plan(t2i_dit* h, int n_req, const int32_t* lat_h, const int32_t
   if (P.rows > c.max_tokens) return fail(h, T2I_ERR_SHAPE, "image tokens exceed max_tokens");
   const int M = c.text_tokens;
   P.txt_rows = n_req * M + (P.branches == 2 ? M : 0);
-  const int BQ = attention_query_tile(h->bf(), c.head_dim);
+  const int BQ = attention_query_tile(h->bf(), c.head_dim, 0);
+  const int BQX = attention_query_tile(h->bf(), c.head_dim, 1);
   P.img.n = n_req * P.branches;
   P.self.n = P.cross.n = P.img.n;
-  int tiles = 0;
+  int tiles = 0, xtiles = 0;
   for (int br = 0; br < P.branches; ++br)
     for (int r = 0; r < n_req; ++r) {
       const int s = br * n_req + r;
@@ -326,11 +327,14 @@ t2i_status build_plan(t2i_dit* h, int n_req, const int32_t* lat_h, const int32_t
       P.self.k_len[s] = len;
       P.cross.k_start[s] = br == 0 ? r * M : n_req * M;
       P.cross.k_len[s] = M;
-      P.self.tile_start[s] = P.cross.tile_start[s] = tiles;
+      P.self.tile_start[s] = tiles;
+      P.cross.tile_start[s] = xtiles;
       tiles += (len + BQ - 1) / BQ;
+      xtiles += (len + BQX - 1) / BQX;
     }
   P.img.start[P.img.n] = P.rows;
-  P.self.tile_start[P.self.n] = P.cross.tile_start[P.cross.n] = tiles;
+  P.self.tile_start[P.self.n] = tiles;
+  P.cross.tile_start[P.cross.n] = xtiles;
   if (c.arch == T2I_ARCH_MMDIT) {
     // residual rows are stream-major: text rows [0, txt_rows) with sequence s
     // at s*M, then the image rows (offset txt_rows) in the cross-DiT order

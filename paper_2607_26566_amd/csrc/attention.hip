@@ -62,13 +62,24 @@ __device__ __forceinline__ void attn_barrier() {
   asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
 }
 
-// Flattened tile -> (head, sequence, query tile).  Tiles of one head and one
-// sequence are consecutive so that they land on one XCD and share K/V in L2.
+// Flattened tile -> (head, sequence, query tile).  HEAD_MINOR = false: tiles
+// of one head and one sequence are consecutive so that they land on one XCD
+// and share K/V in L2.  HEAD_MINOR = true (cross-attention, whose K/V for all
+// heads fit in L2): the heads of one query tile are consecutive, so the
+// 128-byte lines of its Q and O rows, shared by neighbouring heads, are read
+// and written once.
+template <bool HEAD_MINOR = false>
 __device__ __forceinline__ void decode_tile(const AttnMap& m, int heads, int L, int& h, int& s,
                                             int& j) {
   const int total = m.tile_start[m.n];
-  h = L / total;
-  const int t = L - h * total;
+  int t;
+  if (HEAD_MINOR) {
+    t = L / heads;
+    h = L - t * heads;
+  } else {
+    h = L / total;
+    t = L - h * total;
+  }
   s = 0;
 #pragma unroll 1
   for (int i = 1; i < m.n; ++i) s += (t >= m.tile_start[i]) ? 1 : 0;
@@ -103,11 +114,14 @@ __global__ __launch_bounds__(NW * 64, 8 / NW) void attn_bf16_kernel(AttnMap map,
   constexpr int VSTAGE = HDO * 128;    // V^T rows of 64 keys
   constexpr int NI = 2 * CPR;          // 1-KB load instructions per tile (K, then V^T)
   static_assert(HD % 8 == 0 && KSTAGE % 1024 == 0, "head dim");
+  // the next tile's scores are computed one step ahead, so the ring needs a
+  // stage for it besides the current tile's and the one being refilled
+  static_assert(ST >= 3, "stages");
   __shared__ __attribute__((aligned(1024))) char smem[ST * (KSTAGE + VSTAGE)];
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   int hh, s, j;
-  decode_tile(map, heads, xcd_remap_attn(blockIdx.x, gridDim.x), hh, s, j);
+  decode_tile<ROLE == 1>(map, heads, xcd_remap_attn(blockIdx.x, gridDim.x), hh, s, j);
   const int q_beg = map.q_start[s], q_end = q_beg + map.q_len[s];
   // key tiles: those of segment 1, then those of segment 2
   const int k1 = map.k_start[s], n1 = map.k_len[s];
@@ -249,8 +263,10 @@ __global__ __launch_bounds__(NW * 64, 8 / NW) void attn_bf16_kernel(AttnMap map,
   auto step = [&](int ti, f32x16 (&cur)[2], float& lm, f32x16 (&nxt)[2], float& lm_nxt) {
     int kv0, k_end;
     tile_keys(ti, kv0, k_end);
-    // tile ti+1 landed (tile ti+2 may still be in flight), for every wave
-    wait_vmcnt_dyn(ti + 2 < nt ? n_w : 0);
+    // tile ti+1 landed (the ST-3 tiles after it may still be in flight), for
+    // every wave
+    const int young = min(ST - 3, nt - 2 - ti);
+    wait_vmcnt_dyn(young > 0 ? young * n_w : 0);
     attn_barrier();
     if (ti + ST - 1 < nt) issue(ti + ST - 1);     // into the stage of tile ti-1
     if (kv0 + BKV > k_end) {
@@ -421,11 +437,16 @@ __global__ __launch_bounds__(64) void attn_f32_kernel(AttnMap map, int heads,
   }
 }
 
-// bf16: 8 waves x 32 queries per workgroup; fp32: 64 queries
+// bf16: 8 waves x 32 queries per workgroup, 4 stages.  Cross-attention to
+// the text (two key tiles per query tile): 4 waves x 32 queries and 3 stages,
+// so that two workgroups share a CU and one's loads overlap the other's
+// compute.  fp32: 64 queries.
 constexpr int kAttnWaves = 8, kAttnStages = 4;
-int attention_query_tile(bool bf16_io, int head_dim) {
+constexpr int kCrossWaves = 4, kCrossStages = 3;
+int attention_query_tile(bool bf16_io, int head_dim, int role) {
   (void)head_dim;
-  return bf16_io ? kAttnWaves * 32 : 64;
+  if (!bf16_io) return 64;
+  return (role == 1 ? kCrossWaves : kAttnWaves) * 32;
 }
 
 template <int HD>
@@ -437,8 +458,8 @@ static hipError_t launch_hd(bool bf16_io, int role, int heads, const AttnMap& ma
   if (bf16_io) {
     const float scale_log2 = 1.4426950408889634f / sqrtf((float)HD);
     if (role == 1)
-      hipLaunchKernelGGL((attn_bf16_kernel<HD, kAttnWaves, kAttnStages, 1>), dim3(tiles),
-                         dim3(kAttnWaves * 64), 0, st, map, heads, (const bf16*)q, ldq,
+      hipLaunchKernelGGL((attn_bf16_kernel<HD, kCrossWaves, kCrossStages, 1>), dim3(tiles),
+                         dim3(kCrossWaves * 64), 0, st, map, heads, (const bf16*)q, ldq,
                          (const bf16*)k, ldk, (const bf16*)v, ldv, (bf16*)o, ldo, scale_log2);
     else
       hipLaunchKernelGGL((attn_bf16_kernel<HD, kAttnWaves, kAttnStages, 0>), dim3(tiles),

@@ -199,7 +199,7 @@ hipError_t launch_linear_rows(const float* A, int lda, const void* W, int ldw, b
 hipError_t launch_attention(bool bf16_io, int role, int heads, int head_dim, const AttnMap& map,
                             const void* q, int ldq, const void* k, int ldk, const void* v,
                             int ldv, void* o, int ldo, hipStream_t st);
-int attention_query_tile(bool bf16_io, int head_dim);
+int attention_query_tile(bool bf16_io, int head_dim, int role = 0);
 
 hipError_t launch_ln_modulate(bool bf16_out, int rows, int D, const float* x, int ldx,
                               const float* mod, int ld_mod, int shift_off, int scale_off,
