@@ -119,7 +119,10 @@ __global__ __launch_bounds__(NW * 64, 8 / NW) void attn_bf16_kernel(AttnMap map,
   static_assert(ST >= 3, "stages");
   __shared__ __attribute__((aligned(1024))) char smem[ST * (KSTAGE + VSTAGE)];
 
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  // the wave index is uniform: keep it scalar so that per-wave choices below
+  // are scalar branches
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   int hh, s, j;
   decode_tile<ROLE == 1>(map, heads, xcd_remap_attn(blockIdx.x, gridDim.x), hh, s, j);
   const int q_beg = map.q_start[s], q_end = q_beg + map.q_len[s];
@@ -175,11 +178,13 @@ __global__ __launch_bounds__(NW * 64, 8 / NW) void attn_bf16_kernel(AttnMap map,
   // Wave w issues instructions w, w+8, ...: n_w per tile.
   constexpr int IPW = (NI + NW - 1) / NW;
   int g_off[IPW], g_key[IPW], l_off[IPW];
+  size_t f_off[IPW];   // element offset from the tile's first key (full tiles)
   const int n_w = (NI - wave + NW - 1) / NW;
 #pragma unroll
   for (int ii = 0; ii < IPW; ++ii) {
     const int i = wave + NW * ii;
     g_off[ii] = g_key[ii] = l_off[ii] = 0;
+    f_off[ii] = 0;
     if (i < CPR) {
       const int o = i * 1024 + lane * 16;
       const int r = o / PK, slot = (o - r * PK) / 16;
@@ -187,18 +192,35 @@ __global__ __launch_bounds__(NW * 64, 8 / NW) void attn_bf16_kernel(AttnMap map,
       g_key[ii] = swap23(r);
       g_off[ii] = hh * HD + c * 8;
       l_off[ii] = i * 1024;                      // wave-uniform base; +16 per lane implied
+      f_off[ii] = (size_t)g_key[ii] * ldk + g_off[ii];
     } else if (i < NI) {
       const int o = (i - CPR) * 1024 + lane * 16;
       const int d = o / 128, c = (lane & 7) ^ ((d >> 1) & 7);
       g_key[ii] = c * 8;                         // key offset of the chunk
       g_off[ii] = hh * HD + d;                   // V^T row
       l_off[ii] = KSTAGE + (i - CPR) * 1024;
+      f_off[ii] = (size_t)g_off[ii] * ldvt + g_key[ii];
     }
   }
   auto issue = [&](int ti) {
     int kv0, k_end;
     tile_keys(ti, kv0, k_end);
     char* base = kst(ti % ST);
+    if (kv0 + BKV <= k_end) {
+      // full tile: scalar tile bases plus the precomputed lane offsets
+      const bf16* kb = K + (size_t)kv0 * ldk;
+      const bf16* vb = Vt + kv0;
+#pragma unroll
+      for (int ii = 0; ii < IPW; ++ii) {
+        const int i = wave + NW * ii;
+        if (i >= NI) break;
+        const bf16* src = (i < CPR ? kb : vb) + f_off[ii];
+        __builtin_amdgcn_global_load_lds((__attribute__((address_space(1))) void*)src,
+                                         (__attribute__((address_space(3))) void*)(base + l_off[ii]),
+                                         16, 0, 0);
+      }
+      return;
+    }
 #pragma unroll
     for (int ii = 0; ii < IPW; ++ii) {
       const int i = wave + NW * ii;
