@@ -37,31 +37,49 @@ __device__ __forceinline__ float wave_sum_dpp(float v) {
 // keep enough loads in flight (the kernel is bound by memory latency).
 constexpr int kLnRows = 4;
 
-template <typename OutT>
+// NV: float4 per row known at compile time (0 = any width up to kMaxV4 * 256),
+// so that registers are sized for the row.  The modulation rows are loaded
+// together with the row, before the reductions that they do not depend on.
+template <typename OutT, int NV>
 __global__ __launch_bounds__(256) void ln_mod_kernel(const float* __restrict__ x, int ldx, int rows,
                                                      int D, const float* __restrict__ mod,
                                                      int ld_mod, int shift_off, int scale_off,
                                                      SeqMap map, OutT* __restrict__ out, int ldo,
                                                      float eps) {
+  constexpr int NI = NV ? (NV + 63) / 64 : kMaxV4;
   const int lane = threadIdx.x & 63;
   const int row = blockIdx.x * kLnRows + (threadIdx.x >> 6);
   if (row >= rows) return;
-  const int nv = D >> 2;
+  const int nv = NV ? NV : D >> 2;
   const float4* xr = (const float4*)(x + (size_t)row * ldx);
-  float4 v[kMaxV4];
+  const float* md = mod + (size_t)map.modrow[seq_of_row(map, row)] * ld_mod;
+  const float4* sh = (const float4*)(md + shift_off);
+  const float4* sc = (const float4*)(md + scale_off);
+  // (any-width instances load the modulation rows at their use, which keeps
+  // their register count down)
+  constexpr bool PRE = NV != 0;
+  float4 v[NI], shv[PRE ? NI : 1], scv[PRE ? NI : 1];
   float s = 0.f;
 #pragma unroll
-  for (int i = 0; i < kMaxV4; ++i) {
+  for (int i = 0; i < NI; ++i) {
     const int c = lane + 64 * i;
     if (c < nv) {
       v[i] = xr[c];
-      s += (v[i].x + v[i].y) + (v[i].z + v[i].w);
+      if constexpr (PRE) {
+        shv[i] = sh[c];
+        scv[i] = sc[c];
+      }
     }
+  }
+#pragma unroll
+  for (int i = 0; i < NI; ++i) {
+    const int c = lane + 64 * i;
+    if (c < nv) s += (v[i].x + v[i].y) + (v[i].z + v[i].w);
   }
   const float mean = wave_sum_dpp(s) / (float)D;
   float q = 0.f;
 #pragma unroll
-  for (int i = 0; i < kMaxV4; ++i) {
+  for (int i = 0; i < NI; ++i) {
     const int c = lane + 64 * i;
     if (c < nv) {
       const float a = v[i].x - mean, b = v[i].y - mean, cc = v[i].z - mean, d = v[i].w - mean;
@@ -69,15 +87,12 @@ __global__ __launch_bounds__(256) void ln_mod_kernel(const float* __restrict__ x
     }
   }
   const float rstd = 1.0f / sqrtf(wave_sum_dpp(q) / (float)D + eps);
-  const float* md = mod + (size_t)map.modrow[seq_of_row(map, row)] * ld_mod;
-  const float4* sh = (const float4*)(md + shift_off);
-  const float4* sc = (const float4*)(md + scale_off);
   OutT* orow = out + (size_t)row * ldo;
 #pragma unroll
-  for (int i = 0; i < kMaxV4; ++i) {
+  for (int i = 0; i < NI; ++i) {
     const int c = lane + 64 * i;
     if (c < nv) {
-      const float4 a = sh[c], b = sc[c];
+      const float4 a = PRE ? shv[PRE ? i : 0] : sh[c], b = PRE ? scv[PRE ? i : 0] : sc[c];
       const float y0 = (v[i].x - mean) * rstd * (1.f + b.x) + a.x;
       const float y1 = (v[i].y - mean) * rstd * (1.f + b.y) + a.y;
       const float y2 = (v[i].z - mean) * rstd * (1.f + b.z) + a.z;
@@ -95,12 +110,17 @@ hipError_t launch_ln_modulate(bool bf16_out, int rows, int D, const float* x, in
                               const SeqMap& map, void* out, int ldo, float eps, hipStream_t st) {
   if (rows <= 0) return hipSuccess;
   dim3 grid((rows + kLnRows - 1) / kLnRows), block(256);
-  if (bf16_out)
-    hipLaunchKernelGGL(ln_mod_kernel<bf16>, grid, block, 0, st, x, ldx, rows, D, mod, ld_mod,
-                       shift_off, scale_off, map, (bf16*)out, ldo, eps);
-  else
-    hipLaunchKernelGGL(ln_mod_kernel<float>, grid, block, 0, st, x, ldx, rows, D, mod, ld_mod,
-                       shift_off, scale_off, map, (float*)out, ldo, eps);
+#define T2I_LN(T_, NV_)                                                                      \
+  hipLaunchKernelGGL((ln_mod_kernel<T_, NV_>), grid, block, 0, st, x, ldx, rows, D, mod, ld_mod, \
+                     shift_off, scale_off, map, (T_*)out, ldo, eps)
+  if (bf16_out) {
+    if (D == 1152) T2I_LN(bf16, 288);
+    else if (D == 3072) T2I_LN(bf16, 768);
+    else T2I_LN(bf16, 0);
+  } else {
+    T2I_LN(float, 0);
+  }
+#undef T2I_LN
   return hipGetLastError();
 }
 
