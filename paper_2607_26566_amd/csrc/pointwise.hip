@@ -428,9 +428,22 @@ hipError_t launch_bias_rows_f32(const void* bias, bool bias_bf16, int rows, int 
 // Final layer: per image token and guidance branch,
 //   out = LNmod(x; shift, scale) W_out^T + b_out     (P = p*p*C outputs)
 // then v = v_u + g (v_c - v_u), unpatchify, noise_pred = v, latent += dt v.
-// One wave per token; lane f < P ends up holding output feature f.
+// One wave per token, both guidance branches together (each weight load
+// serves both).  Each lane accumulates its share of every output (same
+// per-lane FMA order as a per-output loop); for P a power of two the P sums
+// are then finished by one butterfly reduce-scatter whose pairings are those
+// of wave_sum, so every output is added up in exactly the same order.
+template <typename TW, int PT>
+__device__ __forceinline__ float4 ld_w4(const TW* w) {
+  if constexpr (sizeof(TW) == 2) {
+    const bf16x4 q = *(const bf16x4*)w;
+    return float4{(float)q[0], (float)q[1], (float)q[2], (float)q[3]};
+  } else {
+    return *(const float4*)w;
+  }
+}
 
-template <typename TW>
+template <typename TW, int PT, int NV>
 __global__ __launch_bounds__(256) void final_kernel(const float* __restrict__ x, ReqMap rm,
                                                     const TW* __restrict__ w_out,
                                                     const TW* __restrict__ b_out,
@@ -439,70 +452,136 @@ __global__ __launch_bounds__(256) void final_kernel(const float* __restrict__ x,
                                                     int p, float eps, float guidance,
                                                     float* __restrict__ lat,
                                                     float* __restrict__ noise_pred) {
+  constexpr int NI = NV ? (NV + 63) / 64 : kMaxV4;
   const int lane = threadIdx.x & 63;
   const int tok = blockIdx.x * 4 + (threadIdx.x >> 6);
   if (tok >= rm.tokens_total) return;
   const int r = req_of_token(rm, tok);
-  const int P = p * p * C;
-  const int nv = D >> 2;
+  const int P = PT ? PT : p * p * C;
+  const int nv = NV ? NV : D >> 2;
   const float* md = mod + (size_t)rm.modrow[r] * ld_mod;
   const float4* sh = (const float4*)(md + shift_off);
   const float4* sc = (const float4*)(md + scale_off);
-  float mine[2] = {0.f, 0.f};
-  for (int br = 0; br < rm.branches; ++br) {
+  const int nb = rm.branches;
+  float4 v[2][NI];
+  // LN-modulate both branches' rows in registers (static indices throughout,
+  // so that everything stays in registers)
+#pragma unroll
+  for (int br = 0; br < 2; ++br) {
+    if (br >= nb) continue;
     const float4* xr = (const float4*)(x + ((size_t)br * rm.tokens_total + tok) * D);
-    float4 v[kMaxV4];
     float s = 0.f;
 #pragma unroll
-    for (int i = 0; i < kMaxV4; ++i) {
+    for (int i = 0; i < NI; ++i) {
       const int c = lane + 64 * i;
       if (c < nv) {
-        v[i] = xr[c];
-        s += (v[i].x + v[i].y) + (v[i].z + v[i].w);
+        v[br][i] = xr[c];
+        s += (v[br][i].x + v[br][i].y) + (v[br][i].z + v[br][i].w);
       }
     }
     const float mean = wave_sum(s) / (float)D;
     float q = 0.f;
 #pragma unroll
-    for (int i = 0; i < kMaxV4; ++i) {
+    for (int i = 0; i < NI; ++i) {
       const int c = lane + 64 * i;
       if (c < nv) {
-        const float a = v[i].x - mean, b = v[i].y - mean, cc = v[i].z - mean, d = v[i].w - mean;
+        const float a = v[br][i].x - mean, b = v[br][i].y - mean, cc = v[br][i].z - mean,
+                    d = v[br][i].w - mean;
         q += (a * a + b * b) + (cc * cc + d * d);
       }
     }
     const float rstd = 1.0f / sqrtf(wave_sum(q) / (float)D + eps);
 #pragma unroll
-    for (int i = 0; i < kMaxV4; ++i) {
+    for (int i = 0; i < NI; ++i) {
       const int c = lane + 64 * i;
       if (c < nv) {
         const float4 a = sh[c], b = sc[c];
-        v[i].x = (v[i].x - mean) * rstd * (1.f + b.x) + a.x;
-        v[i].y = (v[i].y - mean) * rstd * (1.f + b.y) + a.y;
-        v[i].z = (v[i].z - mean) * rstd * (1.f + b.z) + a.z;
-        v[i].w = (v[i].w - mean) * rstd * (1.f + b.w) + a.w;
+        v[br][i].x = (v[br][i].x - mean) * rstd * (1.f + b.x) + a.x;
+        v[br][i].y = (v[br][i].y - mean) * rstd * (1.f + b.y) + a.y;
+        v[br][i].z = (v[br][i].z - mean) * rstd * (1.f + b.z) + a.z;
+        v[br][i].w = (v[br][i].w - mean) * rstd * (1.f + b.w) + a.w;
       }
-    }
-    for (int f = 0; f < P; ++f) {
-      const TW* wr = w_out + (size_t)f * D;
-      float part = 0.f;
-#pragma unroll
-      for (int i = 0; i < kMaxV4; ++i) {
-        const int c = lane + 64 * i;
-        if (c < nv) {
-          part = fmaf(v[i].x, to_f32(wr[4 * c + 0]), part);
-          part = fmaf(v[i].y, to_f32(wr[4 * c + 1]), part);
-          part = fmaf(v[i].z, to_f32(wr[4 * c + 2]), part);
-          part = fmaf(v[i].w, to_f32(wr[4 * c + 3]), part);
-        }
-      }
-      const float tot = wave_sum(part) + to_f32(b_out[f]);
-      if (lane == f) mine[br] = tot;
     }
   }
-  if (lane >= P) return;
-  const float vel = rm.branches == 2 ? mine[1] + guidance * (mine[0] - mine[1]) : mine[0];
-  const int f = lane;
+  float mine[2] = {0.f, 0.f};
+  int f_own = lane;   // output this lane ends with
+  if constexpr (PT > 0) {
+    // per-lane partial sums of every output, then the reduce-scatter
+    float acc[2][PT];
+#pragma unroll
+    for (int f = 0; f < PT; ++f) acc[0][f] = acc[1][f] = 0.f;
+#pragma unroll
+    for (int i = 0; i < NI; ++i) {
+      const int c = lane + 64 * i;
+      if (c < nv) {
+#pragma unroll
+        for (int f = 0; f < PT; ++f) {
+          const float4 w = ld_w4<TW, PT>(w_out + (size_t)f * D + 4 * c);
+#pragma unroll
+          for (int br = 0; br < 2; ++br) {
+            acc[br][f] = fmaf(v[br][i].x, w.x, acc[br][f]);
+            acc[br][f] = fmaf(v[br][i].y, w.y, acc[br][f]);
+            acc[br][f] = fmaf(v[br][i].z, w.z, acc[br][f]);
+            acc[br][f] = fmaf(v[br][i].w, w.w, acc[br][f]);
+          }
+        }
+      }
+    }
+    // step st (lane bit o = 32 >> st) halves the outputs a lane holds -- it
+    // keeps the half given by that bit -- until one is left, then plain
+    // butterfly steps
+    int base = 0;
+#pragma unroll
+    for (int st = 0; st < 6; ++st) {
+      const int o = 32 >> st;
+      const int K = PT >> st;          // outputs held before this step
+      const bool up = (lane & o) != 0;
+      if (K > 1) {
+        const int h = K / 2;
+#pragma unroll
+        for (int br = 0; br < 2; ++br)
+#pragma unroll
+          for (int t = 0; t < h; ++t) {
+            const float keep = up ? acc[br][t + h] : acc[br][t];
+            const float send = up ? acc[br][t] : acc[br][t + h];
+            acc[br][t] = keep + __shfl_xor(send, o, kWave);
+          }
+        if (up) base += h;
+      } else {
+#pragma unroll
+        for (int br = 0; br < 2; ++br) acc[br][0] += __shfl_xor(acc[br][0], o, kWave);
+      }
+    }
+    f_own = base;
+    const float bo = to_f32(b_out[f_own]);
+    mine[0] = acc[0][0] + bo;
+    mine[1] = acc[1][0] + bo;
+  } else {
+#pragma unroll
+    for (int br = 0; br < 2; ++br) {
+      if (br >= nb) continue;
+      for (int f = 0; f < P; ++f) {
+        const TW* wr = w_out + (size_t)f * D;
+        float part = 0.f;
+#pragma unroll
+        for (int i = 0; i < NI; ++i) {
+          const int c = lane + 64 * i;
+          if (c < nv) {
+            part = fmaf(v[br][i].x, to_f32(wr[4 * c + 0]), part);
+            part = fmaf(v[br][i].y, to_f32(wr[4 * c + 1]), part);
+            part = fmaf(v[br][i].z, to_f32(wr[4 * c + 2]), part);
+            part = fmaf(v[br][i].w, to_f32(wr[4 * c + 3]), part);
+          }
+        }
+        const float tot = wave_sum(part) + to_f32(b_out[f]);
+        if (lane == f) mine[br] = tot;
+      }
+    }
+  }
+  // one lane per output writes (for PT, the first of the lanes that hold it)
+  if (PT > 0 ? (lane & (64 / (PT > 0 ? PT : 64) - 1)) != 0 : lane >= P) return;
+  const float vel = nb == 2 ? mine[1] + guidance * (mine[0] - mine[1]) : mine[0];
+  const int f = f_own;
   const int a = f / (p * C), b = (f / C) % p, c = f % C;
   const int lt = tok - rm.tok_off[r];
   const int W = rm.w[r], H = rm.h[r], gw = W / p;
@@ -519,14 +598,21 @@ hipError_t launch_final_layer(const float* x, const ReqMap& rm, const void* w_ou
                               float guidance, float* latents, float* noise_pred, hipStream_t st) {
   if (rm.tokens_total == 0) return hipSuccess;
   dim3 grid((rm.tokens_total + 3) / 4), block(256);
-  if (w_bf16)
-    hipLaunchKernelGGL(final_kernel<bf16>, grid, block, 0, st, x, rm, (const bf16*)w_out,
-                       (const bf16*)b_out, mod, ld_mod, shift_off, scale_off, D, C, p, eps,
-                       guidance, latents, noise_pred);
-  else
-    hipLaunchKernelGGL(final_kernel<float>, grid, block, 0, st, x, rm, (const float*)w_out,
-                       (const float*)b_out, mod, ld_mod, shift_off, scale_off, D, C, p, eps,
-                       guidance, latents, noise_pred);
+  const int P = p * p * C;
+#define T2I_FIN(TW_, PT_, NV_)                                                                 \
+  hipLaunchKernelGGL((final_kernel<TW_, PT_, NV_>), grid, block, 0, st, x, rm, (const TW_*)w_out, \
+                     (const TW_*)b_out, mod, ld_mod, shift_off, scale_off, D, C, p, eps, guidance, \
+                     latents, noise_pred)
+  if (w_bf16) {
+    if (P == 16 && D == 1152) T2I_FIN(bf16, 16, 288);
+    else if (P == 64 && D == 3072) T2I_FIN(bf16, 64, 768);
+    else if (P == 16) T2I_FIN(bf16, 16, 0);
+    else T2I_FIN(bf16, 0, 0);
+  } else {
+    if (P == 16) T2I_FIN(float, 16, 0);
+    else T2I_FIN(float, 0, 0);
+  }
+#undef T2I_FIN
   return hipGetLastError();
 }
 
