@@ -147,49 +147,91 @@ __global__ void pe_table_kernel(float2* __restrict__ tab, int npos, int qd) {
 
 constexpr int kEmbTok = 32;
 
-template <typename TW>
+// PT: patch features p*p*C known at compile time (16, 64), else 0 (any
+// P <= 64): with constant trip counts the weights load as 16-byte vectors and
+// the patch rows as float4, with no per-feature branches.
+template <typename TW, int PT>
 __global__ __launch_bounds__(256) void embed_kernel(const float* __restrict__ lat, ReqMap rm,
                                                     const TW* __restrict__ w_pe,
                                                     const TW* __restrict__ b_pe, int D, int C,
                                                     int p, const float2* __restrict__ pe,
                                                     float* __restrict__ x0, float* __restrict__ x,
                                                     int copies) {
-  __shared__ float patch[kEmbTok][64];
+  // rows padded to 68 floats: 16-byte aligned, and neighbouring rows start
+  // four banks apart
+  __shared__ __attribute__((aligned(16))) float patch[kEmbTok][68];
   __shared__ int grid_pos[kEmbTok][2];
-  const int P = p * p * C;
+  __shared__ long long tok_base[kEmbTok];
+  __shared__ int tok_w[kEmbTok], tok_hw[kEmbTok];
+  const int P = PT ? PT : p * p * C;
   const int T = rm.tokens_total;
   const int t0 = blockIdx.x * kEmbTok, d = blockIdx.y * 256 + threadIdx.x;
-  for (int i = threadIdx.x; i < kEmbTok * P; i += 256) {
-    const int t = i / P, k = i - t * P, tok = t0 + t;
-    float v = 0.f;
+  // each token's patch origin in its request's latent, once
+  if (threadIdx.x < kEmbTok) {
+    const int t = threadIdx.x, tok = t0 + t;
+    long long base = -1;
+    int W = 0, HW = 0;
     if (tok < T) {
       const int r = req_of_token(rm, tok);
       const int lt = tok - rm.tok_off[r];
-      const int W = rm.w[r], H = rm.h[r], gw = W / p;
-      const int gi = lt / gw, gj = lt - gi * gw;
-      const int c = k % C, ab = k / C, a = ab / p, b = ab - a * p;
-      v = lat[rm.lat_off[r] + (size_t)c * H * W + (size_t)(gi * p + a) * W + gj * p + b];
-      if (k == 0) {
-        grid_pos[t][0] = gi;
-        grid_pos[t][1] = gj;
-      }
+      W = rm.w[r];
+      HW = rm.h[r] * W;
+      const int gw = W / p, gi = lt / gw, gj = lt - gi * gw;
+      base = rm.lat_off[r] + (long long)(gi * p) * W + gj * p;
+      grid_pos[t][0] = gi;
+      grid_pos[t][1] = gj;
     }
-    patch[t][k] = v;
+    tok_base[t] = base;
+    tok_w[t] = W;
+    tok_hw[t] = HW;
+  }
+  __syncthreads();
+  // gather element (t, k = (a p + b) C + c) in the order (c, a, t, b): the
+  // pixels of neighbouring threads are neighbours in a latent row
+  for (int i = threadIdx.x; i < kEmbTok * P; i += 256) {
+    const int b = i % p, rest = i / p;
+    const int t = rest % kEmbTok, ca = rest / kEmbTok;
+    const int a = ca % p, c = ca / p;
+    float v = 0.f;
+    if (tok_base[t] >= 0)
+      v = lat[tok_base[t] + (long long)c * tok_hw[t] + (long long)a * tok_w[t] + b];
+    patch[t][(a * p + b) * C + c] = v;
   }
   __syncthreads();
   if (d >= D) return;
-  float w[64];
+  constexpr int NW = PT ? PT : 64;
+  float w[NW];
+  if constexpr (PT > 0 && sizeof(TW) == 2) {
 #pragma unroll
-  for (int k = 0; k < 64; ++k) w[k] = k < P ? to_f32(w_pe[(size_t)d * P + k]) : 0.f;
+    for (int k8 = 0; k8 < PT / 8; ++k8) {
+      const bf16x8 q = *(const bf16x8*)(w_pe + (size_t)d * PT + 8 * k8);
+#pragma unroll
+      for (int e = 0; e < 8; ++e) w[8 * k8 + e] = (float)q[e];
+    }
+  } else {
+#pragma unroll
+    for (int k = 0; k < NW; ++k) w[k] = k < P ? to_f32(w_pe[(size_t)d * P + k]) : 0.f;
+  }
   const float bias = to_f32(b_pe[d]);
   const int half = D / 2, qd = D / 4, kk = d % half, f = kk % qd;
   for (int t = 0; t < kEmbTok; ++t) {
     const int tok = t0 + t;
     if (tok >= T) break;
     float acc = bias;
+    if constexpr (PT > 0) {
 #pragma unroll
-    for (int k = 0; k < 64; ++k)
-      if (k < P) acc = fmaf(w[k], patch[t][k], acc);
+      for (int k4 = 0; k4 < PT / 4; ++k4) {
+        const float4 pv = *(const float4*)&patch[t][4 * k4];
+        acc = fmaf(w[4 * k4 + 0], pv.x, acc);
+        acc = fmaf(w[4 * k4 + 1], pv.y, acc);
+        acc = fmaf(w[4 * k4 + 2], pv.z, acc);
+        acc = fmaf(w[4 * k4 + 3], pv.w, acc);
+      }
+    } else {
+#pragma unroll
+      for (int k = 0; k < 64; ++k)
+        if (k < P) acc = fmaf(w[k], patch[t][k], acc);
+    }
     if (pe) {
       const float2 sc = pe[grid_pos[t][d < half ? 0 : 1] * qd + f];
       acc += kk < qd ? sc.x : sc.y;
@@ -209,12 +251,19 @@ hipError_t launch_embed(const float* lat, const ReqMap& rm, const void* w_pe, co
                        D / 4);
   }
   dim3 grid((rm.tokens_total + kEmbTok - 1) / kEmbTok, (D + 255) / 256);
-  if (w_bf16)
-    hipLaunchKernelGGL(embed_kernel<bf16>, grid, dim3(256), 0, st, lat, rm, (const bf16*)w_pe,
-                       (const bf16*)b_pe, D, C, p, pe_table, x0, x, copies);
-  else
-    hipLaunchKernelGGL(embed_kernel<float>, grid, dim3(256), 0, st, lat, rm, (const float*)w_pe,
-                       (const float*)b_pe, D, C, p, pe_table, x0, x, copies);
+  const int P = p * p * C;
+#define T2I_EMB(TW_, PT_)                                                                     \
+  hipLaunchKernelGGL((embed_kernel<TW_, PT_>), grid, dim3(256), 0, st, lat, rm, (const TW_*)w_pe, \
+                     (const TW_*)b_pe, D, C, p, pe_table, x0, x, copies)
+  if (w_bf16) {
+    if (P == 16) T2I_EMB(bf16, 16);
+    else if (P == 64) T2I_EMB(bf16, 64);
+    else T2I_EMB(bf16, 0);
+  } else {
+    if (P == 16) T2I_EMB(float, 16);
+    else T2I_EMB(float, 0);
+  }
+#undef T2I_EMB
   return hipGetLastError();
 }
 
