@@ -369,10 +369,57 @@ __global__ void rope_apply_kernel(bf16* __restrict__ qk, int ld, int row0, ReqMa
   }
 }
 
+// Head dims that are multiples of 16: one thread per (row, head, half, group
+// of 4 pairs) moves 16 bytes of q and of k at a time, with 32-bit index math;
+// each pair is rotated exactly as in rope_apply_kernel.
+__global__ void rope_apply4_kernel(bf16* __restrict__ qk, int ld, int row0, ReqMap rm, int heads,
+                                   int hd, int patch, const float2* __restrict__ tab) {
+  const int q = hd / 4, g = q / 4;
+  const int per_row = heads * 2 * g;
+  const int T = rm.tokens_total;
+  const int total = T * rm.branches * per_row;
+  const int D = heads * hd;
+  for (int i = blockIdx.x * 256 + threadIdx.x; i < total; i += gridDim.x * 256) {
+    const int row = i / per_row;
+    int rem = i - row * per_row;
+    const int h = rem / (2 * g);
+    rem -= h * 2 * g;
+    const int half = rem / g, jg = rem - half * g;
+    const int tok = row >= T ? row - T : row;   // branch-major rows, two branches at most
+    const int r = req_of_token(rm, tok);
+    const int lt = tok - rm.tok_off[r];
+    const int gw = rm.w[r] / patch;
+    const int pos = half ? lt % gw : lt / gw;
+    const float2* cs = tab + pos * q + 4 * jg;
+    bf16* base = qk + (size_t)(row0 + row) * ld + h * hd + half * (hd / 2) + 8 * jg;
+#pragma unroll
+    for (int part = 0; part < 2; ++part) {   // q, then k (D columns further)
+      bf16x8* pp = (bf16x8*)(base + part * D);
+      const bf16x8 v = *pp;
+      bf16x8 o;
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const float2 c = cs[e];
+        const float a = (float)v[2 * e], b = (float)v[2 * e + 1];
+        o[2 * e] = (bf16)(a * c.x - b * c.y);
+        o[2 * e + 1] = (bf16)(a * c.y + b * c.x);
+      }
+      *pp = o;
+    }
+  }
+}
+
 hipError_t launch_rope_apply(bf16* qk, int ld, int row0, const ReqMap& rm, int heads, int head_dim,
                              int patch, const float2* table, hipStream_t st) {
   const long total = (long)rm.tokens_total * rm.branches * heads * (head_dim / 2);
   if (total == 0) return hipSuccess;
+  if (head_dim % 16 == 0 && rm.branches <= 2 && ld % 8 == 0 && ((uintptr_t)qk % 16) == 0 &&
+      total / 4 < (1L << 30)) {
+    const int grid = (int)std::min<long>((total / 4 + 255) / 256, 16384);
+    hipLaunchKernelGGL(rope_apply4_kernel, dim3(grid), dim3(256), 0, st, qk, ld, row0, rm, heads,
+                       head_dim, patch, table);
+    return hipGetLastError();
+  }
   const int grid = (int)std::min<long>((total + 255) / 256, 16384);
   hipLaunchKernelGGL(rope_apply_kernel, dim3(grid), dim3(256), 0, st, qk, ld, row0, rm, heads,
                      head_dim, patch, table);
