@@ -309,11 +309,8 @@ t2i_status build_plan(t2i_dit* h, int n_req, const int32_t* lat_h, const int32_t
   if (P.rows > c.max_tokens) return fail(h, T2I_ERR_SHAPE, "image tokens exceed max_tokens");
   const int M = c.text_tokens;
   P.txt_rows = n_req * M + (P.branches == 2 ? M : 0);
-  const int BQ = attention_query_tile(h->bf(), c.head_dim, 0);
-  const int BQX = attention_query_tile(h->bf(), c.head_dim, 1);
   P.img.n = n_req * P.branches;
   P.self.n = P.cross.n = P.img.n;
-  int tiles = 0, xtiles = 0;
   for (int br = 0; br < P.branches; ++br)
     for (int r = 0; r < n_req; ++r) {
       const int s = br * n_req + r;
@@ -327,21 +324,16 @@ t2i_status build_plan(t2i_dit* h, int n_req, const int32_t* lat_h, const int32_t
       P.self.k_len[s] = len;
       P.cross.k_start[s] = br == 0 ? r * M : n_req * M;
       P.cross.k_len[s] = M;
-      P.self.tile_start[s] = tiles;
-      P.cross.tile_start[s] = xtiles;
-      tiles += (len + BQ - 1) / BQ;
-      xtiles += (len + BQX - 1) / BQX;
     }
   P.img.start[P.img.n] = P.rows;
-  P.self.tile_start[P.self.n] = tiles;
-  P.cross.tile_start[P.cross.n] = xtiles;
+  attention_tiles(P.self, h->bf(), c.heads, 0);
+  attention_tiles(P.cross, h->bf(), c.heads, 1);
   if (c.arch == T2I_ARCH_MMDIT) {
     // residual rows are stream-major: text rows [0, txt_rows) with sequence s
     // at s*M, then the image rows (offset txt_rows) in the cross-DiT order
     if (2 * P.img.n > kMaxSeq) return fail(h, T2I_ERR_SHAPE, "too many sequences for MMDiT");
     P.txt_rows = P.img.n * M;
     P.txt.n = P.img.n;
-    int jt = 0;
     for (int s = 0; s < P.img.n; ++s) {
       P.txt.start[s] = s * M;
       P.txt.modrow[s] = s % n_req;
@@ -354,13 +346,11 @@ t2i_status build_plan(t2i_dit* h, int n_req, const int32_t* lat_h, const int32_t
         P.joint.k_len[q] = M;
         P.joint.k2_start[q] = ist;
         P.joint.k2_len[q] = ilen;
-        P.joint.tile_start[q] = jt;
-        jt += (P.joint.q_len[q] + BQ - 1) / BQ;
       }
     }
     P.txt.start[P.txt.n] = P.txt_rows;
     P.joint.n = 2 * P.img.n;
-    P.joint.tile_start[P.joint.n] = jt;
+    attention_tiles(P.joint, true, c.heads, 0);
   }
   for (int r = 0; r < n_req; ++r)
     P.grid_max = std::max(P.grid_max, std::max(lat_h[r], lat_w[r]) / c.patch);
@@ -1341,8 +1331,6 @@ t2i_status t2i_op_attention(int32_t dtype, int32_t heads, int32_t head_dim, int3
   AttnMap m;
   std::memset(&m, 0, sizeof(m));   // no second key segment
   m.n = n_seq;
-  const int BQ = attention_query_tile(dtype == T2I_BF16, head_dim);
-  int tiles = 0;
   for (int s = 0; s < n_seq; ++s) {
     const int s2 = k2_start ? k2_start[s] : 0, n2 = k2_len ? k2_len[s] : 0;
     if (q_start[s] < 0 || q_len[s] < 0 || k_start[s] < 0 || k_len[s] < 0 || s2 < 0 || n2 < 0 ||
@@ -1357,10 +1345,8 @@ t2i_status t2i_op_attention(int32_t dtype, int32_t heads, int32_t head_dim, int3
     m.k_len[s] = k_len[s];
     m.k2_start[s] = s2;
     m.k2_len[s] = n2;
-    m.tile_start[s] = tiles;
-    tiles += (q_len[s] + BQ - 1) / BQ;
   }
-  m.tile_start[n_seq] = tiles;
+  attention_tiles(m, dtype == T2I_BF16, heads, 0);
   hipError_t err = launch_attention(dtype == T2I_BF16, 0, heads, head_dim, m, q, ldq, k, ldk, v, ldv,
                                     o, ldo, (hipStream_t)stream);
   if (err != hipSuccess) return ops_fail(T2I_ERR_DEVICE, hipGetErrorString(err));

@@ -462,13 +462,36 @@ __global__ __launch_bounds__(64) void attn_f32_kernel(AttnMap map, int heads,
 // bf16: 8 waves x 32 queries per workgroup, 4 stages.  Cross-attention to
 // the text (two key tiles per query tile): 4 waves x 32 queries and 3 stages,
 // so that two workgroups share a CU and one's loads overlap the other's
-// compute.  fp32: 64 queries.
+// compute.  Self / joint attention launches that would have fewer
+// workgroups than CUs (short sequences, few heads) halve the workgroup, down
+// to 2 waves.  fp32: 64 queries.
 constexpr int kAttnWaves = 8, kAttnStages = 4;
 constexpr int kCrossWaves = 4, kCrossStages = 3;
-int attention_query_tile(bool bf16_io, int head_dim, int role) {
-  (void)head_dim;
-  if (!bf16_io) return 64;
-  return (role == 1 ? kCrossWaves : kAttnWaves) * 32;
+void attention_tiles(AttnMap& m, bool bf16_io, int heads, int role) {
+  auto fill = [&](int bq) {
+    int t = 0;
+    for (int s = 0; s < m.n; ++s) {
+      m.tile_start[s] = t;
+      t += (m.q_len[s] + bq - 1) / bq;
+    }
+    m.tile_start[m.n] = t;
+    return (long)t * heads;
+  };
+  if (!bf16_io) {
+    m.waves = 2;
+    fill(64);
+    return;
+  }
+  // default workgroup size; self / joint attention halves it while the
+  // launch has fewer workgroups than CUs (256 on MI355X) -- cross-attention,
+  // with two key tiles per query tile, measured slower with smaller groups
+  int w = role == 1 ? kCrossWaves : kAttnWaves;
+  long wgs = fill(32 * w);
+  while (role == 0 && w > 2 && wgs < 256) {
+    w /= 2;
+    wgs = fill(32 * w);
+  }
+  m.waves = w;
 }
 
 template <int HD>
@@ -479,14 +502,21 @@ static hipError_t launch_hd(bool bf16_io, int role, int heads, const AttnMap& ma
   if (tiles == 0) return hipSuccess;
   if (bf16_io) {
     const float scale_log2 = 1.4426950408889634f / sqrtf((float)HD);
-    if (role == 1)
-      hipLaunchKernelGGL((attn_bf16_kernel<HD, kCrossWaves, kCrossStages, 1>), dim3(tiles),
-                         dim3(kCrossWaves * 64), 0, st, map, heads, (const bf16*)q, ldq,
-                         (const bf16*)k, ldk, (const bf16*)v, ldv, (bf16*)o, ldo, scale_log2);
-    else
-      hipLaunchKernelGGL((attn_bf16_kernel<HD, kAttnWaves, kAttnStages, 0>), dim3(tiles),
-                         dim3(kAttnWaves * 64), 0, st, map, heads, (const bf16*)q, ldq,
-                         (const bf16*)k, ldk, (const bf16*)v, ldv, (bf16*)o, ldo, scale_log2);
+#define T2I_ATT(NW_, ST_, R_)                                                                   \
+  hipLaunchKernelGGL((attn_bf16_kernel<HD, NW_, ST_, R_>), dim3(tiles), dim3(NW_ * 64), 0, st, map, \
+                     heads, (const bf16*)q, ldq, (const bf16*)k, ldk, (const bf16*)v, ldv,       \
+                     (bf16*)o, ldo, scale_log2)
+    // smaller workgroups (2 or 4 waves) share a CU and use a 3-stage ring
+    if (role == 1) {
+      if (map.waves == kCrossWaves) T2I_ATT(kCrossWaves, kCrossStages, 1);
+      else return hipErrorInvalidValue;
+    } else {
+      if (map.waves == kAttnWaves) T2I_ATT(kAttnWaves, kAttnStages, 0);
+      else if (map.waves == 4) T2I_ATT(4, 3, 0);
+      else if (map.waves == 2) T2I_ATT(2, 3, 0);
+      else return hipErrorInvalidValue;
+    }
+#undef T2I_ATT
   } else {
     const float scale = 1.0f / sqrtf((float)HD);
     hipLaunchKernelGGL(attn_f32_kernel<HD>, dim3(tiles), dim3(64), 0, st, map, heads,

@@ -369,6 +369,12 @@ hipError_t launch_gemm_bf16(const bf16* A, int lda, const bf16* W, int ldw, cons
 #undef T2I_RED_CASE
     return hipGetLastError();
   }
+  // 128-row tiles unless they would leave CUs idle (e.g. 1024 rows x 1152
+  // columns = 64 tiles); 64 x 64 tiles then (same K order, same results)
+  const long tiles128 = (long)((M + 127) / 128) * ((N + (N % 144 == 0 ? 143 : 127)) /
+                                                    (N % 144 == 0 ? 144 : 128));
+  if (tiles128 < 256)
+    return gemm_bf16_dispatch<64, 64, 2>(A, lda, W, ldw, bias, M, N, K, kind, epi, vec_ok, st);
   if (N % 144 == 0)
     return gemm_bf16_dispatch<128, 144, 4>(A, lda, W, ldw, bias, M, N, K, kind, epi, vec_ok, st);
   return gemm_bf16_dispatch<128, 128, 2>(A, lda, W, ldw, bias, M, N, K, kind, epi, vec_ok, st);

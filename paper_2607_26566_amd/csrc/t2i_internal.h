@@ -35,6 +35,7 @@ struct SeqMap {
 // (prefix sum of ceil(q_len/BQ)).
 struct AttnMap {
   int n;
+  int waves;   // 32-query waves per workgroup (bf16 kernel): the query tile is 32 * waves
   int q_start[kMaxSeq], q_len[kMaxSeq], k_start[kMaxSeq], k_len[kMaxSeq];
   int k2_start[kMaxSeq], k2_len[kMaxSeq];
   int tile_start[kMaxSeq + 1];
@@ -199,7 +200,11 @@ hipError_t launch_linear_rows(const float* A, int lda, const void* W, int ldw, b
 hipError_t launch_attention(bool bf16_io, int role, int heads, int head_dim, const AttnMap& map,
                             const void* q, int ldq, const void* k, int ldk, const void* v,
                             int ldv, void* o, int ldo, hipStream_t st);
-int attention_query_tile(bool bf16_io, int head_dim, int role = 0);
+// Query tiling of a map whose q_len are set: chooses the waves per workgroup
+// (fewer, smaller workgroups when the default tiling would not fill the
+// chip) and fills waves and tile_start.  Every 32-query group is computed
+// the same way whatever the tiling.
+void attention_tiles(AttnMap& m, bool bf16_io, int heads, int role);
 
 hipError_t launch_ln_modulate(bool bf16_out, int rows, int D, const float* x, int ldx,
                               const float* mod, int ld_mod, int shift_off, int scale_off,
