@@ -255,9 +255,12 @@ hipError_t gemm_dma_dispatch(const bf16* A, int lda, const bf16* W, int ldw, con
 }
 
 // Large-M projections (tile shapes and orders measured on MI355X at the DiT's
-// and the joint-attention model's shapes).  A CU moves ~17 bytes per clock
-// from L2 into LDS whatever the tile, so bytes per FLOP -- (BM + BN) / (BM BN)
-// -- decide, together with filling whole rounds of 256 workgroups:
+// and the joint-attention model's shapes).  Operand loads that miss the XCD's
+// L2 bound these GEMMs: a CU takes 30-57 bytes per clock of direct loads from
+// L2 but only 10-13 from the memory-side cache or HBM, and in these GEMMs it
+// averages ~17.  Bytes per FLOP -- (BM + BN) / (BM BN) -- and the L2 reuse of
+// the tile order decide, together with filling whole rounds of 256
+// workgroups:
 //   256 x 288 (8 waves of 64 x 144) where N is a multiple of 288 and the tiles
 //             make whole rounds (fc1: N = 4608, M = 8192 -> 512 tiles);
 //   256 x 256 for long K where N is a multiple of 256 with whole rounds

@@ -48,7 +48,8 @@ def run_linear(dtype, epi, A, W, b, resid=None, gate=None, with_copy=False):
 
 GEMM_SHAPES = [(300, 192, 128), (1000, 1152, 1152), (64, 3456, 1152), (8192, 1152, 4608),
                (129, 4608, 1152), (240, 2304, 1152), (1, 128, 64), (4096, 3456, 1152),
-               (3000, 1296, 1152), (2100, 200, 128), (2100, 202, 64), (8192, 4608, 1152)]
+               (3000, 1296, 1152), (2100, 200, 128), (2100, 202, 64), (8192, 4608, 1152),
+               (1900, 4608, 1152), (2000, 4096, 128)]
 
 
 @pytest.mark.parametrize("M,N,K", GEMM_SHAPES)
@@ -60,6 +61,22 @@ def test_linear_bf16_store_and_gelu(M, N, K):
     assert rel_l2(to_host(out), ref) < 3e-3
     out, _, _ = run_linear(_lib.T2I_BF16, _lib.T2I_EPI_GELU, A, W, b)
     assert rel_l2(to_host(out), dit.gelu_tanh(ref)) < 3e-3
+
+
+def test_linear_bf16_tilings_agree_bitwise():
+    """The same rows through the three GEMM kernels -- direct-load 256-row
+    tiles (2100 rows), register-staged 128 x 144 tiles (1900 rows) and 64 x 64
+    tiles (300 rows) -- come out bitwise equal: every kernel accumulates K in
+    the same order, which is what makes a packed batch equal its requests run
+    alone."""
+    N, K = 4608, 1152
+    A, W, b = rnd(70, (2100, K)), rnd(71, (N, K), 0.05), rnd(72, (N,), 0.1)
+    outs = []
+    for M in (2100, 1900, 300):
+        out, _, _ = run_linear(_lib.T2I_BF16, _lib.T2I_EPI_GELU, A[:M], W, b)
+        outs.append(to_host(out)[:300])
+    say(f"tilings: max |diff| {np.abs(outs[0] - outs[1]).max():.1e}, {np.abs(outs[0] - outs[2]).max():.1e}")
+    assert np.array_equal(outs[0], outs[1]) and np.array_equal(outs[0], outs[2])
 
 
 @pytest.mark.parametrize("M,N,K", [(300, 192, 128), (1000, 1152, 4608), (8192, 1152, 1152),
