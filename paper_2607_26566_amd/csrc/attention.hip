@@ -149,24 +149,27 @@ __global__ __launch_bounds__(NW * 64, 8 / NW) void attn_bf16_kernel(AttnMap map,
   // Q fragments (B operand of S^T): query qr, d = 16c + 8hl .. +7, pre-multiplied
   // by log2(e)/sqrt(d) so that scores come out in log2 units; the shift slot
   // d = HD is element 0 of chunk HD/16 in the lanes of half (HD%16)/8
+  // (loaded here, scaled after the first tile loads are issued, so that the
+  // two latencies overlap)
   constexpr int BC = HD / 16, BH = (HD % 16) / 8;
   bf16x8 qf[DC];
 #pragma unroll
   for (int c = 0; c < DC; ++c) {
     const int d = c * 16 + hl * 8;
     qf[c] = bf16x8{};
-    if (qr < q_end && d < HD) {
-      const bf16x8 raw = *(const bf16x8*)(Q + (size_t)qr * ldq + hh * HD + d);
+    if (qr < q_end && d < HD) qf[c] = *(const bf16x8*)(Q + (size_t)qr * ldq + hh * HD + d);
+  }
+  auto scale_q = [&]() {
 #pragma unroll
-      for (int e = 0; e < 8; ++e) qf[c][e] = (bf16)((float)raw[e] * scale_log2);
-    }
-  }
-  // V^T rows HD .. HDO-1 of every stage: the ones row, then zeros
-  for (int i = tid; i < ST * (HDO - HD) * 64; i += NW * 64) {
-    const int st = i / ((HDO - HD) * 64), rem = i - st * (HDO - HD) * 64;
-    const int row = HD + rem / 64, col = rem & 63;
-    ((bf16*)(vst(st) + row * 128))[col] = (bf16)(row == HD ? 1.f : 0.f);
-  }
+    for (int c = 0; c < DC; ++c)
+#pragma unroll
+      for (int e = 0; e < 8; ++e) qf[c][e] = (bf16)((float)qf[c][e] * scale_log2);
+    // the ones row (V^T row HD) of every stage; the padding rows after it
+    // only feed O^T rows that are never read
+    if constexpr (ONES)
+      for (int i = tid; i < ST * 64; i += NW * 64)
+        ((bf16*)(vst(i >> 6) + HD * 128))[i & 63] = (bf16)1.f;
+  };
 
   // Tile loads: HBM -> LDS directly (global_load_lds_dwordx4), instruction i of
   // a tile writes bytes 1024i .. +1023 of the stage, lane l 16 bytes at 16l.
@@ -366,6 +369,7 @@ __global__ __launch_bounds__(NW * 64, 8 / NW) void attn_bf16_kernel(AttnMap map,
 #pragma unroll
   for (int ti = 0; ti < ST - 1; ++ti)
     if (ti < nt) issue(ti);
+  scale_q();
   wait_vmcnt_dyn(n_w * (min(nt, ST - 1) - 1));
   attn_barrier();
   f32x16 sa[2], sb[2];
