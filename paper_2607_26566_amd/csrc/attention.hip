@@ -25,9 +25,15 @@
 //
 // attn_f32_kernel: plain fp32 online softmax, one thread per query, for the
 // fp32 model.
+#include <algorithm>
+
 #include "t2i_internal.h"
 
 namespace t2i {
+
+// Word 3 of a raw buffer resource on gfx950: 32-bit data format, no swizzle;
+// offsets are bytes and reads at or past the extent return zero.
+constexpr int kBufWord3 = 0x00020000;
 
 __device__ __forceinline__ int xcd_remap_attn(int b, int nb) {
   const int q = nb >> 3, r = nb & 7;
@@ -45,6 +51,13 @@ __device__ __forceinline__ int swap23(int r) {
   return (r & ~12) | ((r & 4) << 1) | ((r & 8) >> 1);
 }
 
+// s_waitcnt vmcnt(N), lgkmcnt / expcnt untouched
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() {
+  static_assert(N >= 0 && N < 16, "vmcnt");
+  __builtin_amdgcn_s_waitcnt(N | (7 << 4) | (15 << 8));
+}
+
 // s_waitcnt vmcnt(n) for a wave-uniform n < 16 known only at run time.
 __device__ __forceinline__ void wait_vmcnt_dyn(int n) {
   switch (n) {
@@ -58,8 +71,12 @@ __device__ __forceinline__ void wait_vmcnt_dyn(int n) {
 
 __device__ __forceinline__ void attn_barrier() {
   // this wave's LDS accesses are complete, then s_barrier (no wait for
-  // outstanding global loads, which __syncthreads would add)
-  asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
+  // outstanding global loads, which __syncthreads would add).  The wait is
+  // the builtin so that the compiler's wait-count tracking sees it: after it
+  // no scalar load can be pending, and the waits for LDS fragment reads
+  // further on can then count reads instead of draining them all.
+  __builtin_amdgcn_s_waitcnt(0xC07F);   // lgkmcnt(0), vmcnt / expcnt untouched
+  asm volatile("s_barrier" ::: "memory");
 }
 
 // Flattened tile -> (head, sequence, query tile).  HEAD_MINOR = false: tiles
@@ -130,15 +147,13 @@ __global__ __launch_bounds__(NW * 64, 8 / NW) void attn_bf16_kernel(AttnMap map,
   const int k1 = map.k_start[s], n1 = map.k_len[s];
   const int k2 = map.k2_start[s], n2 = map.k2_len[s];
   const int t1 = (n1 + BKV - 1) / BKV, nt = t1 + (n2 + BKV - 1) / BKV;
-  auto tile_keys = [&](int ti, int& kv0, int& kend) {
-    if (ti < t1) {
-      kv0 = k1 + ti * BKV;
-      kend = k1 + n1;
-    } else {
-      kv0 = k2 + (ti - t1) * BKV;
-      kend = k2 + n2;
-    }
-  };
+  // tile ti starts at key (ti < t1 ? k1 : k2 - 64 t1) + 64 ti; only the last
+  // tile of a segment can be ragged
+  const int kb2 = k2 - t1 * BKV;
+  const int rag1 = (n1 % BKV) ? t1 - 1 : -1, rag2 = (n2 % BKV) ? nt - 1 : -1;
+  auto tile_kv0 = [&](int ti) { return (ti < t1 ? k1 : kb2) + ti * BKV; };
+  auto tile_end = [&](int ti) { return ti < t1 ? k1 + n1 : k2 + n2; };
+  auto tile_full = [&](int ti) { return ti != rag1 && ti != rag2; };
   // 32x32x16 MFMA lane roles: column (query) ql, k-half hl; C element 4i + jj
   // of a lane is row 8i + 4hl + jj
   const int ql = lane & 31, hl = lane >> 5;
@@ -171,17 +186,25 @@ __global__ __launch_bounds__(NW * 64, 8 / NW) void attn_bf16_kernel(AttnMap map,
         ((bf16*)(vst(i >> 6) + HD * 128))[i & 63] = (bf16)1.f;
   };
 
-  // Tile loads: HBM -> LDS directly (global_load_lds_dwordx4), instruction i of
-  // a tile writes bytes 1024i .. +1023 of the stage, lane l 16 bytes at 16l.
+  // Tile loads: HBM -> LDS directly (buffer_load_dwordx4 ... lds), instruction
+  // i of a tile writes bytes 1024i .. +1023 of the stage, lane l 16 bytes at
+  // 16l.
   //   K (i < CPR): row r = key swap23(r), chunk slot swizzled; keys past the
   //     sequence are clamped to its last key (their scores are masked);
   //   V^T (i >= CPR): row d, 128 bytes = 64 keys, chunk slot c ^ ((d>>1)&7);
   //     chunks wholly past the sequence are read from the tile's first chunk
   //     (their probabilities are 0).
+  // Addresses: buffer resources based at K and V^T, the tile's position as
+  // the scalar offset and per-lane 32-bit byte offsets.  The buffer form of the LDS DMA, not
+  // the global one: the compiler counts an outstanding global-form DMA as an
+  // out-of-order LDS event and then drains every LDS fragment read with
+  // lgkmcnt(0), while the buffer form is tracked by vmcnt alone, so the reads
+  // of the main loop get exact waits.  The launcher keeps every offset below
+  // 2^31.
   // Wave w issues instructions w, w+8, ...: n_w per tile.
   constexpr int IPW = (NI + NW - 1) / NW;
   int g_off[IPW], g_key[IPW], l_off[IPW];
-  size_t f_off[IPW];   // element offset from the tile's first key (full tiles)
+  uint32_t f_off[IPW];   // byte offset from the tile base (full tiles)
   const int n_w = (NI - wave + NW - 1) / NW;
 #pragma unroll
   for (int ii = 0; ii < IPW; ++ii) {
@@ -195,61 +218,74 @@ __global__ __launch_bounds__(NW * 64, 8 / NW) void attn_bf16_kernel(AttnMap map,
       g_key[ii] = swap23(r);
       g_off[ii] = hh * HD + c * 8;
       l_off[ii] = i * 1024;                      // wave-uniform base; +16 per lane implied
-      f_off[ii] = (size_t)g_key[ii] * ldk + g_off[ii];
+      f_off[ii] = 2u * (uint32_t)(g_key[ii] * ldk + g_off[ii]);
     } else if (i < NI) {
       const int o = (i - CPR) * 1024 + lane * 16;
       const int d = o / 128, c = (lane & 7) ^ ((d >> 1) & 7);
       g_key[ii] = c * 8;                         // key offset of the chunk
       g_off[ii] = hh * HD + d;                   // V^T row
       l_off[ii] = KSTAGE + (i - CPR) * 1024;
-      f_off[ii] = (size_t)g_off[ii] * ldvt + g_key[ii];
+      f_off[ii] = 2u * (uint32_t)(g_off[ii] * ldvt + g_key[ii]);
     }
   }
+  // the launcher keeps every byte offset below 2^31, the extent given here
+  const __amdgpu_buffer_rsrc_t rk =
+      __builtin_amdgcn_make_buffer_rsrc((void*)K, 0, 0x7fffffff, kBufWord3);
+  const __amdgpu_buffer_rsrc_t rv =
+      __builtin_amdgcn_make_buffer_rsrc((void*)Vt, 0, 0x7fffffff, kBufWord3);
   auto issue = [&](int ti) {
-    int kv0, k_end;
-    tile_keys(ti, kv0, k_end);
+    const int kv0 = tile_kv0(ti);
+    const int sk = kv0 * (2 * ldk), sv = 2 * kv0;   // the tile's byte offsets
     char* base = kst(ti % ST);
-    if (kv0 + BKV <= k_end) {
-      // full tile: scalar tile bases plus the precomputed lane offsets
-      const bf16* kb = K + (size_t)kv0 * ldk;
-      const bf16* vb = Vt + kv0;
+    auto load = [&](int ii, int i, uint32_t off) {
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(
+          i < CPR ? rk : rv, (__attribute__((address_space(3))) void*)(base + l_off[ii]), 16,
+          off, i < CPR ? sk : sv, 0, 0);
+    };
+    if (tile_full(ti)) {
 #pragma unroll
       for (int ii = 0; ii < IPW; ++ii) {
         const int i = wave + NW * ii;
         if (i >= NI) break;
-        const bf16* src = (i < CPR ? kb : vb) + f_off[ii];
-        __builtin_amdgcn_global_load_lds((__attribute__((address_space(1))) void*)src,
-                                         (__attribute__((address_space(3))) void*)(base + l_off[ii]),
-                                         16, 0, 0);
+        load(ii, i, f_off[ii]);
       }
       return;
     }
+    // ragged tile: clamp keys past the sequence
+    const int k_end = tile_end(ti);
 #pragma unroll
     for (int ii = 0; ii < IPW; ++ii) {
       const int i = wave + NW * ii;
       if (i >= NI) break;
-      const bf16* src;
-      if (i < CPR) {
-        src = K + (size_t)min(kv0 + g_key[ii], k_end - 1) * ldk + g_off[ii];
-      } else {
-        const int gk = kv0 + g_key[ii];
-        src = Vt + (size_t)g_off[ii] * ldvt + (gk < k_end ? gk : kv0);
-      }
-      __builtin_amdgcn_global_load_lds((__attribute__((address_space(1))) void*)src,
-                                       (__attribute__((address_space(3))) void*)(base + l_off[ii]),
-                                       16, 0, 0);
+      if (i < CPR)
+        load(ii, i, 2u * (uint32_t)((min(kv0 + g_key[ii], k_end - 1) - kv0) * ldk + g_off[ii]));
+      else
+        load(ii, i, 2u * (uint32_t)(g_off[ii] * ldvt + (kv0 + g_key[ii] < k_end ? g_key[ii] : 0)));
     }
   };
   // K fragment (A operand) of key block kb, 16-wide d chunk c for this lane:
   // LDS row 32kb + ql, 16-byte chunk 2c + hl (zero past HD)
   bf16x8 kone = bf16x8{};      // the K side of the shift slot
   kone[0] = (bf16)1.f;
+  // The chunk holding the shift slot (c = HD/16) takes the constant by a
+  // per-lane select after an unmasked read: a lane-masked read would write
+  // EXEC, which ends the compiler's scheduling region and keeps the
+  // exponentials from interleaving with these MFMAs.
   auto kfrag = [&](int st, int kb, int c) {
-    const int r = 32 * kb + ql, cc = 2 * c + hl;
-    if (cc == CPR) return kone;
-    if (cc > CPR) return bf16x8{};
-    const int slot = KRS ? cc ^ ((r / KRS) & (CPR - 1)) : cc;
-    return *(const bf16x8*)(kst(st) + r * PK + slot * 16);
+    const int r = 32 * kb + ql;
+    auto at = [&](int cc) {
+      const int slot = KRS ? cc ^ ((r / KRS) & (CPR - 1)) : cc;
+      return *(const bf16x8*)(kst(st) + r * PK + slot * 16);
+    };
+    if (c < BC) return at(2 * c + hl);
+    if constexpr (CPR & 1) {
+      // half 0: data chunk HD/8 - 1; half 1: the shift slot
+      const bf16x8 v = at(2 * c);
+      return hl ? kone : v;
+    } else {
+      // half 0: the shift slot; half 1: zero
+      return hl ? bf16x8{} : kone;
+    }
   };
   auto qk = [&](int ti, f32x16 (&sc)[2]) {
     const int st = ti % ST;
@@ -286,15 +322,19 @@ __global__ __launch_bounds__(NW * 64, 8 / NW) void attn_bf16_kernel(AttnMap map,
   // one tile: S^T of tile ti is in cur with lane maximum lm; the next tile's
   // S^T and lane maximum go to nxt / lm_nxt
   auto step = [&](int ti, f32x16 (&cur)[2], float& lm, f32x16 (&nxt)[2], float& lm_nxt) {
-    int kv0, k_end;
-    tile_keys(ti, kv0, k_end);
     // tile ti+1 landed (the ST-3 tiles after it may still be in flight), for
-    // every wave
+    // every wave; immediate counts in the steady state
     const int young = min(ST - 3, nt - 2 - ti);
-    wait_vmcnt_dyn(young > 0 ? young * n_w : 0);
+    if (young == ST - 3) {
+      if (NI % NW == 0 || n_w == IPW) wait_vmcnt<(ST - 3) * IPW>();
+      else wait_vmcnt<(ST - 3) * (IPW - 1)>();
+    } else {
+      wait_vmcnt_dyn(young > 0 ? young * n_w : 0);
+    }
     attn_barrier();
     if (ti + ST - 1 < nt) issue(ti + ST - 1);     // into the stage of tile ti-1
-    if (kv0 + BKV > k_end) {
+    if (!tile_full(ti)) {
+      const int kv0 = tile_kv0(ti), k_end = tile_end(ti);
       // ragged tile: mask the scores past the sequence.  V^T chunks wholly
       // past it were copied from the tile's first chunk, finite when the
       // sequence length is a multiple of 8.  Otherwise a chunk the sequence
@@ -333,35 +373,55 @@ __global__ __launch_bounds__(NW * 64, 8 / NW) void attn_bf16_kernel(AttnMap map,
       m_ref = m_new;
       if (hl == BH) qf[BC][0] = (bf16)(-m_new);
     }
-    // straight-line part: the next tile's scores (independent MFMAs) overlap
-    // this tile's exponentials; for the last tile the "next" scores come from
-    // a stale stage and are never used
-    qk(ti + 1, nxt);
-    // P^T fragments: chunk q (16 keys) = elements 8(q&1) .. +7 of cur[q>>1]
+    // Straight-line part in a fixed issue order.  Slot s issues one MFMA --
+    // the next tile's S^T for s < NQK (chunk s/2, key block s%2), else P V
+    // for (key chunk, d tile) -- then its share of this tile's exponentials
+    // and the LDS fragment read LA slots ahead.  A scheduling barrier between
+    // slots keeps the exponentials spread over the MFMAs instead of bunched
+    // (the compiler otherwise clusters them).  P chunk q is complete before
+    // the first P V MFMA that uses it.  For the last tile the "next" scores
+    // come from a stale stage and are never used.
+    constexpr int NQK = 2 * DC, NPV = 4 * DT, NSL = NQK + NPV, LA = 3;
+    constexpr int NE = NQK + 3 * DT;   // slots carrying exponentials
+    const int stn = (ti + 1) % ST;
+    const char* vb = vst(ti % ST);
+    // V^T row 32dt + ql, keys 16q + 8hl .. +7
+    auto frag = [&](int sl) {
+      if (sl < NQK) return kfrag(stn, sl & 1, sl >> 1);
+      const int q = (sl - NQK) / DT, dt = (sl - NQK) % DT, row = dt * 32 + ql;
+      return *(const bf16x8*)(vb + row * 128 + (((2 * q + hl) ^ ((row >> 1) & 7)) << 4));
+    };
+    bf16x8 fr[NSL];
+    float pe[32];     // exponential i = P chunk i/8, element i%8
     bf16x8 pf[4];
     float psum = 0.f;
 #pragma unroll
-    for (int q = 0; q < 4; ++q)
+    for (int sl = 0; sl <= LA; ++sl) fr[sl] = frag(sl);
+    __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
-      for (int e = 0; e < 8; ++e) {
-        const float p = __builtin_amdgcn_exp2f(cur[q >> 1][8 * (q & 1) + e]);
-        if (!ONES) psum += p;
-        pf[q][e] = (bf16)p;
+    for (int sl = 0; sl < NSL; ++sl) {
+      if (sl < NQK) {
+        const int c = sl >> 1, kb = sl & 1;
+        nxt[kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fr[sl], qf[c],
+                                                          c == 0 ? f32x16{} : nxt[kb], 0, 0, 0);
+      } else {
+        const int q = (sl - NQK) / DT, dt = (sl - NQK) % DT;
+        o[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fr[sl], pf[q], o[dt], 0, 0, 0);
       }
-    if (!ONES) l_run += psum;
-    // key chunk outer, d tile inner: DT independent accumulation chains; V^T
-    // row 32dt + ql, keys 16q + 8hl .. +7
-    const char* vb = vst(ti % ST);
+      const int e0 = sl < NE ? (32 * sl + NE - 1) / NE : 32;
+      const int e1 = sl + 1 < NE ? (32 * (sl + 1) + NE - 1) / NE : 32;
 #pragma unroll
-    for (int q = 0; q < 4; ++q) {
+      for (int i = e0; i < e1; ++i) {
+        pe[i] = __builtin_amdgcn_exp2f(cur[i >> 4][i & 15]);
+        if (!ONES) psum += pe[i];
+        if ((i & 7) == 7)
 #pragma unroll
-      for (int dt = 0; dt < DT; ++dt) {
-        const int row = dt * 32 + ql;
-        const bf16x8 vf =
-            *(const bf16x8*)(vb + row * 128 + (((2 * q + hl) ^ ((row >> 1) & 7)) << 4));
-        o[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf, pf[q], o[dt], 0, 0, 0);
+          for (int e = 0; e < 8; ++e) pf[i >> 3][e] = (bf16)pe[(i & ~7) + e];
       }
+      if (sl + LA + 1 < NSL) fr[sl + LA + 1] = frag(sl + LA + 1);
+      __builtin_amdgcn_sched_barrier(0);
     }
+    if (!ONES) l_run += psum;
     lm_nxt = lane_max(nxt);
   };
 
@@ -505,6 +565,13 @@ static hipError_t launch_hd(bool bf16_io, int role, int heads, const AttnMap& ma
   const int tiles = map.tile_start[map.n] * heads;
   if (tiles == 0) return hipSuccess;
   if (bf16_io) {
+    // tile loads address K and V^T with byte offsets below 2^31
+    size_t k_rows = 0;
+    for (int s = 0; s < map.n; ++s)
+      k_rows = std::max(k_rows, (size_t)std::max(map.k_start[s] + map.k_len[s],
+                                                 map.k2_start[s] + map.k2_len[s]));
+    if ((size_t)2 * heads * HD * ldv > 0x7fffffff || (size_t)2 * (k_rows + 64) * ldk > 0x7fffffff)
+      return hipErrorInvalidValue;
     const float scale_log2 = 1.4426950408889634f / sqrtf((float)HD);
 #define T2I_ATT(NW_, ST_, R_)                                                                   \
   hipLaunchKernelGGL((attn_bf16_kernel<HD, NW_, ST_, R_>), dim3(tiles), dim3(NW_ * 64), 0, st, map, \
