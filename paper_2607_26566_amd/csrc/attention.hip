@@ -52,20 +52,24 @@ __device__ __forceinline__ int swap23(int r) {
 }
 
 // s_waitcnt vmcnt(N), lgkmcnt / expcnt untouched
+// (vmcnt is 6 bits: bits 3..0 and 15..14 of the immediate)
 template <int N>
 __device__ __forceinline__ void wait_vmcnt() {
-  static_assert(N >= 0 && N < 16, "vmcnt");
-  __builtin_amdgcn_s_waitcnt(N | (7 << 4) | (15 << 8));
+  static_assert(N >= 0 && N < 64, "vmcnt");
+  __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4) | (15 << 8));
 }
 
-// s_waitcnt vmcnt(n) for a wave-uniform n < 16 known only at run time.
+// s_waitcnt vmcnt(n) for a wave-uniform n < 32 known only at run time
+// (larger n wait for vmcnt(31), which is stricter).
 __device__ __forceinline__ void wait_vmcnt_dyn(int n) {
   switch (n) {
-#define T2I_W(N_) case N_: __builtin_amdgcn_s_waitcnt((N_) | (7 << 4) | (15 << 8)); break;
+#define T2I_W(N_) case N_: wait_vmcnt<N_>(); break;
     T2I_W(0) T2I_W(1) T2I_W(2) T2I_W(3) T2I_W(4) T2I_W(5) T2I_W(6) T2I_W(7)
-    T2I_W(8) T2I_W(9) T2I_W(10) T2I_W(11) T2I_W(12) T2I_W(13) T2I_W(14)
+    T2I_W(8) T2I_W(9) T2I_W(10) T2I_W(11) T2I_W(12) T2I_W(13) T2I_W(14) T2I_W(15)
+    T2I_W(16) T2I_W(17) T2I_W(18) T2I_W(19) T2I_W(20) T2I_W(21) T2I_W(22) T2I_W(23)
+    T2I_W(24) T2I_W(25) T2I_W(26) T2I_W(27) T2I_W(28) T2I_W(29) T2I_W(30)
 #undef T2I_W
-    default: __builtin_amdgcn_s_waitcnt((15) | (7 << 4) | (15 << 8)); break;
+    default: wait_vmcnt<31>(); break;
   }
 }
 
@@ -129,7 +133,6 @@ __global__ __launch_bounds__(NW * 64, 8 / NW) void attn_bf16_kernel(AttnMap map,
   constexpr int KRS = (CPR == 4 || CPR == 8 || CPR == 16) ? 16 / CPR : 0;
   constexpr int KSTAGE = BKV * PK;     // bytes
   constexpr int VSTAGE = HDO * 128;    // V^T rows of 64 keys
-  constexpr int NI = 2 * CPR;          // 1-KB load instructions per tile (K, then V^T)
   static_assert(HD % 8 == 0 && KSTAGE % 1024 == 0, "head dim");
   // the next tile's scores are computed one step ahead, so the ring needs a
   // stage for it besides the current tile's and the one being refilled
@@ -187,80 +190,89 @@ __global__ __launch_bounds__(NW * 64, 8 / NW) void attn_bf16_kernel(AttnMap map,
   };
 
   // Tile loads: HBM -> LDS directly (buffer_load_dwordx4 ... lds), instruction
-  // i of a tile writes bytes 1024i .. +1023 of the stage, lane l 16 bytes at
-  // 16l.
-  //   K (i < CPR): row r = key swap23(r), chunk slot swizzled; keys past the
-  //     sequence are clamped to its last key (their scores are masked);
-  //   V^T (i >= CPR): row d, 128 bytes = 64 keys, chunk slot c ^ ((d>>1)&7);
-  //     chunks wholly past the sequence are read from the tile's first chunk
-  //     (their probabilities are 0).
+  // c of a tensor's tile writes bytes 1024c .. +1023 of its part of the
+  // stage, lane l 16 bytes at 16l.
+  //   K: row r = key swap23(r), chunk slot swizzled; keys past the sequence
+  //     are clamped to its last key (their scores are masked);
+  //   V^T: row d, 128 bytes = 64 keys, chunk slot c ^ ((d>>1)&7); chunks
+  //     wholly past the sequence are read from the tile's first chunk (their
+  //     probabilities are 0).
   // Addresses: buffer resources based at K and V^T, the tile's position as
-  // the scalar offset and per-lane 32-bit byte offsets.  The buffer form of the LDS DMA, not
-  // the global one: the compiler counts an outstanding global-form DMA as an
-  // out-of-order LDS event and then drains every LDS fragment read with
-  // lgkmcnt(0), while the buffer form is tracked by vmcnt alone, so the reads
-  // of the main loop get exact waits.  The launcher keeps every offset below
-  // 2^31.
-  // Wave w issues instructions w, w+8, ...: n_w per tile.
-  constexpr int IPW = (NI + NW - 1) / NW;
-  int g_off[IPW], g_key[IPW], l_off[IPW];
-  uint32_t f_off[IPW];   // byte offset from the tile base (full tiles)
-  const int n_w = (NI - wave + NW - 1) / NW;
+  // the scalar offset and per-lane 32-bit byte offsets.  The buffer form of
+  // the LDS DMA, not the global one: the compiler counts an outstanding
+  // global-form DMA as an out-of-order LDS event and then drains every LDS
+  // fragment read with lgkmcnt(0), while the buffer form is tracked by vmcnt
+  // alone, so the reads of the main loop get exact waits.  The launcher keeps
+  // every offset below 2^31.
+  // Only waves 0 .. NWD-1 issue loads -- the first half of them K, the second
+  // half V^T, IPD instructions each -- so that the scalar work of a tile
+  // (one M0 update per instruction) is not repeated by every wave: the CU's
+  // scalar unit is shared by all its waves, which reach this point together.
+  // Head dimensions of 128 and more keep 8 issuing waves (4 instructions
+  // each), as the per-lane offsets of more instructions per wave would not
+  // fit in the loop's registers.
+  constexpr int NWD = NW < 4 ? NW : (CPR >= 16 ? NW : 4), WPT = NWD / 2;
+  constexpr int IPD = (CPR + WPT - 1) / WPT;
+  const bool dma_wave = wave < NWD, is_v = wave >= WPT;
+  const int c_first = (wave % WPT) * IPD;
+  const int n_w = dma_wave ? min(IPD, CPR - c_first) : 0;   // loads per tile
+  auto k_lane = [&](int c, int& key, int& col) {   // K instruction c: key row, column
+    const int o = c * 1024 + lane * 16;
+    const int r = o / PK, slot = (o - r * PK) / 16;
+    key = swap23(r);
+    col = hh * HD + 8 * (KRS ? slot ^ ((r / KRS) & (CPR - 1)) : slot);
+  };
+  auto v_lane = [&](int c, int& row, int& key) {   // V^T instruction c: row, key
+    const int o = c * 1024 + lane * 16, d = o / 128;
+    row = hh * HD + d;
+    key = 8 * ((lane & 7) ^ ((d >> 1) & 7));
+  };
+  uint32_t f_off[IPD];   // byte offset from the tile base (full tiles)
 #pragma unroll
-  for (int ii = 0; ii < IPW; ++ii) {
-    const int i = wave + NW * ii;
-    g_off[ii] = g_key[ii] = l_off[ii] = 0;
-    f_off[ii] = 0;
-    if (i < CPR) {
-      const int o = i * 1024 + lane * 16;
-      const int r = o / PK, slot = (o - r * PK) / 16;
-      const int c = KRS ? slot ^ ((r / KRS) & (CPR - 1)) : slot;
-      g_key[ii] = swap23(r);
-      g_off[ii] = hh * HD + c * 8;
-      l_off[ii] = i * 1024;                      // wave-uniform base; +16 per lane implied
-      f_off[ii] = 2u * (uint32_t)(g_key[ii] * ldk + g_off[ii]);
-    } else if (i < NI) {
-      const int o = (i - CPR) * 1024 + lane * 16;
-      const int d = o / 128, c = (lane & 7) ^ ((d >> 1) & 7);
-      g_key[ii] = c * 8;                         // key offset of the chunk
-      g_off[ii] = hh * HD + d;                   // V^T row
-      l_off[ii] = KSTAGE + (i - CPR) * 1024;
-      f_off[ii] = 2u * (uint32_t)(g_off[ii] * ldvt + g_key[ii]);
+  for (int cc = 0; cc < IPD; ++cc) {
+    const int c = min(c_first + cc, CPR - 1);
+    int a, b;
+    if (is_v) {
+      v_lane(c, a, b);
+      f_off[cc] = 2u * (uint32_t)(a * ldvt + b);
+    } else {
+      k_lane(c, a, b);
+      f_off[cc] = 2u * (uint32_t)(a * ldk + b);
     }
   }
   // the launcher keeps every byte offset below 2^31, the extent given here
-  const __amdgpu_buffer_rsrc_t rk =
-      __builtin_amdgcn_make_buffer_rsrc((void*)K, 0, 0x7fffffff, kBufWord3);
-  const __amdgpu_buffer_rsrc_t rv =
-      __builtin_amdgcn_make_buffer_rsrc((void*)Vt, 0, 0x7fffffff, kBufWord3);
+  const __amdgpu_buffer_rsrc_t rsrc = __builtin_amdgcn_make_buffer_rsrc(
+      is_v ? (void*)Vt : (void*)K, 0, 0x7fffffff, kBufWord3);
   auto issue = [&](int ti) {
+    if (!dma_wave) return;
     const int kv0 = tile_kv0(ti);
-    const int sk = kv0 * (2 * ldk), sv = 2 * kv0;   // the tile's byte offsets
-    char* base = kst(ti % ST);
-    auto load = [&](int ii, int i, uint32_t off) {
+    const int soff = is_v ? 2 * kv0 : kv0 * (2 * ldk);   // the tile's byte offset
+    char* lb = kst(ti % ST) + (is_v ? KSTAGE : 0) + c_first * 1024;
+    auto load = [&](int cc, uint32_t off) {
       __builtin_amdgcn_raw_ptr_buffer_load_lds(
-          i < CPR ? rk : rv, (__attribute__((address_space(3))) void*)(base + l_off[ii]), 16,
-          off, i < CPR ? sk : sv, 0, 0);
+          rsrc, (__attribute__((address_space(3))) void*)(lb + cc * 1024), 16, off, soff, 0, 0);
     };
     if (tile_full(ti)) {
 #pragma unroll
-      for (int ii = 0; ii < IPW; ++ii) {
-        const int i = wave + NW * ii;
-        if (i >= NI) break;
-        load(ii, i, f_off[ii]);
+      for (int cc = 0; cc < IPD; ++cc) {
+        if (cc >= n_w) break;
+        load(cc, f_off[cc]);
       }
       return;
     }
     // ragged tile: clamp keys past the sequence
     const int k_end = tile_end(ti);
 #pragma unroll
-    for (int ii = 0; ii < IPW; ++ii) {
-      const int i = wave + NW * ii;
-      if (i >= NI) break;
-      if (i < CPR)
-        load(ii, i, 2u * (uint32_t)((min(kv0 + g_key[ii], k_end - 1) - kv0) * ldk + g_off[ii]));
-      else
-        load(ii, i, 2u * (uint32_t)(g_off[ii] * ldvt + (kv0 + g_key[ii] < k_end ? g_key[ii] : 0)));
+    for (int cc = 0; cc < IPD; ++cc) {
+      if (cc >= n_w) break;
+      int a, b;
+      if (is_v) {
+        v_lane(c_first + cc, a, b);
+        load(cc, 2u * (uint32_t)(a * ldvt + (kv0 + b < k_end ? b : 0)));
+      } else {
+        k_lane(c_first + cc, a, b);
+        load(cc, 2u * (uint32_t)((min(kv0 + a, k_end - 1) - kv0) * ldk + b));
+      }
     }
   };
   // K fragment (A operand) of key block kb, 16-wide d chunk c for this lane:
@@ -321,18 +333,33 @@ __global__ __launch_bounds__(NW * 64, 8 / NW) void attn_bf16_kernel(AttnMap map,
 
   // one tile: S^T of tile ti is in cur with lane maximum lm; the next tile's
   // S^T and lane maximum go to nxt / lm_nxt
-  auto step = [&](int ti, f32x16 (&cur)[2], float& lm, f32x16 (&nxt)[2], float& lm_nxt) {
-    // tile ti+1 landed (the ST-3 tiles after it may still be in flight), for
-    // every wave; immediate counts in the steady state
-    const int young = min(ST - 3, nt - 2 - ti);
-    if (young == ST - 3) {
-      if (NI % NW == 0 || n_w == IPW) wait_vmcnt<(ST - 3) * IPW>();
-      else wait_vmcnt<(ST - 3) * (IPW - 1)>();
-    } else {
-      wait_vmcnt_dyn(young > 0 ? young * n_w : 0);
+  //
+  // With ST >= 5 stages the workgroup synchronises once per two tiles (at
+  // even ti): tiles ti+1 and ti+2 (read by the two steps' next-tile scores)
+  // have landed, the ST-5 after them may still be in flight, and tiles
+  // ti+ST-2 and ti+ST-1 go into the stages of ti-2 and ti-1, which every
+  // wave has finished with.  With fewer stages it synchronises every tile:
+  // tile ti+1 landed, ST-3 in flight, tile ti+ST-1 into the stage of ti-1.
+  constexpr bool PAIR = ST >= 5;
+  constexpr int YOUNG = PAIR ? ST - 5 : ST - 3;   // tiles left in flight
+  static_assert((YOUNG + 2) * IPD < 64, "vmcnt");
+  auto step = [&](int ti, f32x16 (&cur)[2], float& lm, f32x16 (&nxt)[2], float& lm_nxt,
+                  bool sync) {
+    if (!PAIR || sync) {
+      // immediate counts in the steady state
+      const int young = min(YOUNG, nt - (PAIR ? 3 : 2) - ti);
+      if (!dma_wave) {
+      } else if (young == YOUNG && n_w == IPD) {
+        wait_vmcnt<YOUNG * IPD>();
+      } else if (young == YOUNG && n_w == IPD - 1) {
+        wait_vmcnt<YOUNG * (IPD - 1)>();
+      } else {
+        wait_vmcnt_dyn(young > 0 ? young * n_w : 0);
+      }
+      attn_barrier();
+      if (PAIR && ti + ST - 2 < nt) issue(ti + ST - 2);
+      if (ti + ST - 1 < nt) issue(ti + ST - 1);
     }
-    attn_barrier();
-    if (ti + ST - 1 < nt) issue(ti + ST - 1);     // into the stage of tile ti-1
     if (!tile_full(ti)) {
       const int kv0 = tile_kv0(ti), k_end = tile_end(ti);
       // ragged tile: mask the scores past the sequence.  V^T chunks wholly
@@ -373,72 +400,102 @@ __global__ __launch_bounds__(NW * 64, 8 / NW) void attn_bf16_kernel(AttnMap map,
       m_ref = m_new;
       if (hl == BH) qf[BC][0] = (bf16)(-m_new);
     }
-    // Straight-line part in a fixed issue order.  Slot s issues one MFMA --
-    // the next tile's S^T for s < NQK (chunk s/2, key block s%2), else P V
-    // for (key chunk, d tile) -- then its share of this tile's exponentials
-    // and the LDS fragment read LA slots ahead.  A scheduling barrier between
-    // slots keeps the exponentials spread over the MFMAs instead of bunched
-    // (the compiler otherwise clusters them).  P chunk q is complete before
-    // the first P V MFMA that uses it.  For the last tile the "next" scores
-    // come from a stale stage and are never used.
-    constexpr int NQK = 2 * DC, NPV = 4 * DT, NSL = NQK + NPV, LA = 3;
-    constexpr int NE = NQK + 3 * DT;   // slots carrying exponentials
-    const int stn = (ti + 1) % ST;
-    const char* vb = vst(ti % ST);
-    // V^T row 32dt + ql, keys 16q + 8hl .. +7
-    auto frag = [&](int sl) {
-      if (sl < NQK) return kfrag(stn, sl & 1, sl >> 1);
-      const int q = (sl - NQK) / DT, dt = (sl - NQK) % DT, row = dt * 32 + ql;
-      return *(const bf16x8*)(vb + row * 128 + (((2 * q + hl) ^ ((row >> 1) & 7)) << 4));
-    };
-    bf16x8 fr[NSL];
-    float pe[32];     // exponential i = P chunk i/8, element i%8
-    bf16x8 pf[4];
-    float psum = 0.f;
+    if constexpr (DC <= 5) {
+      // Straight-line part in a fixed issue order.  Slot s issues one MFMA --
+      // the next tile's S^T for s < NQK (chunk s/2, key block s%2), else P V
+      // for (key chunk, d tile) -- then its share of this tile's exponentials
+      // and the LDS fragment read LA slots ahead.  A scheduling barrier between
+      // slots keeps the exponentials spread over the MFMAs instead of bunched
+      // (the compiler otherwise clusters them).  P chunk q is complete before
+      // the first P V MFMA that uses it.  For the last tile the "next" scores
+      // come from a stale stage and are never used.
+      constexpr int NQK = 2 * DC, NPV = 4 * DT, NSL = NQK + NPV, LA = 3;
+      constexpr int NE = NQK + 3 * DT;   // slots carrying exponentials
+      const int stn = (ti + 1) % ST;
+      const char* vb = vst(ti % ST);
+      // V^T row 32dt + ql, keys 16q + 8hl .. +7
+      auto frag = [&](int sl) {
+        if (sl < NQK) return kfrag(stn, sl & 1, sl >> 1);
+        const int q = (sl - NQK) / DT, dt = (sl - NQK) % DT, row = dt * 32 + ql;
+        return *(const bf16x8*)(vb + row * 128 + (((2 * q + hl) ^ ((row >> 1) & 7)) << 4));
+      };
+      bf16x8 fr[NSL];
+      float pe[32];     // exponential i = P chunk i/8, element i%8
+      bf16x8 pf[4];
+      float psum = 0.f;
 #pragma unroll
-    for (int sl = 0; sl <= LA; ++sl) fr[sl] = frag(sl);
-    __builtin_amdgcn_sched_barrier(0);
-#pragma unroll
-    for (int sl = 0; sl < NSL; ++sl) {
-      if (sl < NQK) {
-        const int c = sl >> 1, kb = sl & 1;
-        nxt[kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fr[sl], qf[c],
-                                                          c == 0 ? f32x16{} : nxt[kb], 0, 0, 0);
-      } else {
-        const int q = (sl - NQK) / DT, dt = (sl - NQK) % DT;
-        o[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fr[sl], pf[q], o[dt], 0, 0, 0);
-      }
-      const int e0 = sl < NE ? (32 * sl + NE - 1) / NE : 32;
-      const int e1 = sl + 1 < NE ? (32 * (sl + 1) + NE - 1) / NE : 32;
-#pragma unroll
-      for (int i = e0; i < e1; ++i) {
-        pe[i] = __builtin_amdgcn_exp2f(cur[i >> 4][i & 15]);
-        if (!ONES) psum += pe[i];
-        if ((i & 7) == 7)
-#pragma unroll
-          for (int e = 0; e < 8; ++e) pf[i >> 3][e] = (bf16)pe[(i & ~7) + e];
-      }
-      if (sl + LA + 1 < NSL) fr[sl + LA + 1] = frag(sl + LA + 1);
+      for (int sl = 0; sl <= LA; ++sl) fr[sl] = frag(sl);
       __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+      for (int sl = 0; sl < NSL; ++sl) {
+        if (sl < NQK) {
+          const int c = sl >> 1, kb = sl & 1;
+          nxt[kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fr[sl], qf[c],
+                                                            c == 0 ? f32x16{} : nxt[kb], 0, 0, 0);
+        } else {
+          const int q = (sl - NQK) / DT, dt = (sl - NQK) % DT;
+          o[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fr[sl], pf[q], o[dt], 0, 0, 0);
+        }
+        const int e0 = sl < NE ? (32 * sl + NE - 1) / NE : 32;
+        const int e1 = sl + 1 < NE ? (32 * (sl + 1) + NE - 1) / NE : 32;
+#pragma unroll
+        for (int i = e0; i < e1; ++i) {
+          pe[i] = __builtin_amdgcn_exp2f(cur[i >> 4][i & 15]);
+          if (!ONES) psum += pe[i];
+          if ((i & 7) == 7)
+#pragma unroll
+            for (int e = 0; e < 8; ++e) pf[i >> 3][e] = (bf16)pe[(i & ~7) + e];
+        }
+        if (sl + LA + 1 < NSL) fr[sl + LA + 1] = frag(sl + LA + 1);
+        __builtin_amdgcn_sched_barrier(0);
+      }
+      if (!ONES) l_run += psum;
+    } else {
+      // larger head dimensions: the compiler's schedule (the fixed order
+      // needs more registers than the loop has there) -- the next tile's
+      // scores, then this tile's exponentials and P V
+      qk(ti + 1, nxt);
+      bf16x8 pf[4];
+      float psum = 0.f;
+#pragma unroll
+      for (int q = 0; q < 4; ++q)
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+          const float p = __builtin_amdgcn_exp2f(cur[q >> 1][8 * (q & 1) + e]);
+          if (!ONES) psum += p;
+          pf[q][e] = (bf16)p;
+        }
+      if (!ONES) l_run += psum;
+      const char* vb = vst(ti % ST);
+#pragma unroll
+      for (int q = 0; q < 4; ++q)
+#pragma unroll
+        for (int dt = 0; dt < DT; ++dt) {
+          const int row = dt * 32 + ql;
+          const bf16x8 vf =
+              *(const bf16x8*)(vb + row * 128 + (((2 * q + hl) ^ ((row >> 1) & 7)) << 4));
+          o[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf, pf[q], o[dt], 0, 0, 0);
+        }
     }
-    if (!ONES) l_run += psum;
     lm_nxt = lane_max(nxt);
   };
 
-  // prologue: tiles 0 .. ST-2 in flight, tile 0's scores
+  // prologue: the tiles before the first step's loads in flight, tile 0's
+  // scores
+  constexpr int PRE = PAIR ? ST - 2 : ST - 1;
 #pragma unroll
-  for (int ti = 0; ti < ST - 1; ++ti)
+  for (int ti = 0; ti < PRE; ++ti)
     if (ti < nt) issue(ti);
   scale_q();
-  wait_vmcnt_dyn(n_w * (min(nt, ST - 1) - 1));
+  wait_vmcnt_dyn(n_w * (min(nt, PRE) - 1));
   attn_barrier();
   f32x16 sa[2], sb[2];
   float la, lb;
   qk(0, sa);
   la = lane_max(sa);
   for (int ti = 0; ti < nt; ti += 2) {
-    step(ti, sa, la, sb, lb);
-    if (ti + 1 < nt) step(ti + 1, sb, lb, sa, la);
+    step(ti, sa, la, sb, lb, true);
+    if (ti + 1 < nt) step(ti + 1, sb, lb, sa, la, false);
   }
 
   float l;
@@ -529,7 +586,14 @@ __global__ __launch_bounds__(64) void attn_f32_kernel(AttnMap map, int heads,
 // compute.  Self / joint attention launches that would have fewer
 // workgroups than CUs (short sequences, few heads) halve the workgroup, down
 // to 2 waves.  fp32: 64 queries.
-constexpr int kAttnWaves = 8, kAttnStages = 4;
+constexpr int kAttnWaves = 8;
+// 8-wave workgroups: 5 stages (one barrier per two key tiles) up to head
+// dimension 72; 4 above, where the loop's registers leave no room for the
+// longer pipeline
+template <int HD>
+constexpr int attn_stages() {
+  return HD <= 72 ? 5 : 4;
+}
 constexpr int kCrossWaves = 4, kCrossStages = 3;
 void attention_tiles(AttnMap& m, bool bf16_io, int heads, int role) {
   auto fill = [&](int bq) {
@@ -582,7 +646,7 @@ static hipError_t launch_hd(bool bf16_io, int role, int heads, const AttnMap& ma
       if (map.waves == kCrossWaves) T2I_ATT(kCrossWaves, kCrossStages, 1);
       else return hipErrorInvalidValue;
     } else {
-      if (map.waves == kAttnWaves) T2I_ATT(kAttnWaves, kAttnStages, 0);
+      if (map.waves == kAttnWaves) T2I_ATT(kAttnWaves, attn_stages<HD>(), 0);
       else if (map.waves == 4) T2I_ATT(4, 3, 0);
       else if (map.waves == 2) T2I_ATT(2, 3, 0);
       else return hipErrorInvalidValue;
