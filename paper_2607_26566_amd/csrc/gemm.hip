@@ -334,7 +334,9 @@ hipError_t launch_gemm_bf16(const bf16* A, int lda, const bf16* W, int ldw, cons
   // register-staged tiles (the faster ones at M ~ 1000 measured), with K
   // split over several workgroups when there are too few tiles to fill the
   // chip (e.g. the 512-row text stream against K = 3072 or 12288).
-  if (M >= 2048 && (N % 144 == 0 || N % 128 == 0) && kind != EPI_SILU)
+  // (the direct-load kernels address each operand with 32-bit byte offsets)
+  const bool dma_fits = (size_t)2 * M * lda < 0x7fffffff && (size_t)2 * N * ldw < 0x7fffffff;
+  if (M >= 2048 && (N % 144 == 0 || N % 128 == 0) && kind != EPI_SILU && dma_fits)
     return launch_gemm_dma(A, lda, W, ldw, bias, M, N, K, kind, epi, vec_ok, st);
   const int splits = splitk_ws ? splitk_factor(N, K) : 1;
   if (splits > 1 && (size_t)splits * M * N <= splitk_floats && kind != EPI_SILU) {

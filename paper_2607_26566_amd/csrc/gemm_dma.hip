@@ -1,4 +1,4 @@
-// bf16 MFMA GEMM fed by direct HBM->LDS loads (gfx950 global_load_lds_dwordx4).
+// bf16 MFMA GEMM fed by direct HBM->LDS loads (gfx950 buffer_load_dwordx4 ... lds).
 //
 // y = A W^T + b for the DiT's projections at large M.  A workgroup owns a
 // BM x BN output tile; its waves (WGM x WGN) each own a (BM/WGM) x (BN/WGN)
@@ -20,7 +20,13 @@
 //     into the stage everybody finished with, and runs its MFMAs;
 //   * every wave issues the same number of load instructions per tile
 //     (waves with fewer blocks repeat their last one, which rewrites identical
-//     bytes), so the vmcnt thresholds are compile-time constants.
+//     bytes), so the vmcnt thresholds are compile-time constants;
+//   * loads address A and W through buffer resources (per-lane 32-bit byte
+//     offsets, the K position as scalar offset; the caller keeps both
+//     operands below 2^31 bytes).  The buffer form rather than the global
+//     one because the compiler tracks it by vmcnt alone: an outstanding
+//     global-form LDS load counts as an out-of-order LDS event, after which
+//     every fragment read is drained with lgkmcnt(0) instead of counted.
 //
 // The epilogue is the one of gemm.hip: C^T fragments (operands swapped) give a
 // lane four consecutive output columns of one row, stored with one 8-byte
@@ -44,11 +50,21 @@ __device__ __forceinline__ void wait_vmcnt() {
   __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4) | (15 << 8));
 }
 
+// one 16-byte-per-lane buffer load into LDS at the wave-uniform address lds
+template <int AUX>
+__device__ __forceinline__ void dma16(__amdgpu_buffer_rsrc_t r, char* lds, uint32_t voff, int soff) {
+  __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (__attribute__((address_space(3))) void*)lds, 16,
+                                           voff, soff, 0, AUX);
+}
+
 __device__ __forceinline__ void block_barrier() {
   // this wave's LDS reads are complete (a stage may be refilled right after
   // the barrier), then a plain s_barrier: no release fence, which would wait
-  // for every outstanding global load, and a compiler barrier for memory ops
-  asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
+  // for every outstanding global load, and a compiler barrier for memory ops.
+  // The wait is the builtin, so that the compiler's wait-count tracking knows
+  // nothing is pending after it.
+  __builtin_amdgcn_s_waitcnt(0xC07F);   // lgkmcnt(0), vmcnt / expcnt untouched
+  asm volatile("s_barrier" ::: "memory");
 }
 
 template <int KIND>
@@ -97,6 +113,7 @@ __global__ __launch_bounds__(64 * WGM * WGN, 1) void gemm_dma_kernel(
   constexpr bool CT = KIND != EPI_SPLIT_VT;
   static_assert(BM % 8 == 0 && BN % 8 == 0 && WM % 16 == 0 && WN % 16 == 0, "tile shape");
   static_assert(ST >= 2 && ST <= 4, "stages");
+  static_assert(ABLK % NW == 0, "A / W blocks split evenly over the load rounds");
   __shared__ __attribute__((aligned(1024))) bf16 smem[ST * STAGE];
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -111,8 +128,10 @@ __global__ __launch_bounds__(64 * WGM * WGN, 1) void gemm_dma_kernel(
   const int in_grp = tile - grp * per_group;
   const int m0 = (first + in_grp % rows_in) * BM, n0 = (in_grp / rows_in) * BN;
 
-  // this lane's source of every block it loads (k offset added per tile)
-  const bf16* src[BPW];
+  // this lane's byte offset of every block it loads, from A or W (the k
+  // position is added per tile as the scalar offset); load round i reads A
+  // while i < ABLK / NW
+  uint32_t src[BPW];
   int dst[BPW];   // byte offset of the block inside a stage (wave-uniform)
 #pragma unroll
   for (int i = 0; i < BPW; ++i) {
@@ -120,18 +139,19 @@ __global__ __launch_bounds__(64 * WGM * WGN, 1) void gemm_dma_kernel(
     if (b >= TBLK) b -= NW;               // repeat this wave's previous block
     const int lr = (b < ABLK ? b : b - ABLK) * 8 + (lane >> 3);   // row within A or W tile
     const int c = (lane & 7) ^ ((lr >> 1) & 7);                   // logical chunk of this slot
-    src[i] = b < ABLK ? A + (size_t)min(m0 + lr, M - 1) * lda + c * 8
-                      : W + (size_t)min(n0 + lr, N - 1) * ldw + c * 8;
+    src[i] = 2u * (uint32_t)(i < ABLK / NW ? min(m0 + lr, M - 1) * lda + c * 8
+                                           : min(n0 + lr, N - 1) * ldw + c * 8);
     dst[i] = b * 1024;
   }
+  const __amdgpu_buffer_rsrc_t ra =
+      __builtin_amdgcn_make_buffer_rsrc((void*)A, 0, 0x7fffffff, 0x00020000);
+  const __amdgpu_buffer_rsrc_t rw =
+      __builtin_amdgcn_make_buffer_rsrc((void*)W, 0, 0x7fffffff, 0x00020000);
   auto issue = [&](int t, int stage) {
-    const int k0 = t * 64;
+    const int kb = t * 128;   // byte offset of the tile's 64 k values
 #pragma unroll
     for (int i = 0; i < BPW; ++i)
-      __builtin_amdgcn_global_load_lds(
-          (__attribute__((address_space(1))) void*)(src[i] + k0),
-          (__attribute__((address_space(3))) void*)((char*)smem + stage * STAGE * 2 + dst[i]),
-          16, 0, AUX);
+      dma16<AUX>(i < ABLK / NW ? ra : rw, (char*)smem + stage * STAGE * 2 + dst[i], src[i], kb);
   };
 
   f32x4 acc[TM][TN];
