@@ -68,7 +68,8 @@ __device__ __forceinline__ void block_barrier() {
 }
 
 template <int KIND>
-__device__ __forceinline__ void dma_epi4(const Epi& e, int m, int nb, const float v[4]) {
+__device__ __forceinline__ void dma_epi4(const Epi& e, int m, int nb, const float v[4],
+                                         const float4* xpre = nullptr) {
   if (KIND == EPI_STORE_F32) {
     *(float4*)((float*)e.out + (size_t)m * e.ldo + nb) = float4{v[0], v[1], v[2], v[3]};
   } else if (KIND == EPI_STORE || KIND == EPI_GELU || KIND == EPI_SILU) {
@@ -86,7 +87,7 @@ __device__ __forceinline__ void dma_epi4(const Epi& e, int m, int nb, const floa
     if (KIND == EPI_RESID_GATED)
       g4 = *(const float4*)(e.gate + (size_t)e.map.modrow[seq_of_row(e.map, m)] * e.ld_gate + nb);
     float4* xp = (float4*)(e.x + (size_t)m * e.ldx + nb);
-    float4 x4 = *xp;
+    float4 x4 = xpre ? *xpre : *xp;
     x4.x += g4.x * v[0];
     x4.y += g4.y * v[1];
     x4.z += g4.z * v[2];
@@ -184,6 +185,28 @@ __global__ __launch_bounds__(64 * WGM * WGN, 1) void gemm_dma_kernel(
     }
   };
 
+  // Gated residual updates with small per-wave tiles read this lane's fp32
+  // residual values before the main loop: all workgroups of such a launch
+  // reach the epilogue together, and its HBM reads would otherwise come after
+  // the loop instead of under it.  Issued before the first tile loads, so the
+  // vmcnt thresholds below (which count younger loads) stay exact.  (Measured
+  // faster for the gated updates -- out-projection, fc2 -- and slightly
+  // slower for the plain one after cross-attention, which keeps the old
+  // order.)
+  constexpr bool PREX = CT && KIND == EPI_RESID_GATED && TM * TN <= 18;
+  float4 xpre[PREX ? TM : 1][PREX ? TN : 1];
+  if constexpr (PREX) {
+#pragma unroll
+    for (int i = 0; i < TM; ++i)
+#pragma unroll
+      for (int j = 0; j < TN; ++j) {
+        const int m = m0 + wm * WM + i * 16 + fr, nb = n0 + wn * WN + j * 16 + g * 4;
+        xpre[i][j] = float4{0.f, 0.f, 0.f, 0.f};
+        if (m < M && vec_ok && nb + 3 < N)
+          xpre[i][j] = *(const float4*)(epi.x + (size_t)m * epi.ldx + nb);
+      }
+  }
+
   const int KT = K / 64;
 #pragma unroll
   for (int s = 0; s < ST - 1; ++s)
@@ -216,7 +239,8 @@ __global__ __launch_bounds__(64 * WGM * WGN, 1) void gemm_dma_kernel(
           const bf16x4 b4 = *(const bf16x4*)(bias + nb);
           const float v[4] = {acc[i][j][0] + (float)b4[0], acc[i][j][1] + (float)b4[1],
                               acc[i][j][2] + (float)b4[2], acc[i][j][3] + (float)b4[3]};
-          dma_epi4<KIND>(epi, m, nb, v);
+          if constexpr (PREX) dma_epi4<KIND>(epi, m, nb, v, &xpre[i][j]);
+          else dma_epi4<KIND>(epi, m, nb, v);
         } else {
 #pragma unroll
           for (int r = 0; r < 4; ++r)
