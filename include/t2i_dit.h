@@ -88,7 +88,10 @@ typedef struct t2i_dit_config {
   int32_t text_tokens;       /* tokens per prompt (>= 1) */
   int32_t freq_dim;          /* sinusoidal timestep width (even) */
   int32_t max_tokens;        /* most image tokens one call carries, summed over
-                                requests and guidance branches */
+                                requests and guidance branches; bf16 models
+                                need 4*(rows+64)*hidden < 2^31, rows being
+                                max_tokens plus the MMDiT text rows (the
+                                attention's 32-bit byte offsets) */
   int32_t max_requests;      /* most requests per call, <= T2I_MAX_REQ */
   int32_t max_steps;         /* most steps of one t2i_dit_sample call */
   float ln_eps;              /* LayerNorm epsilon */

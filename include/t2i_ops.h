@@ -57,7 +57,10 @@ t2i_status t2i_op_linear(int32_t dtype, int32_t epilogue, int32_t M, int32_t N,
  *   fp32: V is row-major like K, row stride ldv.
  *   bf16: V is given transposed, V^T [heads*head_dim][ldv] (the key index is
  *         contiguous), the layout the fused qkv projection writes; every key
- *         segment must start at a multiple of 8 and end within ldv.
+ *         segment must start at a multiple of 8 and end within ldv.  The
+ *         kernel addresses K and V^T with 32-bit byte offsets:
+ *         2*heads*head_dim*ldv and 2*(last key row + 64)*ldk must stay below
+ *         2^31, else T2I_ERR_SHAPE.
  */
 t2i_status t2i_op_attention(int32_t dtype, int32_t heads, int32_t head_dim,
                             int32_t n_seq, const int32_t* q_start,

@@ -132,6 +132,14 @@ const char* check_config(const t2i_dit_config* c) {
   if (!(c->ln_eps > 0.f) || !(c->t_scale > 0.f)) return "bad ln_eps/t_scale";
   if (c->arch == T2I_ARCH_MMDIT && c->dtype != T2I_BF16) return "MMDiT runs in bf16 only";
   if (c->dtype == T2I_BF16 && c->text_tokens % 8) return "bf16 models need text_tokens % 8 == 0";
+  if (c->dtype == T2I_BF16) {
+    // bf16 attention addresses q|k and V^T with byte offsets below 2^31
+    const size_t rows = (size_t)c->max_tokens +
+                        (c->arch == T2I_ARCH_MMDIT ? (size_t)2 * c->max_requests * c->text_tokens : 0);
+    if ((size_t)4 * (rows + 64) * c->hidden > 0x7fffffff ||
+        (size_t)2 * c->hidden * ((rows + 63) / 64 * 64) > 0x7fffffff)
+      return "max_tokens too large for the bf16 attention's 2 GiB operand limit";
+  }
   return nullptr;
 }
 
@@ -1345,6 +1353,15 @@ t2i_status t2i_op_attention(int32_t dtype, int32_t heads, int32_t head_dim, int3
     m.k_len[s] = k_len[s];
     m.k2_start[s] = s2;
     m.k2_len[s] = n2;
+  }
+  if (dtype == T2I_BF16) {
+    long k_rows = 0;
+    for (int s = 0; s < n_seq; ++s)
+      k_rows = std::max({k_rows, (long)k_start[s] + k_len[s],
+                         k2_start ? (long)k2_start[s] + k2_len[s] : 0L});
+    if ((size_t)2 * heads * head_dim * ldv > 0x7fffffff ||
+        (size_t)2 * (k_rows + 64) * ldk > 0x7fffffff)
+      return ops_fail(T2I_ERR_SHAPE, "bf16 attention operands exceed 2 GiB of addressing");
   }
   attention_tiles(m, dtype == T2I_BF16, heads, 0);
   hipError_t err = launch_attention(dtype == T2I_BF16, 0, heads, head_dim, m, q, ldq, k, ldk, v, ldv,

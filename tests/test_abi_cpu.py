@@ -75,7 +75,9 @@ def test_invalid_configs_are_rejected():
     lib = t2i.load()
     w = synth.workload("dit512")
     for field, bad in [("hidden", 100), ("heads", 7), ("head_dim", 40), ("max_requests", 99),
-                       ("dtype", 5), ("patch", 0), ("text_tokens", 0)]:
+                       ("dtype", 5), ("patch", 0), ("text_tokens", 0),
+                       # bf16 attention operands past 2^31 bytes of addressing
+                       ("max_tokens", 1 << 19)]:
         cfg = t2i.Config.from_shape(w)
         setattr(cfg.c, field, bad)
         assert lib.t2i_dit_weight_count(cfg.ref()) == 0, field
@@ -217,6 +219,11 @@ def test_op_argument_errors():
     k2 = (C.c_int32 * 1)(4)
     assert lib.t2i_op_attention(1, 2, 72, 1, qs, ql, qs, ql, k2, ql, 0x1000, 144, 0x2000,
                                 144, 0x3000, 144, 0x4000, 144, None) == 2
+    # V^T beyond 2^31 bytes of 32-bit offsets (2 heads x 72 rows x ldv x 2 B)
+    big = ((1 << 31) // (2 * 2 * 72) + 8) // 8 * 8
+    assert lib.t2i_op_attention(1, 2, 72, 1, qs, ql, qs, ql, None, None, 0x1000, 144, 0x2000,
+                                144, 0x3000, big, 0x4000, 144, None) == 2
+    assert b"2 GiB" in lib.t2i_ops_last_error()
 
 
 @pytest.mark.parametrize("name", ["dit1024_cfg", "mmdit1024", "tiny_f32"])
