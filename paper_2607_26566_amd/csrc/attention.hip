@@ -3,9 +3,11 @@
 //
 // attn_bf16_kernel: flash-style, one workgroup = 8 waves = 256 queries of one
 // head of one sequence; each wave owns 32 queries.  Keys and values stream
-// through a 4-stage LDS ring, 64 keys per tile, filled by direct HBM->LDS
-// loads three tiles ahead.  Everything is arranged so that a lane always holds
-// data of ONE query:
+// through an LDS ring, 64 keys per tile, filled by direct HBM->LDS buffer
+// loads that four of the waves issue several tiles ahead (5 stages and one
+// barrier per two tiles up to head dimension 72; 4 stages above; 3 stages in
+// the 2- and 4-wave workgroups of small launches and cross-attention).
+// Everything is arranged so that a lane always holds data of ONE query:
 //   * scores are computed transposed, S^T = K Q^T, with
 //     v_mfma_f32_32x32x16_bf16 (A = K fragment from LDS, B = the query's Q
 //     fragment, kept in registers for the whole loop): lane l gets query
@@ -21,7 +23,8 @@
 //   * row sums come from a ones row of V^T where the head dimension has
 //     padding (72 -> 96), else from a per-lane sum combined once at the end;
 //   * the next tile's scores are issued before this tile's exponentials, so
-//     the two overlap.
+//     the two overlap -- up to head dimension 72 in a fixed slot order that
+//     spreads the exponentials over the MFMAs.
 //
 // attn_f32_kernel: plain fp32 online softmax, one thread per query, for the
 // fp32 model.
@@ -580,7 +583,7 @@ __global__ __launch_bounds__(64) void attn_f32_kernel(AttnMap map, int heads,
   }
 }
 
-// bf16: 8 waves x 32 queries per workgroup, 4 stages.  Cross-attention to
+// bf16: 8 waves x 32 queries per workgroup (stages: attn_stages).  Cross-attention to
 // the text (two key tiles per query tile): 4 waves x 32 queries and 3 stages,
 // so that two workgroups share a CU and one's loads overlap the other's
 // compute.  Self / joint attention launches that would have fewer
