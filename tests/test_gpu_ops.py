@@ -222,6 +222,55 @@ def test_attention_bf16_full_size_sampled_rows():
     assert rel_l2(got[rows], ref) < 6e-3
 
 
+def _packed_keys(lengths):
+    """Key row starts (multiples of 8, as the bf16 kernel requires) for
+    sequences of the given key counts, and the total row count."""
+    starts, at = [], 0
+    for n in lengths:
+        starts.append(at)
+        at += (n + 7) // 8 * 8
+    return starts, max(at, 8)
+
+
+@pytest.mark.parametrize("d", [72, 128])
+def test_attention_bf16_eight_wave_pipeline_edges(d):
+    """16 heads x 16 sequences of 256 queries: 256 workgroups, so the 8-wave
+    kernel runs (5-stage ring with one barrier per two key tiles at d = 72,
+    4 stages at 128).  Key counts give 1 .. 8 key tiles, odd and even, full
+    and ragged; a second call splits every sequence's keys into two ragged
+    segments (the first segment's last tile ragged in the middle of the
+    sequence)."""
+    H, nq1 = 16, 256
+    lens = [1, 63, 64, 65, 128, 130, 192, 200, 256, 300, 320, 333, 384, 400, 448, 460]
+    starts, nk = _packed_keys(lens)
+    q = rnd(60 + d, (16 * nq1, H * d))
+    k, v = rnd(61 + d, (nk, H * d)), rnd(62 + d, (nk, H * d))
+    seqs = [(i * nq1, nq1, starts[i], lens[i]) for i in range(16)]
+    say(f"attention bf16 8-wave edges d={d}")
+    got = run_attention(_lib.T2I_BF16, H, d, seqs, q, k, v)
+    err = rel_l2(got, attention_ref(seqs, q, k, v, H))
+    say(f"  one segment rel_l2 {err:.2e}")
+    assert err < 6e-3
+    # two segments: n1 + n2 keys, n1 ragged
+    n1 = [1, 7, 40, 63, 65, 77, 100, 129, 1, 33, 64, 70, 130, 191, 200, 250]
+    n2 = [64, 1, 100, 63, 65, 200, 13, 129, 300, 64, 1, 256, 70, 8, 192, 210]
+    st1, tot1 = _packed_keys(n1)
+    st2, tot2 = _packed_keys(n2)
+    k = rnd(63 + d, (tot1 + tot2, H * d))
+    v = rnd(64 + d, (tot1 + tot2, H * d))
+    seqs = [(i * nq1, nq1, st1[i], n1[i]) for i in range(16)]
+    seg2 = [(tot1 + st2[i], n2[i]) for i in range(16)]
+    got = run_attention(_lib.T2I_BF16, H, d, seqs, q, k, v, seg2)
+    ref = np.zeros(q.shape)
+    for (q0, n_q, k0, n_k), (k20, n_k2) in zip(seqs, seg2):
+        idx = np.r_[np.arange(k0, k0 + n_k), np.arange(k20, k20 + n_k2)]
+        ref[q0:q0 + n_q] = dit.attention(q[q0:q0 + n_q].astype(np.float64),
+                                         k[idx].astype(np.float64), v[idx].astype(np.float64), H)
+    err = rel_l2(got, ref)
+    say(f"  two segments rel_l2 {err:.2e}")
+    assert err < 6e-3
+
+
 JOINT_CASES = [
     # (name, H, d, [(q_start, q_len, k_start, k_len)], [(k2_start, k2_len)], nq, nk)
     ("txt+img", 2, 128, [(0, 64, 0, 64), (64, 256, 0, 64)], [(64, 256), (64, 256)], 320, 320),
