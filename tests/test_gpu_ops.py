@@ -121,6 +121,34 @@ def test_linear_bf16_wide_sampled_rows(M, N, K, epi):
     assert err < (3e-3 if epi < 3 else 1e-4)
 
 
+def test_linear_bf16_operand_over_2gib():
+    """An A operand past 2^31 bytes (M = 2^20 + 37 rows of K = 1024): the
+    direct-load tiles address operands with 32-bit offsets, so the library
+    takes the register-staged tiles here; sampled rows, the last included,
+    against the oracle."""
+    lib = t2i.load()
+    M, N, K = (1 << 20) + 37, 144, 1024
+    assert 2 * M * K > 0x7fffffff
+    g = torch.Generator(device=DEV).manual_seed(70)
+    dA = torch.randn(M, K, generator=g, device=DEV).to(torch.bfloat16)
+    W, b = rnd(71, (N, K), 0.05), rnd(72, (N,), 0.1)
+    dW, db = to_dev(W, "bf16"), to_dev(b, "bf16")
+    out = torch.zeros((M, N), dtype=torch.bfloat16, device=DEV)
+    say("linear bf16 with a 2 GiB+ operand")
+    _lib.check(lib.t2i_op_linear(_lib.T2I_BF16, 0, M, N, K, dA.data_ptr(), K, dW.data_ptr(), K,
+                                 db.data_ptr(), out.data_ptr(), N, None, 0, None, None,
+                                 _stream()))
+    torch.cuda.synchronize()
+    rows = [0, 1, 4097, 1 << 19, (1 << 20) - 1, M - 2, M - 1]
+    A_rows = dA[rows].float().cpu().numpy().astype(np.float64)
+    ref = dit.linear(A_rows, W.astype(np.float64), b.astype(np.float64))
+    err = rel_l2(out[rows].float().cpu().numpy(), ref)
+    say(f"  rel_l2 {err:.2e}")
+    assert err < 3e-3
+    del dA, out
+    torch.cuda.empty_cache()
+
+
 @pytest.mark.parametrize("M,N,K,epi", [(64, 128, 256, 0), (100, 520, 128, 2), (77, 33, 90, 4)])
 def test_linear_f32(M, N, K, epi):
     A, W, b = rnd(10, (M, K), bf=False), rnd(11, (N, K), 0.05, bf=False), rnd(12, (N,), 0.1, bf=False)
