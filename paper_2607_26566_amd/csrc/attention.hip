@@ -527,6 +527,182 @@ __global__ __launch_bounds__(NW * 64, 8 / NW) void attn_bf16_kernel(AttnMap map,
 }
 
 // ---------------------------------------------------------------------------
+// Cross-attention to a text of at most 128 keys (two key tiles).  Both tiles
+// are loaded once into LDS, all scores are computed, and the softmax uses
+// the exact row maximum (no running maximum, no rescaling, no next-tile
+// lookahead).  The smaller register and LDS footprint (two stages) lets three
+// 4-wave workgroups share a CU instead of two: these launches are short and
+// bound by latency, so the extra workgroups in flight are what counts.
+// Layouts (K rows in swap23 key order, V^T chunk swizzle, ones row of V^T for
+// the row sums, Q scaled by log2(e)/sqrt(d)) are those of attn_bf16_kernel.
+template <int HD, int NW>
+__global__ __launch_bounds__(NW * 64, 12 / NW) void attn_cross_kernel(
+    AttnMap map, int heads, const bf16* __restrict__ Q, int ldq, const bf16* __restrict__ K,
+    int ldk, const bf16* __restrict__ Vt, int ldvt, bf16* __restrict__ O, int ldo,
+    float scale_log2) {
+  constexpr int BQ = NW * 32, BKV = 64;
+  constexpr int DC = (HD + 15) / 16;   // 16-wide d chunks of S^T = K Q^T
+  constexpr int DT = (HD + 31) / 32, HDO = DT * 32;
+  constexpr bool ONES = HD < HDO;
+  constexpr int CPR = HD / 8, PK = 2 * HD, NI = 2 * CPR;
+  constexpr int KRS = (CPR == 4 || CPR == 8 || CPR == 16) ? 16 / CPR : 0;
+  constexpr int KSTAGE = BKV * PK, VSTAGE = HDO * 128;
+  static_assert(HD % 8 == 0 && KSTAGE % 1024 == 0, "head dim");
+  __shared__ __attribute__((aligned(1024))) char smem[2 * (KSTAGE + VSTAGE)];
+
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  int hh, s, j;
+  decode_tile<true>(map, heads, xcd_remap_attn(blockIdx.x, gridDim.x), hh, s, j);
+  const int q_beg = map.q_start[s], q_end = q_beg + map.q_len[s];
+  const int k0 = map.k_start[s], k_end = k0 + map.k_len[s];
+  const int nt = (map.k_len[s] + BKV - 1) / BKV;   // 1 or 2 (the launcher checks)
+  const int ql = lane & 31, hl = lane >> 5;
+  const int qr = q_beg + j * BQ + wave * 32 + ql;
+  auto kst = [&](int t) { return smem + t * (KSTAGE + VSTAGE); };
+  auto vst = [&](int t) { return smem + t * (KSTAGE + VSTAGE) + KSTAGE; };
+
+  // tile loads (as in attn_bf16_kernel; keys past the sequence clamped to its
+  // last key, V^T chunks wholly past it read from the tile's first chunk)
+  const __amdgpu_buffer_rsrc_t rk =
+      __builtin_amdgcn_make_buffer_rsrc((void*)K, 0, 0x7fffffff, kBufWord3);
+  const __amdgpu_buffer_rsrc_t rv =
+      __builtin_amdgcn_make_buffer_rsrc((void*)Vt, 0, 0x7fffffff, kBufWord3);
+  for (int t = 0; t < nt; ++t) {
+    const int kv0 = k0 + t * BKV;
+#pragma unroll
+    for (int ii = 0; ii < (NI + NW - 1) / NW; ++ii) {
+      const int i = wave + NW * ii;
+      if (i >= NI) break;
+      if (i < CPR) {
+        const int o = i * 1024 + lane * 16, r = o / PK, slot = (o - r * PK) / 16;
+        const int c = KRS ? slot ^ ((r / KRS) & (CPR - 1)) : slot;
+        const int key = min(kv0 + swap23(r), k_end - 1);
+        __builtin_amdgcn_raw_ptr_buffer_load_lds(
+            rk, (__attribute__((address_space(3))) void*)(kst(t) + i * 1024), 16,
+            2u * (uint32_t)(key * ldk + hh * HD + c * 8), 0, 0, 0);
+      } else {
+        const int o = (i - CPR) * 1024 + lane * 16, d = o / 128;
+        const int gk = kv0 + 8 * ((lane & 7) ^ ((d >> 1) & 7));
+        __builtin_amdgcn_raw_ptr_buffer_load_lds(
+            rv, (__attribute__((address_space(3))) void*)(vst(t) + (i - CPR) * 1024), 16,
+            2u * (uint32_t)((hh * HD + d) * ldvt + (gk < k_end ? gk : kv0)), 0, 0, 0);
+      }
+    }
+  }
+  // Q fragments, scaled; the ones row of both stages
+  bf16x8 qf[DC];
+#pragma unroll
+  for (int c = 0; c < DC; ++c) {
+    const int d = c * 16 + hl * 8;
+    qf[c] = bf16x8{};
+    if (qr < q_end && d < HD) qf[c] = *(const bf16x8*)(Q + (size_t)qr * ldq + hh * HD + d);
+#pragma unroll
+    for (int e = 0; e < 8; ++e) qf[c][e] = (bf16)((float)qf[c][e] * scale_log2);
+  }
+  if constexpr (ONES)
+    for (int i = tid; i < 2 * 64; i += NW * 64) ((bf16*)(vst(i >> 6) + HD * 128))[i & 63] = (bf16)1.f;
+  wait_vmcnt<0>();
+  attn_barrier();
+  // a chunk the sequence ends inside holds bytes from beyond it: zero the
+  // columns past the sequence (their probabilities are 0)
+  if (k_end & 7) {
+    const int t = nt - 1, c0 = k_end - (k0 + t * BKV);
+    char* vb = vst(t);
+    for (int i = tid; i < HD * 64; i += NW * 64) {
+      const int d = i >> 6, col = i & 63;
+      if (col >= c0)
+        *(bf16*)(vb + d * 128 + (((col >> 3) ^ ((d >> 1) & 7)) << 4) + (col & 7) * 2) = (bf16)0.f;
+    }
+    attn_barrier();
+  }
+
+  // S^T of both tiles, masked past the sequence
+  f32x16 sc[2][2];
+#pragma unroll
+  for (int t = 0; t < 2; ++t) {
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb) sc[t][kb] = f32x16{};
+    if (t < nt) {
+#pragma unroll
+      for (int c = 0; c < DC; ++c) {
+#pragma unroll
+        for (int kb = 0; kb < 2; ++kb) {
+          const int r = 32 * kb + ql, cc = 2 * c + hl;
+          bf16x8 kf = bf16x8{};
+          if (cc < CPR) {
+            const int slot = KRS ? cc ^ ((r / KRS) & (CPR - 1)) : cc;
+            kf = *(const bf16x8*)(kst(t) + r * PK + slot * 16);
+          }
+          sc[t][kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[c], sc[t][kb], 0, 0, 0);
+        }
+      }
+    }
+  }
+  float mx = -INFINITY;
+#pragma unroll
+  for (int t = 0; t < 2; ++t)
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+      for (int e = 0; e < 16; ++e) {
+        const int key = k0 + t * BKV + swap23(32 * kb + 8 * (e >> 2) + 4 * hl + (e & 3));
+        if (key >= k_end) sc[t][kb][e] = -INFINITY;
+        mx = fmaxf(mx, sc[t][kb][e]);
+      }
+  mx = fmaxf(mx, __shfl_xor(mx, 32, 64));   // the query's keys sit in lanes ql and ql + 32
+
+  // P V over both tiles; row sums from the ones row or per lane
+  f32x16 o[DT];
+#pragma unroll
+  for (int dt = 0; dt < DT; ++dt) o[dt] = f32x16{};
+  float psum = 0.f;
+#pragma unroll
+  for (int t = 0; t < 2; ++t) {
+    if (t >= nt) break;
+    const char* vb = vst(t);
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      bf16x8 pf;
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        const float p = __builtin_amdgcn_exp2f(sc[t][q >> 1][8 * (q & 1) + e] - mx);
+        if (!ONES) psum += p;
+        pf[e] = (bf16)p;
+      }
+#pragma unroll
+      for (int dt = 0; dt < DT; ++dt) {
+        const int row = dt * 32 + ql;
+        const bf16x8 vf =
+            *(const bf16x8*)(vb + row * 128 + (((2 * q + hl) ^ ((row >> 1) & 7)) << 4));
+        o[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf, pf, o[dt], 0, 0, 0);
+      }
+    }
+  }
+  float l;
+  if (ONES) {
+    constexpr int R = HD % 32;
+    l = __shfl(o[HD / 32][4 * (R / 8) + (R % 4)], ((R % 8) / 4) * 32 + ql, 64);
+  } else {
+    l = psum + __shfl_xor(psum, 32, 64);
+  }
+  if (qr >= q_end) return;
+  const float inv = 1.0f / l;
+#pragma unroll
+  for (int dt = 0; dt < DT; ++dt)
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int d = dt * 32 + i * 8 + hl * 4;
+      if (d < HD) {
+        bf16x4 w;
+#pragma unroll
+        for (int jj = 0; jj < 4; ++jj) w[jj] = (bf16)(o[dt][4 * i + jj] * inv);
+        *(bf16x4*)(O + (size_t)qr * ldo + hh * HD + d) = w;
+      }
+    }
+}
+
+// ---------------------------------------------------------------------------
 
 template <int HD>
 __global__ __launch_bounds__(64) void attn_f32_kernel(AttnMap map, int heads,
@@ -646,7 +822,15 @@ static hipError_t launch_hd(bool bf16_io, int role, int heads, const AttnMap& ma
                      (bf16*)o, ldo, scale_log2)
     // smaller workgroups (2 or 4 waves) share a CU and use a 3-stage ring
     if (role == 1) {
-      if (map.waves == kCrossWaves) T2I_ATT(kCrossWaves, kCrossStages, 1);
+      // texts of at most 128 keys in one segment: the two-tile kernel
+      bool short_text = map.waves == kCrossWaves;
+      for (int s = 0; s < map.n && short_text; ++s)
+        short_text = map.k_len[s] >= 1 && map.k_len[s] <= 128 && map.k2_len[s] == 0;
+      if (short_text)
+        hipLaunchKernelGGL((attn_cross_kernel<HD, kCrossWaves>), dim3(tiles), dim3(kCrossWaves * 64),
+                           0, st, map, heads, (const bf16*)q, ldq, (const bf16*)k, ldk,
+                           (const bf16*)v, ldv, (bf16*)o, ldo, scale_log2);
+      else if (map.waves == kCrossWaves) T2I_ATT(kCrossWaves, kCrossStages, 1);
       else return hipErrorInvalidValue;
     } else {
       if (map.waves == kAttnWaves) T2I_ATT(kAttnWaves, attn_stages<HD>(), 0);

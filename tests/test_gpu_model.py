@@ -85,6 +85,29 @@ def test_dit512_teacher_forced_steps(dit512):
             assert err < 1e-2
 
 
+@pytest.mark.parametrize("text_tokens", [8, 64, 128])
+def test_cross_dit_text_lengths(text_tokens):
+    """Cross-attention over one key tile (8), one full tile (64) and two full
+    tiles (128), two requests and guidance 4.5, at full width, 2 blocks."""
+    w = synth.reduced(synth.workload("dit512"), depth=2, text_tokens=text_tokens,
+                      requests=((32, 32), (16, 48)), guidance=4.5)
+    M = Model(w)
+    lats, texts = synth.latents(w), synth.texts(w)
+    tx = M.text_dev(texts)
+    x = M.latents_dev(lats)
+    v = step_gpu(M, x, list(w.requests), [0.7, 0.3], tx, guidance=w.guidance)
+    parts = M.split(v, [l.shape for l in lats])
+    for r, t in enumerate((0.7, 0.3)):
+        vc = dit.forward(M.W, w, lats[r], t, texts[r])
+        vu = dit.forward(M.W, w, lats[r], t, None)
+        err = rel_l2(parts[r].ravel(), sampler.cfg_combine(vc, vu, w.guidance).ravel())
+        say(f"cross text {text_tokens} request {r}: v rel_l2 {err:.2e}")
+        assert err < 1e-2
+    del M
+    gc.collect()
+    torch.cuda.empty_cache()
+
+
 def test_dit512_determinism_and_block_updates(dit512):
     M, w = dit512, dit512.w
     lats, texts = synth.latents(w), synth.texts(w)
