@@ -530,13 +530,15 @@ __global__ __launch_bounds__(NW * 64, 8 / NW) void attn_bf16_kernel(AttnMap map,
 // Cross-attention to a text of at most 128 keys (two key tiles).  Both tiles
 // are loaded once into LDS, all scores are computed, and the softmax uses
 // the exact row maximum (no running maximum, no rescaling, no next-tile
-// lookahead).  The smaller register and LDS footprint (two stages) lets three
-// 4-wave workgroups share a CU instead of two: these launches are short and
-// bound by latency, so the extra workgroups in flight are what counts.
+// lookahead).  The smaller register and LDS footprint (two stages, 127
+// VGPRs and 40 KB at head dimension 72) lets four 4-wave workgroups share a
+// CU instead of two: these launches are short and bound by latency, so the
+// workgroups in flight are what counts (at 1024 px with guidance, 1024
+// workgroups: one round of the chip).
 // Layouts (K rows in swap23 key order, V^T chunk swizzle, ones row of V^T for
 // the row sums, Q scaled by log2(e)/sqrt(d)) are those of attn_bf16_kernel.
 template <int HD, int NW>
-__global__ __launch_bounds__(NW * 64, 12 / NW) void attn_cross_kernel(
+__global__ __launch_bounds__(NW * 64, (HD <= 72 ? 16 : 12) / NW) void attn_cross_kernel(
     AttnMap map, int heads, const bf16* __restrict__ Q, int ldq, const bf16* __restrict__ K,
     int ldk, const bf16* __restrict__ Vt, int ldvt, bf16* __restrict__ O, int ldo,
     float scale_log2) {
@@ -546,9 +548,14 @@ __global__ __launch_bounds__(NW * 64, 12 / NW) void attn_cross_kernel(
   constexpr bool ONES = HD < HDO;
   constexpr int CPR = HD / 8, PK = 2 * HD, NI = 2 * CPR;
   constexpr int KRS = (CPR == 4 || CPR == 8 || CPR == 16) ? 16 / CPR : 0;
-  constexpr int KSTAGE = BKV * PK, VSTAGE = HDO * 128;
+  // V^T rows kept per stage: the data and the ones row.  The P V MFMAs also
+  // read the padding rows up to HDO - 1, which only feed O^T rows that are
+  // never used: for stage 0 they are stage 1's K rows, for stage 1 a pad.
+  // (Head dimension 72: 40 KB in all, four workgroups per CU.)
+  constexpr int VROWS = ONES ? HD + 1 : HDO;
+  constexpr int KSTAGE = BKV * PK, VSTAGE = VROWS * 128, VPAD = (HDO - VROWS) * 128;
   static_assert(HD % 8 == 0 && KSTAGE % 1024 == 0, "head dim");
-  __shared__ __attribute__((aligned(1024))) char smem[2 * (KSTAGE + VSTAGE)];
+  __shared__ __attribute__((aligned(1024))) char smem[2 * (KSTAGE + VSTAGE) + VPAD];
 
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
