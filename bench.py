@@ -39,7 +39,7 @@ WORKLOAD = "dit1024_cfg"
 # blank lines removed, see code_digest): reported only while the code is
 # unchanged.
 MEASURED_TRAFFIC = {
-    ("dit1024_cfg", "attn_self"): (107.1e6, "paper_2607_26566_amd/csrc/attention.hip", "48c18d20fb3c3ce1"),
+    ("dit1024_cfg", "attn_self"): (107.1e6, "paper_2607_26566_amd/csrc/attention.hip", "57a3ad7f1a640275"),
 }
 
 
