@@ -187,9 +187,10 @@ Layout layout(const t2i_dit_config& c) {
   L.vtt = take(c.arch == T2I_ARCH_CROSS_DIT && bfv ? (size_t)c.depth * D * L.ldvt_txt * 2 : 0);
   L.rope = take(mm ? (size_t)(4096 / c.patch) * (c.head_dim / 4) * sizeof(float2) : 0);
   L.pe = take(mm ? 0 : (size_t)(4096 / c.patch) * (c.hidden / 4) * sizeof(float2));
-  // split-K partial sums of the text stream's narrow projections (at most 4
-  // slices of up to 2047 rows)
-  L.splitk_floats = mm ? (size_t)4 * std::min<size_t>(txt_rows, 2047) * D : 0;
+  // split-K partial sums of the text projections against long K (the MMDiT
+  // text stream's narrow layers; the cross-DiT's caption projection, K =
+  // text_dim): at most 4 slices of up to 2047 rows
+  L.splitk_floats = (mm || bfv) ? (size_t)4 * std::min<size_t>(txt_rows, 2047) * D : 0;
   L.splitk = take(L.splitk_floats * 4);
   L.tfreq = take(Tt * c.freq_dim * 4);
   L.th1 = take(Tt * D * 4);
@@ -554,7 +555,9 @@ t2i_status text_prep(t2i_dit* h, const Plan& P, const void* prompt, int nb, hipS
     HIP_TRY(h, launch_rope_table(h->at<float2>(h->L.rope), P.grid_max, c.head_dim / 4, st));
     return T2I_OK;
   }
-  HIP_TRY(h, linear(h, prompt, c.text_dim, W_Y, P.n_req * M, D, c.text_dim, EPI_STORE, e, st));
+  // a few hundred rows against K = text_dim: K split over workgroups
+  HIP_TRY(h, linear(h, prompt, c.text_dim, W_Y, P.n_req * M, D, c.text_dim, EPI_STORE, e, st,
+                    /*allow_split=*/true));
   if (P.branches == 2)
     HIP_TRY(h, launch_broadcast_rows(h->w[B_Y], h->bf(), M, D,
                                      ytxt + (size_t)P.n_req * M * D * h->act(), st));

@@ -345,8 +345,15 @@ hipError_t launch_gemm_bf16(const bf16* A, int lda, const bf16* W, int ldw, cons
     pe.out = splitk_ws;
     pe.ldo = N;
     const int pvec = N % 4 == 0;
+    // 64 x 64 tiles where 128-row tiles would leave most CUs idle (the
+    // caption projection of one request: 120 rows); same K order, same sums
+    const long t128 = (long)((M + 127) / 128) * ((N + (N % 144 == 0 ? 143 : 127)) /
+                                                  (N % 144 == 0 ? 144 : 128));
     hipError_t err =
-        N % 144 == 0
+        t128 * splits < 256
+            ? gemm_bf16_dispatch<64, 64, 2>(A, lda, W, ldw, bias, M, N, K / splits, EPI_PARTIAL,
+                                            pe, pvec, st, splits)
+        : N % 144 == 0
             ? gemm_bf16_dispatch<128, 144, 4>(A, lda, W, ldw, bias, M, N, K / splits, EPI_PARTIAL,
                                               pe, pvec, st, splits)
             : gemm_bf16_dispatch<128, 128, 2>(A, lda, W, ldw, bias, M, N, K / splits, EPI_PARTIAL,
@@ -575,7 +582,14 @@ hipError_t launch_linear_rows_group(const float* A, int lda, const PtrGroup& g, 
   for (int i = 0; i < groups; ++i)
     if ((uintptr_t)g.W[i] & 15) return hipErrorInvalidValue;
   dim3 grid((M + 7) / 8, (N + 15) / 16, groups), block(256);
-  if (w_bf16)
+  if (w_bf16 && M <= 2) {
+    // one step's conditioning rows: a 2-row instance needs fewer registers,
+    // so more waves stream weights at once (each row's sums are those of the
+    // 8-row instance)
+    grid.x = 1;
+    hipLaunchKernelGGL((linear_rows_group_kernel<bf16, 2, EPI_STORE>), grid, block, 0, st, A, lda,
+                       g, ldw, M, N, K, epi);
+  } else if (w_bf16)
     hipLaunchKernelGGL((linear_rows_group_kernel<bf16, 8, EPI_STORE>), grid, block, 0, st, A, lda,
                        g, ldw, M, N, K, epi);
   else
