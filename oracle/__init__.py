@@ -12,7 +12,7 @@ latent under text conditioning, the ``denoise`` update between steps, and the
 step-to-step cache-skip rule.  The paper fixes the role of these pieces (a bf16
 diffusion transformer called on ``latents`` and ``prompt_embeds`` returning
 ``noise_pred``; an iterative loop) but no architectural constant, so every
-convention below is a stated reading, listed again in the design doc.
+convention below is a stated reading of it.
 
 Everything is float64 numpy, one request (one sequence) at a time, written as
 the definitions read: no blocking, no fusion, no reordering.
