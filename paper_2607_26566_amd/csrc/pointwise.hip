@@ -647,6 +647,16 @@ __global__ __launch_bounds__(256) void final_kernel(const float* __restrict__ x,
                                                     float* __restrict__ lat,
                                                     float* __restrict__ noise_pred) {
   constexpr int NI = NV ? (NV + 63) / 64 : kMaxV4;
+  // DiT width 1152, 16 outputs, bf16: the workgroup's four waves read the
+  // projection (36 KB) from LDS, staged once, instead of each from L2
+  constexpr bool WLDS = PT == 16 && NV == 288 && sizeof(TW) == 2;
+  __shared__ __attribute__((aligned(16))) TW wsh[WLDS ? 16 * 4 * 288 : 1];
+  if constexpr (WLDS) {
+    for (int i = threadIdx.x; i < 16 * 4 * 288 / 8; i += 256)
+      ((bf16x8*)wsh)[i] = ((const bf16x8*)w_out)[i];
+    __syncthreads();
+  }
+  const TW* wsrc = WLDS ? wsh : w_out;
   const int lane = threadIdx.x & 63;
   const int tok = blockIdx.x * 4 + (threadIdx.x >> 6);
   if (tok >= rm.tokens_total) return;
@@ -710,7 +720,7 @@ __global__ __launch_bounds__(256) void final_kernel(const float* __restrict__ x,
       if (c < nv) {
 #pragma unroll
         for (int f = 0; f < PT; ++f) {
-          const float4 w = ld_w4<TW, PT>(w_out + (size_t)f * D + 4 * c);
+          const float4 w = ld_w4<TW, PT>(wsrc + (size_t)f * D + 4 * c);
 #pragma unroll
           for (int br = 0; br < 2; ++br) {
             acc[br][f] = fmaf(v[br][i].x, w.x, acc[br][f]);
