@@ -7,8 +7,9 @@
  * returns `noise_pred`; an orchestrator loop calls it once per denoising step
  * and applies `denoise(noise_pred, latents)`.  The paper calls this inference
  * compute-bound (Sec. 3.1) and requires identical results under fixed seeds
- * (Sec. 4, "Function-as-a-Service Paradigm"; Sec. 8.1 "validated the identity
- * of generated images").  This library is that model function and its loop:
+ * (Sec. 4, "Function-as-a-Service Paradigm"; Sec. 8.1 checks that its system
+ * produces the same images as the unmodified models).  This library is that
+ * model function and its loop:
  *
  *   t2i_dit_init    load: bind the caller's device weights and workspace
  *   t2i_dit_step    one model evaluation (+ guidance, + optional Euler update)

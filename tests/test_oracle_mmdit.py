@@ -2,6 +2,7 @@
 import math
 
 import numpy as np
+import pytest
 
 import synth
 from oracle import dit, mmdit
@@ -186,3 +187,209 @@ def test_sampler_runs_mmdit_velocity_guidance_and_cached_residual():
     assert np.allclose(v3, v2, atol=1e-10)
     # the unconditional text stream starts from the bias alone
     assert np.allclose(mmdit.embed_text(W, TINY, None), np.tile(W["y_embed.b"], (3, 1)))
+
+
+# ---------------------------------------------------------------- both streams by scalar loops
+
+def brute_joint_block(W, w, b, x_txt, x_img, c, rows, cols):
+    """One joint block written with scalar loops from its definition, returning
+    BOTH streams: per-stream adaLN-Zero, LN-modulate, q|k|v projection, RoPE on
+    the image queries and keys only, one softmax attention over the text rows
+    followed by the image rows, then per stream the gated output projection and
+    the gated tanh-GELU MLP with that stream's own weights and gates."""
+    D, H, F = w.hidden, w.heads, w.mlp_hidden
+    d = D // H
+
+    def lin(vec, Wm, bv):
+        return [bv[o] + sum(Wm[o][i] * vec[i] for i in range(len(vec))) for o in range(len(bv))]
+
+    def ln(vec):
+        mu = sum(vec) / len(vec)
+        var = sum((a - mu) ** 2 for a in vec) / len(vec)
+        return [(a - mu) / math.sqrt(var + w.ln_eps) for a in vec]
+
+    def rot(vec, r, cc):
+        out = list(vec)
+        for h in range(H):
+            for half, pos in ((0, r), (1, cc)):
+                for j in range(d // 4):
+                    a = h * d + half * (d // 2) + 2 * j
+                    ang = pos * 10000.0 ** (-j / (d // 4))
+                    out[a] = vec[a] * math.cos(ang) - vec[a + 1] * math.sin(ang)
+                    out[a + 1] = vec[a] * math.sin(ang) + vec[a + 1] * math.cos(ang)
+        return out
+
+    sc = [a / (1 + math.exp(-a)) for a in c]
+    xs = {"txt": [list(r) for r in x_txt], "img": [list(r) for r in x_img]}
+    mod, qs, ks, vs = {}, [], [], []
+    for s in mmdit.STREAMS:
+        p = f"blocks.{b}.{s}."
+        m = lin(sc, W[p + "ada.w"], W[p + "ada.b"])
+        mod[s] = [m[i * D:(i + 1) * D] for i in range(6)]
+        for t, row in enumerate(xs[s]):
+            hv = [n * (1 + mod[s][1][i]) + mod[s][0][i] for i, n in enumerate(ln(row))]
+            qkv = lin(hv, W[p + "qkv.w"], W[p + "qkv.b"])
+            q, k, v = qkv[:D], qkv[D:2 * D], qkv[2 * D:]
+            if s == "img":
+                q, k = rot(q, rows[t], cols[t]), rot(k, rows[t], cols[t])
+            qs.append(q), ks.append(k), vs.append(v)
+    o = []
+    for qi in qs:
+        out = [0.0] * D
+        for h in range(H):
+            sc_ = [sum(qi[h * d + e] * kj[h * d + e] for e in range(d)) / math.sqrt(d) for kj in ks]
+            mx = max(sc_)
+            ex = [math.exp(a - mx) for a in sc_]
+            z = sum(ex)
+            for e in range(d):
+                out[h * d + e] = sum(ex[j] * vs[j][h * d + e] for j in range(len(ks))) / z
+        o.append(out)
+    nt = len(xs["txt"])
+    outs = {"txt": o[:nt], "img": o[nt:]}
+    new = {}
+    for s in mmdit.STREAMS:
+        p = f"blocks.{b}.{s}."
+        sh1, s1, g1, sh2, s2, g2 = mod[s]
+        res = []
+        for t, row in enumerate(xs[s]):
+            po = lin(outs[s][t], W[p + "o.w"], W[p + "o.b"])
+            r = [row[i] + g1[i] * po[i] for i in range(D)]
+            hv = [n * (1 + s2[i]) + sh2[i] for i, n in enumerate(ln(r))]
+            u = lin(hv, W[p + "fc1.w"], W[p + "fc1.b"])
+            u = [0.5 * a * (1 + math.tanh(math.sqrt(2 / math.pi) * (a + 0.044715 * a ** 3)))
+                 for a in u]
+            f = lin(u, W[p + "fc2.w"], W[p + "fc2.b"])
+            res.append([r[i] + g2[i] * f[i] for i in range(D)])
+        new[s] = np.array(res).reshape(len(res), D)
+    return new["txt"], new["img"]
+
+
+def _joint_inputs(seed=31):
+    rng = np.random.default_rng(seed)
+    D = TINY.hidden
+    return (rng.standard_normal((3, D)), rng.standard_normal((6, D)) * 0.7,
+            rng.standard_normal(D))
+
+
+def test_joint_block_both_streams_brute_force():
+    """Text and image stream outputs of joint_block against scalar loops."""
+    W = weights()
+    xt, xi, c = _joint_inputs()
+    rows, cols = mmdit.grid_positions(2, 3)
+    for b in range(TINY.depth):
+        nt, ni = mmdit.joint_block(W, TINY, b, xt, xi, c, rows, cols)
+        bt, bi = brute_joint_block(W, TINY, b, xt, xi, c, rows, cols)
+        assert np.allclose(nt, bt, rtol=1e-11, atol=1e-12), b
+        assert np.allclose(ni, bi, rtol=1e-11, atol=1e-12), b
+
+
+def test_forward_two_blocks_brute_force_composition():
+    """mmdit.forward = embed (loops) -> 2 brute joint blocks -> final layer
+    (loops) on the image stream; the text stream after the blocks too."""
+    W = weights()
+    rng = np.random.default_rng(32)
+    C, p, D = TINY.latent_channels, TINY.patch, TINY.hidden
+    lat = rng.standard_normal((C, 4, 6))
+    text = rng.standard_normal((TINY.text_tokens, TINY.text_dim))
+    t = 0.61
+    v, xt_o, xi_o = mmdit.forward(W, TINY, lat, t, text)
+    gh, gw = 2, 3
+    xi = np.zeros((gh * gw, D))
+    for i in range(gh):
+        for j in range(gw):
+            for o in range(D):
+                s = W["x_embed.b"][o]
+                for a in range(p):
+                    for bb in range(p):
+                        for cc in range(C):
+                            s += W["x_embed.w"][o, (a * p + bb) * C + cc] * lat[cc, i * p + a, j * p + bb]
+                xi[i * gw + j, o] = s
+    xt = np.array([[W["y_embed.b"][o] + sum(W["y_embed.w"][o, k] * text[r, k]
+                                             for k in range(TINY.text_dim))
+                    for o in range(D)] for r in range(TINY.text_tokens)])
+    # conditioning by loops (sinusoid, Linear, SiLU, Linear)
+    half = TINY.freq_dim // 2
+    s_t = TINY.t_scale * t
+    e = [math.cos(s_t * math.exp(-math.log(10000.0) * k / half)) for k in range(half)] + \
+        [math.sin(s_t * math.exp(-math.log(10000.0) * k / half)) for k in range(half)]
+    h1 = [W["t_embed.b1"][o] + sum(W["t_embed.w1"][o, k] * e[k] for k in range(len(e)))
+          for o in range(D)]
+    h1 = [a / (1 + math.exp(-a)) for a in h1]
+    c = [W["t_embed.b2"][o] + sum(W["t_embed.w2"][o, k] * h1[k] for k in range(D)) for o in range(D)]
+    rows, cols = mmdit.grid_positions(gh, gw)
+    for b in range(TINY.depth):
+        xt, xi = brute_joint_block(W, TINY, b, xt, xi, c, rows, cols)
+    assert np.allclose(xt_o, xt, rtol=1e-10, atol=1e-11)
+    assert np.allclose(xi_o, xi, rtol=1e-10, atol=1e-11)
+    sc = [a / (1 + math.exp(-a)) for a in c]
+    fm = [W["final.ada.b"][o] + sum(W["final.ada.w"][o, k] * sc[k] for k in range(D))
+          for o in range(2 * D)]
+    out = np.zeros_like(lat)
+    for i in range(gh):
+        for j in range(gw):
+            r = xi[i * gw + j]
+            mu = r.mean()
+            sd = math.sqrt(((r - mu) ** 2).mean() + TINY.ln_eps)
+            hm = [(r[k] - mu) / sd * (1 + fm[D + k]) + fm[k] for k in range(D)]
+            for a in range(p):
+                for bb in range(p):
+                    for cc in range(C):
+                        f = (a * p + bb) * C + cc
+                        out[cc, i * p + a, j * p + bb] = W["final.out.b"][f] + sum(
+                            W["final.out.w"][f, k] * hm[k] for k in range(D))
+    assert np.allclose(v, out, rtol=1e-10, atol=1e-11)
+
+
+class _Redirect(dict):
+    """A weight dict that answers reads of one stream's tensors with another
+    stream's: simulates an oracle that indexes the wrong parameter."""
+
+    def __init__(self, base, frm, to):
+        super().__init__(base)
+        self.frm, self.to = frm, to
+
+    def __getitem__(self, k):
+        for part in self.frm:
+            if part in k:
+                k = k.replace(part, self.to[part])
+        return dict.__getitem__(self, k)
+
+
+@pytest.mark.parametrize("mutation", ["txt_uses_img_o_proj", "txt_uses_img_modulation",
+                                      "txt_uses_img_mlp", "o_rows_shifted", "rope_on_text",
+                                      "txt_uses_img_qkv"])
+def test_pins_catch_planted_text_stream_mistakes(monkeypatch, mutation):
+    """Plant a plausible text-stream mistake in the MMDiT oracle; the
+    scalar-loop pin of the text stream must see it."""
+    W = weights()
+    xt, xi, c = _joint_inputs(33)
+    rows, cols = mmdit.grid_positions(2, 3)
+    bt, bi = brute_joint_block(W, TINY, 0, xt, xi, c, rows, cols)
+    nt, _ = mmdit.joint_block(W, TINY, 0, xt, xi, c, rows, cols)
+    assert np.max(np.abs(nt - bt)) < 1e-11
+    Wm = W
+    if mutation == "txt_uses_img_o_proj":
+        Wm = _Redirect(W, ["txt.o."], {"txt.o.": "img.o."})
+    elif mutation == "txt_uses_img_modulation":
+        Wm = _Redirect(W, ["txt.ada."], {"txt.ada.": "img.ada."})
+    elif mutation == "txt_uses_img_mlp":
+        Wm = _Redirect(W, ["txt.fc2."], {"txt.fc2.": "img.fc2."})
+    elif mutation == "txt_uses_img_qkv":
+        Wm = _Redirect(W, ["txt.qkv."], {"txt.qkv.": "img.qkv."})
+    elif mutation == "o_rows_shifted":
+        orig = mmdit.attention
+        monkeypatch.setattr(mmdit, "attention", lambda q, k, v, h: np.roll(orig(q, k, v, h), 1, axis=0))
+    elif mutation == "rope_on_text":
+        # the text rows rotated as if they were tokens (i, 0) of the grid
+        orig = mmdit.attention
+        nt_rows = xt.shape[0]
+
+        def attn_rot(q, k, v, h):
+            q, k = np.array(q), np.array(k)
+            pos = np.arange(nt_rows)
+            q[:nt_rows] = mmdit.rope_2d(q[:nt_rows], pos + 1, pos * 0, h)
+            k[:nt_rows] = mmdit.rope_2d(k[:nt_rows], pos + 1, pos * 0, h)
+            return orig(q, k, v, h)
+        monkeypatch.setattr(mmdit, "attention", attn_rot)
+    mt, _ = mmdit.joint_block(Wm, TINY, 0, xt, xi, c, rows, cols)
+    assert np.max(np.abs(mt - bt)) > 1e-6
