@@ -167,11 +167,12 @@ __global__ __launch_bounds__(NW * 64, 8 / NW) void attn_bf16_kernel(AttnMap map,
   auto kst = [&](int st) { return smem + st * (KSTAGE + VSTAGE); };
   auto vst = [&](int st) { return smem + st * (KSTAGE + VSTAGE) + KSTAGE; };
 
-  // Q fragments (B operand of S^T): query qr, d = 16c + 8hl .. +7, pre-multiplied
-  // by log2(e)/sqrt(d) so that scores come out in log2 units; the shift slot
-  // d = HD is element 0 of chunk HD/16 in the lanes of half (HD%16)/8
-  // (loaded here, scaled after the first tile loads are issued, so that the
-  // two latencies overlap)
+  // Q fragments (B operand of S^T): query qr, d = 16c + 8hl .. +7, as stored
+  // (bf16, unscaled: scores leave the MFMA in raw units, and the softmax
+  // scale log2(e)/sqrt(d) is applied in fp32 to each score before its
+  // exponential, so that no rounding of a scaled Q enters the logits); the
+  // shift slot d = HD is element 0 of chunk HD/16 in the lanes of half
+  // (HD%16)/8
   constexpr int BC = HD / 16, BH = (HD % 16) / 8;
   bf16x8 qf[DC];
 #pragma unroll
@@ -180,11 +181,7 @@ __global__ __launch_bounds__(NW * 64, 8 / NW) void attn_bf16_kernel(AttnMap map,
     qf[c] = bf16x8{};
     if (qr < q_end && d < HD) qf[c] = *(const bf16x8*)(Q + (size_t)qr * ldq + hh * HD + d);
   }
-  auto scale_q = [&]() {
-#pragma unroll
-    for (int c = 0; c < DC; ++c)
-#pragma unroll
-      for (int e = 0; e < 8; ++e) qf[c][e] = (bf16)((float)qf[c][e] * scale_log2);
+  auto init_ones = [&]() {
     // the ones row (V^T row HD) of every stage; the padding rows after it
     // only feed O^T rows that are never read
     if constexpr (ONES)
@@ -325,10 +322,12 @@ __global__ __launch_bounds__(NW * 64, 8 / NW) void attn_bf16_kernel(AttnMap map,
     return fmaxf(m0, m1);
   };
 
-  // Online softmax with a lazily updated maximum m (kept bf16-representable,
-  // as it rides in Q's shift slot): scores arrive as S' = s - m.  While no S'
-  // exceeds 8 the stale maximum is kept: probabilities stay <= 256 and the
-  // common scale cancels between numerator and row sum.
+  // Online softmax with a lazily updated maximum m of the raw scores (kept
+  // bf16-representable, as it rides in Q's shift slot): scores arrive as
+  // S' = s - m and the probabilities are exp2(scale_log2 * S').  While no
+  // scaled S' exceeds 8 the stale maximum is kept: probabilities stay <= 256
+  // and the common scale cancels between numerator and row sum.
+  const float lazy_thr = 8.0f / scale_log2;   // 8 in log2 units, as a raw score
   f32x16 o[DT];
 #pragma unroll
   for (int dt = 0; dt < DT; ++dt) o[dt] = f32x16{};
@@ -389,12 +388,12 @@ __global__ __launch_bounds__(NW * 64, 8 / NW) void attn_bf16_kernel(AttnMap map,
             cur[kb][e] = -INFINITY;
       lm = lane_max(cur);
     }
-    if (ti == 0 || __any(lm > 8.0f)) {
+    if (ti == 0 || __any(lm > lazy_thr)) {
       // new maximum: the query's 64 scores sit in lanes ql and ql + 32
       const float mx = fmaxf(lm, __shfl_xor(lm, 32, 64)) + m_ref;   // tile maximum
       const float m_old = ti == 0 ? -INFINITY : m_ref;
       const float m_new = (float)(bf16)fmaxf(m_old, mx);
-      const float alpha = __builtin_amdgcn_exp2f(m_old - m_new);
+      const float alpha = __builtin_amdgcn_exp2f((m_old - m_new) * scale_log2);
 #pragma unroll
       for (int kb = 0; kb < 2; ++kb) cur[kb] -= (m_new - m_ref);
 #pragma unroll
@@ -443,7 +442,7 @@ __global__ __launch_bounds__(NW * 64, 8 / NW) void attn_bf16_kernel(AttnMap map,
         const int e1 = sl + 1 < NE ? (32 * (sl + 1) + NE - 1) / NE : 32;
 #pragma unroll
         for (int i = e0; i < e1; ++i) {
-          pe[i] = __builtin_amdgcn_exp2f(cur[i >> 4][i & 15]);
+          pe[i] = __builtin_amdgcn_exp2f(cur[i >> 4][i & 15] * scale_log2);
           if (!ONES) psum += pe[i];
           if ((i & 7) == 7)
 #pragma unroll
@@ -464,7 +463,7 @@ __global__ __launch_bounds__(NW * 64, 8 / NW) void attn_bf16_kernel(AttnMap map,
       for (int q = 0; q < 4; ++q)
 #pragma unroll
         for (int e = 0; e < 8; ++e) {
-          const float p = __builtin_amdgcn_exp2f(cur[q >> 1][8 * (q & 1) + e]);
+          const float p = __builtin_amdgcn_exp2f(cur[q >> 1][8 * (q & 1) + e] * scale_log2);
           if (!ONES) psum += p;
           pf[q][e] = (bf16)p;
         }
@@ -489,7 +488,7 @@ __global__ __launch_bounds__(NW * 64, 8 / NW) void attn_bf16_kernel(AttnMap map,
 #pragma unroll
   for (int ti = 0; ti < PRE; ++ti)
     if (ti < nt) issue(ti);
-  scale_q();
+  init_ones();
   wait_vmcnt_dyn(n_w * (min(nt, PRE) - 1));
   attn_barrier();
   f32x16 sa[2], sb[2];
@@ -536,7 +535,8 @@ __global__ __launch_bounds__(NW * 64, 8 / NW) void attn_bf16_kernel(AttnMap map,
 // workgroups in flight are what counts (at 1024 px with guidance, 1024
 // workgroups: one round of the chip).
 // Layouts (K rows in swap23 key order, V^T chunk swizzle, ones row of V^T for
-// the row sums, Q scaled by log2(e)/sqrt(d)) are those of attn_bf16_kernel.
+// the row sums, unscaled Q with the softmax scale applied in fp32 to the
+// scores) are those of attn_bf16_kernel.
 template <int HD, int NW>
 __global__ __launch_bounds__(NW * 64, (HD <= 72 ? 16 : 12) / NW) void attn_cross_kernel(
     AttnMap map, int heads, const bf16* __restrict__ Q, int ldq, const bf16* __restrict__ K,
@@ -597,15 +597,13 @@ __global__ __launch_bounds__(NW * 64, (HD <= 72 ? 16 : 12) / NW) void attn_cross
       }
     }
   }
-  // Q fragments, scaled; the ones row of both stages
+  // Q fragments (unscaled); the ones row of both stages
   bf16x8 qf[DC];
 #pragma unroll
   for (int c = 0; c < DC; ++c) {
     const int d = c * 16 + hl * 8;
     qf[c] = bf16x8{};
     if (qr < q_end && d < HD) qf[c] = *(const bf16x8*)(Q + (size_t)qr * ldq + hh * HD + d);
-#pragma unroll
-    for (int e = 0; e < 8; ++e) qf[c][e] = (bf16)((float)qf[c][e] * scale_log2);
   }
   if constexpr (ONES)
     for (int i = tid; i < 2 * 64; i += NW * 64) ((bf16*)(vst(i >> 6) + HD * 128))[i & 63] = (bf16)1.f;
@@ -658,6 +656,8 @@ __global__ __launch_bounds__(NW * 64, (HD <= 72 ? 16 : 12) / NW) void attn_cross
         mx = fmaxf(mx, sc[t][kb][e]);
       }
   mx = fmaxf(mx, __shfl_xor(mx, 32, 64));   // the query's keys sit in lanes ql and ql + 32
+  // probabilities exp2(scale_log2 * (s - mx)), one fma per score
+  const float mxs = mx * scale_log2;
 
   // P V over both tiles; row sums from the ones row or per lane
   f32x16 o[DT];
@@ -673,7 +673,7 @@ __global__ __launch_bounds__(NW * 64, (HD <= 72 ? 16 : 12) / NW) void attn_cross
       bf16x8 pf;
 #pragma unroll
       for (int e = 0; e < 8; ++e) {
-        const float p = __builtin_amdgcn_exp2f(sc[t][q >> 1][8 * (q & 1) + e] - mx);
+        const float p = __builtin_amdgcn_exp2f(fmaf(sc[t][q >> 1][8 * (q & 1) + e], scale_log2, -mxs));
         if (!ONES) psum += p;
         pf[e] = (bf16)p;
       }

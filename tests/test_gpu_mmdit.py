@@ -126,7 +126,9 @@ def test_mmdit_small_cached_sampling(small):
     state = M.m.new_cache_state(toks, 2)
     shapes = [l.shape for l in lats]
     states = [sampler.CacheState() for _ in lats]
+    vstates = [sampler.CacheState() for _ in lats]   # the oracle's cached residuals
     skips = []
+    n_vel_skips = 0
     for k in range(n):
         xk = M.split(x.cpu().numpy(), shapes)
         rel, skip = t2i.t2i_cache_check(M.m, x, hw, sched[k], k, n, tau, state, branches=2)
@@ -144,9 +146,22 @@ def test_mmdit_small_cached_sampling(small):
                 assert abs(rel[r] - d) <= 1e-6 * abs(d) + 1e-12, (k, r, rel[r], d)
             assert bool(skip[r]) == sk, (k, r)
         skips.append(skip)
+        npred = torch.zeros_like(x)
         t2i.t2i_dit_step(M.m, x, hw, sched[k], tx, guidance=w.guidance, t_next=sched[k + 1],
-                         skip=skip, cache_state=state)
-    torch.cuda.synchronize()
+                         skip=skip, cache_state=state, noise_pred=npred)
+        torch.cuda.synchronize()
+        # guided velocity of every request, computed or skipped (teacher-forced:
+        # the oracle refreshes its own residual at each computed step)
+        vk = M.split(npred.cpu().numpy().astype(np.float64), shapes)
+        for r in range(w.n_req):
+            ref, _ = sampler.model_velocity(M.W, w, xk[r].astype(np.float64), sched[k, r],
+                                            texts[r], w.guidance, vstates[r], skip=bool(skip[r]))
+            err = rel_l2(vk[r], ref)
+            assert err < 1e-2, (k, r, bool(skip[r]), err)
+            if skip[r]:
+                n_vel_skips += 1
+                say(f"mmdit small cache step {k} request {r}: skipped-step v rel_l2 {err:.2e}")
+    assert n_vel_skips > 0
     say(f"mmdit small cache: {int(np.sum(skips))} skipped request-steps of {n * w.n_req}")
     x2 = M.latents_dev(lats)
     state2 = M.m.new_cache_state(toks, 2)

@@ -85,10 +85,12 @@ def test_dit512_teacher_forced_steps(dit512):
             assert err < 1e-2
 
 
-@pytest.mark.parametrize("text_tokens", [8, 64, 128])
+@pytest.mark.parametrize("text_tokens", [8, 64, 128, 200])
 def test_cross_dit_text_lengths(text_tokens):
-    """Cross-attention over one key tile (8), one full tile (64) and two full
-    tiles (128), two requests and guidance 4.5, at full width, 2 blocks."""
+    """Cross-attention over one key tile (8), one full tile (64), two full
+    tiles (128) and four tiles, the last ragged (200: text longer than 128
+    keys runs the pipelined attention kernel), two requests and guidance 4.5,
+    at full width, 2 blocks."""
     w = synth.reduced(synth.workload("dit512"), depth=2, text_tokens=text_tokens,
                       requests=((32, 32), (16, 48)), guidance=4.5)
     M = Model(w)
@@ -216,6 +218,95 @@ def test_dit1024_cfg_full_size_sampled(dit1024):
     assert rel_l2(x.cpu().numpy(), sampler.euler_update(lats[0].astype(np.float64), ref, t, tn).ravel()) < 1e-5
 
 
+def _oracle_blocks_threaded(M, w, x_k, t, texts):
+    """The oracle's residual stream after every block for both guidance
+    branches (conditional, unconditional), each branch in its own thread so
+    that their single-threaded elementwise parts overlap; progress per block."""
+    import threading
+    c = dit.conditioning(M.W, w, t)
+    x0 = dit.embed(M.W, w, x_k)
+    out = [None, None]
+
+    def run(br):
+        txt = texts if br == 0 else np.zeros((w.text_tokens, w.text_dim))
+        y = dit.text_project(M.W, w, txt)
+        x = x0
+        for b in range(w.depth):
+            x = dit.block(M.W, w, b, x, y, dit.block_modulation(M.W, w, c, b))
+            if b % 7 == 6:
+                say(f"  oracle branch {br}: {b + 1} blocks")
+        out[br] = x
+    th = [threading.Thread(target=run, args=(br,)) for br in (0, 1)]
+    for t_ in th:
+        t_.start()
+    for t_ in th:
+        t_.join()
+    return c, x0, out
+
+
+def _per_row_rel(got, ref):
+    """Relative L2 error of every row (last axis)."""
+    num = np.linalg.norm(got - ref, axis=-1)
+    den = np.linalg.norm(ref, axis=-1)
+    return num / den
+
+
+@pytest.mark.timeout(900)
+def test_dit1024_cfg_full_step_every_element(dit1024):
+    """The headline step at full size, teacher-forced: 4096 tokens x 2
+    guidance branches through all 28 blocks.  The GPU runs steps 0..9 on its
+    own, then step 10 is compared with the oracle started from the GPU's x_10:
+    every element of the residual stream after the blocks (each branch, also
+    row by row), of each branch's velocity before guidance, of the guided
+    velocity and of x_11."""
+    M, w = dit1024, dit1024.w
+    lats, texts = synth.latents(w), synth.texts(w)
+    hw = list(w.requests)
+    tx = M.text_dev(texts)
+    N, D, g = w.tokens(0), w.hidden, w.guidance
+    s = sampler.schedule(w.steps)
+    k = 10
+    x = M.latents_dev(lats)
+    for j in range(k):
+        t2i.t2i_dit_step(M.m, x, hw, [s[j]], tx, guidance=g, t_next=[s[j + 1]])
+    torch.cuda.synchronize()
+    x_k = x.cpu().numpy().astype(np.float64).reshape(lats[0].shape)
+    hid = torch.zeros((2 * N, D), dtype=torch.float32, device=DEV)
+    xg = x.clone()
+    v = step_gpu(M, xg, hw, [s[k]], tx, guidance=g, t_next=[s[k + 1]], hidden_out=hid)
+    x_next = xg.cpu().numpy().astype(np.float64)
+    hid_g = hid.cpu().numpy().astype(np.float64)
+    # guidance 0 returns the unconditional branch of the same two-branch step
+    v_u = step_gpu(M, x.clone(), hw, [s[k]], tx, guidance=0.0)
+    v_c = v_u + (v - v_u) / g
+    say("dit1024 full step: GPU done, oracle running")
+    c, x0, xl = _oracle_blocks_threaded(M, w, x_k, s[k], texts[0])
+    h, ww = hw[0]
+    for br in range(2):
+        got = hid_g[br * N:(br + 1) * N]
+        err = rel_l2(got - x0, xl[br] - x0)
+        rows = _per_row_rel(got - x0, xl[br] - x0)
+        say(f"dit1024 full step branch {br}: block residual rel_l2 {err:.2e}, "
+            f"worst row {rows.max():.2e} (row {int(rows.argmax())})")
+        assert err < 1e-2 and rows.max() < 3e-2
+    vc_ref = dit.final_layer(M.W, w, xl[0], c, h, ww)
+    vu_ref = dit.final_layer(M.W, w, xl[1], c, h, ww)
+    v_ref = sampler.cfg_combine(vc_ref, vu_ref, g)
+    for name, got, ref in (("v_c", v_c, vc_ref), ("v_u", v_u, vu_ref), ("v", v, v_ref)):
+        err = rel_l2(got, ref.ravel())
+        # per token: the p x p x C values of one patch
+        tok = _per_row_rel(dit.patchify(got.reshape(ref.shape), w.patch),
+                           dit.patchify(ref, w.patch))
+        say(f"dit1024 full step {name}: rel_l2 {err:.2e}, worst token {tok.max():.2e}")
+        assert err < 1e-2 and tok.max() < 3e-2
+    xr = sampler.euler_update(x_k, v_ref, s[k], s[k + 1])
+    err = rel_l2(x_next, xr.ravel())
+    say(f"dit1024 full step x_k+1: rel_l2 {err:.2e}")
+    assert err < 1e-2
+    assert np.linalg.norm(x_next - xr.ravel()) <= \
+        abs(s[k + 1] - s[k]) * 1e-2 * np.linalg.norm(v_ref) + 1e-6 * np.linalg.norm(xr)
+
+
 # ---------------------------------------------------------------- packed multi-request
 
 @pytest.fixture(scope="module")
@@ -266,6 +357,12 @@ def test_packed_cache_decisions_match_oracle(packed8):
     shapes = [l.shape for l in lats]
     states = [sampler.CacheState() for _ in lats]
     gpu_skips, margins = [], []
+    # velocity parity of the 256-px requests on every step, computed or
+    # skipped: the oracle keeps its own cached residual, refreshed at each
+    # computed step from the GPU's latent (teacher-forced)
+    vel_req = [r for r in range(w.n_req) if w.tokens(r) <= 256]
+    vstates = {r: sampler.CacheState() for r in vel_req}
+    n_vel_skips = 0
     for k in range(n):
         xk = M.split(x.cpu().numpy(), shapes)
         rel, skip = t2i.t2i_cache_check(M.m, x, hw, sched[k], k, n, w.cache_tau, state)
@@ -287,8 +384,20 @@ def test_packed_cache_decisions_match_oracle(packed8):
                 margins.append(abs(acc_before + d - w.cache_tau))
             assert bool(skip[r]) == sk, (k, r)
         gpu_skips.append(skip)
-        t2i.t2i_dit_step(M.m, x, hw, sched[k], tx, t_next=sched[k + 1], skip=skip, cache_state=state)
-    torch.cuda.synchronize()
+        npred = torch.zeros_like(x)
+        t2i.t2i_dit_step(M.m, x, hw, sched[k], tx, t_next=sched[k + 1], skip=skip, cache_state=state,
+                         noise_pred=npred)
+        torch.cuda.synchronize()
+        vk = M.split(npred.cpu().numpy().astype(np.float64), shapes)
+        for r in vel_req:
+            ref, _ = sampler.model_velocity(M.W, w, xk[r].astype(np.float64), sched[k, r], texts[r],
+                                            1.0, vstates[r], skip=bool(skip[r]))
+            err = rel_l2(vk[r], ref)
+            assert err < 1e-2, (k, r, bool(skip[r]), err)
+            if skip[r]:
+                n_vel_skips += 1
+                say(f"packed cache step {k} request {r}: skipped-step v rel_l2 {err:.2e}")
+    assert n_vel_skips > 0, "no skipped step among the requests compared"
     n_skip = int(np.sum(gpu_skips))
     say(f"packed cache: {n_skip} skipped request-steps of {n * w.n_req}; min margin {min(margins):.3e}")
     # the sampling loop reproduces the step-by-step run bitwise
@@ -299,3 +408,65 @@ def test_packed_cache_decisions_match_oracle(packed8):
     torch.cuda.synchronize()
     assert np.array_equal(skip_log, np.array(gpu_skips, dtype=np.uint8))
     assert np.array_equal(x2.cpu().numpy(), x.cpu().numpy())
+
+
+def test_packed_per_step_cache_mode_and_resume(packed8):
+    """The per-step reading of the cache rule (skip iff d_k < tau) on the GPU:
+    decisions equal the oracle's rule applied to the GPU's latents.  Then a
+    sample interrupted after step k -- latents and cache state saved to host
+    memory, restored into fresh buffers, resumed with start_step = k on a
+    second handle over the same weights -- equals the uninterrupted sample
+    bitwise, decisions included."""
+    M, w = packed8, packed8.w
+    lats, texts = synth.latents(w), synth.texts(w)
+    hw = list(w.requests)
+    t0 = synth.start_times(w)
+    n, tau, mode = w.steps, w.cache_tau, t2i.T2I_CACHE_PER_STEP
+    sched = np.stack([sampler.schedule(n, a) for a in t0], axis=1)
+    tx = M.text_dev(texts)
+    toks = [w.tokens(r) for r in range(w.n_req)]
+    shapes = [l.shape for l in lats]
+    # uninterrupted sample in per-step mode
+    x_full = M.latents_dev(lats)
+    st_full = M.m.new_cache_state(toks, 1)
+    log_full, rel_full = t2i.t2i_dit_sample(M.m, x_full, hw, tx, n, timesteps=sched,
+                                            cache_tau=tau, cache_mode=mode, cache_state=st_full)
+    torch.cuda.synchronize()
+    # the same loop step by step, decisions checked against the oracle's rule
+    x = M.latents_dev(lats)
+    state = M.m.new_cache_state(toks, 1)
+    states = [sampler.CacheState() for _ in lats]
+    k_stop = n // 2
+    for k in range(k_stop):
+        xk = M.split(x.cpu().numpy(), shapes)
+        rel, skip = t2i.t2i_cache_check(M.m, x, hw, sched[k], k, n, tau, state, mode=mode)
+        for r in range(w.n_req):
+            m = dit.cache_signal(M.W, w, xk[r].astype(np.float64), sched[k, r])
+            st = states[r]
+            sk, d = sampler.cache_decide(st, m, k, n, tau, sampler.MODE_PER_STEP)
+            if not sk:
+                st.residual = True
+            if k > 0:
+                assert abs(rel[r] - d) <= 1e-6 * abs(d) + 1e-12, (k, r, rel[r], d)
+            assert bool(skip[r]) == sk, (k, r)
+            assert log_full[k, r] == skip[r], (k, r)
+        t2i.t2i_dit_step(M.m, x, hw, sched[k], tx, t_next=sched[k + 1], skip=skip,
+                         cache_state=state)
+    torch.cuda.synchronize()
+    say(f"per-step cache: {int(log_full.sum())} skipped request-steps of {n * w.n_req}")
+    assert log_full.sum() > 0
+    # checkpoint to host, restore into fresh buffers, resume on a second handle
+    ck_x, ck_state = x.cpu().numpy().copy(), state.cpu().numpy().copy()
+    del x, state
+    m2 = t2i.t2i_dit_init(M.cfg, M.dev)
+    x2 = torch.from_numpy(ck_x).to(DEV)
+    st2 = torch.from_numpy(ck_state).to(DEV)
+    log2, _ = t2i.t2i_dit_sample(m2, x2, hw, tx, n, timesteps=sched, start_step=k_stop,
+                                 cache_tau=tau, cache_mode=mode, cache_state=st2)
+    torch.cuda.synchronize()
+    assert np.array_equal(log2[k_stop:], log_full[k_stop:])
+    assert np.array_equal(x2.cpu().numpy(), x_full.cpu().numpy())
+    m2.close()
+    del m2
+    gc.collect()
+    torch.cuda.empty_cache()

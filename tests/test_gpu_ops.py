@@ -250,6 +250,28 @@ def test_attention_bf16_full_size_sampled_rows():
     assert rel_l2(got[rows], ref) < 6e-3
 
 
+@pytest.mark.parametrize("sharp", [4.0, 8.0, 16.0])
+def test_attention_bf16_sharp_logits(sharp):
+    """Large logits: queries scaled by 4..16 and key norms growing along the
+    sequence, so that later key tiles keep raising the row maximum (the
+    kernel's lazy rescale, taken when a score exceeds the kept maximum by 2^8,
+    fires after the first tile) and the softmax is sharp."""
+    H, d, nq, nk = 4, 72, 300, 1000
+    q = synth.round_bf16(rnd(80, (nq, H * d)) * sharp)
+    ramp = np.linspace(0.4, 1.6, nk, dtype=np.float32)[:, None]
+    k = synth.round_bf16(rnd(81, (nk, H * d)) * ramp)
+    v = rnd(82, (nk, H * d))
+    seqs = [(0, nq, 0, nk)]
+    got = run_attention(_lib.T2I_BF16, H, d, seqs, q, k, v)
+    ref = attention_ref(seqs, q, k, v, H)
+    err = rel_l2(got, ref)
+    rows = np.linalg.norm(got - ref, axis=1) / np.linalg.norm(ref, axis=1)
+    lg = np.abs(q[:, :d].astype(np.float64) @ k[:, :d].astype(np.float64).T) / np.sqrt(d)
+    say(f"attention bf16 sharp x{sharp}: max |logit| {lg.max():.1f}, rel_l2 {err:.2e}, "
+        f"worst row {rows.max():.2e}")
+    assert err < 6e-3 and rows.max() < 3e-2
+
+
 def _packed_keys(lengths):
     """Key row starts (multiples of 8, as the bf16 kernel requires) for
     sequences of the given key counts, and the total row count."""
