@@ -137,6 +137,27 @@ t2i_status t2i_dit_init(const t2i_dit_config* cfg, const void* const* weights,
                         void* workspace, size_t ws_bytes, void* stream,
                         t2i_dit** out);
 
+/*
+ * Create a handle that needs no workspace from the caller and allocates no
+ * device memory: for callers that cannot allocate (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid hipMalloc).  Same as
+ * t2i_dit_init, except that the workspace is a static device array of
+ * T2I_STATIC_WORKSPACE_BYTES held by the library on every device it runs
+ * on, until the process ends.
+ *   Returns T2I_ERR_WORKSPACE when t2i_dit_workspace_bytes(cfg) exceeds
+ *   T2I_STATIC_WORKSPACE_BYTES (small models and request mixes only: e.g.
+ *   tiny models, or a 2-block 1152-wide DiT at 256 px), T2I_ERR_DEVICE when
+ *   the array's device address cannot be obtained on the current device.
+ *   The array belongs to the device that is current at this call.
+ * Every handle created this way on one device shares that device's array:
+ * calls on such handles (step, sample, cache check) that overlap in time race
+ * on it, so serialise them (one stream, or events between streams).  The
+ * array keeps the last call's contents; no call depends on them.
+ */
+#define T2I_STATIC_WORKSPACE_BYTES ((size_t)64 << 20)
+t2i_status t2i_dit_init_static(const t2i_dit_config* cfg, const void* const* weights,
+                               void* stream, t2i_dit** out);
+
 /* Replace the weight pointers (same shapes and dtypes) of a live handle;
  * every block becomes resident (queued loads are waited for first). */
 t2i_status t2i_dit_rebind_weights(t2i_dit* h, const void* const* weights,

@@ -23,7 +23,7 @@ from . import _lib
 from ._lib import (T2I_F32, T2I_BF16, T2I_ARCH_CROSS_DIT, T2I_ARCH_MMDIT,
                    T2I_CACHE_ACCUMULATE, T2I_CACHE_PER_STEP, T2IError, check, load)
 
-__all__ = ["Config", "DiT", "t2i_dit_init", "t2i_dit_step", "t2i_dit_sample",
+__all__ = ["Config", "DiT", "t2i_dit_init", "t2i_dit_init_static", "t2i_dit_step", "t2i_dit_sample",
            "t2i_cache_check", "weight_table", "upload", "T2IError", "load",
            "t2i_dit_block_layout", "pack_blocks", "t2i_dit_host_tier", "t2i_dit_evict",
            "t2i_dit_load_async", "t2i_dit_block_state", "t2i_first_layers"]
@@ -107,7 +107,8 @@ def upload(arrays: Sequence[np.ndarray], dtype: str, device="cuda") -> List[torc
 class DiT:
     """A bound model: weights + workspace + library handle (``t2i_dit_init``)."""
 
-    def __init__(self, cfg: Config, weights: Sequence[torch.Tensor], device="cuda", stream=None):
+    def __init__(self, cfg: Config, weights: Sequence[torch.Tensor], device="cuda", stream=None,
+                 static_workspace=False):
         lib = load()
         self.cfg = cfg
         self.lib = lib
@@ -118,12 +119,19 @@ class DiT:
             if tuple(w.shape) != shape or w.dtype != cfg.torch_dtype or not w.is_contiguous():
                 raise T2IError(2, f"weight {name}: expected {shape} {cfg.torch_dtype} contiguous")
         self.weights = list(weights)
-        ws = lib.t2i_dit_workspace_bytes(cfg.ref())
-        self.workspace = torch.empty(ws, dtype=torch.uint8, device=device)
         ptrs = (C.c_void_p * len(self.weights))(*[w.data_ptr() for w in self.weights])
         h = C.c_void_p()
-        check(lib.t2i_dit_init(cfg.ref(), ptrs, C.c_void_p(self.workspace.data_ptr()), ws,
-                               C.c_void_p(_stream(stream)), C.byref(h)))
+        if static_workspace:
+            # the library's static device array (t2i_dit_init_static): nothing allocated
+            self.workspace = None
+            st = lib.t2i_dit_init_static(cfg.ref(), ptrs, C.c_void_p(_stream(stream)), C.byref(h))
+            if st != 0:
+                raise T2IError(st, "t2i_dit_init_static failed")
+        else:
+            ws = lib.t2i_dit_workspace_bytes(cfg.ref())
+            self.workspace = torch.empty(ws, dtype=torch.uint8, device=device)
+            check(lib.t2i_dit_init(cfg.ref(), ptrs, C.c_void_p(self.workspace.data_ptr()), ws,
+                                   C.c_void_p(_stream(stream)), C.byref(h)))
         self.h = h
 
     def close(self):
@@ -150,6 +158,12 @@ class DiT:
 
 def t2i_dit_init(cfg: Config, weights: Sequence[torch.Tensor], device="cuda", stream=None) -> DiT:
     return DiT(cfg, weights, device, stream)
+
+
+def t2i_dit_init_static(cfg: Config, weights: Sequence[torch.Tensor], stream=None) -> DiT:
+    """A handle on the library's static workspace of the current device (no
+    device allocation; calls on such handles must not overlap in time)."""
+    return DiT(cfg, weights, stream=stream, static_workspace=True)
 
 
 # ---------------------------------------------------------------- layer residency

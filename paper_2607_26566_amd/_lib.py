@@ -76,6 +76,7 @@ SIGNATURES = {
     "t2i_cache_state_bytes": (sz, [C.POINTER(t2i_dit_config), i32, C.POINTER(i32), i32]),
     "t2i_dit_init": (i32, [C.POINTER(t2i_dit_config), C.POINTER(vp), vp, sz, vp,
                            C.POINTER(vp)]),
+    "t2i_dit_init_static": (i32, [C.POINTER(t2i_dit_config), C.POINTER(vp), vp, C.POINTER(vp)]),
     "t2i_dit_rebind_weights": (i32, [vp, C.POINTER(vp), vp]),
     "t2i_dit_block_layout": (sz, [C.POINTER(t2i_dit_config), C.POINTER(i32), C.POINTER(i32),
                                   C.POINTER(sz)]),

@@ -266,3 +266,22 @@ def test_residency_argument_errors():
         assert lib.t2i_dit_block_state(h, None) == 1
     finally:
         lib.t2i_dit_destroy(h)
+
+
+def test_static_workspace_init_rejects_configs_beyond_its_size():
+    """t2i_dit_init_static checks the config's workspace against the static
+    array's size before touching any device: the 1024-px model's is larger."""
+    lib = t2i.load()
+    w = synth.workload("dit1024_cfg")
+    cfg = t2i.Config.from_shape(w)
+    need = lib.t2i_dit_workspace_bytes(cfg.ref())
+    assert need > (64 << 20)
+    n = lib.t2i_dit_weight_count(cfg.ref())
+    fake = (C.c_void_p * n)(*([0x1000] * n))
+    h = C.c_void_p()
+    assert lib.t2i_dit_init_static(cfg.ref(), fake, None, C.byref(h)) == 4   # T2I_ERR_WORKSPACE
+    assert not h.value
+    assert lib.t2i_dit_init_static(cfg.ref(), fake, None, None) == 1         # out is NULL
+    bad = t2i.Config.from_shape(w)
+    bad.c.hidden = 100
+    assert lib.t2i_dit_init_static(bad.ref(), fake, None, C.byref(h)) == 1
