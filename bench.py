@@ -97,6 +97,21 @@ def class_work(w):
     }
 
 
+def step_class_bytes(w):
+    """Algorithmic HBM bytes of the once-per-step kernels: patch embedding
+    (latent read, x0 and one residual copy per branch written), final layer
+    (residual rows read; latent read, latent and velocity written) and the
+    cache check (x0 and m_prev read, m written)."""
+    T, D = w.image_tokens, w.hidden
+    lat = 4.0 * T * w.patch_dim
+    return {"embed": lat + 4.0 * T * D * (1 + w.branches),
+            "final": 4.0 * T * D * w.branches + 3 * lat,
+            "cache": 3 * 4.0 * T * D}
+
+
+PEAK_F32_TFLOPS = 157.3        # MI355X fp32 vector (SIMT), 256 CU x 2.4 GHz
+
+
 def step_flops(w):
     cw = class_work(w)
     return w.depth * sum(v for kind, v, _ in cw.values() if kind == "flop")
@@ -171,8 +186,9 @@ def lora_cost(t2i, table, dev, rank):
         nbytes += 2 * dev[i].numel() * dev[i].element_size() + (a.numel() + b.numel()) * a.element_size()
     torch.cuda.synchronize()
     ms = sum(e0.elapsed_time(e1) for e0, e1 in evs)
-    return {"rank": rank, "layers": len(idx), "gpu_ms": round(ms, 3),
-            "hbm_gbs": round(nbytes / (ms / 1e3) / 1e9, 1)}
+    gbs = nbytes / (ms / 1e3) / 1e9
+    return {"rank": rank, "layers": len(idx), "gpu_ms": round(ms, 3), "bytes": nbytes,
+            "hbm_gbs": round(gbs, 1), "hbm_frac": round(gbs / PEAK_HBM_GBS, 4)}
 
 
 def sched_bench(tenants=64, ready_per_tenant=4, decisions=20000):
@@ -209,6 +225,59 @@ def sched_bench(tenants=64, ready_per_tenant=4, decisions=20000):
             "cpu_baseline": {"value": round(orate, 1), "unit": "decisions/s", "cores": 1,
                              "kind": "oracle",
                              "sample": f"{decisions // 20} decisions of the Python oracle"}}
+
+
+def request_flops(w, r):
+    """GEMM + attention FLOPs of one request's rows in one step (all guidance
+    branches), as class_work counts them."""
+    n, D, F, M = w.tokens(r), w.hidden, w.mlp_hidden, w.text_tokens
+    dh = w.heads * w.head_dim
+    per_row = 2.0 * (3 * D * D + D * D + D * D + D * D + 2 * F * D)
+    attn = 4.0 * n * n * dh + 4.0 * n * M * dh
+    return w.depth * w.branches * (n * per_row + attn)
+
+
+def cache_bench(t2i, m, w, x, x_init, hw, tx, sched, n_samples, warmup):
+    """Whole samples with the step-skip cache on (tau of the workload, 0.1 if
+    it has none): effective steps/s, and the FLOPs of the requests that ran
+    their blocks (skipped requests cost x0 + R and the final layer only)."""
+    import numpy as np
+    import torch
+    tau = w.cache_tau if w.cache_tau > 0 else 0.1
+    toks = [w.tokens(r) for r in range(w.n_req)]
+    state = m.new_cache_state(toks, w.branches)
+    n = w.steps
+    ts = np.array(sched)
+
+    def one():
+        x.copy_(x_init)
+        return t2i.t2i_dit_sample(m, x, hw, tx, n, guidance=w.guidance, timesteps=ts,
+                                  cache_tau=tau, cache_state=state)[0]
+    for _ in range(warmup):
+        one()
+    torch.cuda.synchronize()
+    logs = []
+    t0 = time.perf_counter()
+    for _ in range(n_samples):
+        logs.append(one())
+    torch.cuda.synchronize()
+    el = time.perf_counter() - t0
+    rf = np.array([request_flops(w, r) for r in range(w.n_req)])
+    executed = sum(float(((1 - lg) * rf[None, :]).sum()) for lg in logs)
+    full = float(rf.sum()) * n * n_samples
+    steps = n * n_samples
+    skipped = int(sum(lg.sum() for lg in logs))
+    return {
+        "metric": f"effective denoising steps/s with the step-skip cache (tau {tau}) on {w.name}",
+        "value": round(steps / el, 3), "unit": "steps/s", "steps": steps,
+        "ms_per_step": round(el * 1e3 / steps, 3), "higher_is_better": True,
+        "data": "synthetic", "cache_tau": tau,
+        "skipped_request_steps": skipped, "request_steps": steps * w.n_req,
+        "executed_flop_frac": round(executed / full, 4),
+        "executed_tflops": round(executed / el / 1e12, 1),
+        "executed_frac_of_peak": round(executed / el / 1e12 / PEAK_BF16_TFLOPS, 4),
+        "skip_log_first_sample": logs[0].tolist(),
+    }
 
 
 PCIE5_X16_GBS = 63.0   # PCIe 5.0 x16, one direction: 32 GT/s x 16 lanes x 128/130
@@ -305,6 +374,9 @@ WORKLOADS = {
                   "mmdit1024: latent 16x128x128, patch 2 -> 4096 image tokens + 512 text tokens "
                   "(4096 -> 3072), hidden 3072, 19 joint blocks, 24 heads x 128, MLP 12288, "
                   "2D RoPE, seed 3"),
+    "tiny_f32": ("denoising steps/s of the tiny fp32 DiT (64 tokens)",
+                 "tiny_f32: fp32, latent 4x16x16, patch 2 -> 64 tokens, hidden 128, 2 blocks, "
+                 "2 heads x 64, MLP 512, 16 text tokens x 128, 4 steps, seed 0"),
     "packed8": ("denoising steps/s of a packed 8-request batch (12032 tokens)",
                 "packed8: 3x256px + 3x512px + 2x1024px requests packed (256/1024/4096 tokens "
                 "each, 12032 total), own timestep each, hidden 1152, 28 blocks, 16 heads x 72, "
@@ -325,6 +397,8 @@ def main():
                     help="also time merging a rank-R LoRA into every 2-D block weight")
     ap.add_argument("--loading", action="store_true",
                     help="time first-layers caching with progressive loading instead")
+    ap.add_argument("--cache", action="store_true",
+                    help="time whole samples with the step-skip cache on (effective steps/s)")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="run only a plain 1 GiB device copy (HBM counter calibration)")
     args = ap.parse_args()
@@ -377,7 +451,7 @@ def main():
     lats, texts = synth.latents(w), synth.texts(w)
     hw = list(w.requests)
     x = torch.from_numpy(np.concatenate([l.ravel() for l in lats])).cuda()
-    tx = torch.from_numpy(np.stack(texts)).to("cuda", torch.bfloat16)
+    tx = torch.from_numpy(np.stack(texts)).to("cuda", torch.bfloat16 if w.dtype == "bf16" else torch.float32)
     n = w.steps
     t0s = synth.start_times(w)
     sched = [[t0 * (1.0 - k / n) for t0 in t0s] for k in range(n + 1)]
@@ -390,6 +464,21 @@ def main():
         def one_step(n_blocks=-1):
             t2i.t2i_dit_step(m, x, hw, sched[0], tx, guidance=w.guidance, n_blocks=n_blocks)
         print(json.dumps(loading_bench(t2i, m, cfg, w, dev, one_step)), flush=True)
+        return
+
+    if args.cache:
+        x_init = x.clone()
+        out = cache_bench(t2i, m, w, x, x_init, hw, tx, sched, max(1, args.steps // n),
+                          max(1, args.warmup // n + 1))
+        # the same samples with the cache off, for comparison
+        t_off = time.perf_counter()
+        for _ in range(max(1, args.steps // n)):
+            x.copy_(x_init)
+            t2i.t2i_dit_sample(m, x, hw, tx, n, guidance=w.guidance, timesteps=np.array(sched))
+        torch.cuda.synchronize()
+        out["cache_off_steps_per_s"] = round(max(1, args.steps // n) * n / (time.perf_counter() - t_off), 3)
+        out["config"] = {"workload": WORKLOADS[args.workload][1].replace("cache skip off", "cache skip on")}
+        print(json.dumps(out), flush=True)
         return
 
     lib = t2i.load()
@@ -426,10 +515,12 @@ def main():
     kind, work_block, per_blk = cw[dominant]
     blocks = w.depth * args.steps                      # blocks executed in the timed region
     dom_s = tot.value / 1e3
+    f32 = w.dtype != "bf16"
+    peak_flops = PEAK_F32_TFLOPS if f32 else PEAK_BF16_TFLOPS
     if kind == "flop":
         ach = work_block * blocks / dom_s / 1e12
-        roof = {"bound": "mfma", "achieved": round(ach, 1), "peak": PEAK_BF16_TFLOPS,
-                "unit": "TFLOP/s", "frac": round(ach / PEAK_BF16_TFLOPS, 4), "traffic": None}
+        roof = {"bound": "alu" if f32 else "mfma", "achieved": round(ach, 1), "peak": peak_flops,
+                "unit": "TFLOP/s", "frac": round(ach / peak_flops, 4), "traffic": None}
     else:
         ach = work_block * blocks / dom_s / 1e9
         roof = {"bound": "hbm", "achieved": round(ach, 1), "peak": PEAK_HBM_GBS,
@@ -452,6 +543,16 @@ def main():
     gemm_attn_ms = sum(v[0] for k, v in per_class.items() if k in cw and cw[k][0] == "flop")
     ln_ms = per_class["ln_mod"][0]
     ln_bytes = cw["ln_mod"][1] * w.depth
+    # HBM fraction of the memory-bound kernels over the profiled step
+    sb = step_class_bytes(w)
+    hbm = {"ln_mod": (ln_bytes, ln_ms)}
+    for k in ("embed", "final"):
+        if per_class.get(k, (0, 0))[1]:
+            hbm[k] = (sb[k], per_class[k][0])
+    hbm_frac = {k: {"gbs": round(b / (t / 1e3) / 1e9, 1),
+                    "frac": round(b / (t / 1e3) / 1e9 / PEAK_HBM_GBS, 4),
+                    "avg_launch_ms": round(t / max(per_class[k][1], 1), 4)}
+                for k, (b, t) in hbm.items() if t > 0}
 
     # a whole sample (conditioning and text computed once per sample)
     x.copy_(torch.from_numpy(np.concatenate([l.ravel() for l in lats])).cuda())
@@ -479,10 +580,11 @@ def main():
                    "parallelism": "none (1 GPU)"},
         "roofline": roof,
         "gemm_attn_tflops_step": round(flops * sps / 1e12, 1),
-        "gemm_attn_frac_of_peak_step": round(flops * sps / 1e12 / PEAK_BF16_TFLOPS, 4),
+        "gemm_attn_frac_of_peak_step": round(flops * sps / 1e12 / peak_flops, 4),
         "gemm_attn_tflops_kernels": round(flops / (gemm_attn_ms / 1e3) / 1e12, 1),
-        "gemm_attn_frac_of_peak_kernels": round(flops / (gemm_attn_ms / 1e3) / 1e12 / PEAK_BF16_TFLOPS, 4),
+        "gemm_attn_frac_of_peak_kernels": round(flops / (gemm_attn_ms / 1e3) / 1e12 / peak_flops, 4),
         "ln_mod_gbs": round(ln_bytes / (ln_ms / 1e3) / 1e9, 1) if ln_ms > 0 else None,
+        "hbm_frac": hbm_frac,
         "images_per_s": round(w.n_req / sample_s, 3),
         "sample_steps_per_s": round(n / sample_s, 3),
         "kernel_avg_ms": kernel_ms,

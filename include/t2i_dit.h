@@ -369,7 +369,11 @@ t2i_status t2i_dit_block_state(t2i_dit* h, int32_t* state);
 typedef enum {
   T2I_K_GEMM_QKV = 0, T2I_K_ATTN_SELF = 1, T2I_K_GEMM_O = 2, T2I_K_GEMM_XQ = 3,
   T2I_K_ATTN_CROSS = 4, T2I_K_GEMM_XO = 5, T2I_K_LN = 6, T2I_K_GEMM_FC1 = 7,
-  T2I_K_GEMM_FC2 = 8, T2I_K_COUNT = 9
+  T2I_K_GEMM_FC2 = 8,
+  T2I_K_EMBED = 9,    /* patch + position embedding of a step */
+  T2I_K_FINAL = 10,   /* final layer + guidance + Euler update */
+  T2I_K_CACHE = 11,   /* cache-skip signal and decision */
+  T2I_K_COUNT = 12
 } t2i_kernel_class;
 
 t2i_status t2i_dit_profile(t2i_dit* h, uint32_t class_mask);

@@ -19,7 +19,7 @@ T2I_EPI_STORE, T2I_EPI_GELU, T2I_EPI_SILU, T2I_EPI_RESID, T2I_EPI_RESID_GATED = 
 T2I_MAX_SEQ, T2I_MAX_REQ = 64, 32
 
 KERNEL_CLASSES = ["gemm_qkv", "attn_self", "gemm_o", "gemm_xq", "attn_cross", "gemm_xo",
-                  "ln_mod", "gemm_fc1", "gemm_fc2"]
+                  "ln_mod", "gemm_fc1", "gemm_fc2", "embed", "final", "cache"]
 
 STATUS_NAMES = {0: "T2I_OK", 1: "T2I_ERR_INVALID_ARG", 2: "T2I_ERR_SHAPE",
                 3: "T2I_ERR_UNSUPPORTED", 4: "T2I_ERR_WORKSPACE",

@@ -11,6 +11,7 @@
 #include <cstdio>
 #include <cstring>
 #include <string>
+#include <utility>
 #include <vector>
 
 #include "../../include/t2i_dit.h"
@@ -147,9 +148,10 @@ const char* check_config(const t2i_dit_config* c) {
 // workspace layout
 
 struct Layout {
-  size_t x, x0, h, xb, qkv, vt, o, u, ytxt, kv, vtt, rope, pe, splitk, tfreq, th1, tsc, mod, partial,
-      total;
+  size_t x, x0, xf, h, xb, qkv, vt, o, u, ytxt, kv, vtt, rope, pe, splitk, tfreq, th1, tsc, mod,
+      partial, total;
   size_t splitk_floats = 0;
+  bool has_xf = false;          // xf allocated (cross-DiT, several requests)
   int ldvt = 0, ldvt_txt = 0;   // token strides of the transposed V buffers
 };
 
@@ -172,6 +174,11 @@ Layout layout(const t2i_dit_config& c) {
   };
   L.x = take(rows * D * 4);
   L.x0 = take(rows * D * 4);
+  // cross-DiT batches of several requests: the image rows of every request
+  // in the call's layout while the blocks run on the computing requests only
+  // (compacted; see step_body)
+  L.has_xf = !mm && c.max_requests > 1;
+  L.xf = take(L.has_xf ? (size_t)c.max_tokens * D * 4 : 0);
   L.h = take(rows * D * A);
   L.xb = take(c.dtype == T2I_BF16 ? rows * D * 2 : 0);
   L.qkv = take(rows * 3 * D * A);
@@ -646,21 +653,23 @@ t2i_status run_blocks_cross(t2i_dit* h, const Plan& P, int nb, hipStream_t st) {
                                                P.img, hb, D, c.ln_eps, st));
     Epi e = make_epi();
     e.out = qkv;
-    if (bf) {   // q|k row-major [R, 2D], v transposed [D][ldvt]
+    if (bf) {   // q (scaled for the softmax) | k row-major [R, 2D], v transposed [D][ldvt]
       e.ldo = 2 * D;
       e.vt = vt;
       e.ldvt = h->L.ldvt;
       e.vcol0 = 2 * D;
+      e.qscale = attn_q_scale(c.head_dim);
+      e.qcols = D;
       TIMED(h, T2I_K_GEMM_QKV, st, linear(h, hb, D, wb + X_QKV, R, 3 * D, D, EPI_SPLIT_VT, e, st));
       TIMED(h, T2I_K_ATTN_SELF, st,
             launch_attention(bf, 0, c.heads, c.head_dim, P.self, qkv, 2 * D, qkv + D * A, 2 * D, vt,
-                             h->L.ldvt, o, D, st));
+                             h->L.ldvt, o, D, st, true));
     } else {
       e.ldo = 3 * D;
       TIMED(h, T2I_K_GEMM_QKV, st, linear(h, hb, D, wb + X_QKV, R, 3 * D, D, EPI_STORE, e, st));
       TIMED(h, T2I_K_ATTN_SELF, st,
             launch_attention(bf, 0, c.heads, c.head_dim, P.self, qkv, 3 * D, qkv + D * A, 3 * D,
-                             qkv + 2 * D * A, 3 * D, o, D, st));
+                             qkv + 2 * D * A, 3 * D, o, D, st, false));
     }
     e = make_epi();
     e.x = x;
@@ -674,6 +683,10 @@ t2i_status run_blocks_cross(t2i_dit* h, const Plan& P, int nb, hipStream_t st) {
     e = make_epi();
     e.out = qkv;
     e.ldo = D;
+    if (bf) {   // the cross-attention query, scaled for the softmax
+      e.qscale = attn_q_scale(c.head_dim);
+      e.qcols = D;
+    }
     TIMED(h, T2I_K_GEMM_XQ, st,
           linear(h, bf ? (const void*)xb : (const void*)x, D, wb + X_XQ, R, D, D, EPI_STORE, e, st));
     const char* kv = h->at<char>(h->L.kv) + (size_t)b * txt_rows_max * 2 * D * A;
@@ -681,11 +694,11 @@ t2i_status run_blocks_cross(t2i_dit* h, const Plan& P, int nb, hipStream_t st) {
       TIMED(h, T2I_K_ATTN_CROSS, st,
             launch_attention(bf, 1, c.heads, c.head_dim, P.cross, qkv, D, kv, D,
                              h->at<bf16>(h->L.vtt) + (size_t)b * D * h->L.ldvt_txt,
-                             h->L.ldvt_txt, o, D, st));
+                             h->L.ldvt_txt, o, D, st, true));
     else
       TIMED(h, T2I_K_ATTN_CROSS, st,
             launch_attention(bf, 1, c.heads, c.head_dim, P.cross, qkv, D, kv, 2 * D, kv + D * A,
-                             2 * D, o, D, st));
+                             2 * D, o, D, st, false));
     e = make_epi();
     e.x = x;
     e.ldx = D;
@@ -733,12 +746,14 @@ t2i_status run_blocks_mmdit(t2i_dit* h, const Plan& P, int nb, hipStream_t st) {
       TIMED(h, T2I_K_LN, st, launch_ln_modulate(true, R, D, x + (size_t)r0 * D, D, mod, mw, mo,
                                                  mo + D, *maps[s], hb + (size_t)r0 * D, D,
                                                  c.ln_eps, st));
-      Epi e = make_epi();   // q|k row-major [rows, 2D], v transposed [D][ldvt]
+      Epi e = make_epi();   // q (scaled) | k row-major [rows, 2D], v transposed [D][ldvt]
       e.out = qkv + (size_t)r0 * 2 * D;
       e.ldo = 2 * D;
       e.vt = vt + r0;
       e.ldvt = h->L.ldvt;
       e.vcol0 = 2 * D;
+      e.qscale = attn_q_scale(c.head_dim);
+      e.qcols = D;
       TIMED(h, T2I_K_GEMM_QKV, st,
             linear(h, hb + (size_t)r0 * D, D, wi + J_QKV, R, 3 * D, D, EPI_SPLIT_VT, e, st));
     }
@@ -746,7 +761,7 @@ t2i_status run_blocks_mmdit(t2i_dit* h, const Plan& P, int nb, hipStream_t st) {
                                  st));
     TIMED(h, T2I_K_ATTN_SELF, st,
           launch_attention(true, 0, c.heads, c.head_dim, P.joint, qkv, 2 * D, qkv + D, 2 * D, vt,
-                           h->L.ldvt, o, D, st));
+                           h->L.ldvt, o, D, st, true));
     for (int s = 0; s < 2; ++s) {
       const int r0 = r0s[s], R = ns[s], wi = W_BLOCK0 + b * 2 * J_PER_STREAM + s * J_PER_STREAM;
       const int mo = b * 12 * D + s * 6 * D;
@@ -808,10 +823,12 @@ t2i_status cache_check_impl(t2i_dit* h, const Plan& P, int step, int n_steps, do
   double* partial = h->at<double>(h->L.partial);
   // block 0's first LN-modulation (MMDiT: of the image stream)
   const int sh = is_mmdit(h) ? 6 * c.hidden : 0;
+  HIP_TRY(h, prof_mark(h, T2I_K_CACHE, true, st));
   HIP_TRY(h, launch_cache_signal(h->at<float>(h->L.x0), P.rm, h->at<float>(h->L.mod),
                                  mod_width(c), sh, sh + c.hidden, c.hidden, c.ln_eps, cp.m_prev,
                                  cp.hdr, step, partial, st));
   HIP_TRY(h, launch_cache_decide(P.rm, partial, cp.hdr, step, n_steps, tau, mode, st));
+  HIP_TRY(h, prof_mark(h, T2I_K_CACHE, false, st));
   h->hdr_host.resize(P.n_req);
   HIP_TRY(h, hipMemcpyAsync(h->hdr_host.data(), cp.hdr, sizeof(CacheHeader) * P.n_req,
                             hipMemcpyDeviceToHost, st));
@@ -875,6 +892,58 @@ t2i_status drain_loads(t2i_dit* h) {
   return T2I_OK;
 }
 
+// The plan restricted to the requests in `mask`: their image rows packed in
+// the same branch-major order; latent offsets, modulation rows and text rows
+// (per request, plus the shared unconditional prompt) stay those of P, so the
+// blocks compute for each of them exactly what they compute in P.  `g`
+// receives the row segments that move P's layout to the compacted one.
+void compute_subplan(const t2i_dit* h, const Plan& P, uint32_t mask, Plan& Q, RowCopyMap& g) {
+  const int M = h->cfg.text_tokens;
+  Q = P;
+  int orig[kMaxReq];
+  int n = 0, tok = 0;
+  for (int r = 0; r < P.n_req; ++r) {
+    if (!((mask >> r) & 1u)) continue;
+    orig[n] = r;
+    Q.rm.tok_off[n] = tok;
+    Q.rm.lat_off[n] = P.rm.lat_off[r];
+    Q.rm.h[n] = P.rm.h[r];
+    Q.rm.w[n] = P.rm.w[r];
+    Q.rm.modrow[n] = P.rm.modrow[r];
+    Q.rm.dt[n] = P.rm.dt[r];
+    tok += P.rm.tok_off[r + 1] - P.rm.tok_off[r];
+    ++n;
+  }
+  Q.n_req = Q.rm.n = n;
+  Q.rm.tok_off[n] = tok;
+  Q.rm.tokens_total = Q.T_img = tok;
+  Q.rows = tok * P.branches;
+  Q.img.n = Q.self.n = Q.cross.n = n * P.branches;
+  g.n = 0;
+  int moved = 0;
+  for (int br = 0; br < P.branches; ++br)
+    for (int i = 0; i < n; ++i) {
+      const int r = orig[i], s = br * n + i;
+      const int start = br * tok + Q.rm.tok_off[i];
+      const int len = Q.rm.tok_off[i + 1] - Q.rm.tok_off[i];
+      Q.img.start[s] = start;
+      Q.img.modrow[s] = P.rm.modrow[r];
+      Q.self.q_start[s] = Q.cross.q_start[s] = start;
+      Q.self.q_len[s] = Q.cross.q_len[s] = len;
+      Q.self.k_start[s] = start;
+      Q.self.k_len[s] = len;
+      Q.cross.k_start[s] = br == 0 ? r * M : P.n_req * M;
+      Q.cross.k_len[s] = M;
+      g.src[g.n] = br * P.T_img + P.rm.tok_off[r];
+      g.dst[g.n] = start;
+      moved += len;
+      g.row_end[g.n++] = moved;
+    }
+  Q.img.start[Q.img.n] = Q.rows;
+  attention_tiles(Q.self, h->bf(), h->cfg.heads, 0);
+  attention_tiles(Q.cross, h->bf(), h->cfg.heads, 1);
+}
+
 // Embed, blocks (or cached residual), final layer for one step whose
 // conditioning rows start at `modbase`.
 t2i_status step_body(t2i_dit* h, Plan& P, const float* latents_in, float* latents,
@@ -884,17 +953,36 @@ t2i_status step_body(t2i_dit* h, Plan& P, const float* latents_in, float* latent
   const int D = c.hidden;
   float* x = h->at<float>(h->L.x);
   float* x0 = h->at<float>(h->L.x0);
-  float* xi = x + (size_t)img_row0(h, P) * D;   // image stream of the residual
-  HIP_TRY(h, embed(h, P, latents_in, x0, xi, P.branches, st));
-  if (is_mmdit(h))
-    HIP_TRY(h, hipMemcpyAsync(x, h->at<float>(h->L.ytxt), (size_t)P.txt_rows * D * 4,
-                              hipMemcpyDeviceToDevice, st));
   uint32_t skip_mask = 0, compute_mask = 0;
   for (int r = 0; r < P.n_req; ++r) {
     if (skip && skip[r]) skip_mask |= 1u << r;
     else compute_mask |= 1u << r;
   }
-  if (compute_mask) {
+  // When some requests of a cross-DiT batch reuse their cached residual and
+  // others compute, the blocks run on the computing requests' rows alone:
+  // the call's image rows live in xf, the computing ones are gathered into
+  // x, run, and scattered back.  (Not with a callback input, whose residuals
+  // are laid out over every request.)
+  const bool compact = skip_mask && compute_mask && nb > 0 && !is_mmdit(h) && !P.ctl &&
+                       h->L.has_xf;
+  float* xi = compact ? h->at<float>(h->L.xf)
+                      : x + (size_t)img_row0(h, P) * D;   // image rows, the call's layout
+  TIMED(h, T2I_K_EMBED, st, embed(h, P, latents_in, x0, xi, P.branches, st));
+  if (is_mmdit(h))
+    HIP_TRY(h, hipMemcpyAsync(x, h->at<float>(h->L.ytxt), (size_t)P.txt_rows * D * 4,
+                              hipMemcpyDeviceToDevice, st));
+  if (compact) {
+    Plan Q;
+    RowCopyMap g;
+    compute_subplan(h, P, compute_mask, Q, g);
+    HIP_TRY(h, launch_copy_rows(xi, x, g, D, st));
+    t2i_status s = run_blocks(h, Q, nb, st);
+    if (s != T2I_OK) return s;
+    P.done = Q.done;
+    RowCopyMap back = g;
+    std::swap(back.src, back.dst);
+    HIP_TRY(h, launch_copy_rows(x, xi, back, D, st));
+  } else if (compute_mask) {
     t2i_status s = run_blocks(h, P, nb, st);
     if (s != T2I_OK) return s;
   }
@@ -912,9 +1000,10 @@ t2i_status step_body(t2i_dit* h, Plan& P, const float* latents_in, float* latent
   }
   const int mw = mod_width(c);
   const int fb = final_base(c);
-  HIP_TRY(h, launch_final_layer(xi, P.rm, h->w[fb + 2], h->w[fb + 3], h->bf(), h->at<float>(h->L.mod),
-                                mw, mw - 2 * D, mw - D, D, c.latent_channels, c.patch, c.ln_eps,
-                                P.guidance, latents, noise_pred, st));
+  TIMED(h, T2I_K_FINAL, st,
+        launch_final_layer(xi, P.rm, h->w[fb + 2], h->w[fb + 3], h->bf(), h->at<float>(h->L.mod),
+                           mw, mw - 2 * D, mw - D, D, c.latent_channels, c.patch, c.ln_eps,
+                           P.guidance, latents, noise_pred, st));
   return T2I_OK;
 }
 
@@ -1368,7 +1457,7 @@ t2i_status t2i_op_attention(int32_t dtype, int32_t heads, int32_t head_dim, int3
   }
   attention_tiles(m, dtype == T2I_BF16, heads, 0);
   hipError_t err = launch_attention(dtype == T2I_BF16, 0, heads, head_dim, m, q, ldq, k, ldk, v, ldv,
-                                    o, ldo, (hipStream_t)stream);
+                                    o, ldo, (hipStream_t)stream, false);
   if (err != hipSuccess) return ops_fail(T2I_ERR_DEVICE, hipGetErrorString(err));
   return T2I_OK;
 }

@@ -111,8 +111,10 @@ __device__ __forceinline__ void decode_tile(const AttnMap& m, int heads, int L, 
 }
 
 // ROLE: 0 = self / joint attention, 1 = cross-attention to text (separate
-// instances, so that profiles tell them apart)
-template <int HD, int NW, int ST, int ROLE>
+// instances, so that profiles tell them apart).  QS: Q arrives already
+// multiplied by scale_log2 (the model's projections write it so, rounding the
+// scaled value once), else the scale is applied in fp32 to each score.
+template <int HD, int NW, int ST, int ROLE, bool QS>
 __global__ __launch_bounds__(NW * 64, 8 / NW) void attn_bf16_kernel(AttnMap map, int heads,
                                                            const bf16* __restrict__ Q, int ldq,
                                                            const bf16* __restrict__ K, int ldk,
@@ -167,11 +169,11 @@ __global__ __launch_bounds__(NW * 64, 8 / NW) void attn_bf16_kernel(AttnMap map,
   auto kst = [&](int st) { return smem + st * (KSTAGE + VSTAGE); };
   auto vst = [&](int st) { return smem + st * (KSTAGE + VSTAGE) + KSTAGE; };
 
-  // Q fragments (B operand of S^T): query qr, d = 16c + 8hl .. +7, as stored
-  // (bf16, unscaled: scores leave the MFMA in raw units, and the softmax
-  // scale log2(e)/sqrt(d) is applied in fp32 to each score before its
-  // exponential, so that no rounding of a scaled Q enters the logits); the
-  // shift slot d = HD is element 0 of chunk HD/16 in the lanes of half
+  // Q fragments (B operand of S^T): query qr, d = 16c + 8hl .. +7, as stored.
+  // Unless Q comes pre-scaled (QS), scores leave the MFMA in raw units and
+  // the softmax scale log2(e)/sqrt(d) is applied in fp32 to each score before
+  // its exponential: a scaled copy of a bf16 Q would be rounded a second time.
+  // The shift slot d = HD is element 0 of chunk HD/16 in the lanes of half
   // (HD%16)/8
   constexpr int BC = HD / 16, BH = (HD % 16) / 8;
   bf16x8 qf[DC];
@@ -322,12 +324,14 @@ __global__ __launch_bounds__(NW * 64, 8 / NW) void attn_bf16_kernel(AttnMap map,
     return fmaxf(m0, m1);
   };
 
-  // Online softmax with a lazily updated maximum m of the raw scores (kept
+  // Online softmax with a lazily updated maximum m of the scores (kept
   // bf16-representable, as it rides in Q's shift slot): scores arrive as
-  // S' = s - m and the probabilities are exp2(scale_log2 * S').  While no
-  // scaled S' exceeds 8 the stale maximum is kept: probabilities stay <= 256
-  // and the common scale cancels between numerator and row sum.
-  const float lazy_thr = 8.0f / scale_log2;   // 8 in log2 units, as a raw score
+  // S' = s - m and the probabilities are exp2(sc * S'), sc = 1 for a
+  // pre-scaled Q, else scale_log2.  While no sc * S' exceeds 8 the stale
+  // maximum is kept: probabilities stay <= 256 and the common scale cancels
+  // between numerator and row sum.
+  const float sc = QS ? 1.0f : scale_log2;
+  const float lazy_thr = 8.0f / sc;   // 8 in log2 units
   f32x16 o[DT];
 #pragma unroll
   for (int dt = 0; dt < DT; ++dt) o[dt] = f32x16{};
@@ -393,7 +397,7 @@ __global__ __launch_bounds__(NW * 64, 8 / NW) void attn_bf16_kernel(AttnMap map,
       const float mx = fmaxf(lm, __shfl_xor(lm, 32, 64)) + m_ref;   // tile maximum
       const float m_old = ti == 0 ? -INFINITY : m_ref;
       const float m_new = (float)(bf16)fmaxf(m_old, mx);
-      const float alpha = __builtin_amdgcn_exp2f((m_old - m_new) * scale_log2);
+      const float alpha = __builtin_amdgcn_exp2f(QS ? m_old - m_new : (m_old - m_new) * sc);
 #pragma unroll
       for (int kb = 0; kb < 2; ++kb) cur[kb] -= (m_new - m_ref);
 #pragma unroll
@@ -442,7 +446,7 @@ __global__ __launch_bounds__(NW * 64, 8 / NW) void attn_bf16_kernel(AttnMap map,
         const int e1 = sl + 1 < NE ? (32 * (sl + 1) + NE - 1) / NE : 32;
 #pragma unroll
         for (int i = e0; i < e1; ++i) {
-          pe[i] = __builtin_amdgcn_exp2f(cur[i >> 4][i & 15] * scale_log2);
+          pe[i] = __builtin_amdgcn_exp2f(QS ? cur[i >> 4][i & 15] : cur[i >> 4][i & 15] * sc);
           if (!ONES) psum += pe[i];
           if ((i & 7) == 7)
 #pragma unroll
@@ -463,7 +467,8 @@ __global__ __launch_bounds__(NW * 64, 8 / NW) void attn_bf16_kernel(AttnMap map,
       for (int q = 0; q < 4; ++q)
 #pragma unroll
         for (int e = 0; e < 8; ++e) {
-          const float p = __builtin_amdgcn_exp2f(cur[q >> 1][8 * (q & 1) + e] * scale_log2);
+          const float x = cur[q >> 1][8 * (q & 1) + e];
+          const float p = __builtin_amdgcn_exp2f(QS ? x : x * sc);
           if (!ONES) psum += p;
           pf[q][e] = (bf16)p;
         }
@@ -535,9 +540,8 @@ __global__ __launch_bounds__(NW * 64, 8 / NW) void attn_bf16_kernel(AttnMap map,
 // workgroups in flight are what counts (at 1024 px with guidance, 1024
 // workgroups: one round of the chip).
 // Layouts (K rows in swap23 key order, V^T chunk swizzle, ones row of V^T for
-// the row sums, unscaled Q with the softmax scale applied in fp32 to the
-// scores) are those of attn_bf16_kernel.
-template <int HD, int NW>
+// the row sums) and the QS convention are those of attn_bf16_kernel.
+template <int HD, int NW, bool QS>
 __global__ __launch_bounds__(NW * 64, (HD <= 72 ? 16 : 12) / NW) void attn_cross_kernel(
     AttnMap map, int heads, const bf16* __restrict__ Q, int ldq, const bf16* __restrict__ K,
     int ldk, const bf16* __restrict__ Vt, int ldvt, bf16* __restrict__ O, int ldo,
@@ -597,7 +601,7 @@ __global__ __launch_bounds__(NW * 64, (HD <= 72 ? 16 : 12) / NW) void attn_cross
       }
     }
   }
-  // Q fragments (unscaled); the ones row of both stages
+  // Q fragments (as stored); the ones row of both stages
   bf16x8 qf[DC];
 #pragma unroll
   for (int c = 0; c < DC; ++c) {
@@ -623,11 +627,11 @@ __global__ __launch_bounds__(NW * 64, (HD <= 72 ? 16 : 12) / NW) void attn_cross
   }
 
   // S^T of both tiles, masked past the sequence
-  f32x16 sc[2][2];
+  f32x16 sc_[2][2];
 #pragma unroll
   for (int t = 0; t < 2; ++t) {
 #pragma unroll
-    for (int kb = 0; kb < 2; ++kb) sc[t][kb] = f32x16{};
+    for (int kb = 0; kb < 2; ++kb) sc_[t][kb] = f32x16{};
     if (t < nt) {
 #pragma unroll
       for (int c = 0; c < DC; ++c) {
@@ -639,7 +643,7 @@ __global__ __launch_bounds__(NW * 64, (HD <= 72 ? 16 : 12) / NW) void attn_cross
             const int slot = KRS ? cc ^ ((r / KRS) & (CPR - 1)) : cc;
             kf = *(const bf16x8*)(kst(t) + r * PK + slot * 16);
           }
-          sc[t][kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[c], sc[t][kb], 0, 0, 0);
+          sc_[t][kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[c], sc_[t][kb], 0, 0, 0);
         }
       }
     }
@@ -652,12 +656,13 @@ __global__ __launch_bounds__(NW * 64, (HD <= 72 ? 16 : 12) / NW) void attn_cross
 #pragma unroll
       for (int e = 0; e < 16; ++e) {
         const int key = k0 + t * BKV + swap23(32 * kb + 8 * (e >> 2) + 4 * hl + (e & 3));
-        if (key >= k_end) sc[t][kb][e] = -INFINITY;
-        mx = fmaxf(mx, sc[t][kb][e]);
+        if (key >= k_end) sc_[t][kb][e] = -INFINITY;
+        mx = fmaxf(mx, sc_[t][kb][e]);
       }
   mx = fmaxf(mx, __shfl_xor(mx, 32, 64));   // the query's keys sit in lanes ql and ql + 32
-  // probabilities exp2(scale_log2 * (s - mx)), one fma per score
-  const float mxs = mx * scale_log2;
+  // probabilities exp2(sc * (s - mx)): a subtraction, or one fma per score
+  const float sc = QS ? 1.0f : scale_log2;
+  const float mxs = mx * sc;
 
   // P V over both tiles; row sums from the ones row or per lane
   f32x16 o[DT];
@@ -673,7 +678,8 @@ __global__ __launch_bounds__(NW * 64, (HD <= 72 ? 16 : 12) / NW) void attn_cross
       bf16x8 pf;
 #pragma unroll
       for (int e = 0; e < 8; ++e) {
-        const float p = __builtin_amdgcn_exp2f(fmaf(sc[t][q >> 1][8 * (q & 1) + e], scale_log2, -mxs));
+        const float x = sc_[t][q >> 1][8 * (q & 1) + e];
+        const float p = __builtin_amdgcn_exp2f(QS ? x - mx : fmaf(x, sc, -mxs));
         if (!ONES) psum += p;
         pf[e] = (bf16)p;
       }
@@ -808,7 +814,7 @@ void attention_tiles(AttnMap& m, bool bf16_io, int heads, int role) {
   m.waves = w;
 }
 
-template <int HD>
+template <int HD, bool QS>
 static hipError_t launch_hd(bool bf16_io, int role, int heads, const AttnMap& map, const void* q,
                             int ldq, const void* k, int ldk, const void* v, int ldv, void* o,
                             int ldo, hipStream_t st) {
@@ -822,9 +828,9 @@ static hipError_t launch_hd(bool bf16_io, int role, int heads, const AttnMap& ma
                                                  map.k2_start[s] + map.k2_len[s]));
     if ((size_t)2 * heads * HD * ldv > 0x7fffffff || (size_t)2 * (k_rows + 64) * ldk > 0x7fffffff)
       return hipErrorInvalidValue;
-    const float scale_log2 = 1.4426950408889634f / sqrtf((float)HD);
+    const float scale_log2 = attn_q_scale(HD);
 #define T2I_ATT(NW_, ST_, R_)                                                                   \
-  hipLaunchKernelGGL((attn_bf16_kernel<HD, NW_, ST_, R_>), dim3(tiles), dim3(NW_ * 64), 0, st, map, \
+  hipLaunchKernelGGL((attn_bf16_kernel<HD, NW_, ST_, R_, QS>), dim3(tiles), dim3(NW_ * 64), 0, st, map, \
                      heads, (const bf16*)q, ldq, (const bf16*)k, ldk, (const bf16*)v, ldv,       \
                      (bf16*)o, ldo, scale_log2)
     // smaller workgroups (2 or 4 waves) share a CU and use a 3-stage ring
@@ -834,7 +840,7 @@ static hipError_t launch_hd(bool bf16_io, int role, int heads, const AttnMap& ma
       for (int s = 0; s < map.n && short_text; ++s)
         short_text = map.k_len[s] >= 1 && map.k_len[s] <= 128 && map.k2_len[s] == 0;
       if (short_text)
-        hipLaunchKernelGGL((attn_cross_kernel<HD, kCrossWaves>), dim3(tiles), dim3(kCrossWaves * 64),
+        hipLaunchKernelGGL((attn_cross_kernel<HD, kCrossWaves, QS>), dim3(tiles), dim3(kCrossWaves * 64),
                            0, st, map, heads, (const bf16*)q, ldq, (const bf16*)k, ldk,
                            (const bf16*)v, ldv, (bf16*)o, ldo, scale_log2);
       else if (map.waves == kCrossWaves) T2I_ATT(kCrossWaves, kCrossStages, 1);
@@ -857,15 +863,21 @@ static hipError_t launch_hd(bool bf16_io, int role, int heads, const AttnMap& ma
 
 hipError_t launch_attention(bool bf16_io, int role, int heads, int head_dim, const AttnMap& map,
                             const void* q, int ldq, const void* k, int ldk, const void* v, int ldv,
-                            void* o, int ldo, hipStream_t st) {
+                            void* o, int ldo, hipStream_t st, bool q_prescaled) {
+#define T2I_HD(D_)                                                                             \
+  case D_:                                                                                     \
+    return q_prescaled && bf16_io                                                              \
+               ? launch_hd<D_, true>(bf16_io, role, heads, map, q, ldq, k, ldk, v, ldv, o, ldo, st) \
+               : launch_hd<D_, false>(bf16_io, role, heads, map, q, ldq, k, ldk, v, ldv, o, ldo, st);
   switch (head_dim) {
-    case 8: return launch_hd<8>(bf16_io, role, heads, map, q, ldq, k, ldk, v, ldv, o, ldo, st);
-    case 32: return launch_hd<32>(bf16_io, role, heads, map, q, ldq, k, ldk, v, ldv, o, ldo, st);
-    case 64: return launch_hd<64>(bf16_io, role, heads, map, q, ldq, k, ldk, v, ldv, o, ldo, st);
-    case 72: return launch_hd<72>(bf16_io, role, heads, map, q, ldq, k, ldk, v, ldv, o, ldo, st);
-    case 128: return launch_hd<128>(bf16_io, role, heads, map, q, ldq, k, ldk, v, ldv, o, ldo, st);
+    T2I_HD(8)
+    T2I_HD(32)
+    T2I_HD(64)
+    T2I_HD(72)
+    T2I_HD(128)
     default: return hipErrorInvalidValue;
   }
+#undef T2I_HD
 }
 
 }  // namespace t2i

@@ -74,11 +74,13 @@ __device__ __forceinline__ void dma_epi4(const Epi& e, int m, int nb, const floa
     *(float4*)((float*)e.out + (size_t)m * e.ldo + nb) = float4{v[0], v[1], v[2], v[3]};
   } else if (KIND == EPI_STORE || KIND == EPI_GELU || KIND == EPI_SILU) {
     bf16x4 w;
+    const float qs = KIND == EPI_STORE && nb < e.qcols ? e.qscale : 1.f;
 #pragma unroll
     for (int r = 0; r < 4; ++r) {
       float y = v[r];
       if (KIND == EPI_GELU) y = gelu_tanh(y);
       if (KIND == EPI_SILU) y = silu(y);
+      if (KIND == EPI_STORE) y *= qs;
       w[r] = (bf16)y;
     }
     *(bf16x4*)((bf16*)e.out + (size_t)m * e.ldo + nb) = w;

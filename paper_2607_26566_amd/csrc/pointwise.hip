@@ -564,6 +564,96 @@ __global__ __launch_bounds__(256) void lora_merge_kernel(int n_out, int n_in, in
   }
 }
 
+// bf16 LoRA merge on MFMA.  A workgroup (4 waves) owns a 64-row x 128-column
+// tile of W.  It first issues the loads of its W tile (16 bytes per lane,
+// rows contiguous, four per thread, so the HBM reads are in flight from the
+// start), then stages the tile's rank slice of B [64][RK] and of A,
+// transposed to [128][RK] (k contiguous, as both MFMA operands want it), in
+// LDS, zero-padded past `rank`; each wave computes two 32x32 tiles of B A on
+// v_mfma_f32_32x32x16_bf16 (fp32 accumulation over the rank), writes them to
+// LDS as fp32, and every thread then finishes its W chunks: W + alpha (B A),
+// rounded once to bf16.  Needs n_in % 8 == 0, ldw % 8 == 0 and 16-byte
+// aligned W and A rows (the launcher checks and falls back otherwise).
+constexpr int kLoraTM = 64, kLoraTN = 128;
+
+template <int RK>
+__global__ __launch_bounds__(256) void lora_merge_mfma_kernel(int n_out, int n_in, int rank,
+                                                              float alpha, bf16* __restrict__ W,
+                                                              int ldw, const bf16* __restrict__ A,
+                                                              const bf16* __restrict__ B) {
+  constexpr int KP = RK + 8;                         // LDS row pitch of the operands (bf16)
+  constexpr int PP = kLoraTN + 4;                    // LDS row pitch of the product (fp32)
+  constexpr int OPS = (kLoraTM + kLoraTN) * KP * 2;  // operand bytes
+  constexpr int PRB = kLoraTM * PP * 4;              // product bytes
+  __shared__ __attribute__((aligned(16))) char smem[OPS > PRB ? OPS : PRB];
+  bf16* Bs = (bf16*)smem;                  // [64][KP]
+  bf16* At = Bs + kLoraTM * KP;            // [128][KP]
+  float* Ps = (float*)smem;                // [64][PP], after the MFMAs
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int o0 = blockIdx.y * kLoraTM, i0 = blockIdx.x * kLoraTN;
+
+  // this thread's W chunks: row (tid >> 4) + 16 c, 8 columns at 8 (tid & 15)
+  constexpr int NC = kLoraTM * kLoraTN / 8 / 256;
+  const int cc = (tid & 15) * 8;
+  bf16x8 wv[NC];
+#pragma unroll
+  for (int c = 0; c < NC; ++c) {
+    const int o = o0 + (tid >> 4) + 16 * c, i = i0 + cc;
+    wv[c] = bf16x8{};
+    if (o < n_out && i < n_in) wv[c] = *(const bf16x8*)(W + (size_t)o * ldw + i);
+  }
+  // operands into LDS, zero past rank / the matrix edges
+  for (int e = tid; e < kLoraTM * (RK / 8); e += 256) {
+    const int r = e / (RK / 8), k = (e - r * (RK / 8)) * 8;
+    bf16x8 v = bf16x8{};
+    if (o0 + r < n_out)
+#pragma unroll
+      for (int j = 0; j < 8; ++j)
+        if (k + j < rank) v[j] = B[(size_t)(o0 + r) * rank + k + j];
+    *(bf16x8*)(Bs + r * KP + k) = v;
+  }
+  for (int e = tid; e < RK * (kLoraTN / 8); e += 256) {
+    const int k = e / (kLoraTN / 8), c = (e - k * (kLoraTN / 8)) * 8;
+    bf16x8 v = bf16x8{};
+    if (k < rank && i0 + c < n_in) v = *(const bf16x8*)(A + (size_t)k * n_in + i0 + c);
+#pragma unroll
+    for (int j = 0; j < 8; ++j) At[(c + j) * KP + k] = v[j];
+  }
+  __syncthreads();
+  // wave w: rows 32 (w & 1) .., columns 64 (w >> 1) .. (two 32-wide tiles)
+  const int l32 = lane & 31, hl = lane >> 5;
+  const int ro = 32 * (wave & 1), co = 64 * (wave >> 1);
+  f32x16 acc[2] = {f32x16{}, f32x16{}};
+#pragma unroll
+  for (int k = 0; k < RK; k += 16) {
+    const bf16x8 bo = *(const bf16x8*)(Bs + (ro + l32) * KP + k + 8 * hl);
+#pragma unroll
+    for (int t = 0; t < 2; ++t) {
+      const bf16x8 ai = *(const bf16x8*)(At + (co + 32 * t + l32) * KP + k + 8 * hl);
+      acc[t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(bo, ai, acc[t], 0, 0, 0);
+    }
+  }
+  __syncthreads();   // the operands are no longer read: the product takes their place
+#pragma unroll
+  for (int t = 0; t < 2; ++t)
+#pragma unroll
+    for (int e = 0; e < 16; ++e)
+      Ps[(ro + 8 * (e >> 2) + 4 * hl + (e & 3)) * PP + co + 32 * t + l32] = acc[t][e];
+  __syncthreads();
+#pragma unroll
+  for (int c = 0; c < NC; ++c) {
+    const int r = (tid >> 4) + 16 * c, o = o0 + r, i = i0 + cc;
+    if (o >= n_out || i >= n_in) continue;
+    const float4 p0 = *(const float4*)(Ps + r * PP + cc);
+    const float4 p1 = *(const float4*)(Ps + r * PP + cc + 4);
+    const float pv[8] = {p0.x, p0.y, p0.z, p0.w, p1.x, p1.y, p1.z, p1.w};
+    bf16x8 out;
+#pragma unroll
+    for (int j = 0; j < 8; ++j) out[j] = (bf16)fmaf(alpha, pv[j], (float)wv[c][j]);
+    *(bf16x8*)(W + (size_t)o * ldw + i) = out;
+  }
+}
+
 template <typename T>
 static hipError_t lora_dispatch(int n_out, int n_in, int rank, float alpha, void* W, int ldw,
                                 const void* A, const void* B, hipStream_t st) {
@@ -583,6 +673,20 @@ hipError_t launch_lora_merge(bool bf16_io, int n_out, int n_in, int rank, float 
                              int ldw, const void* A, const void* B, hipStream_t st) {
   if (n_out <= 0 || n_in <= 0) return hipSuccess;
   if (rank < 1 || rank > kLoraMaxRank) return hipErrorInvalidValue;
+  const bool vec = n_in % 8 == 0 && ldw % 8 == 0 && (uintptr_t)W % 16 == 0 &&
+                   (uintptr_t)A % 16 == 0;
+  if (bf16_io && vec) {
+    dim3 grid((n_in + kLoraTN - 1) / kLoraTN, (n_out + kLoraTM - 1) / kLoraTM);
+#define T2I_LORA_MF(RK_)                                                                       \
+  hipLaunchKernelGGL((lora_merge_mfma_kernel<RK_>), grid, dim3(256), 0, st, n_out, n_in, rank, \
+                     alpha, (bf16*)W, ldw, (const bf16*)A, (const bf16*)B)
+    if (rank <= 16) T2I_LORA_MF(16);
+    else if (rank <= 32) T2I_LORA_MF(32);
+    else if (rank <= 64) T2I_LORA_MF(64);
+    else T2I_LORA_MF(128);
+#undef T2I_LORA_MF
+    return hipGetLastError();
+  }
   return bf16_io ? lora_dispatch<bf16>(n_out, n_in, rank, alpha, W, ldw, A, B, st)
                  : lora_dispatch<float>(n_out, n_in, rank, alpha, W, ldw, A, B, st);
 }
@@ -595,6 +699,33 @@ hipError_t launch_add_inplace(float* x, const float* r, size_t n, hipStream_t st
   if (n == 0) return hipSuccess;
   const int grid = (int)std::min<size_t>((n + 255) / 256, 8192);
   hipLaunchKernelGGL(add_inplace_kernel, dim3(grid), dim3(256), 0, st, x, r, n);
+  return hipGetLastError();
+}
+
+// Segment i moves rows [src[i], src[i] + len[i]) of `from` to rows
+// [dst[i], ...) of `to`, D floats per row; one grid-stride pass over all
+// segments' float4s (segments never overlap).
+__global__ void copy_rows_kernel(const float* __restrict__ from, float* __restrict__ to,
+                                 RowCopyMap m, int D) {
+  const int q = D / 4;
+  const long total = (long)m.row_end[m.n - 1] * q;
+  for (long i = blockIdx.x * 256L + threadIdx.x; i < total; i += (long)gridDim.x * 256) {
+    const int row = (int)(i / q), c = (int)(i - (long)row * q);
+    int s = 0;
+#pragma unroll 1
+    for (int k = 0; k + 1 < m.n; ++k) s += row >= m.row_end[k] ? 1 : 0;
+    const int r = row - (s ? m.row_end[s - 1] : 0);
+    ((float4*)to)[(long)(m.dst[s] + r) * q + c] = ((const float4*)from)[(long)(m.src[s] + r) * q + c];
+  }
+}
+
+hipError_t launch_copy_rows(const float* from, float* to, const RowCopyMap& m, int D,
+                            hipStream_t st) {
+  if (m.n == 0) return hipSuccess;
+  const long total = (long)m.row_end[m.n - 1] * (D / 4);
+  if (total == 0) return hipSuccess;
+  const int grid = (int)std::min<long>((total + 255) / 256, 8192);
+  hipLaunchKernelGGL(copy_rows_kernel, dim3(grid), dim3(256), 0, st, from, to, m, D);
   return hipGetLastError();
 }
 

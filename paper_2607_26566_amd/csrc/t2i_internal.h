@@ -126,15 +126,22 @@ struct Epi {
   const float* gate;  // gate rows: gate[modrow(seq(row)) * ld_gate + col]
   int ld_gate;
   SeqMap map;
+  // STORE / SPLIT_VT: columns < qcols (a multiple of 4) are multiplied by
+  // qscale before their one rounding to bf16 -- the attention queries,
+  // written already scaled by log2(e)/sqrt(d) (0 = no column scaled)
+  float qscale;
+  int qcols;
 };
 
 template <typename OutT>
 __device__ __forceinline__ void epi_apply(const Epi& e, int kind, int m, int n, float y) {
   if (kind == EPI_STORE) {
+    if (n < e.qcols) y *= e.qscale;
     ((OutT*)e.out)[(size_t)m * e.ldo + n] = from_f32<OutT>(y);
   } else if (kind == EPI_STORE_F32) {
     ((float*)e.out)[(size_t)m * e.ldo + n] = y;
   } else if (kind == EPI_SPLIT_VT) {
+    if (n < e.qcols) y *= e.qscale;
     if (n < e.vcol0) ((OutT*)e.out)[(size_t)m * e.ldo + n] = from_f32<OutT>(y);
     else e.vt[(size_t)(n - e.vcol0) * e.ldvt + m] = (bf16)y;
   } else if (kind == EPI_GELU) {
@@ -196,10 +203,17 @@ hipError_t launch_linear_rows(const float* A, int lda, const void* W, int ldw, b
                               const void* bias, int M, int N, int K, int kind, const Epi& epi,
                               hipStream_t st);
 
-// role: 0 self / joint attention, 1 cross-attention (same kernel, own instance)
+// role: 0 self / joint attention, 1 cross-attention (same kernel, own instance).
+// q_prescaled (bf16 only): Q was written multiplied by log2(e)/sqrt(head_dim)
+// (Epi::qscale), so scores come out of the MFMA in log2 units; otherwise the
+// kernel applies that scale to each score in fp32.
 hipError_t launch_attention(bool bf16_io, int role, int heads, int head_dim, const AttnMap& map,
                             const void* q, int ldq, const void* k, int ldk, const void* v,
-                            int ldv, void* o, int ldo, hipStream_t st);
+                            int ldv, void* o, int ldo, hipStream_t st, bool q_prescaled);
+// log2(e) / sqrt(head_dim): the query scale of q_prescaled attention
+inline float attn_q_scale(int head_dim) {
+  return 1.4426950408889634f / __builtin_sqrtf((float)head_dim);
+}
 // Query tiling of a map whose q_len are set: chooses the waves per workgroup
 // (fewer, smaller workgroups when the default tiling would not fill the
 // chip) and fills waves and tile_start.  Every 32-query group is computed
@@ -239,6 +253,16 @@ hipError_t launch_rope_apply(bf16* qk, int ld, int row0, const ReqMap& rm, int h
 // W <- W + alpha B A (LoRA merge), W [n_out, n_in] stride ldw, rank <= 128
 hipError_t launch_lora_merge(bool bf16_io, int n_out, int n_in, int rank, float alpha, void* W,
                              int ldw, const void* A, const void* B, hipStream_t st);
+// Row segments to move between two fp32 [rows, D] buffers: segment i takes
+// rows src[i] .. of the source to rows dst[i] .. of the destination; row_end
+// is the running total of segment lengths (segment i has row_end[i] -
+// row_end[i-1] rows).  D % 4 == 0.
+struct RowCopyMap {
+  int n;
+  int src[kMaxSeq], dst[kMaxSeq], row_end[kMaxSeq];
+};
+hipError_t launch_copy_rows(const float* from, float* to, const RowCopyMap& m, int D,
+                            hipStream_t st);
 // x[i] += r[i] for i < n (fp32)
 hipError_t launch_add_inplace(float* x, const float* r, size_t n, hipStream_t st);
 // dst[r][:] = float(bias[:]) for r < rows (bf16 or fp32 bias)

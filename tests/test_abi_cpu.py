@@ -285,3 +285,12 @@ def test_static_workspace_init_rejects_configs_beyond_its_size():
     bad = t2i.Config.from_shape(w)
     bad.c.hidden = 100
     assert lib.t2i_dit_init_static(bad.ref(), fake, None, C.byref(h)) == 1
+
+
+def test_static_workspace_test_configs_fit():
+    """The configs the static-workspace GPU test runs stay within the array."""
+    lib = t2i.load()
+    for name, kw in (("dit1024_cfg", dict(depth=2, requests=((32, 32), (16, 32)))),
+                     ("tiny_f32", dict(requests=((16, 16), (16, 8))))):
+        cfg = t2i.Config.from_shape(synth.reduced(synth.workload(name), **kw))
+        assert 0 < lib.t2i_dit_workspace_bytes(cfg.ref()) <= (64 << 20), name

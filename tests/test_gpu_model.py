@@ -470,3 +470,41 @@ def test_packed_per_step_cache_mode_and_resume(packed8):
     del m2
     gc.collect()
     torch.cuda.empty_cache()
+
+
+def test_packed_mixed_skip_runs_blocks_on_computing_requests_only(packed8):
+    """A step in which some requests reuse their cached residual and the
+    others compute runs the blocks on the computing requests' rows alone.
+    Their velocities and updated latents equal, bitwise, those of the same
+    step with every request computing; the skipped requests' equal those of
+    the step with every request skipping."""
+    M, w = packed8, packed8.w
+    lats, texts = synth.latents(w), synth.texts(w)
+    hw = list(w.requests)
+    n = w.n_req
+    ts = list(synth.start_times(w))
+    t1 = [0.9 * t for t in ts]
+    t2 = [0.85 * t for t in ts]
+    tx = M.text_dev(texts)
+    toks = [w.tokens(r) for r in range(n)]
+    state = M.m.new_cache_state(toks, 1)
+    x = M.latents_dev(lats)
+    t2i.t2i_dit_step(M.m, x.clone(), hw, ts, tx, skip=[0] * n, cache_state=state)
+    shapes = [l.shape for l in lats]
+
+    def run(skip):
+        st, xx = state.clone(), x.clone()
+        v = torch.zeros_like(xx)
+        t2i.t2i_dit_step(M.m, xx, hw, t1, tx, t_next=t2, skip=skip, cache_state=st, noise_pred=v)
+        torch.cuda.synchronize()
+        return M.split(v.cpu().numpy(), shapes), M.split(xx.cpu().numpy(), shapes)
+
+    for mixed in ([0, 1, 1, 0, 1, 0, 1, 1], [1, 1, 1, 1, 1, 1, 0, 1], [0, 1, 0, 1, 0, 1, 0, 1]):
+        v_mix, x_mix = run(mixed)
+        v_all, x_all = run([0] * n)
+        v_none, x_none = run([1] * n)
+        for r in range(n):
+            v_ref, x_ref = (v_none, x_none) if mixed[r] else (v_all, x_all)
+            assert np.array_equal(v_mix[r], v_ref[r]), (mixed, r)
+            assert np.array_equal(x_mix[r], x_ref[r]), (mixed, r)
+        say(f"mixed skip {mixed}: computing and skipped requests bitwise as in the uniform steps")

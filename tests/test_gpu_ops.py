@@ -373,6 +373,7 @@ def test_ln_modulate(dtype, rows, D):
 
 
 @pytest.mark.parametrize("dtype,n_out,n_in,rank", [(1, 3072, 3072, 64), (1, 1152, 4608, 16),
+                                                    (1, 1000, 1160, 40), (1, 77, 304, 128),
                                                     (1, 77, 300, 128), (0, 200, 130, 8)])
 def test_lora_merge(dtype, n_out, n_in, rank):
     """W + alpha B A against the oracle: fp32 to 1e-6; bf16 equal to the oracle

@@ -28,7 +28,7 @@ def _step(m, w, lats, texts, hw, ts, tn):
 
 
 @pytest.mark.parametrize("name,kw", [
-    ("dit1024_cfg", dict(depth=2, requests=((32, 48), (32, 32)))),
+    ("dit1024_cfg", dict(depth=2, requests=((32, 32), (16, 32)))),
     ("tiny_f32", dict(requests=((16, 16), (16, 8)))),
 ])
 def test_static_workspace_handle_equals_allocated(name, kw):
