@@ -33,13 +33,14 @@ PEAK_HBM_GBS = 8000.0          # MI355X HBM3E
 WORKLOAD = "dit1024_cfg"
 
 # HBM bytes per launch measured with rocprofv3 (FETCH_SIZE x 2.00 + WRITE_SIZE
-# x 1.00, factors from a 1 GiB copy; profiles/attn_self_dit1024_hbm_traffic.md),
+# x 1.00, factors from a 1 GiB copy and a 1 GiB read through the direct-to-LDS
+# load path),
 # keyed by (workload, kernel class) with the source file it was measured on
 # and the first 16 hex digits of the sha256 of that file's code (comments and
 # blank lines removed, see code_digest): reported only while the code is
 # unchanged.
 MEASURED_TRAFFIC = {
-    ("dit1024_cfg", "attn_self"): (107.1e6, "paper_2607_26566_amd/csrc/attention.hip", "57a3ad7f1a640275"),
+    ("dit1024_cfg", "attn_self"): (107.1e6, "paper_2607_26566_amd/csrc/attention.hip", "023d7294fb9a12a0"),
 }
 
 
@@ -399,6 +400,8 @@ def main():
                     help="time first-layers caching with progressive loading instead")
     ap.add_argument("--cache", action="store_true",
                     help="time whole samples with the step-skip cache on (effective steps/s)")
+    ap.add_argument("--dma-calibration", action="store_true",
+                    help="run only a 1 GiB read through the direct-to-LDS load path")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="run only a plain 1 GiB device copy (HBM counter calibration)")
     args = ap.parse_args()
@@ -416,6 +419,20 @@ def main():
     import synth
     import paper_2607_26566_amd as t2i
     from paper_2607_26566_amd import _lib
+
+    if args.dma_calibration:
+        import ctypes as C
+        nbytes = 1 << 30
+        a = torch.ones(nbytes // 4, dtype=torch.float32, device="cuda")
+        sink = torch.zeros(1024, dtype=torch.float32, device="cuda")
+        lib = t2i.load()
+        st = C.c_void_p(torch.cuda.current_stream().cuda_stream)
+        for _ in range(5):
+            _lib.check(lib.t2i_op_dma_read(C.c_void_p(a.data_ptr()), nbytes,
+                                           C.c_void_p(sink.data_ptr()), st))
+        torch.cuda.synchronize()
+        print(json.dumps({"dma_bytes_read": nbytes, "launches": 5}))
+        return
 
     if args.copy_calibration:
         n = 1 << 28                      # 2^28 floats = 1 GiB

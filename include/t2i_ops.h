@@ -97,6 +97,16 @@ t2i_status t2i_op_lora_merge(int32_t dtype, int32_t n_out, int32_t n_in, int32_t
                              float alpha, void* W, int32_t ldw, const void* A,
                              const void* B, void* stream);
 
+/*
+ * Memory-counter calibration (not part of the denoising step): reads `bytes`
+ * of src (device, 16-byte aligned; a multiple of 1024 below 2 GiB) exactly
+ * once through the direct HBM -> LDS load path that the GEMM and attention
+ * kernels use, and writes 1024 floats of no meaning to sink (device).  A
+ * profiler's fetched-bytes counter read on this launch gives the factor that
+ * turns the counter into bytes for kernels loading this way.
+ */
+t2i_status t2i_op_dma_read(const void* src, size_t bytes, float* sink, void* stream);
+
 const char* t2i_ops_last_error(void);
 
 #ifdef __cplusplus

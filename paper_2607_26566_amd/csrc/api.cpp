@@ -1481,6 +1481,16 @@ t2i_status t2i_op_ln_modulate(int32_t dtype, int32_t rows, int32_t D, const floa
   return T2I_OK;
 }
 
+t2i_status t2i_op_dma_read(const void* src, size_t bytes, float* sink, void* stream) {
+  if (!src || !sink) return ops_fail(T2I_ERR_INVALID_ARG, "NULL pointer");
+  if (bytes == 0 || bytes % 1024 || bytes > ((size_t)1 << 31) - 1024)
+    return ops_fail(T2I_ERR_SHAPE, "bytes must be a positive multiple of 1024 below 2 GiB");
+  if ((uintptr_t)src % 16) return ops_fail(T2I_ERR_INVALID_ARG, "src must be 16-byte aligned");
+  hipError_t err = launch_dma_read(src, bytes, sink, (hipStream_t)stream);
+  if (err != hipSuccess) return ops_fail(T2I_ERR_DEVICE, hipGetErrorString(err));
+  return T2I_OK;
+}
+
 t2i_status t2i_op_lora_merge(int32_t dtype, int32_t n_out, int32_t n_in, int32_t rank,
                              float alpha, void* W, int32_t ldw, const void* A, const void* B,
                              void* stream) {

@@ -340,4 +340,31 @@ hipError_t launch_gemm_dma(const bf16* A, int lda, const bf16* W, int ldw, const
                                                  st);
 }
 
+// Counter calibration: read `chunks` KB of src once through the same direct
+// HBM -> LDS path (buffer_load_dwordx4 ... lds, 1 KB per wave instruction) the
+// GEMM and attention kernels use, writing nothing to global memory but one
+// float per workgroup.  Waves never wait inside the loop (the hardware stalls
+// issue once its outstanding-load counter is full), so the loads stream.
+__global__ __launch_bounds__(256) void dma_read_kernel(const char* __restrict__ src, int chunks,
+                                                       float* __restrict__ sink) {
+  __shared__ __attribute__((aligned(1024))) char smem[4 * 1024];
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const __amdgpu_buffer_rsrc_t r =
+      __builtin_amdgcn_make_buffer_rsrc((void*)src, 0, 0x7fffffff, 0x00020000);
+  const int nw = gridDim.x * 4;
+  for (int c = blockIdx.x * 4 + wave; c < chunks; c += nw)
+    dma16<0>(r, smem + wave * 1024, (uint32_t)c * 1024u + (uint32_t)lane * 16u, 0);
+  wait_vmcnt<0>();
+  __syncthreads();
+  if (threadIdx.x == 0) sink[blockIdx.x] = *(const float*)smem;
+}
+
+hipError_t launch_dma_read(const void* src, size_t bytes, float* sink, hipStream_t st) {
+  if (bytes == 0) return hipSuccess;
+  if (bytes % 1024 || bytes > ((size_t)1 << 31) - 1024) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(dma_read_kernel, dim3(kDmaReadGroups), dim3(256), 0, st, (const char*)src,
+                     (int)(bytes / 1024), sink);
+  return hipGetLastError();
+}
+
 }  // namespace t2i

@@ -263,6 +263,10 @@ struct RowCopyMap {
 };
 hipError_t launch_copy_rows(const float* from, float* to, const RowCopyMap& m, int D,
                             hipStream_t st);
+// Reads bytes (a multiple of 1024, below 2 GiB) of src once through the
+// direct-to-LDS load path; writes kDmaReadGroups floats to sink.
+constexpr int kDmaReadGroups = 1024;
+hipError_t launch_dma_read(const void* src, size_t bytes, float* sink, hipStream_t st);
 // x[i] += r[i] for i < n (fp32)
 hipError_t launch_add_inplace(float* x, const float* r, size_t n, hipStream_t st);
 // dst[r][:] = float(bias[:]) for r < rows (bf16 or fp32 bias)

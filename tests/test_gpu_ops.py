@@ -403,3 +403,17 @@ def test_lora_merge(dtype, n_out, n_in, rank):
     # accumulation slack where W and alpha B A nearly cancel)
     d = np.abs(got[diff] - ref[diff])
     assert np.all(d <= np.maximum(np.abs(ref[diff]), np.abs(got[diff])) * 2.0 ** -7 + 1e-6)
+
+
+def test_dma_read_calibration_kernel():
+    """The counter-calibration read through the direct-to-LDS path runs and
+    lands the source's bytes in LDS (every workgroup reports a 1.0 it read)."""
+    lib = t2i.load()
+    a = torch.ones(1 << 20, dtype=torch.float32, device=DEV)      # 4 MiB
+    sink = torch.zeros(1024, dtype=torch.float32, device=DEV)
+    _lib.check(lib.t2i_op_dma_read(C.c_void_p(a.data_ptr()), 4 << 20, C.c_void_p(sink.data_ptr()),
+                                   _stream()))
+    torch.cuda.synchronize()
+    assert torch.all(sink == 1.0)
+    assert lib.t2i_op_dma_read(C.c_void_p(a.data_ptr()), 1000, C.c_void_p(sink.data_ptr()),
+                               _stream()) == 2
