@@ -162,7 +162,9 @@ def cpu_baseline(w, W_host, min_seconds=10.0, max_passes=16):
 
 def lora_cost(t2i, table, dev, rank):
     """Time merging one rank-``rank`` LoRA (alpha 1) into every 2-D weight of
-    the blocks, as done once before sampling with an adapter."""
+    the blocks, as done once before sampling with an adapter: one batched
+    launch per weight shape (t2i_op_lora_merge_batch), and for comparison one
+    launch per weight (t2i_op_lora_merge)."""
     import torch
     idx = [i for i, (n, shp) in enumerate(table) if n.startswith("blocks.") and len(shp) == 2]
     g = torch.Generator(device="cuda").manual_seed(0)
@@ -173,23 +175,37 @@ def lora_cost(t2i, table, dev, rank):
         if key not in ad:
             ad[key] = (torch.randn(rank, n_in, generator=g, device="cuda").to(dev[i].dtype) * 0.01,
                        torch.randn(n_out, rank, generator=g, device="cuda").to(dev[i].dtype) * 0.01)
-    torch.cuda.synchronize()
-    # GPU time of each merge (events around each launch), summed
-    evs = []
-    nbytes = 0
+    by_shape = {}
     for i in idx:
-        a, b = ad[table[i][1]]
-        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-        e0.record()
-        t2i.lora_merge(dev[i], a, b, 1.0)
-        e1.record()
-        evs.append((e0, e1))
-        nbytes += 2 * dev[i].numel() * dev[i].element_size() + (a.numel() + b.numel()) * a.element_size()
+        by_shape.setdefault(table[i][1], []).append(i)
+    nbytes = sum(2 * dev[i].numel() * dev[i].element_size() +
+                 sum(t.numel() * t.element_size() for t in ad[table[i][1]]) for i in idx)
     torch.cuda.synchronize()
-    ms = sum(e0.elapsed_time(e1) for e0, e1 in evs)
+
+    def timed(calls):
+        evs = []
+        for fn in calls:
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record()
+            fn()
+            e1.record()
+            evs.append((e0, e1))
+        torch.cuda.synchronize()
+        return sum(e0.elapsed_time(e1) for e0, e1 in evs)
+
+    batched = [lambda s=s, ix=ix: t2i.lora_merge_batch([dev[i] for i in ix], [ad[s][0]] * len(ix),
+                                                       [ad[s][1]] * len(ix), 1.0)
+               for s, ix in by_shape.items()]
+    single = [lambda i=i: t2i.lora_merge(dev[i], ad[table[i][1]][0], ad[table[i][1]][1], 1.0)
+              for i in idx]
+    timed(batched)                       # warm-up
+    ms = timed(batched)
+    ms_single = timed(single)
     gbs = nbytes / (ms / 1e3) / 1e9
-    return {"rank": rank, "layers": len(idx), "gpu_ms": round(ms, 3), "bytes": nbytes,
-            "hbm_gbs": round(gbs, 1), "hbm_frac": round(gbs / PEAK_HBM_GBS, 4)}
+    return {"rank": rank, "layers": len(idx), "launches": sum((len(ix) + 63) // 64
+                                                             for ix in by_shape.values()),
+            "gpu_ms": round(ms, 3), "bytes": nbytes, "hbm_gbs": round(gbs, 1),
+            "hbm_frac": round(gbs / PEAK_HBM_GBS, 4), "per_weight_launch_gpu_ms": round(ms_single, 3)}
 
 
 def sched_bench(tenants=64, ready_per_tenant=4, decisions=20000):

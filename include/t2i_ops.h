@@ -98,6 +98,17 @@ t2i_status t2i_op_lora_merge(int32_t dtype, int32_t n_out, int32_t n_in, int32_t
                              const void* B, void* stream);
 
 /*
+ * The LoRA merge of t2i_op_lora_merge for n weights of one shape (an adapter
+ * applied to every layer of one kind: n_out, n_in, rank, ldw shared), weight
+ * i at W[i] with its own A[i], B[i] -- host arrays of n device pointers.
+ * Results are those of n t2i_op_lora_merge calls, bitwise; one launch per 64
+ * weights instead of one each.  The weights must not overlap.
+ */
+t2i_status t2i_op_lora_merge_batch(int32_t dtype, int32_t n, int32_t n_out, int32_t n_in,
+                                   int32_t rank, float alpha, void* const* W, int32_t ldw,
+                                   const void* const* A, const void* const* B, void* stream);
+
+/*
  * Memory-counter calibration (not part of the denoising step): reads `bytes`
  * of src (device, 16-byte aligned; a multiple of 1024 below 2 GiB) exactly
  * once through the direct HBM -> LDS load path that the GEMM and attention

@@ -303,6 +303,31 @@ def lora_merge(W: torch.Tensor, A: torch.Tensor, B: torch.Tensor, alpha: float, 
         raise T2IError(st, lib.t2i_ops_last_error().decode())
 
 
+def lora_merge_batch(Ws: Sequence[torch.Tensor], As: Sequence[torch.Tensor],
+                     Bs: Sequence[torch.Tensor], alpha: float, stream=None):
+    """``W_i += alpha * B_i @ A_i`` for weights of one shape and dtype
+    (``t2i_op_lora_merge_batch``)."""
+    n = len(Ws)
+    if n == 0 or len(As) != n or len(Bs) != n:
+        raise T2IError(2, "need as many A and B as W (at least one)")
+    W0, A0 = Ws[0], As[0]
+    n_out, n_in = W0.shape
+    rank = A0.shape[0]
+    for W, A, B in zip(Ws, As, Bs):
+        for t in (W, A, B):
+            if not t.is_cuda or not t.is_contiguous() or t.dtype != W0.dtype:
+                raise T2IError(1, "W, A, B must be contiguous device tensors of one dtype")
+        if W.shape != (n_out, n_in) or A.shape != (rank, n_in) or B.shape != (n_out, rank):
+            raise T2IError(2, "every W must be [out, in], A [rank, in], B [out, rank] alike")
+    lib = load()
+    dt = T2I_BF16 if W0.dtype == torch.bfloat16 else T2I_F32
+    ptrs = lambda ts: (C.c_void_p * n)(*[t.data_ptr() for t in ts])
+    st = lib.t2i_op_lora_merge_batch(dt, n, n_out, n_in, rank, float(alpha), ptrs(Ws), n_in,
+                                     ptrs(As), ptrs(Bs), C.c_void_p(_stream(stream)))
+    if st != 0:
+        raise T2IError(st, lib.t2i_ops_last_error().decode())
+
+
 def t2i_cache_check(m: DiT, latents: torch.Tensor, lat_hw, t, step: int, n_steps: int,
                     tau: float, cache_state: torch.Tensor, branches: int = 1,
                     mode: int = T2I_CACHE_ACCUMULATE, stream=None):

@@ -100,6 +100,8 @@ SIGNATURES = {
                                vp, i32, vp, i32, vp, i32, vp, i32, vp]),
     "t2i_op_ln_modulate": (i32, [i32, i32, i32, vp, vp, vp, f32, vp, vp]),
     "t2i_op_dma_read": (i32, [vp, sz, vp, vp]),
+    "t2i_op_lora_merge_batch": (i32, [i32, i32, i32, i32, i32, f32, C.POINTER(vp), i32,
+                                      C.POINTER(vp), C.POINTER(vp), vp]),
     "t2i_op_lora_merge": (i32, [i32, i32, i32, i32, f32, vp, i32, vp, vp, vp]),
     "t2i_sched_create": (i32, [f64, C.POINTER(vp)]),
     "t2i_sched_destroy": (None, [vp]),

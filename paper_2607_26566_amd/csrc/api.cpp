@@ -1481,6 +1481,32 @@ t2i_status t2i_op_ln_modulate(int32_t dtype, int32_t rows, int32_t D, const floa
   return T2I_OK;
 }
 
+t2i_status t2i_op_lora_merge_batch(int32_t dtype, int32_t n, int32_t n_out, int32_t n_in,
+                                   int32_t rank, float alpha, void* const* W, int32_t ldw,
+                                   const void* const* A, const void* const* B, void* stream) {
+  if (dtype != T2I_F32 && dtype != T2I_BF16) return ops_fail(T2I_ERR_INVALID_ARG, "bad dtype");
+  if (n < 1) return ops_fail(T2I_ERR_SHAPE, "n must be >= 1");
+  if (n_out < 1 || n_in < 1 || ldw < n_in) return ops_fail(T2I_ERR_SHAPE, "bad weight shape");
+  if (rank < 1 || rank > 128) return ops_fail(T2I_ERR_SHAPE, "rank must be in 1 .. 128");
+  if (!W || !A || !B) return ops_fail(T2I_ERR_INVALID_ARG, "NULL pointer table");
+  for (int i = 0; i < n; ++i)
+    if (!W[i] || !A[i] || !B[i]) return ops_fail(T2I_ERR_INVALID_ARG, "NULL pointer");
+  if (!std::isfinite(alpha)) return ops_fail(T2I_ERR_INVALID_ARG, "alpha not finite");
+  for (int i0 = 0; i0 < n; i0 += kMaxGroups) {
+    LoraGroup g;
+    const int m = std::min(kMaxGroups, n - i0);
+    for (int i = 0; i < m; ++i) {
+      g.W[i] = W[i0 + i];
+      g.A[i] = A[i0 + i];
+      g.B[i] = B[i0 + i];
+    }
+    hipError_t err = launch_lora_merge_group(dtype == T2I_BF16, m, n_out, n_in, rank, alpha, g,
+                                             ldw, (hipStream_t)stream);
+    if (err != hipSuccess) return ops_fail(T2I_ERR_DEVICE, hipGetErrorString(err));
+  }
+  return T2I_OK;
+}
+
 t2i_status t2i_op_dma_read(const void* src, size_t bytes, float* sink, void* stream) {
   if (!src || !sink) return ops_fail(T2I_ERR_INVALID_ARG, "NULL pointer");
   if (bytes == 0 || bytes % 1024 || bytes > ((size_t)1 << 31) - 1024)

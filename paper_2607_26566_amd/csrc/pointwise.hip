@@ -578,9 +578,11 @@ constexpr int kLoraTM = 64, kLoraTN = 128;
 
 template <int RK>
 __global__ __launch_bounds__(256) void lora_merge_mfma_kernel(int n_out, int n_in, int rank,
-                                                              float alpha, bf16* __restrict__ W,
-                                                              int ldw, const bf16* __restrict__ A,
-                                                              const bf16* __restrict__ B) {
+                                                              float alpha, LoraGroup g, int ldw) {
+  // weight blockIdx.z of the group
+  bf16* __restrict__ W = (bf16*)g.W[blockIdx.z];
+  const bf16* __restrict__ A = (const bf16*)g.A[blockIdx.z];
+  const bf16* __restrict__ B = (const bf16*)g.B[blockIdx.z];
   constexpr int KP = RK + 8;                         // LDS row pitch of the operands (bf16)
   constexpr int PP = kLoraTN + 4;                    // LDS row pitch of the product (fp32)
   constexpr int OPS = (kLoraTM + kLoraTN) * KP * 2;  // operand bytes
@@ -673,13 +675,25 @@ hipError_t launch_lora_merge(bool bf16_io, int n_out, int n_in, int rank, float 
                              int ldw, const void* A, const void* B, hipStream_t st) {
   if (n_out <= 0 || n_in <= 0) return hipSuccess;
   if (rank < 1 || rank > kLoraMaxRank) return hipErrorInvalidValue;
-  const bool vec = n_in % 8 == 0 && ldw % 8 == 0 && (uintptr_t)W % 16 == 0 &&
-                   (uintptr_t)A % 16 == 0;
-  if (bf16_io && vec) {
-    dim3 grid((n_in + kLoraTN - 1) / kLoraTN, (n_out + kLoraTM - 1) / kLoraTM);
+  LoraGroup g;
+  g.W[0] = W;
+  g.A[0] = A;
+  g.B[0] = B;
+  return launch_lora_merge_group(bf16_io, 1, n_out, n_in, rank, alpha, g, ldw, st);
+}
+
+hipError_t launch_lora_merge_group(bool bf16_io, int n, int n_out, int n_in, int rank,
+                                   float alpha, const LoraGroup& g, int ldw, hipStream_t st) {
+  if (n <= 0 || n_out <= 0 || n_in <= 0) return hipSuccess;
+  if (n > kMaxGroups || rank < 1 || rank > kLoraMaxRank) return hipErrorInvalidValue;
+  bool vec = bf16_io && n_in % 8 == 0 && ldw % 8 == 0;
+  for (int i = 0; i < n; ++i)
+    vec = vec && (uintptr_t)g.W[i] % 16 == 0 && (uintptr_t)g.A[i] % 16 == 0;
+  if (vec) {
+    dim3 grid((n_in + kLoraTN - 1) / kLoraTN, (n_out + kLoraTM - 1) / kLoraTM, n);
 #define T2I_LORA_MF(RK_)                                                                       \
   hipLaunchKernelGGL((lora_merge_mfma_kernel<RK_>), grid, dim3(256), 0, st, n_out, n_in, rank, \
-                     alpha, (bf16*)W, ldw, (const bf16*)A, (const bf16*)B)
+                     alpha, g, ldw)
     if (rank <= 16) T2I_LORA_MF(16);
     else if (rank <= 32) T2I_LORA_MF(32);
     else if (rank <= 64) T2I_LORA_MF(64);
@@ -687,8 +701,14 @@ hipError_t launch_lora_merge(bool bf16_io, int n_out, int n_in, int rank, float 
 #undef T2I_LORA_MF
     return hipGetLastError();
   }
-  return bf16_io ? lora_dispatch<bf16>(n_out, n_in, rank, alpha, W, ldw, A, B, st)
-                 : lora_dispatch<float>(n_out, n_in, rank, alpha, W, ldw, A, B, st);
+  for (int i = 0; i < n; ++i) {
+    hipError_t e = bf16_io ? lora_dispatch<bf16>(n_out, n_in, rank, alpha, g.W[i], ldw, g.A[i],
+                                                 g.B[i], st)
+                           : lora_dispatch<float>(n_out, n_in, rank, alpha, g.W[i], ldw, g.A[i],
+                                                  g.B[i], st);
+    if (e != hipSuccess) return e;
+  }
+  return hipSuccess;
 }
 
 __global__ void add_inplace_kernel(float* __restrict__ x, const float* __restrict__ r, size_t n) {

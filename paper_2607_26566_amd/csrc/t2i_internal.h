@@ -251,6 +251,15 @@ hipError_t launch_rope_table(float2* table, int npos, int q, hipStream_t st);
 hipError_t launch_rope_apply(bf16* qk, int ld, int row0, const ReqMap& rm, int heads, int head_dim,
                              int patch, const float2* table, hipStream_t st);
 // W <- W + alpha B A (LoRA merge), W [n_out, n_in] stride ldw, rank <= 128
+// the same merge for n <= kMaxGroups weights of one shape, weight i from
+// W[i] (stride ldw) with A[i], B[i]: one launch
+struct LoraGroup {
+  void* W[kMaxGroups];
+  const void* A[kMaxGroups];
+  const void* B[kMaxGroups];
+};
+hipError_t launch_lora_merge_group(bool bf16_io, int n, int n_out, int n_in, int rank,
+                                   float alpha, const LoraGroup& g, int ldw, hipStream_t st);
 hipError_t launch_lora_merge(bool bf16_io, int n_out, int n_in, int rank, float alpha, void* W,
                              int ldw, const void* A, const void* B, hipStream_t st);
 // Row segments to move between two fp32 [rows, D] buffers: segment i takes

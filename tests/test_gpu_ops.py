@@ -417,3 +417,25 @@ def test_dma_read_calibration_kernel():
     assert torch.all(sink == 1.0)
     assert lib.t2i_op_dma_read(C.c_void_p(a.data_ptr()), 1000, C.c_void_p(sink.data_ptr()),
                                _stream()) == 2
+
+
+@pytest.mark.parametrize("dtype,n_out,n_in,rank", [(1, 300, 256, 24), (1, 64, 1160, 128),
+                                                    (0, 70, 130, 8), (1, 77, 300, 16)])
+def test_lora_merge_batch_equals_single_merges(dtype, n_out, n_in, rank):
+    """One launch over several weights of a shape == one merge per weight, bitwise."""
+    bf = dtype == 1
+    dt = "bf16" if bf else "f32"
+    n = 3
+    Ws = [rnd(90 + i, (n_out, n_in), 0.05, bf=bf) for i in range(n)]
+    As = [rnd(95 + i, (rank, n_in), 0.05, bf=bf) for i in range(n)]
+    Bs = [rnd(99 + i, (n_out, rank), 0.05, bf=bf) for i in range(n)]
+    one = [to_dev(w, dt) for w in Ws]
+    bat = [to_dev(w, dt) for w in Ws]
+    dA = [to_dev(a, dt) for a in As]
+    dB = [to_dev(b, dt) for b in Bs]
+    for w, a, b in zip(one, dA, dB):
+        t2i.lora_merge(w, a, b, 0.7)
+    t2i.lora_merge_batch(bat, dA, dB, 0.7)
+    torch.cuda.synchronize()
+    for x, y in zip(one, bat):
+        assert torch.equal(x, y)
