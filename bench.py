@@ -270,15 +270,26 @@ def cache_bench(t2i, m, w, x, x_init, hw, tx, sched, n_samples, warmup):
         x.copy_(x_init)
         return t2i.t2i_dit_sample(m, x, hw, tx, n, guidance=w.guidance, timesteps=ts,
                                   cache_tau=tau, cache_state=state)[0]
+    from ctypes import c_double, c_int64, byref
+    from paper_2607_26566_amd import _lib
+    lib = t2i.load()
     for _ in range(warmup):
         one()
     torch.cuda.synchronize()
     logs = []
+    # events around the cache-check kernels only (signal + decision, once per step)
+    ci = _lib.KERNEL_CLASSES.index("cache")
+    _lib.check(lib.t2i_dit_profile(m.h, 1 << ci), m.h)
     t0 = time.perf_counter()
     for _ in range(n_samples):
         logs.append(one())
     torch.cuda.synchronize()
     el = time.perf_counter() - t0
+    tot, cnt = c_double(), c_int64()
+    _lib.check(lib.t2i_dit_profile_read(m.h, ci, byref(tot), byref(cnt)), m.h)
+    _lib.check(lib.t2i_dit_profile(m.h, 0), m.h)
+    cache_bytes = step_class_bytes(w)["cache"] * cnt.value
+    cache_gbs = cache_bytes / (tot.value / 1e3) / 1e9 if tot.value > 0 else 0.0
     rf = np.array([request_flops(w, r) for r in range(w.n_req)])
     executed = sum(float(((1 - lg) * rf[None, :]).sum()) for lg in logs)
     full = float(rf.sum()) * n * n_samples
@@ -293,6 +304,8 @@ def cache_bench(t2i, m, w, x, x_init, hw, tx, sched, n_samples, warmup):
         "executed_flop_frac": round(executed / full, 4),
         "executed_tflops": round(executed / el / 1e12, 1),
         "executed_frac_of_peak": round(executed / el / 1e12 / PEAK_BF16_TFLOPS, 4),
+        "hbm_frac": {"cache": {"gbs": round(cache_gbs, 1), "frac": round(cache_gbs / PEAK_HBM_GBS, 4),
+                               "avg_launch_ms": round(tot.value / max(cnt.value, 1), 4)}},
         "skip_log_first_sample": logs[0].tolist(),
     }
 

@@ -30,6 +30,9 @@ namespace t2i {
 hipError_t launch_gemm_dma(const bf16* A, int lda, const bf16* W, int ldw, const bf16* bias,
                            int M, int N, int K, int kind, const Epi& epi, int vec_ok,
                            hipStream_t st);
+hipError_t launch_gemm_dma_small(const bf16* A, int lda, const bf16* W, int ldw, const bf16* bias,
+                                 int M, int N, int K, int kind, const Epi& epi, int vec_ok,
+                                 hipStream_t st);
 
 // Map launch order -> tile order so XCD x (blocks b with b % 8 == x) owns the
 // contiguous tile range of its share.
@@ -341,6 +344,8 @@ hipError_t launch_gemm_bf16(const bf16* A, int lda, const bf16* W, int ldw, cons
   if (M >= 2048 && (N % 144 == 0 || N % 128 == 0) && kind != EPI_SILU && dma_fits)
     return launch_gemm_dma(A, lda, W, ldw, bias, M, N, K, kind, epi, vec_ok, st);
   const int splits = splitk_ws ? splitk_factor(N, K) : 1;
+  if (splits == 1 && N % 144 == 0 && K % 64 == 0 && kind != EPI_SILU && dma_fits && M >= 64)
+    return launch_gemm_dma_small(A, lda, W, ldw, bias, M, N, K, kind, epi, vec_ok, st);
   if (splits > 1 && (size_t)splits * M * N <= splitk_floats && kind != EPI_SILU) {
     Epi pe;
     std::memset(&pe, 0, sizeof(pe));

@@ -57,6 +57,20 @@ __device__ __forceinline__ void dma16(__amdgpu_buffer_rsrc_t r, char* lds, uint3
                                            voff, soff, 0, AUX);
 }
 
+// wait until at most `younger` load rounds of BPW instructions each are
+// outstanding (younger <= 5; compile-time counts)
+template <int BPW>
+__device__ __forceinline__ void wait_rounds(int younger) {
+  switch (younger) {
+    case 0: wait_vmcnt<0>(); break;
+    case 1: wait_vmcnt<BPW>(); break;
+    case 2: wait_vmcnt<(2 * BPW < 64 ? 2 * BPW : 0)>(); break;
+    case 3: wait_vmcnt<(3 * BPW < 64 ? 3 * BPW : 0)>(); break;
+    case 4: wait_vmcnt<(4 * BPW < 64 ? 4 * BPW : 0)>(); break;
+    default: wait_vmcnt<(5 * BPW < 64 ? 5 * BPW : 0)>(); break;
+  }
+}
+
 __device__ __forceinline__ void block_barrier() {
   // this wave's LDS reads are complete (a stage may be refilled right after
   // the barrier), then a plain s_barrier: no release fence, which would wait
@@ -115,7 +129,7 @@ __global__ __launch_bounds__(64 * WGM * WGN, 1) void gemm_dma_kernel(
   constexpr int STAGE = (BM + BN) * 64;                            // bf16 elements per stage
   constexpr bool CT = KIND != EPI_SPLIT_VT;
   static_assert(BM % 8 == 0 && BN % 8 == 0 && WM % 16 == 0 && WN % 16 == 0, "tile shape");
-  static_assert(ST >= 2 && ST <= 4, "stages");
+  static_assert(ST >= 2 && ST <= 7 && (ST - 2) * BPW < 64, "stages");
   static_assert(ABLK % NW == 0, "A / W blocks split evenly over the load rounds");
   __shared__ __attribute__((aligned(1024))) bf16 smem[ST * STAGE];
 
@@ -219,10 +233,7 @@ __global__ __launch_bounds__(64 * WGM * WGN, 1) void gemm_dma_kernel(
       const int t = t0 + i;
       if (t >= KT) break;
       // loads younger than tile t that may stay in flight
-      const int younger = min(ST - 2, KT - 1 - t);
-      if (younger >= 2) wait_vmcnt<2 * BPW>();
-      else if (younger == 1) wait_vmcnt<BPW>();
-      else wait_vmcnt<0>();
+      wait_rounds<BPW>(min(ST - 2, KT - 1 - t));
       block_barrier();
       if (t + ST - 1 < KT) issue(t + ST - 1, (i + ST - 1) % ST);
       compute(i);
@@ -307,8 +318,8 @@ hipError_t gemm_dma_dispatch(const bf16* A, int lda, const bf16* W, int ldw, con
 // averages ~17.  Bytes per FLOP -- (BM + BN) / (BM BN) -- and the L2 reuse of
 // the tile order decide, together with filling whole rounds of 256
 // workgroups:
-//   256 x 288 (8 waves of 64 x 144) where N is a multiple of 288 and the tiles
-//             make whole rounds (fc1: N = 4608, M = 8192 -> 512 tiles);
+//   256 x 288 (8 waves of 64 x 144) where N is a multiple of 288 and its
+//             rounds cost less (fc1: N = 4608, M = 8192 -> 512 tiles);
 //   256 x 256 for long K where N is a multiple of 256 with whole rounds
 //             (joint-attention MLP up-projection: N = 12288 -> 768 tiles);
 //   256 x 144 (8 waves of 32 x 144, three stages) for the other DiT widths;
@@ -317,14 +328,47 @@ hipError_t gemm_dma_dispatch(const bf16* A, int lda, const bf16* W, int ldw, con
 // Row blocks per tile group (see gemm_dma_kernel): 8 for long K, 2 for the
 // 288-wide tiles at short K, 1 for the 144-wide residual updates.  All load
 // with cache policy bit 0 (sc0) set, which measured faster.
+// Projections of a few hundred to ~2000 rows (the 512-px DiT's 1024, the
+// single small requests of a packed batch) on narrower tiles with deeper
+// rings: there the register-staged kernel waits a load latency per K step.
+// Row height 128, 64 or 32: one workgroup per CU (the rings take most of the
+// LDS), so a launch costs about (rounds of 256 tiles) x (the tile's bytes per
+// K step, proportional to BM + 144); the smallest estimate wins, ties to the
+// taller tile (1024 rows: 32 x 144 for the 1152-wide layers -> 256 tiles,
+// 128 x 144 for qkv and fc1).  Every output element accumulates the same
+// MFMAs in the same K order as in every other GEMM path, so results do not
+// depend on the choice.
+hipError_t launch_gemm_dma_small(const bf16* A, int lda, const bf16* W, int ldw, const bf16* bias,
+                                 int M, int N, int K, int kind, const Epi& epi, int vec_ok,
+                                 hipStream_t st) {
+  const long tn = N / 144;
+  auto cost = [&](int bm) { return ((((M + bm - 1) / bm) * tn + 255) / 256) * (bm + 144); };
+  const long c128 = cost(128), c64 = cost(64), c32 = cost(32);
+  if (c128 <= c64 && c128 <= c32)
+    return gemm_dma_dispatch<128, 144, 8, 1, 4, 1>(A, lda, W, ldw, bias, M, N, K, kind, epi, vec_ok,
+                                                   8, st);
+  if (c64 <= c32)
+    return gemm_dma_dispatch<64, 144, 4, 1, 5, 1>(A, lda, W, ldw, bias, M, N, K, kind, epi, vec_ok,
+                                                  8, st);
+  return gemm_dma_dispatch<32, 144, 2, 1, 6, 1>(A, lda, W, ldw, bias, M, N, K, kind, epi, vec_ok,
+                                                16, st);
+}
+
 hipError_t launch_gemm_dma(const bf16* A, int lda, const bf16* W, int ldw, const bf16* bias,
                            int M, int N, int K, int kind, const Epi& epi, int vec_ok,
                            hipStream_t st) {
   const long mt = (M + 255) / 256;
   const bool longk = K >= 2048;
-  if (N % 288 == 0 && (mt * (N / 288)) % 256 == 0)
-    return gemm_dma_dispatch<256, 288, 4, 2, 2, 1>(A, lda, W, ldw, bias, M, N, K, kind, epi, vec_ok,
-                                                   longk ? 8 : 2, st);
+  // 288 wide where its rounds cost less: a round of 256 x 288 tiles takes
+  // ~1.8x a round of 256 x 144 tiles (measured at 8192 rows), so the wider
+  // tile wins when it needs fewer than 5/9 of the rounds (fc1 at 8192 rows:
+  // 2 rounds against 4; the 1152-wide layers at 12 032 rows: 1 against 2)
+  if (N % 288 == 0) {
+    const long r288 = (mt * (N / 288) + 255) / 256, r144 = (mt * (N / 144) + 255) / 256;
+    if (r288 * 9 <= r144 * 5)
+      return gemm_dma_dispatch<256, 288, 4, 2, 2, 1>(A, lda, W, ldw, bias, M, N, K, kind, epi,
+                                                     vec_ok, longk ? 8 : 2, st);
+  }
   if (longk && N % 256 == 0 && (mt * (N / 256)) % 256 == 0)
     return gemm_dma_dispatch<256, 256, 4, 2, 2, 1>(A, lda, W, ldw, bias, M, N, K, kind, epi, vec_ok,
                                                    8, st);
