@@ -626,39 +626,47 @@ __global__ __launch_bounds__(NW * 64, (HD <= 72 ? 16 : 12) / NW) void attn_cross
     attn_barrier();
   }
 
-  // S^T of both tiles, masked past the sequence
+  // S^T of both tiles (the first MFMA of each sum takes a zero accumulator)
   f32x16 sc_[2][2];
 #pragma unroll
   for (int t = 0; t < 2; ++t) {
+    if (t >= nt) break;
 #pragma unroll
-    for (int kb = 0; kb < 2; ++kb) sc_[t][kb] = f32x16{};
-    if (t < nt) {
+    for (int c = 0; c < DC; ++c) {
 #pragma unroll
-      for (int c = 0; c < DC; ++c) {
-#pragma unroll
-        for (int kb = 0; kb < 2; ++kb) {
-          const int r = 32 * kb + ql, cc = 2 * c + hl;
-          bf16x8 kf = bf16x8{};
-          if (cc < CPR) {
-            const int slot = KRS ? cc ^ ((r / KRS) & (CPR - 1)) : cc;
-            kf = *(const bf16x8*)(kst(t) + r * PK + slot * 16);
-          }
-          sc_[t][kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[c], sc_[t][kb], 0, 0, 0);
+      for (int kb = 0; kb < 2; ++kb) {
+        const int r = 32 * kb + ql, cc = 2 * c + hl;
+        bf16x8 kf = bf16x8{};
+        if (cc < CPR) {
+          const int slot = KRS ? cc ^ ((r / KRS) & (CPR - 1)) : cc;
+          kf = *(const bf16x8*)(kst(t) + r * PK + slot * 16);
         }
+        sc_[t][kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[c],
+                                                             c == 0 ? f32x16{} : sc_[t][kb], 0, 0, 0);
       }
     }
   }
+  // Element e of key block kb is key swap23(32 kb + 8 (e >> 2) + (e & 3)) + 8 hl
+  // of its tile (swap23 moves the lane-half bit 2 to bit 3): only the ragged
+  // last tile is masked, against a per-lane threshold and compile-time offsets
   float mx = -INFINITY;
 #pragma unroll
-  for (int t = 0; t < 2; ++t)
+  for (int t = 0; t < 2; ++t) {
+    if (t >= nt) break;
+    const int valid = k_end - (k0 + t * BKV);
+    if (valid < BKV) {
+      const int thr = valid - 8 * hl;
+#pragma unroll
+      for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+        for (int e = 0; e < 16; ++e)
+          if (swap23(32 * kb + 8 * (e >> 2) + (e & 3)) >= thr) sc_[t][kb][e] = -INFINITY;
+    }
 #pragma unroll
     for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
-      for (int e = 0; e < 16; ++e) {
-        const int key = k0 + t * BKV + swap23(32 * kb + 8 * (e >> 2) + 4 * hl + (e & 3));
-        if (key >= k_end) sc_[t][kb][e] = -INFINITY;
-        mx = fmaxf(mx, sc_[t][kb][e]);
-      }
+      for (int e = 0; e < 16; ++e) mx = fmaxf(mx, sc_[t][kb][e]);
+  }
   mx = fmaxf(mx, __shfl_xor(mx, 32, 64));   // the query's keys sit in lanes ql and ql + 32
   // probabilities exp2(sc * (s - mx)): a subtraction, or one fma per score
   const float sc = QS ? 1.0f : scale_log2;
@@ -666,8 +674,6 @@ __global__ __launch_bounds__(NW * 64, (HD <= 72 ? 16 : 12) / NW) void attn_cross
 
   // P V over both tiles; row sums from the ones row or per lane
   f32x16 o[DT];
-#pragma unroll
-  for (int dt = 0; dt < DT; ++dt) o[dt] = f32x16{};
   float psum = 0.f;
 #pragma unroll
   for (int t = 0; t < 2; ++t) {
@@ -688,7 +694,8 @@ __global__ __launch_bounds__(NW * 64, (HD <= 72 ? 16 : 12) / NW) void attn_cross
         const int row = dt * 32 + ql;
         const bf16x8 vf =
             *(const bf16x8*)(vb + row * 128 + (((2 * q + hl) ^ ((row >> 1) & 7)) << 4));
-        o[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf, pf, o[dt], 0, 0, 0);
+        o[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf, pf, t == 0 && q == 0 ? f32x16{} : o[dt],
+                                                        0, 0, 0);
       }
     }
   }
