@@ -947,6 +947,142 @@ __global__ __launch_bounds__(256) void final_kernel(const float* __restrict__ x,
   if (dt != 0.f) lat[li] = lat[li] + dt * vel;
 }
 
+// Final layer of the wide model (64 outputs of width 3072, bf16 weights):
+// a workgroup takes kFwTok tokens so that each 64-column chunk of the
+// projection, staged in LDS as fp32, serves all of them (the per-token wave
+// above reads the 384 KB projection from L2 once per token).  Per guidance
+// branch: the tokens' LayerNorm statistics (two passes over each row, one
+// wave per token), then for each 64-column chunk the modulated rows and the
+// projection's columns go to LDS and every thread accumulates 4 tokens x 2
+// outputs in fp32, K ascending; then guidance, unpatchify, noise_pred and
+// the Euler update as in final_kernel.
+constexpr int kFwTok = 32, kFwK = 64, kFwP = 64;
+
+__global__ __launch_bounds__(256) void final_wide_kernel(const float* __restrict__ x, ReqMap rm,
+                                                         const bf16* __restrict__ w_out,
+                                                         const bf16* __restrict__ b_out,
+                                                         const float* __restrict__ mod, int ld_mod,
+                                                         int shift_off, int scale_off, int D, int C,
+                                                         int p, float eps, float guidance,
+                                                         float* __restrict__ lat,
+                                                         float* __restrict__ noise_pred) {
+  __shared__ float hs[kFwTok][kFwK + 1];
+  __shared__ float ws[kFwP][kFwK + 1];
+  __shared__ float st_mean[kFwTok], st_rstd[kFwTok];
+  __shared__ int st_row[kFwTok];   // modulation row of each token (-1 past the end)
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int tok0 = blockIdx.x * kFwTok;
+  const int T = rm.tokens_total, nb = rm.branches;
+  const int ty = tid >> 5, tx = tid & 31;   // tokens 4 ty .. +3, outputs 2 tx, 2 tx + 1
+  if (tid < kFwTok) {
+    const int t = tok0 + tid;
+    st_row[tid] = t < T ? rm.modrow[req_of_token(rm, t)] : -1;
+  }
+  float res[2][4][2];
+#pragma unroll
+  for (int br = 0; br < 2; ++br) {
+    if (br >= nb) break;
+    __syncthreads();
+    // statistics: wave w takes tokens w, w + 4, ...
+    for (int i = wave; i < kFwTok; i += 4) {
+      const int t = tok0 + i;
+      float mean = 0.f, rstd = 0.f;
+      if (t < T) {
+        const float4* xr = (const float4*)(x + ((size_t)br * T + t) * D);
+        float s = 0.f;
+        for (int c = lane; c < D / 4; c += 64) {
+          const float4 v = xr[c];
+          s += (v.x + v.y) + (v.z + v.w);
+        }
+        mean = wave_sum(s) / (float)D;
+        float q = 0.f;
+        for (int c = lane; c < D / 4; c += 64) {
+          const float4 v = xr[c];
+          const float a = v.x - mean, b = v.y - mean, cc = v.z - mean, d = v.w - mean;
+          q += (a * a + b * b) + (cc * cc + d * d);
+        }
+        rstd = 1.0f / sqrtf(wave_sum(q) / (float)D + eps);
+      }
+      if (lane == 0) {
+        st_mean[i] = mean;
+        st_rstd[i] = rstd;
+      }
+    }
+    float acc[4][2] = {{0.f, 0.f}, {0.f, 0.f}, {0.f, 0.f}, {0.f, 0.f}};
+    for (int k0 = 0; k0 < D; k0 += kFwK) {
+      __syncthreads();
+      // modulated rows: 32 tokens x 64 columns, 8 per thread (2 float4)
+#pragma unroll
+      for (int j = 0; j < 2; ++j) {
+        const int e = tid + 256 * j, t = e >> 4, c4 = (e & 15) * 4;
+        float4 h = float4{0.f, 0.f, 0.f, 0.f};
+        const int mr = st_row[t];
+        if (mr >= 0) {
+          const float4 v = *(const float4*)(x + ((size_t)br * T + tok0 + t) * D + k0 + c4);
+          const float* md = mod + (size_t)mr * ld_mod;
+          const float4 sh = *(const float4*)(md + shift_off + k0 + c4);
+          const float4 sc = *(const float4*)(md + scale_off + k0 + c4);
+          const float mu = st_mean[t], rs = st_rstd[t];
+          h.x = (v.x - mu) * rs * (1.f + sc.x) + sh.x;
+          h.y = (v.y - mu) * rs * (1.f + sc.y) + sh.y;
+          h.z = (v.z - mu) * rs * (1.f + sc.z) + sh.z;
+          h.w = (v.w - mu) * rs * (1.f + sc.w) + sh.w;
+        }
+        hs[t][c4] = h.x;
+        hs[t][c4 + 1] = h.y;
+        hs[t][c4 + 2] = h.z;
+        hs[t][c4 + 3] = h.w;
+      }
+      // the projection's 64 x 64 chunk, 16 per thread (2 x 8 bf16)
+#pragma unroll
+      for (int j = 0; j < 2; ++j) {
+        const int e = tid + 256 * j, f = e >> 3, c8 = (e & 7) * 8;
+        const bf16x8 w = *(const bf16x8*)(w_out + (size_t)f * D + k0 + c8);
+#pragma unroll
+        for (int q = 0; q < 8; ++q) ws[f][c8 + q] = (float)w[q];
+      }
+      __syncthreads();
+#pragma unroll 8
+      for (int k = 0; k < kFwK; ++k) {
+        const float w0 = ws[2 * tx][k], w1 = ws[2 * tx + 1][k];
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const float h = hs[4 * ty + i][k];
+          acc[i][0] = fmaf(h, w0, acc[i][0]);
+          acc[i][1] = fmaf(h, w1, acc[i][1]);
+        }
+      }
+    }
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      res[br][i][0] = acc[i][0];
+      res[br][i][1] = acc[i][1];
+    }
+  }
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const int tok = tok0 + 4 * ty + i;
+    if (tok >= T) continue;
+    const int r = req_of_token(rm, tok);
+    const int lt = tok - rm.tok_off[r];
+    const int W = rm.w[r], H = rm.h[r], gw = W / p;
+    const int gi = lt / gw, gj = lt - gi * gw;
+#pragma unroll
+    for (int j = 0; j < 2; ++j) {
+      const int f = 2 * tx + j;
+      const float bo = (float)b_out[f];
+      const float vc = res[0][i][j] + bo;
+      const float vel = nb == 2 ? (res[1][i][j] + bo) + guidance * (vc - (res[1][i][j] + bo)) : vc;
+      const int a = f / (p * C), b = (f / C) % p, c = f % C;
+      const size_t li =
+          (size_t)rm.lat_off[r] + (size_t)c * H * W + (size_t)(gi * p + a) * W + gj * p + b;
+      if (noise_pred) noise_pred[li] = vel;
+      const float dt = rm.dt[r];
+      if (dt != 0.f) lat[li] = lat[li] + dt * vel;
+    }
+  }
+}
+
 hipError_t launch_final_layer(const float* x, const ReqMap& rm, const void* w_out,
                               const void* b_out, bool w_bf16, const float* mod, int ld_mod,
                               int shift_off, int scale_off, int D, int C, int p, float eps,
@@ -960,7 +1096,12 @@ hipError_t launch_final_layer(const float* x, const ReqMap& rm, const void* w_ou
                      latents, noise_pred)
   if (w_bf16) {
     if (P == 16 && D == 1152) T2I_FIN(bf16, 16, 288);
-    else if (P == 64 && D == 3072) T2I_FIN(bf16, 64, 768);
+    else if (P == kFwP && D % kFwK == 0 && (uintptr_t)w_out % 16 == 0) {
+      hipLaunchKernelGGL(final_wide_kernel, dim3((rm.tokens_total + kFwTok - 1) / kFwTok), block,
+                         0, st, x, rm, (const bf16*)w_out, (const bf16*)b_out, mod, ld_mod,
+                         shift_off, scale_off, D, C, p, eps, guidance, latents, noise_pred);
+      return hipGetLastError();
+    }
     else if (P == 16) T2I_FIN(bf16, 16, 0);
     else T2I_FIN(bf16, 0, 0);
   } else {
