@@ -81,9 +81,12 @@ __device__ __forceinline__ void block_barrier() {
   asm volatile("s_barrier" ::: "memory");
 }
 
+// xpre: this fragment's residual values when already fetched; gated updates
+// take the gate values g4 when have_g, else read them here
 template <int KIND>
 __device__ __forceinline__ void dma_epi4(const Epi& e, int m, int nb, const float v[4],
-                                         const float4* xpre = nullptr) {
+                                         const float4* xpre = nullptr, bool have_g = false,
+                                         float4 g4 = float4{1.f, 1.f, 1.f, 1.f}) {
   if (KIND == EPI_STORE_F32) {
     *(float4*)((float*)e.out + (size_t)m * e.ldo + nb) = float4{v[0], v[1], v[2], v[3]};
   } else if (KIND == EPI_STORE || KIND == EPI_GELU || KIND == EPI_SILU) {
@@ -99,8 +102,7 @@ __device__ __forceinline__ void dma_epi4(const Epi& e, int m, int nb, const floa
     }
     *(bf16x4*)((bf16*)e.out + (size_t)m * e.ldo + nb) = w;
   } else {
-    float4 g4 = float4{1.f, 1.f, 1.f, 1.f};
-    if (KIND == EPI_RESID_GATED)
+    if (KIND == EPI_RESID_GATED && !have_g)
       g4 = *(const float4*)(e.gate + (size_t)e.map.modrow[seq_of_row(e.map, m)] * e.ld_gate + nb);
     float4* xp = (float4*)(e.x + (size_t)m * e.ldx + nb);
     float4 x4 = xpre ? *xpre : *xp;
@@ -131,7 +133,13 @@ __global__ __launch_bounds__(64 * WGM * WGN, 1) void gemm_dma_kernel(
   static_assert(BM % 8 == 0 && BN % 8 == 0 && WM % 16 == 0 && WN % 16 == 0, "tile shape");
   static_assert(ST >= 2 && ST <= 7 && (ST - 2) * BPW < 64, "stages");
   static_assert(ABLK % NW == 0, "A / W blocks split evenly over the load rounds");
-  __shared__ __attribute__((aligned(1024))) bf16 smem[ST * STAGE];
+  // the stage ring, then the epilogue's fp32 bias and gate rows (one LDS
+  // object: with several, the compiler makes every fragment read wait for
+  // all outstanding tile loads)
+  constexpr bool GATED = KIND == EPI_RESID_GATED;
+  __shared__ __attribute__((aligned(1024))) bf16 smem[ST * STAGE + (GATED ? 4 : 2) * BN];
+  float* const ebias = (float*)(smem + ST * STAGE);
+  float* const egate = ebias + BN;
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int wm = wave / WGN, wn = wave % WGN;
@@ -201,6 +209,27 @@ __global__ __launch_bounds__(64 * WGM * WGN, 1) void gemm_dma_kernel(
     }
   };
 
+  // Epilogue operands of a tile that is whole in N: its BN bias values and,
+  // for a gated update whose rows all belong to one sequence, its BN gate
+  // values.  The first BN / 4 threads fetch them now, ahead of every tile
+  // load (so the vmcnt thresholds below, which count younger loads, stay
+  // exact), and put them in LDS after the main loop; the epilogue then reads
+  // LDS only and its stores never wait behind a global load.
+  const bool whole_n = vec_ok && n0 + BN <= N;
+  bool one_seq = false;
+  int grow = 0;
+  if constexpr (GATED) {
+    const int s0 = seq_of_row(epi.map, m0), s1 = seq_of_row(epi.map, min(m0 + BM, M) - 1);
+    one_seq = whole_n && s0 == s1;
+    grow = epi.map.modrow[s0];
+  }
+  const bool stager = tid < BN / 4;
+  bf16x4 sbias{};
+  float4 sgate{};
+  if (whole_n && stager) sbias = *(const bf16x4*)(bias + n0 + 4 * tid);
+  if (GATED && one_seq && stager)
+    sgate = *(const float4*)(epi.gate + (size_t)grow * epi.ld_gate + n0 + 4 * tid);
+
   // Gated residual updates with small per-wave tiles read this lane's fp32
   // residual values before the main loop: all workgroups of such a launch
   // reach the epilogue together, and its HBM reads would otherwise come after
@@ -240,24 +269,62 @@ __global__ __launch_bounds__(64 * WGM * WGN, 1) void gemm_dma_kernel(
     }
   }
 
+  if (whole_n) {
+    if (stager) {
+      *(float4*)&ebias[4 * tid] =
+          float4{(float)sbias[0], (float)sbias[1], (float)sbias[2], (float)sbias[3]};
+      if (GATED && one_seq) *(float4*)&egate[4 * tid] = sgate;
+    }
+    block_barrier();
+  }
+
   if (CT) {
+    if (whole_n) {
 #pragma unroll
-    for (int i = 0; i < TM; ++i) {
-      const int m = m0 + wm * WM + i * 16 + fr;
-      if (m >= M) continue;
+      for (int i = 0; i < TM; ++i) {
+        const int m = m0 + wm * WM + i * 16 + fr;
+        if (m >= M) continue;
+        // plain residual updates: this row's residual values fetched together
+        constexpr bool XL = KIND == EPI_RESID;
+        float4 xl[XL ? TN : 1];
+        if constexpr (XL) {
 #pragma unroll
-      for (int j = 0; j < TN; ++j) {
-        const int nb = n0 + wn * WN + j * 16 + g * 4;
-        if (vec_ok && nb + 3 < N) {
-          const bf16x4 b4 = *(const bf16x4*)(bias + nb);
-          const float v[4] = {acc[i][j][0] + (float)b4[0], acc[i][j][1] + (float)b4[1],
-                              acc[i][j][2] + (float)b4[2], acc[i][j][3] + (float)b4[3]};
-          if constexpr (PREX) dma_epi4<KIND>(epi, m, nb, v, &xpre[i][j]);
-          else dma_epi4<KIND>(epi, m, nb, v);
-        } else {
+          for (int j = 0; j < TN; ++j)
+            xl[j] = *(const float4*)(epi.x + (size_t)m * epi.ldx + n0 + wn * WN + j * 16 + g * 4);
+        }
 #pragma unroll
-          for (int r = 0; r < 4; ++r)
-            if (nb + r < N) epi_apply<bf16>(epi, KIND, m, nb + r, acc[i][j][r] + (float)bias[nb + r]);
+        for (int j = 0; j < TN; ++j) {
+          const int col = wn * WN + j * 16 + g * 4;
+          const float4 b4 = *(const float4*)&ebias[col];
+          const float v[4] = {acc[i][j][0] + b4.x, acc[i][j][1] + b4.y, acc[i][j][2] + b4.z,
+                              acc[i][j][3] + b4.w};
+          const float4* xp = nullptr;
+          if constexpr (PREX) xp = &xpre[i][j];
+          if constexpr (XL) xp = &xl[j];
+          float4 g4 = float4{1.f, 1.f, 1.f, 1.f};
+          if (GATED && one_seq) g4 = *(const float4*)&egate[col];
+          dma_epi4<KIND>(epi, m, n0 + col, v, xp, GATED && one_seq, g4);
+        }
+      }
+    } else {
+#pragma unroll
+      for (int i = 0; i < TM; ++i) {
+        const int m = m0 + wm * WM + i * 16 + fr;
+        if (m >= M) continue;
+#pragma unroll
+        for (int j = 0; j < TN; ++j) {
+          const int nb = n0 + wn * WN + j * 16 + g * 4;
+          if (vec_ok && nb + 3 < N) {
+            const bf16x4 b4 = *(const bf16x4*)(bias + nb);
+            const float v[4] = {acc[i][j][0] + (float)b4[0], acc[i][j][1] + (float)b4[1],
+                                acc[i][j][2] + (float)b4[2], acc[i][j][3] + (float)b4[3]};
+            if constexpr (PREX) dma_epi4<KIND>(epi, m, nb, v, &xpre[i][j]);
+            else dma_epi4<KIND>(epi, m, nb, v);
+          } else {
+#pragma unroll
+            for (int r = 0; r < 4; ++r)
+              if (nb + r < N) epi_apply<bf16>(epi, KIND, m, nb + r, acc[i][j][r] + (float)bias[nb + r]);
+          }
         }
       }
     }
@@ -266,7 +333,7 @@ __global__ __launch_bounds__(64 * WGM * WGN, 1) void gemm_dma_kernel(
     for (int j = 0; j < TN; ++j) {
       const int n = n0 + wn * WN + j * 16 + fr;
       if (n >= N) continue;
-      const float b = (float)bias[n];
+      const float b = whole_n ? ebias[n - n0] : (float)bias[n];
 #pragma unroll
       for (int i = 0; i < TM; ++i) {
         const int mb = m0 + wm * WM + i * 16 + g * 4;

@@ -99,10 +99,14 @@ __device__ __forceinline__ double wave_sum(double v) {
 // The reciprocal is the hardware v_rcp_f32 (about 1 ulp), not an IEEE
 // division: exp(-2z) -> +inf gives rcp(inf) = 0 and u * 0 = -0 for u -> -inf,
 // matching the limit.
+// u * sigmoid(2 z), z = sqrt(2/pi) (u + 0.044715 u^3): exp(-2 z) taken as
+// 2^(u (c1 + c2 u^2)) with the constants folded (one multiply-add and two
+// multiplies before the exponential)
 __device__ __forceinline__ float gelu_tanh(float u) {
-  const float k0 = 0.7978845608028654f;   // sqrt(2/pi)
-  const float z = k0 * fmaf(0.044715f * u, u * u, u);
-  return u * __builtin_amdgcn_rcpf(1.0f + __expf(-2.0f * z));
+  constexpr float c1 = -2.0f * 0.7978845608028654f * 1.4426950408889634f;
+  constexpr float c2 = c1 * 0.044715f;
+  const float t = u * fmaf(c2, u * u, c1);
+  return u * __builtin_amdgcn_rcpf(1.0f + __builtin_amdgcn_exp2f(t));
 }
 
 __device__ __forceinline__ float silu(float v) { return v * __builtin_amdgcn_rcpf(1.0f + __expf(-v)); }
