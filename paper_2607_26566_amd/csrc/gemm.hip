@@ -145,9 +145,36 @@ __device__ __forceinline__ void gemm_bf16_body(const bf16* __restrict__ A, int l
 #pragma unroll
     for (int j = 0; j < TN; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
 
+  // Epilogue operands of a tile that is whole in N (as in gemm_dma.hip): the
+  // BN bias values and, for a gated update whose rows all belong to one
+  // sequence, the BN gate values, fetched with the first tile and kept in LDS,
+  // so that the epilogue's stores never wait behind a global load.
+  constexpr bool GATED = KIND == EPI_RESID_GATED;
+  __shared__ __attribute__((aligned(16))) float ebias[BN];
+  __shared__ __attribute__((aligned(16))) float egate[GATED ? BN : 4];
+  const bool whole_n = !PART && vec_ok && n0 + BN <= N;
+  bool one_seq = false;
+  int grow = 0;
+  if constexpr (GATED) {
+    const int s0 = seq_of_row(epi.map, m0), s1 = seq_of_row(epi.map, min(m0 + BM, M) - 1);
+    one_seq = whole_n && s0 == s1;
+    grow = epi.map.modrow[s0];
+  }
+  const bool stager = tid < BN / 4;
+  bf16x4 sbias{};
+  float4 sgate{};
+  if (whole_n && stager) sbias = *(const bf16x4*)(bias + n0 + 4 * tid);
+  if (GATED && one_seq && stager)
+    sgate = *(const float4*)(epi.gate + (size_t)grow * epi.ld_gate + n0 + 4 * tid);
+
   const int KT = K / BK;
   gload(0);
   sstore(0);
+  if (whole_n && stager) {
+    *(float4*)&ebias[4 * tid] =
+        float4{(float)sbias[0], (float)sbias[1], (float)sbias[2], (float)sbias[3]};
+    if (GATED && one_seq) *(float4*)&egate[4 * tid] = sgate;
+  }
   __syncthreads();
   const int fr = lane & 15, fk = (lane >> 4) * 8;
   for (int kt = 0; kt < KT; ++kt) {
@@ -173,8 +200,51 @@ __device__ __forceinline__ void gemm_bf16_body(const bf16* __restrict__ A, int l
     __syncthreads();
   }
 
-  if (CT) {
+  if (CT && whole_n) {
     // C^T fragment: lane holds row m = (lane & 15), columns 4*(lane >> 4) + 0..3
+#pragma unroll
+    for (int i = 0; i < TM; ++i) {
+      const int m = m0 + wm * WM + i * 16 + fr;
+      if (m >= M) continue;
+      if constexpr (KIND == EPI_RESID || KIND == EPI_RESID_GATED) {
+        // this row's residual values fetched together, then updated
+        float4 xl[TN];
+#pragma unroll
+        for (int j = 0; j < TN; ++j)
+          xl[j] = *(const float4*)(epi.x + (size_t)m * epi.ldx + n0 + wn * WN + j * 16 + (lane >> 4) * 4);
+#pragma unroll
+        for (int j = 0; j < TN; ++j) {
+          const int col = wn * WN + j * 16 + (lane >> 4) * 4;
+          const float4 b4 = *(const float4*)&ebias[col];
+          float4 g4 = float4{1.f, 1.f, 1.f, 1.f};
+          if (GATED) {
+            g4 = one_seq ? *(const float4*)&egate[col]
+                         : *(const float4*)(epi.gate + (size_t)epi.map.modrow[seq_of_row(epi.map, m)] *
+                                                           epi.ld_gate + n0 + col);
+          }
+          float4 x4 = xl[j];
+          x4.x += g4.x * (acc[i][j][0] + b4.x);
+          x4.y += g4.y * (acc[i][j][1] + b4.y);
+          x4.z += g4.z * (acc[i][j][2] + b4.z);
+          x4.w += g4.w * (acc[i][j][3] + b4.w);
+          *(float4*)(epi.x + (size_t)m * epi.ldx + n0 + col) = x4;
+          if (epi.xb) {
+            bf16x4 w{(bf16)x4.x, (bf16)x4.y, (bf16)x4.z, (bf16)x4.w};
+            *(bf16x4*)(epi.xb + (size_t)m * epi.ldx + n0 + col) = w;
+          }
+        }
+      } else {
+#pragma unroll
+        for (int j = 0; j < TN; ++j) {
+          const int col = wn * WN + j * 16 + (lane >> 4) * 4;
+          const float4 b4 = *(const float4*)&ebias[col];
+          const float v[4] = {acc[i][j][0] + b4.x, acc[i][j][1] + b4.y, acc[i][j][2] + b4.z,
+                              acc[i][j][3] + b4.w};
+          epi_store4<EK>(epi, m, n0 + col, v);
+        }
+      }
+    }
+  } else if (CT) {
 #pragma unroll
     for (int i = 0; i < TM; ++i) {
       const int m = m0 + wm * WM + i * 16 + fr;
@@ -195,13 +265,45 @@ __device__ __forceinline__ void gemm_bf16_body(const bf16* __restrict__ A, int l
         }
       }
     }
+  } else if (KIND == EPI_SPLIT_VT && whole_n && m0 + BM <= M && n0 >= epi.vcol0) {
+    // a whole V tile: four consecutive tokens of one V column per store
+#pragma unroll
+    for (int j = 0; j < TN; ++j) {
+      const int n = n0 + wn * WN + j * 16 + fr;
+      const float b = ebias[n - n0];
+      bf16* vt = epi.vt + (size_t)(n - epi.vcol0) * epi.ldvt;
+#pragma unroll
+      for (int i = 0; i < TM; ++i) {
+        const int mb = m0 + wm * WM + i * 16 + (lane >> 4) * 4;
+        bf16x4 v4;
+#pragma unroll
+        for (int r = 0; r < 4; ++r) v4[r] = (bf16)(acc[i][j][r] + b);
+        *(bf16x4*)(vt + mb) = v4;
+      }
+    }
+  } else if (KIND == EPI_SPLIT_VT && whole_n && m0 + BM <= M && n0 + BN <= epi.vcol0) {
+    // a whole q|k tile: no per-element bounds or column-range tests (the
+    // query columns scaled exactly as epi_apply scales them)
+#pragma unroll
+    for (int j = 0; j < TN; ++j) {
+      const int n = n0 + wn * WN + j * 16 + fr;
+      const float b = ebias[n - n0];
+      const float qs = n < epi.qcols ? epi.qscale : 1.f;
+      bf16* o = (bf16*)epi.out + n;
+#pragma unroll
+      for (int i = 0; i < TM; ++i) {
+        const int mb = m0 + wm * WM + i * 16 + (lane >> 4) * 4;
+#pragma unroll
+        for (int r = 0; r < 4; ++r) o[(size_t)(mb + r) * epi.ldo] = (bf16)((acc[i][j][r] + b) * qs);
+      }
+    }
   } else {
     // C fragment: lane holds column (lane & 15), rows 4*(lane >> 4) + 0..3
 #pragma unroll
     for (int j = 0; j < TN; ++j) {
       const int n = n0 + wn * WN + j * 16 + fr;
       if (n >= N) continue;
-      const float b = (float)bias[n];
+      const float b = whole_n ? ebias[n - n0] : (float)bias[n];
 #pragma unroll
       for (int i = 0; i < TM; ++i) {
         const int mb = m0 + wm * WM + i * 16 + (lane >> 4) * 4;

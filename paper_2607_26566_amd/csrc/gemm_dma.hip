@@ -328,6 +328,38 @@ __global__ __launch_bounds__(64 * WGM * WGN, 1) void gemm_dma_kernel(
         }
       }
     }
+  } else if (KIND == EPI_SPLIT_VT && whole_n && m0 + BM <= M && n0 >= epi.vcol0) {
+    // a whole V tile: four consecutive tokens of one V column per store
+#pragma unroll
+    for (int j = 0; j < TN; ++j) {
+      const int n = n0 + wn * WN + j * 16 + fr;
+      const float b = ebias[n - n0];
+      bf16* vt = epi.vt + (size_t)(n - epi.vcol0) * epi.ldvt;
+#pragma unroll
+      for (int i = 0; i < TM; ++i) {
+        const int mb = m0 + wm * WM + i * 16 + g * 4;
+        bf16x4 v4;
+#pragma unroll
+        for (int r = 0; r < 4; ++r) v4[r] = (bf16)(acc[i][j][r] + b);
+        *(bf16x4*)(vt + mb) = v4;
+      }
+    }
+  } else if (KIND == EPI_SPLIT_VT && whole_n && m0 + BM <= M && n0 + BN <= epi.vcol0) {
+    // a whole q|k tile: no per-element bounds or column-range tests (the
+    // query columns scaled exactly as epi_apply scales them)
+#pragma unroll
+    for (int j = 0; j < TN; ++j) {
+      const int n = n0 + wn * WN + j * 16 + fr;
+      const float b = ebias[n - n0];
+      const float qs = n < epi.qcols ? epi.qscale : 1.f;
+      bf16* o = (bf16*)epi.out + n;
+#pragma unroll
+      for (int i = 0; i < TM; ++i) {
+        const int mb = m0 + wm * WM + i * 16 + g * 4;
+#pragma unroll
+        for (int r = 0; r < 4; ++r) o[(size_t)(mb + r) * epi.ldo] = (bf16)((acc[i][j][r] + b) * qs);
+      }
+    }
   } else {
 #pragma unroll
     for (int j = 0; j < TN; ++j) {
