@@ -366,6 +366,27 @@ __global__ __launch_bounds__(NW * 64, 8 / NW) void attn_bf16_kernel(AttnMap map,
       if (PAIR && ti + ST - 2 < nt) issue(ti + ST - 2);
       if (ti + ST - 1 < nt) issue(ti + ST - 1);
     }
+    // Up to head dimension 72: the slot schedule's constants, and its first
+    // LA + 1 fragment reads (K of the next tile, d chunks 0 and 1), issued
+    // before the maximum test below, which they do not depend on, so that
+    // their LDS latency overlaps it
+    constexpr bool SLOTS = DC <= 5;
+    constexpr int NQK = 2 * DC, NPV = 4 * DT, NSL = NQK + NPV, LA = 3;
+    constexpr int NE = NQK + 3 * DT;   // slots carrying exponentials
+    const int stn = (ti + 1) % ST;
+    const char* vb = vst(ti % ST);
+    // slot sl's A operand: K of the next tile for sl < NQK, else V^T row
+    // 32dt + ql, keys 16q + 8hl .. +7
+    auto frag = [&](int sl) {
+      if (sl < NQK) return kfrag(stn, sl & 1, sl >> 1);
+      const int q = (sl - NQK) / DT, dt = (sl - NQK) % DT, row = dt * 32 + ql;
+      return *(const bf16x8*)(vb + row * 128 + (((2 * q + hl) ^ ((row >> 1) & 7)) << 4));
+    };
+    bf16x8 fr[SLOTS ? NSL : 1];
+    if constexpr (SLOTS) {
+#pragma unroll
+      for (int sl = 0; sl <= LA; ++sl) fr[sl] = frag(sl);
+    }
     if (!tile_full(ti)) {
       const int kv0 = tile_kv0(ti), k_end = tile_end(ti);
       // ragged tile: mask the scores past the sequence.  V^T chunks wholly
@@ -406,31 +427,23 @@ __global__ __launch_bounds__(NW * 64, 8 / NW) void attn_bf16_kernel(AttnMap map,
       m_ref = m_new;
       if (hl == BH) qf[BC][0] = (bf16)(-m_new);
     }
-    if constexpr (DC <= 5) {
+    if constexpr (SLOTS) {
       // Straight-line part in a fixed issue order.  Slot s issues one MFMA --
       // the next tile's S^T for s < NQK (chunk s/2, key block s%2), else P V
       // for (key chunk, d tile) -- then its share of this tile's exponentials
       // and the LDS fragment read LA slots ahead.  A scheduling barrier between
       // slots keeps the exponentials spread over the MFMAs instead of bunched
       // (the compiler otherwise clusters them).  P chunk q is complete before
-      // the first P V MFMA that uses it.  For the last tile the "next" scores
-      // come from a stale stage and are never used.
-      constexpr int NQK = 2 * DC, NPV = 4 * DT, NSL = NQK + NPV, LA = 3;
-      constexpr int NE = NQK + 3 * DT;   // slots carrying exponentials
-      const int stn = (ti + 1) % ST;
-      const char* vb = vst(ti % ST);
-      // V^T row 32dt + ql, keys 16q + 8hl .. +7
-      auto frag = [&](int sl) {
-        if (sl < NQK) return kfrag(stn, sl & 1, sl >> 1);
-        const int q = (sl - NQK) / DT, dt = (sl - NQK) % DT, row = dt * 32 + ql;
-        return *(const bf16x8*)(vb + row * 128 + (((2 * q + hl) ^ ((row >> 1) & 7)) << 4));
-      };
-      bf16x8 fr[NSL];
+      // the first P V MFMA that uses it.  The slots from MX0 on, once the
+      // next tile's S^T MFMAs have finished, also take the lane maximum of
+      // those scores, a share per slot, off the path between tiles.  For the
+      // last tile the "next" scores come from a stale stage and are never
+      // used.
+      constexpr int MX0 = NQK + 2, NMX = NSL - MX0;
       float pe[32];     // exponential i = P chunk i/8, element i%8
       bf16x8 pf[4];
       float psum = 0.f;
-#pragma unroll
-      for (int sl = 0; sl <= LA; ++sl) fr[sl] = frag(sl);
+      float mx = -INFINITY;
       __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
       for (int sl = 0; sl < NSL; ++sl) {
@@ -452,10 +465,19 @@ __global__ __launch_bounds__(NW * 64, 8 / NW) void attn_bf16_kernel(AttnMap map,
 #pragma unroll
             for (int e = 0; e < 8; ++e) pf[i >> 3][e] = (bf16)pe[(i & ~7) + e];
         }
+        if (sl >= MX0) {
+          const int v0 = 32 * (sl - MX0) / NMX, v1 = 32 * (sl - MX0 + 1) / NMX;
+#pragma unroll
+          for (int v = v0; v < v1; ++v) mx = fmaxf(mx, nxt[v >> 4][v & 15]);
+          // keep the share in this slot (otherwise the chain is sunk to the
+          // next tile's maximum test, in front of its first MFMA)
+          asm volatile("" : "+v"(mx));
+        }
         if (sl + LA + 1 < NSL) fr[sl + LA + 1] = frag(sl + LA + 1);
         __builtin_amdgcn_sched_barrier(0);
       }
       if (!ONES) l_run += psum;
+      lm_nxt = mx;
     } else {
       // larger head dimensions: the compiler's schedule (the fixed order
       // needs more registers than the loop has there) -- the next tile's
@@ -483,8 +505,8 @@ __global__ __launch_bounds__(NW * 64, 8 / NW) void attn_bf16_kernel(AttnMap map,
               *(const bf16x8*)(vb + row * 128 + (((2 * q + hl) ^ ((row >> 1) & 7)) << 4));
           o[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf, pf[q], o[dt], 0, 0, 0);
         }
+      lm_nxt = lane_max(nxt);
     }
-    lm_nxt = lane_max(nxt);
   };
 
   // prologue: the tiles before the first step's loads in flight, tile 0's
