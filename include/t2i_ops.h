@@ -71,6 +71,22 @@ t2i_status t2i_op_attention(int32_t dtype, int32_t heads, int32_t head_dim,
                             int32_t ldv, void* o, int32_t ldo, void* stream);
 
 /*
+ * Cross-attention of image queries to their request's text (Sec. 4's model
+ * `forward`, the DiT block's attention to the caption): the operation of
+ * t2i_op_attention with one key segment per sequence, bf16 only (else
+ * T2I_ERR_INVALID_ARG), run by the kernels the model uses for it -- texts
+ * of at most 128 keys (k_len 1..128) by the two-tile kernel that keeps them
+ * in LDS across query tiles, longer texts by the pipelined one.  Arguments,
+ * layouts (V given transposed) and limits are those of t2i_op_attention.
+ */
+t2i_status t2i_op_cross_attention(int32_t dtype, int32_t heads, int32_t head_dim,
+                                  int32_t n_seq, const int32_t* q_start,
+                                  const int32_t* q_len, const int32_t* k_start,
+                                  const int32_t* k_len, const void* q, int32_t ldq,
+                                  const void* k, int32_t ldk, const void* v,
+                                  int32_t ldv, void* o, int32_t ldo, void* stream);
+
+/*
  * LayerNorm (no affine, biased variance) fused with adaLN modulation:
  * out = (x - mean) / sqrt(var + eps) * (1 + scale) + shift per row of
  * x [rows, D] fp32; shift, scale fp32 [D]; out dtype (bf16 or fp32) [rows, D].

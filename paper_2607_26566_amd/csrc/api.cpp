@@ -1462,6 +1462,45 @@ t2i_status t2i_op_attention(int32_t dtype, int32_t heads, int32_t head_dim, int3
   return T2I_OK;
 }
 
+t2i_status t2i_op_cross_attention(int32_t dtype, int32_t heads, int32_t head_dim, int32_t n_seq,
+                                  const int32_t* q_start, const int32_t* q_len,
+                                  const int32_t* k_start, const int32_t* k_len, const void* q,
+                                  int32_t ldq, const void* k, int32_t ldk, const void* v,
+                                  int32_t ldv, void* o, int32_t ldo, void* stream) {
+  if (dtype != T2I_BF16) return ops_fail(T2I_ERR_INVALID_ARG, "cross-attention is bf16 only");
+  if (heads < 1 || (head_dim != 8 && head_dim != 32 && head_dim != 64 && head_dim != 72 &&
+                    head_dim != 128))
+    return ops_fail(T2I_ERR_SHAPE, "unsupported head_dim");
+  if (n_seq < 1 || n_seq > kMaxSeq) return ops_fail(T2I_ERR_SHAPE, "bad n_seq");
+  if (!q_start || !q_len || !k_start || !k_len || !q || !k || !v || !o)
+    return ops_fail(T2I_ERR_INVALID_ARG, "NULL pointer");
+  const int w = heads * head_dim;
+  if (ldq < w || ldk < w || ldo < w || ldq % 8 || ldk % 8 || ldv % 8 || ldo % 8)
+    return ops_fail(T2I_ERR_SHAPE, "bad leading dimension");
+  AttnMap m;
+  std::memset(&m, 0, sizeof(m));
+  m.n = n_seq;
+  long k_rows = 0;
+  for (int s = 0; s < n_seq; ++s) {
+    if (q_start[s] < 0 || q_len[s] < 0 || k_start[s] < 0 || k_len[s] < 1)
+      return ops_fail(T2I_ERR_SHAPE, "bad sequence bounds");
+    if (k_start[s] % 8 || (long)k_start[s] + k_len[s] > ldv)
+      return ops_fail(T2I_ERR_SHAPE, "bf16 attention needs key starts % 8 == 0 and keys within ldv");
+    m.q_start[s] = q_start[s];
+    m.q_len[s] = q_len[s];
+    m.k_start[s] = k_start[s];
+    m.k_len[s] = k_len[s];
+    k_rows = std::max(k_rows, (long)k_start[s] + k_len[s]);
+  }
+  if ((size_t)2 * heads * head_dim * ldv > 0x7fffffff || (size_t)2 * (k_rows + 64) * ldk > 0x7fffffff)
+    return ops_fail(T2I_ERR_SHAPE, "bf16 attention operands exceed 2 GiB of addressing");
+  attention_tiles(m, true, heads, 1);
+  hipError_t err = launch_attention(true, 1, heads, head_dim, m, q, ldq, k, ldk, v, ldv, o, ldo,
+                                    (hipStream_t)stream, false);
+  if (err != hipSuccess) return ops_fail(T2I_ERR_DEVICE, hipGetErrorString(err));
+  return T2I_OK;
+}
+
 t2i_status t2i_op_ln_modulate(int32_t dtype, int32_t rows, int32_t D, const float* x,
                               const float* shift, const float* scale, float eps, void* out,
                               void* stream) {

@@ -556,15 +556,21 @@ __global__ __launch_bounds__(NW * 64, 8 / NW) void attn_bf16_kernel(AttnMap map,
 // Cross-attention to a text of at most 128 keys (two key tiles).  Both tiles
 // are loaded once into LDS, all scores are computed, and the softmax uses
 // the exact row maximum (no running maximum, no rescaling, no next-tile
-// lookahead).  The smaller register and LDS footprint (two stages, 127
-// VGPRs and 40 KB at head dimension 72) lets four 4-wave workgroups share a
-// CU instead of two: these launches are short and bound by latency, so the
-// workgroups in flight are what counts (at 1024 px with guidance, 1024
-// workgroups: one round of the chip).
+// lookahead).  A workgroup takes R consecutive query tiles of one head: the
+// text's K / V^T stay in LDS from one to the next (reloaded only where the
+// tiles cross into another sequence), and the next tile's Q fragments are
+// fetched while this tile computes, so that its loads, its MFMAs and the
+// previous tile's output stores overlap instead of the whole launch passing
+// through them in step (with R = 1, one round of small workgroups does).
+// The register and LDS footprint (40 KB at head dimension 72) lets four
+// 4-wave workgroups share a CU at R = 1 and two at R > 1.  Workgroups of
+// neighbouring heads take the same query tiles at the same time, so the
+// 128-byte lines of the Q and O rows, shared by neighbouring heads, are read
+// and written once.
 // Layouts (K rows in swap23 key order, V^T chunk swizzle, ones row of V^T for
 // the row sums) and the QS convention are those of attn_bf16_kernel.
-template <int HD, int NW, bool QS>
-__global__ __launch_bounds__(NW * 64, (HD <= 72 ? 16 : 12) / NW) void attn_cross_kernel(
+template <int HD, int NW, bool QS, int R>
+__global__ __launch_bounds__(NW * 64, (R > 1 ? 8 : (HD <= 72 ? 16 : 12)) / NW) void attn_cross_kernel(
     AttnMap map, int heads, const bf16* __restrict__ Q, int ldq, const bf16* __restrict__ K,
     int ldk, const bf16* __restrict__ Vt, int ldvt, bf16* __restrict__ O, int ldo,
     float scale_log2) {
@@ -577,7 +583,6 @@ __global__ __launch_bounds__(NW * 64, (HD <= 72 ? 16 : 12) / NW) void attn_cross
   // V^T rows kept per stage: the data and the ones row.  The P V MFMAs also
   // read the padding rows up to HDO - 1, which only feed O^T rows that are
   // never used: for stage 0 they are stage 1's K rows, for stage 1 a pad.
-  // (Head dimension 72: 40 KB in all, four workgroups per CU.)
   constexpr int VROWS = ONES ? HD + 1 : HDO;
   constexpr int KSTAGE = BKV * PK, VSTAGE = VROWS * 128, VPAD = (HDO - VROWS) * 128;
   static_assert(HD % 8 == 0 && KSTAGE % 1024 == 0, "head dim");
@@ -585,163 +590,227 @@ __global__ __launch_bounds__(NW * 64, (HD <= 72 ? 16 : 12) / NW) void attn_cross
 
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-  int hh, s, j;
-  decode_tile<true>(map, heads, xcd_remap_attn(blockIdx.x, gridDim.x), hh, s, j);
-  const int q_beg = map.q_start[s], q_end = q_beg + map.q_len[s];
-  const int k0 = map.k_start[s], k_end = k0 + map.k_len[s];
-  const int nt = (map.k_len[s] + BKV - 1) / BKV;   // 1 or 2 (the launcher checks)
+  const int total = map.tile_start[map.n];   // query tiles of all sequences
+  const int L = xcd_remap_attn(blockIdx.x, gridDim.x);
+  const int hh = L % heads, t_first = (L / heads) * R;
   const int ql = lane & 31, hl = lane >> 5;
-  const int qr = q_beg + j * BQ + wave * 32 + ql;
   auto kst = [&](int t) { return smem + t * (KSTAGE + VSTAGE); };
   auto vst = [&](int t) { return smem + t * (KSTAGE + VSTAGE) + KSTAGE; };
+  auto seq_of = [&](int t) {
+    int s = 0;
+#pragma unroll 1
+    for (int i = 1; i < map.n; ++i) s += (t >= map.tile_start[i]) ? 1 : 0;
+    return s;
+  };
 
-  // tile loads (as in attn_bf16_kernel; keys past the sequence clamped to its
-  // last key, V^T chunks wholly past it read from the tile's first chunk)
+  // K / V^T tile loads of sequence s (as in attn_bf16_kernel; keys past the
+  // sequence clamped to its last key, V^T chunks wholly past it read from the
+  // tile's first chunk)
   const __amdgpu_buffer_rsrc_t rk =
       __builtin_amdgcn_make_buffer_rsrc((void*)K, 0, 0x7fffffff, kBufWord3);
   const __amdgpu_buffer_rsrc_t rv =
       __builtin_amdgcn_make_buffer_rsrc((void*)Vt, 0, 0x7fffffff, kBufWord3);
-  for (int t = 0; t < nt; ++t) {
-    const int kv0 = k0 + t * BKV;
+  auto load_kv = [&](int s) {
+    const int k0 = map.k_start[s], k_end = k0 + map.k_len[s];
+    const int nt = (map.k_len[s] + BKV - 1) / BKV;   // 1 or 2 (the launcher checks)
+    for (int t = 0; t < nt; ++t) {
+      const int kv0 = k0 + t * BKV;
 #pragma unroll
-    for (int ii = 0; ii < (NI + NW - 1) / NW; ++ii) {
-      const int i = wave + NW * ii;
-      if (i >= NI) break;
-      if (i < CPR) {
-        const int o = i * 1024 + lane * 16, r = o / PK, slot = (o - r * PK) / 16;
-        const int c = KRS ? slot ^ ((r / KRS) & (CPR - 1)) : slot;
-        const int key = min(kv0 + swap23(r), k_end - 1);
-        __builtin_amdgcn_raw_ptr_buffer_load_lds(
-            rk, (__attribute__((address_space(3))) void*)(kst(t) + i * 1024), 16,
-            2u * (uint32_t)(key * ldk + hh * HD + c * 8), 0, 0, 0);
-      } else {
-        const int o = (i - CPR) * 1024 + lane * 16, d = o / 128;
-        const int gk = kv0 + 8 * ((lane & 7) ^ ((d >> 1) & 7));
-        __builtin_amdgcn_raw_ptr_buffer_load_lds(
-            rv, (__attribute__((address_space(3))) void*)(vst(t) + (i - CPR) * 1024), 16,
-            2u * (uint32_t)((hh * HD + d) * ldvt + (gk < k_end ? gk : kv0)), 0, 0, 0);
+      for (int ii = 0; ii < (NI + NW - 1) / NW; ++ii) {
+        const int i = wave + NW * ii;
+        if (i >= NI) break;
+        if (i < CPR) {
+          const int o = i * 1024 + lane * 16, r = o / PK, slot = (o - r * PK) / 16;
+          const int c = KRS ? slot ^ ((r / KRS) & (CPR - 1)) : slot;
+          const int key = min(kv0 + swap23(r), k_end - 1);
+          __builtin_amdgcn_raw_ptr_buffer_load_lds(
+              rk, (__attribute__((address_space(3))) void*)(kst(t) + i * 1024), 16,
+              2u * (uint32_t)(key * ldk + hh * HD + c * 8), 0, 0, 0);
+        } else {
+          const int o = (i - CPR) * 1024 + lane * 16, d = o / 128;
+          const int gk = kv0 + 8 * ((lane & 7) ^ ((d >> 1) & 7));
+          __builtin_amdgcn_raw_ptr_buffer_load_lds(
+              rv, (__attribute__((address_space(3))) void*)(vst(t) + (i - CPR) * 1024), 16,
+              2u * (uint32_t)((hh * HD + d) * ldvt + (gk < k_end ? gk : kv0)), 0, 0, 0);
+        }
       }
     }
-  }
-  // Q fragments (as stored); the ones row of both stages
-  bf16x8 qf[DC];
+  };
+  // after the loads of sequence s have landed: a chunk the sequence ends
+  // inside holds bytes from beyond it; zero the columns past the sequence
+  // (their probabilities are 0)
+  auto fix_ragged = [&](int s) {
+    const int k_end = map.k_start[s] + map.k_len[s];
+    if (k_end & 7) {
+      const int t = (map.k_len[s] + BKV - 1) / BKV - 1, c0 = k_end - (map.k_start[s] + t * BKV);
+      char* vb = vst(t);
+      for (int i = tid; i < HD * 64; i += NW * 64) {
+        const int d = i >> 6, col = i & 63;
+        if (col >= c0)
+          *(bf16*)(vb + d * 128 + (((col >> 3) ^ ((d >> 1) & 7)) << 4) + (col & 7) * 2) = (bf16)0.f;
+      }
+      attn_barrier();
+    }
+  };
+  // Q fragments of query tile t (as stored): exactly DC loads per lane, from
+  // a clamped row and column, so the vmcnt thresholds below can count them;
+  // mask_q then zeroes the ones outside the tile, once the data are needed
+  auto q_row = [&](int t, int& q_end) {
+    const int s = seq_of(t);
+    q_end = map.q_start[s] + map.q_len[s];
+    return map.q_start[s] + (t - map.tile_start[s]) * BQ + wave * 32 + ql;
+  };
+  auto load_q = [&](int t, bf16x8 (&f)[DC]) {
+    int q_end;
+    const int qc = min(q_row(t, q_end), q_end - 1);
 #pragma unroll
-  for (int c = 0; c < DC; ++c) {
-    const int d = c * 16 + hl * 8;
-    qf[c] = bf16x8{};
-    if (qr < q_end && d < HD) qf[c] = *(const bf16x8*)(Q + (size_t)qr * ldq + hh * HD + d);
-  }
+    for (int c = 0; c < DC; ++c)
+      f[c] = *(const bf16x8*)(Q + (size_t)qc * ldq + hh * HD + min(c * 16 + hl * 8, HD - 8));
+  };
+  auto mask_q = [&](int t, const bf16x8 (&src)[DC], bf16x8 (&f)[DC]) {
+    int q_end;
+    const int qr = q_row(t, q_end);
+#pragma unroll
+    for (int c = 0; c < DC; ++c)
+      f[c] = (qr < q_end && c * 16 + hl * 8 < HD) ? src[c] : bf16x8{};
+  };
+
+  int s_cur = seq_of(t_first);
+  bf16x8 qf[DC], qn[DC];
+  load_q(t_first, qn);
+  load_kv(s_cur);
+  const bool pre = R > 1 && t_first + 1 < total;
+  bf16x8 qa[DC];
+  if (pre) load_q(t_first + 1, qa);
+  // the ones rows of both stages (the tile loads never write them)
   if constexpr (ONES)
     for (int i = tid; i < 2 * 64; i += NW * 64) ((bf16*)(vst(i >> 6) + HD * 128))[i & 63] = (bf16)1.f;
-  wait_vmcnt<0>();
+  if (pre) wait_vmcnt<DC>();   // all but the next tile's Q
+  else wait_vmcnt<0>();
   attn_barrier();
-  // a chunk the sequence ends inside holds bytes from beyond it: zero the
-  // columns past the sequence (their probabilities are 0)
-  if (k_end & 7) {
-    const int t = nt - 1, c0 = k_end - (k0 + t * BKV);
-    char* vb = vst(t);
-    for (int i = tid; i < HD * 64; i += NW * 64) {
-      const int d = i >> 6, col = i & 63;
-      if (col >= c0)
-        *(bf16*)(vb + d * 128 + (((col >> 3) ^ ((d >> 1) & 7)) << 4) + (col & 7) * 2) = (bf16)0.f;
-    }
-    attn_barrier();
-  }
+  fix_ragged(s_cur);
+  mask_q(t_first, qn, qf);
+#pragma unroll
+  for (int c = 0; c < DC; ++c) qn[c] = qa[c];
 
-  // S^T of both tiles (the first MFMA of each sum takes a zero accumulator)
-  f32x16 sc_[2][2];
+  for (int r = 0; r < R; ++r) {
+    const int tq = t_first + r;
+    if (tq >= total) break;
+    if (r > 0) {
+      mask_q(tq, qn, qf);
+      const int s_new = seq_of(tq);
+      if (s_new != s_cur) {
+        attn_barrier();   // every wave is done with the old K / V^T
+        load_kv(s_new);
+        wait_vmcnt<0>();
+        attn_barrier();
+        fix_ragged(s_new);
+        s_cur = s_new;
+      }
+      if (r + 1 < R && tq + 1 < total) load_q(tq + 1, qn);
+    }
+    const int s = s_cur;
+    const int q_end = map.q_start[s] + map.q_len[s];
+    const int qr = map.q_start[s] + (tq - map.tile_start[s]) * BQ + wave * 32 + ql;
+    const int k0 = map.k_start[s], k_end = k0 + map.k_len[s];
+    const int nt = (map.k_len[s] + BKV - 1) / BKV;
+
+    // S^T of both tiles (the first MFMA of each sum takes a zero accumulator)
+    f32x16 sc_[2][2];
 #pragma unroll
-  for (int t = 0; t < 2; ++t) {
-    if (t >= nt) break;
+    for (int t = 0; t < 2; ++t) {
+      if (t >= nt) break;
 #pragma unroll
-    for (int c = 0; c < DC; ++c) {
+      for (int c = 0; c < DC; ++c) {
 #pragma unroll
-      for (int kb = 0; kb < 2; ++kb) {
-        const int r = 32 * kb + ql, cc = 2 * c + hl;
-        bf16x8 kf = bf16x8{};
-        if (cc < CPR) {
-          const int slot = KRS ? cc ^ ((r / KRS) & (CPR - 1)) : cc;
-          kf = *(const bf16x8*)(kst(t) + r * PK + slot * 16);
+        for (int kb = 0; kb < 2; ++kb) {
+          const int rr = 32 * kb + ql, cc = 2 * c + hl;
+          bf16x8 kf = bf16x8{};
+          if (cc < CPR) {
+            const int slot = KRS ? cc ^ ((rr / KRS) & (CPR - 1)) : cc;
+            kf = *(const bf16x8*)(kst(t) + rr * PK + slot * 16);
+          }
+          sc_[t][kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[c],
+                                                               c == 0 ? f32x16{} : sc_[t][kb], 0, 0, 0);
         }
-        sc_[t][kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[c],
-                                                             c == 0 ? f32x16{} : sc_[t][kb], 0, 0, 0);
       }
     }
-  }
-  // Element e of key block kb is key swap23(32 kb + 8 (e >> 2) + (e & 3)) + 8 hl
-  // of its tile (swap23 moves the lane-half bit 2 to bit 3): only the ragged
-  // last tile is masked, against a per-lane threshold and compile-time offsets
-  float mx = -INFINITY;
+    // Element e of key block kb is key swap23(32 kb + 8 (e >> 2) + (e & 3)) + 8 hl
+    // of its tile (swap23 moves the lane-half bit 2 to bit 3): only the ragged
+    // last tile is masked, against a per-lane threshold and compile-time offsets
+    float mx = -INFINITY;
 #pragma unroll
-  for (int t = 0; t < 2; ++t) {
-    if (t >= nt) break;
-    const int valid = k_end - (k0 + t * BKV);
-    if (valid < BKV) {
-      const int thr = valid - 8 * hl;
+    for (int t = 0; t < 2; ++t) {
+      if (t >= nt) break;
+      const int valid = k_end - (k0 + t * BKV);
+      if (valid < BKV) {
+        const int thr = valid - 8 * hl;
+#pragma unroll
+        for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+          for (int e = 0; e < 16; ++e)
+            if (swap23(32 * kb + 8 * (e >> 2) + (e & 3)) >= thr) sc_[t][kb][e] = -INFINITY;
+      }
 #pragma unroll
       for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
-        for (int e = 0; e < 16; ++e)
-          if (swap23(32 * kb + 8 * (e >> 2) + (e & 3)) >= thr) sc_[t][kb][e] = -INFINITY;
+        for (int e = 0; e < 16; ++e) mx = fmaxf(mx, sc_[t][kb][e]);
     }
-#pragma unroll
-    for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-      for (int e = 0; e < 16; ++e) mx = fmaxf(mx, sc_[t][kb][e]);
-  }
-  mx = fmaxf(mx, __shfl_xor(mx, 32, 64));   // the query's keys sit in lanes ql and ql + 32
-  // probabilities exp2(sc * (s - mx)): a subtraction, or one fma per score
-  const float sc = QS ? 1.0f : scale_log2;
-  const float mxs = mx * sc;
+    mx = fmaxf(mx, __shfl_xor(mx, 32, 64));   // the query's keys sit in lanes ql and ql + 32
+    // probabilities exp2(sc * (s - mx)): a subtraction, or one fma per score
+    const float sc = QS ? 1.0f : scale_log2;
+    const float mxs = mx * sc;
 
-  // P V over both tiles; row sums from the ones row or per lane
-  f32x16 o[DT];
-  float psum = 0.f;
+    // P V over both tiles; row sums from the ones row or per lane
+    f32x16 o[DT];
+    float psum = 0.f;
 #pragma unroll
-  for (int t = 0; t < 2; ++t) {
-    if (t >= nt) break;
-    const char* vb = vst(t);
+    for (int t = 0; t < 2; ++t) {
+      if (t >= nt) break;
+      const char* vb = vst(t);
 #pragma unroll
-    for (int q = 0; q < 4; ++q) {
-      bf16x8 pf;
+      for (int q = 0; q < 4; ++q) {
+        bf16x8 pf;
 #pragma unroll
-      for (int e = 0; e < 8; ++e) {
-        const float x = sc_[t][q >> 1][8 * (q & 1) + e];
-        const float p = __builtin_amdgcn_exp2f(QS ? x - mx : fmaf(x, sc, -mxs));
-        if (!ONES) psum += p;
-        pf[e] = (bf16)p;
-      }
+        for (int e = 0; e < 8; ++e) {
+          const float x = sc_[t][q >> 1][8 * (q & 1) + e];
+          const float p = __builtin_amdgcn_exp2f(QS ? x - mx : fmaf(x, sc, -mxs));
+          if (!ONES) psum += p;
+          pf[e] = (bf16)p;
+        }
 #pragma unroll
-      for (int dt = 0; dt < DT; ++dt) {
-        const int row = dt * 32 + ql;
-        const bf16x8 vf =
-            *(const bf16x8*)(vb + row * 128 + (((2 * q + hl) ^ ((row >> 1) & 7)) << 4));
-        o[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf, pf, t == 0 && q == 0 ? f32x16{} : o[dt],
-                                                        0, 0, 0);
-      }
-    }
-  }
-  float l;
-  if (ONES) {
-    constexpr int R = HD % 32;
-    l = __shfl(o[HD / 32][4 * (R / 8) + (R % 4)], ((R % 8) / 4) * 32 + ql, 64);
-  } else {
-    l = psum + __shfl_xor(psum, 32, 64);
-  }
-  if (qr >= q_end) return;
-  const float inv = 1.0f / l;
-#pragma unroll
-  for (int dt = 0; dt < DT; ++dt)
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const int d = dt * 32 + i * 8 + hl * 4;
-      if (d < HD) {
-        bf16x4 w;
-#pragma unroll
-        for (int jj = 0; jj < 4; ++jj) w[jj] = (bf16)(o[dt][4 * i + jj] * inv);
-        *(bf16x4*)(O + (size_t)qr * ldo + hh * HD + d) = w;
+        for (int dt = 0; dt < DT; ++dt) {
+          const int row = dt * 32 + ql;
+          const bf16x8 vf =
+              *(const bf16x8*)(vb + row * 128 + (((2 * q + hl) ^ ((row >> 1) & 7)) << 4));
+          o[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf, pf, t == 0 && q == 0 ? f32x16{} : o[dt],
+                                                          0, 0, 0);
+        }
       }
     }
+    float l;
+    if (ONES) {
+      constexpr int RR = HD % 32;
+      l = __shfl(o[HD / 32][4 * (RR / 8) + (RR % 4)], ((RR % 8) / 4) * 32 + ql, 64);
+    } else {
+      l = psum + __shfl_xor(psum, 32, 64);
+    }
+    if (qr < q_end) {
+      const float inv = 1.0f / l;
+#pragma unroll
+      for (int dt = 0; dt < DT; ++dt)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const int d = dt * 32 + i * 8 + hl * 4;
+          if (d < HD) {
+            bf16x4 w;
+#pragma unroll
+            for (int jj = 0; jj < 4; ++jj) w[jj] = (bf16)(o[dt][4 * i + jj] * inv);
+            *(bf16x4*)(O + (size_t)qr * ldo + hh * HD + d) = w;
+          }
+        }
+    }
+  }
 }
 
 // ---------------------------------------------------------------------------
@@ -868,11 +937,23 @@ static hipError_t launch_hd(bool bf16_io, int role, int heads, const AttnMap& ma
       bool short_text = map.waves == kCrossWaves;
       for (int s = 0; s < map.n && short_text; ++s)
         short_text = map.k_len[s] >= 1 && map.k_len[s] <= 128 && map.k2_len[s] == 0;
-      if (short_text)
-        hipLaunchKernelGGL((attn_cross_kernel<HD, kCrossWaves, QS>), dim3(tiles), dim3(kCrossWaves * 64),
-                           0, st, map, heads, (const bf16*)q, ldq, (const bf16*)k, ldk,
-                           (const bf16*)v, ldv, (bf16*)o, ldo, scale_log2);
-      else if (map.waves == kCrossWaves) T2I_ATT(kCrossWaves, kCrossStages, 1);
+      // two query tiles per workgroup where the launch then still fills the
+      // chip in one round at two workgroups per CU (1024 px with guidance:
+      // 64 tiles x 16 heads -> 512 workgroups; measured 21.5 -> 20.2 us); a
+      // second round of them (packed batches of ~1500 tile-head pairs)
+      // measured slower than one tile per workgroup
+      const int qt = map.tile_start[map.n];
+      const long pairs = (long)((qt + 1) / 2) * heads;
+      if (short_text && tiles >= 1024 && pairs <= 512) {
+        hipLaunchKernelGGL((attn_cross_kernel<HD, kCrossWaves, QS, 2>),
+                           dim3(((qt + 1) / 2) * heads), dim3(kCrossWaves * 64), 0, st, map, heads,
+                           (const bf16*)q, ldq, (const bf16*)k, ldk, (const bf16*)v, ldv, (bf16*)o,
+                           ldo, scale_log2);
+      } else if (short_text) {
+        hipLaunchKernelGGL((attn_cross_kernel<HD, kCrossWaves, QS, 1>), dim3(tiles),
+                           dim3(kCrossWaves * 64), 0, st, map, heads, (const bf16*)q, ldq,
+                           (const bf16*)k, ldk, (const bf16*)v, ldv, (bf16*)o, ldo, scale_log2);
+      } else if (map.waves == kCrossWaves) T2I_ATT(kCrossWaves, kCrossStages, 1);
       else return hipErrorInvalidValue;
     } else {
       if (map.waves == kAttnWaves) T2I_ATT(kAttnWaves, attn_stages<HD>(), 0);

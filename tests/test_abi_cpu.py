@@ -224,6 +224,21 @@ def test_op_argument_errors():
     assert lib.t2i_op_attention(1, 2, 72, 1, qs, ql, qs, ql, None, None, 0x1000, 144, 0x2000,
                                 144, 0x3000, big, 0x4000, 144, None) == 2
     assert b"2 GiB" in lib.t2i_ops_last_error()
+    # cross-attention: bf16 only, at least one key, aligned key start, key range within ldv
+    ks8 = (C.c_int32 * 1)(8)
+    ks4 = (C.c_int32 * 1)(4)
+    assert lib.t2i_op_cross_attention(0, 2, 72, 1, qs, ql, qs, ql, 0x1000, 144, 0x2000, 144,
+                                      0x3000, 64, 0x4000, 144, None) == 1
+    assert lib.t2i_op_cross_attention(1, 2, 72, 1, qs, ql, qs, kl, 0x1000, 144, 0x2000, 144,
+                                      0x3000, 64, 0x4000, 144, None) == 2
+    assert lib.t2i_op_cross_attention(1, 2, 72, 1, qs, ql, ks4, ql, 0x1000, 144, 0x2000, 144,
+                                      0x3000, 64, 0x4000, 144, None) == 2
+    assert lib.t2i_op_cross_attention(1, 2, 72, 1, qs, ql, ks8, ql, 0x1000, 144, 0x2000, 144,
+                                      0x3000, 8, 0x4000, 144, None) == 2
+    assert lib.t2i_op_cross_attention(1, 2, 48, 1, qs, ql, qs, ql, 0x1000, 96, 0x2000, 96,
+                                      0x3000, 64, 0x4000, 96, None) == 2
+    assert lib.t2i_op_cross_attention(1, 2, 72, 1, qs, ql, qs, ql, None, 144, 0x2000, 144,
+                                      0x3000, 64, 0x4000, 144, None) == 1
 
 
 @pytest.mark.parametrize("name", ["dit1024_cfg", "mmdit1024", "tiny_f32"])

@@ -194,6 +194,66 @@ def run_attention(dtype, heads, d, seqs, q, k, v, seg2=None):
     return to_host(o)
 
 
+def run_cross_attention(heads, d, seqs, q, k, v):
+    """seqs: (q_start, q_len, k_start, k_len); bf16, V passed transposed."""
+    lib = t2i.load()
+    n = len(seqs)
+    qs, ql, ks, kl = ((C.c_int32 * n)(*[s[i] for s in seqs]) for i in range(4))
+    w = heads * d
+    ldv = (v.shape[0] + 63) // 64 * 64
+    vt = np.zeros((w, ldv), dtype=np.float32)
+    vt[:, :v.shape[0]] = v.T
+    vt[:, v.shape[0]:] = np.nan              # padding must never be read into results
+    dq, dk, dv = to_dev(q, "bf16"), to_dev(k, "bf16"), to_dev(vt, "bf16")
+    o = torch.zeros(dq.shape, dtype=dq.dtype, device=DEV)
+    st = lib.t2i_op_cross_attention(_lib.T2I_BF16, heads, d, n, qs, ql, ks, kl, dq.data_ptr(), w,
+                                    dk.data_ptr(), w, dv.data_ptr(), ldv, o.data_ptr(), w,
+                                    _stream())
+    _lib.check(st)
+    torch.cuda.synchronize()
+    return to_host(o)
+
+
+def _text_seqs(q_lens, k_lens):
+    """Packed query sequences, each with its own text block starting at a multiple of 8."""
+    seqs, q0, k0 = [], 0, 0
+    for nq, nk in zip(q_lens, k_lens):
+        seqs.append((q0, nq, k0, nk))
+        q0 += nq
+        k0 += (nk + 7) // 8 * 8
+    return seqs, q0, k0
+
+
+# (name, heads, query lengths, text lengths).  The two-tile kernel takes two
+# 128-query tiles per workgroup from 1024 (tile, head) pairs on: the 1024-px
+# guided shape (2 x 4096 queries, 16 heads, 120 keys); 21 sequences of three
+# tiles each plus one of one tile (64 tiles), so that many workgroups take
+# their two tiles from two sequences with different texts (ragged, 1 key, a
+# full 128); a small launch of one tile per workgroup; a text longer than 128
+# keys (the pipelined kernel).
+CROSS_CASES = [
+    ("guided-1024px", 16, [4096, 4096], [120, 120]),
+    ("straddling-pairs", 16, [384] * 21 + [100], [120, 77, 1, 128, 64, 13, 8] * 3 + [50]),
+    ("one-tile-per-group", 4, [500, 300], [120, 77]),
+    ("long-text", 4, [300, 200], [200, 130]),
+]
+
+
+@pytest.mark.parametrize("name,H,q_lens,k_lens", CROSS_CASES, ids=[c[0] for c in CROSS_CASES])
+def test_cross_attention_bf16(name, H, q_lens, k_lens):
+    say(f"cross-attention bf16 {name}")
+    d = 72
+    seqs, nq, nk = _text_seqs(q_lens, k_lens)
+    q, k, v = rnd(40, (nq, H * d)), rnd(41, (nk, H * d)), rnd(42, (nk, H * d))
+    got = run_cross_attention(H, d, seqs, q, k, v)
+    ref = attention_ref(seqs, q, k, v, H)
+    err = rel_l2(got, ref)
+    row_err = np.linalg.norm(got - ref, axis=1) / np.linalg.norm(ref, axis=1)
+    say(f"  rel_l2 {err:.2e}, worst row {row_err.max():.2e}")
+    assert err < 6e-3
+    assert row_err.max() < 3e-2
+
+
 def attention_ref(seqs, q, k, v, heads):
     out = np.zeros(q.shape)
     for (q0, nq, k0, nk) in seqs:
