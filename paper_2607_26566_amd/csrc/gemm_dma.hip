@@ -387,6 +387,213 @@ __global__ __launch_bounds__(64 * WGM * WGN, 1) void gemm_dma_kernel(
   }
 }
 
+// s_waitcnt vmcnt(n) for a wave-uniform n known only at run time; n > 15
+// waits for vmcnt(15), which is stricter
+__device__ __forceinline__ void wait_vmcnt_dyn15(int n) {
+  switch (n) {
+#define T2I_W(N_) case N_: wait_vmcnt<N_>(); break;
+    T2I_W(0) T2I_W(1) T2I_W(2) T2I_W(3) T2I_W(4) T2I_W(5) T2I_W(6) T2I_W(7)
+    T2I_W(8) T2I_W(9) T2I_W(10) T2I_W(11) T2I_W(12) T2I_W(13) T2I_W(14)
+#undef T2I_W
+    default: wait_vmcnt<15>(); break;
+  }
+}
+
+// The split q|k|v projection when it takes several rounds of 256 x 144 tiles
+// (the 1024-px guided step: 768 tiles, three per CU).  In gemm_dma_kernel
+// every workgroup of a round reaches its epilogue at the same time and the
+// MFMA pipes idle through it (~6 us per round).  Here a workgroup runs its
+// tiles b, b + G, b + 2G, ... (G workgroups, the same tile order as one
+// workgroup per tile) with two sets of accumulators: while it computes tile
+// r, each K step also stores one of the 18 fragments of tile r - 1, so the
+// stores and their arithmetic fill the gaps between MFMAs; only the last
+// tile's epilogue stands alone.  The tile loads run on across tiles (the
+// last two K steps of a tile issue the next tile's first two stages).
+// Stores and loads share vmcnt, which completes in issue order: the wait for
+// stage g counts as younger the one stage issued after it and the stores
+// of the two K steps since it was issued (4 two-byte stores per q|k
+// fragment, 1 eight-byte store per V fragment -- lower bounds on what the
+// compiler emits, so the waits are never too lax); compiler barriers keep
+// each step's stores after its loads.  Each output element is computed and
+// rounded exactly as by gemm_dma_kernel.  Requirements (launch_gemm_dma
+// checks): whole tiles (M % 256 == 0, N % 144 == 0), K = 1152 (18 K steps, one
+// fragment per step), vcol0 % 144 == 0 (every tile all q|k or all V),
+// vectorisable epilogue, at most kPipeTiles tiles per workgroup.
+constexpr int kPipeTiles = 6;
+
+__global__ __launch_bounds__(512, 1) void gemm_dma_vt_pipe_kernel(
+    const bf16* __restrict__ A, int lda, const bf16* __restrict__ W, int ldw,
+    const bf16* __restrict__ bias, int M, int N, Epi epi, int tiles_n, int group_m, int total) {
+  constexpr int BM = 256, BN = 144, NW = 8, WM = 32, TM = 2, TN = 9, ST = 3, KT = 18;
+  constexpr int ABLK = BM / 8, BBLK = BN / 8, TBLK = ABLK + BBLK, BPW = (TBLK + NW - 1) / NW;
+  constexpr int STAGE = (BM + BN) * 64;
+  static_assert(TM * TN == KT && KT % ST == 0 && BPW == 7, "one fragment per K step");
+  // the stage ring, then 1 KB per tile for its bias row (bf16; the first
+  // 288 bytes used)
+  __shared__ __attribute__((aligned(1024))) bf16 smem[ST * STAGE + kPipeTiles * 512];
+  const bf16* const ebias = smem + ST * STAGE;   // tile r's row at r * 512
+
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int fr = lane & 15, g = lane >> 4;
+  const int G = gridDim.x, b = blockIdx.x;
+  const int R = (total - b + G - 1) / G;   // this workgroup's tiles (1 .. kPipeTiles)
+  const int tiles_m = M / BM;
+  auto tile_of = [&](int r, int& m0, int& n0) {
+    const int tile = xcd_remap_dma(b + r * G, total);
+    const int per_group = group_m * tiles_n, grp = tile / per_group;
+    const int first = grp * group_m, rows_in = min(tiles_m - first, group_m);
+    const int in_grp = tile - grp * per_group;
+    m0 = (first + in_grp % rows_in) * BM;
+    n0 = (in_grp / rows_in) * BN;
+  };
+  int dst[BPW];
+  auto make_src = [&](int m0, int n0, uint32_t (&src)[BPW]) {
+#pragma unroll
+    for (int i = 0; i < BPW; ++i) {
+      int blk = wave + i * NW;
+      if (blk >= TBLK) blk -= NW;   // repeat this wave's previous block
+      const int lr = (blk < ABLK ? blk : blk - ABLK) * 8 + (lane >> 3);
+      const int c = (lane & 7) ^ ((lr >> 1) & 7);
+      src[i] = 2u * (uint32_t)(i < ABLK / NW ? (m0 + lr) * lda + c * 8 : (n0 + lr) * ldw + c * 8);
+      dst[i] = blk * 1024;
+    }
+  };
+  const __amdgpu_buffer_rsrc_t ra =
+      __builtin_amdgcn_make_buffer_rsrc((void*)A, 0, 0x7fffffff, 0x00020000);
+  const __amdgpu_buffer_rsrc_t rw =
+      __builtin_amdgcn_make_buffer_rsrc((void*)W, 0, 0x7fffffff, 0x00020000);
+  auto issue = [&](const uint32_t (&src)[BPW], int t, int slot) {
+#pragma unroll
+    for (int i = 0; i < BPW; ++i)
+      dma16<1>(i < ABLK / NW ? ra : rw, (char*)smem + slot * STAGE * 2 + dst[i], src[i], t * 128);
+  };
+
+  // every tile's bias row straight into LDS, one direct load per tile from
+  // wave 0, before any tile load (so that no wait below has to count them;
+  // lanes past the row read neighbouring columns or, past N, zeros)
+  if (wave == 0) {
+    const __amdgpu_buffer_rsrc_t rb =
+        __builtin_amdgcn_make_buffer_rsrc((void*)bias, 0, (uint32_t)N * 2u, 0x00020000);
+#pragma unroll
+    for (int r = 0; r < kPipeTiles; ++r) {
+      if (r >= R) break;
+      int m0r, n0r;
+      tile_of(r, m0r, n0r);
+      dma16<0>(rb, (char*)(ebias + r * 512), 2u * (uint32_t)(n0r + lane * 8), 0);
+    }
+  }
+
+  int m0, n0, m0n = 0, n0n = 0;
+  uint32_t src_c[BPW], src_n[BPW];
+  tile_of(0, m0, n0);
+  make_src(m0, n0, src_c);
+  if (R > 1) tile_of(1, m0n, n0n);
+#pragma unroll
+  for (int s = 0; s < ST - 1; ++s) issue(src_c, s, s);
+
+  f32x4 acc[TM][TN];
+  bf16x4 prev[TM][TN];   // the previous tile's outputs, rounded, waiting to be stored
+#pragma unroll
+  for (int i = 0; i < TM; ++i)
+#pragma unroll
+    for (int j = 0; j < TN; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+  auto frag = [&](const bf16* base, int row, int c) {
+    return *(const bf16x8*)((const char*)base + row * 128 + ((c ^ ((row >> 1) & 7)) << 4));
+  };
+  auto compute = [&](int slot) {
+    const bf16* sA = smem + slot * STAGE;
+    const bf16* sB = sA + BM * 64;
+#pragma unroll
+    for (int kk = 0; kk < 2; ++kk) {
+      bf16x8 af[TM], bfr[TN];
+#pragma unroll
+      for (int i = 0; i < TM; ++i) af[i] = frag(sA, wave * WM + i * 16 + fr, kk * 4 + g);
+#pragma unroll
+      for (int j = 0; j < TN; ++j) bfr[j] = frag(sB, j * 16 + fr, kk * 4 + g);
+#pragma unroll
+      for (int i = 0; i < TM; ++i)
+#pragma unroll
+        for (int j = 0; j < TN; ++j)
+          acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af[i], bfr[j], acc[i][j], 0, 0, 0);
+    }
+  };
+  // fragment (i, j) of a finished tile at (tm0, tn0) with bias row r, rounded
+  // exactly as the whole-tile epilogues of gemm_dma_kernel round it: V
+  // columns acc + b, q|k columns (acc + b) * qscale for the query columns
+  auto round_frag = [&](int i, int j, int tn0, bool is_v, int r) {
+    const int n = tn0 + j * 16 + fr;
+    const float bv = (float)ebias[r * 512 + j * 16 + fr];
+    const float qs = !is_v && n < epi.qcols ? epi.qscale : 1.f;
+    bf16x4 w;
+#pragma unroll
+    for (int rr = 0; rr < 4; ++rr)
+      w[rr] = is_v ? (bf16)(acc[i][j][rr] + bv) : (bf16)((acc[i][j][rr] + bv) * qs);
+    return w;
+  };
+  // its stores: V^T four tokens per store, q|k one element per store
+  auto store_frag = [&](bf16x4 w, int i, int j, int tm0, int tn0, bool is_v) {
+    const int n = tn0 + j * 16 + fr, mb = tm0 + wave * WM + i * 16 + g * 4;
+    if (is_v) {
+      *(bf16x4*)(epi.vt + (size_t)(n - epi.vcol0) * epi.ldvt + mb) = w;
+    } else {
+      bf16* o = (bf16*)epi.out + n;
+#pragma unroll
+      for (int rr = 0; rr < 4; ++rr) o[(size_t)(mb + rr) * epi.ldo] = w[rr];
+    }
+  };
+
+  bool cur_v = n0 >= epi.vcol0, prev_v = false;
+  int pm0 = 0, pn0 = 0;
+  int e_last = 0;   // stores per K step during the previous tile
+  for (int r = 0; r < R; ++r) {
+    const int e_cur = r > 0 ? (prev_v ? 1 : 4) : 0;   // stores per K step during this tile
+    const bool next = r + 1 < R;
+#pragma unroll
+    for (int t = 0; t < KT; ++t) {
+      // younger than stage (r, t): the stores of the two steps since it was
+      // issued and the stage issued one step after it (if any)
+      const int e2 = t >= 2 ? e_cur : e_last, e1 = t >= 1 ? e_cur : e_last;
+      const bool younger_stage = t + 1 < KT || next;
+      wait_vmcnt_dyn15(e2 + e1 + (younger_stage ? BPW : 0));
+      block_barrier();
+      if (t + ST - 1 < KT) {
+        issue(src_c, t + ST - 1, (t + ST - 1) % ST);
+      } else if (next) {
+        make_src(m0n, n0n, src_n);
+        issue(src_n, t + ST - 1 - KT, (t + ST - 1) % ST);
+      }
+      asm volatile("" ::: "memory");   // this step's stores stay after its loads
+      compute(t % ST);
+      if (r > 0) store_frag(prev[t / TN][t % TN], t / TN, t % TN, pm0, pn0, prev_v);
+      asm volatile("" ::: "memory");   // ... and before the next step's wait
+    }
+    if (next) {
+#pragma unroll
+      for (int i = 0; i < TM; ++i)
+#pragma unroll
+        for (int j = 0; j < TN; ++j) {
+          prev[i][j] = round_frag(i, j, n0, cur_v, r);
+          acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+        }
+      prev_v = cur_v;
+      pm0 = m0;
+      pn0 = n0;
+      m0 = m0n;
+      n0 = n0n;
+      cur_v = n0 >= epi.vcol0;
+      make_src(m0, n0, src_c);
+      if (r + 2 < R) tile_of(r + 2, m0n, n0n);
+      e_last = e_cur;
+    } else {
+      // the last tile's epilogue
+#pragma unroll
+      for (int f = 0; f < TM * TN; ++f)
+        store_frag(round_frag(f / TN, f % TN, n0, cur_v, r), f / TN, f % TN, m0, n0, cur_v);
+    }
+  }
+}
+
 template <int BM, int BN, int WGM, int WGN, int ST, int AUX>
 hipError_t gemm_dma_dispatch(const bf16* A, int lda, const bf16* W, int ldw, const bf16* bias,
                              int M, int N, int K, int kind, const Epi& epi, int vec_ok,
@@ -474,6 +681,13 @@ hipError_t launch_gemm_dma(const bf16* A, int lda, const bf16* W, int ldw, const
                                                    8, st);
   if (N % 144 == 0) {
     const int gm = longk ? 8 : (kind == EPI_RESID || kind == EPI_RESID_GATED) ? 1 : 8;
+    const long tiles = mt * (N / 144);
+    if (kind == EPI_SPLIT_VT && vec_ok && M % 256 == 0 && K == 18 * 64 && epi.vcol0 % 144 == 0 &&
+        tiles > 256 && tiles <= (long)kPipeTiles * 256) {
+      hipLaunchKernelGGL(gemm_dma_vt_pipe_kernel, dim3(256), dim3(512), 0, st, A, lda, W, ldw, bias,
+                         M, N, epi, N / 144, gm, (int)tiles);
+      return hipGetLastError();
+    }
     return gemm_dma_dispatch<256, 144, 8, 1, 3, 1>(A, lda, W, ldw, bias, M, N, K, kind, epi, vec_ok,
                                                    gm, st);
   }
