@@ -346,7 +346,13 @@ __global__ __launch_bounds__(64 * WGM * WGN, 1) void gemm_dma_kernel(
     // except 256 x 256 (the joint-attention model's fc1 measured 2.8 %
     // slower), not for the small-M tiles (no gain at 1024 rows).
     constexpr bool STAGED = BM == 256 && BN != 256 && KIND != EPI_STORE_F32 && KIND != EPI_SILU;
-    if (STAGED && whole_n) {
+    // (16-byte row chunks: row strides and bases must keep them aligned)
+    constexpr bool F32O = KIND == EPI_RESID || KIND == EPI_RESID_GATED;
+    const bool aligned16 =
+        F32O ? ((uintptr_t)epi.x % 16 == 0 && epi.ldx % 4 == 0 &&
+                (!epi.xb || ((uintptr_t)epi.xb % 16 == 0 && epi.ldx % 8 == 0)))
+             : ((uintptr_t)epi.out % 16 == 0 && epi.ldo % 8 == 0);
+    if (STAGED && whole_n && aligned16) {
       constexpr bool F32OUT = KIND == EPI_RESID || KIND == EPI_RESID_GATED;
       constexpr int SROW = WN * (F32OUT ? 4 : 2);   // bytes per staged row
       static_assert(NW * 16 * WN * 4 <= ST * STAGE * 2, "staging fits the ring");
