@@ -558,6 +558,12 @@ def main():
     sps = args.steps / elapsed
     flops = step_flops(w)
     cw = class_work(w)
+    # where the cross-attention runs inside its query projection (one kernel,
+    # timed as gemm_xq), that kernel's work is both classes'
+    xq_fused = ("attn_cross" in cw and per_class.get("attn_cross", (0, 0))[1] == 0
+                and per_class.get("gemm_xq", (0, 0))[1] > 0)
+    if xq_fused:
+        cw["gemm_xq"] = ("flop", cw["gemm_xq"][1] + cw["attn_cross"][1], cw["gemm_xq"][2])
     kind, work_block, per_blk = cw[dominant]
     blocks = w.depth * args.steps                      # blocks executed in the timed region
     dom_s = tot.value / 1e3
@@ -634,6 +640,7 @@ def main():
         "images_per_s": round(w.n_req / sample_s, 3),
         "sample_steps_per_s": round(n / sample_s, 3),
         "kernel_avg_ms": kernel_ms,
+        "gemm_xq_includes_cross_attention": xq_fused,
         "kernel_class_rate": class_rate,
         "flops_per_step": flops,
     }

@@ -87,6 +87,36 @@ t2i_status t2i_op_cross_attention(int32_t dtype, int32_t heads, int32_t head_dim
                                   int32_t ldv, void* o, int32_t ldo, void* stream);
 
 /*
+ * The DiT block's cross-attention together with its query projection (Sec. 4's
+ * model `forward`): q = A W^T + b for the query rows, then the operation of
+ * t2i_op_cross_attention with those queries, bf16 only.  The queries are
+ * kept multiplied by log2(e)/sqrt(head_dim) (rounded once to bf16, as the
+ * model's projection writes them), so the softmax takes base-2 exponentials
+ * of the scores directly.
+ *   A [M, K] (row stride lda) with M = the largest q_start[s] + q_len[s];
+ *   W [heads*head_dim, K] (row stride ldw), bias [heads*head_dim];
+ *   K % 64 == 0, lda, ldw >= K and multiples of 8; text of 1 .. 128 keys per
+ *   sequence (k_len), key starts % 8 == 0; K/V layouts (V given transposed),
+ *   ldk, ldv, ldo and the 2^31-byte limits as for t2i_op_attention.
+ * fused = 0: the projection writes the queries to q_buf [M, ldq] (caller-
+ *   owned, ldq >= heads*head_dim, % 8 == 0), then the cross-attention kernel
+ *   reads them: two launches.
+ * fused = 1: one kernel; the queries never leave the chip (q_buf unused, may
+ *   be NULL).  Needs head_dim 72, K % 192 == 0, sequences contiguous from
+ *   row 0 whose lengths are multiples of 256, 16-byte aligned A and W and
+ *   8-byte aligned bias and o, else T2I_ERR_SHAPE.  Both settings give the
+ *   same bits; the model takes the fused one wherever it applies.
+ */
+t2i_status t2i_op_linear_cross_attention(int32_t fused, int32_t heads, int32_t head_dim,
+                                         int32_t n_seq, const int32_t* q_start,
+                                         const int32_t* q_len, const int32_t* k_start,
+                                         const int32_t* k_len, int32_t K, const void* A,
+                                         int32_t lda, const void* W, int32_t ldw,
+                                         const void* bias, const void* k, int32_t ldk,
+                                         const void* v, int32_t ldv, void* q_buf,
+                                         int32_t ldq, void* o, int32_t ldo, void* stream);
+
+/*
  * LayerNorm (no affine, biased variance) fused with adaLN modulation:
  * out = (x - mean) / sqrt(var + eps) * (1 + scale) + shift per row of
  * x [rows, D] fp32; shift, scale fp32 [D]; out dtype (bf16 or fp32) [rows, D].

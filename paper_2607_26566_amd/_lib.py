@@ -101,6 +101,9 @@ SIGNATURES = {
     "t2i_op_cross_attention": (i32, [i32, i32, i32, i32, C.POINTER(i32), C.POINTER(i32),
                                      C.POINTER(i32), C.POINTER(i32), vp, i32, vp, i32, vp, i32,
                                      vp, i32, vp]),
+    "t2i_op_linear_cross_attention": (i32, [i32, i32, i32, i32, C.POINTER(i32), C.POINTER(i32),
+                                            C.POINTER(i32), C.POINTER(i32), i32, vp, i32, vp,
+                                            i32, vp, vp, i32, vp, i32, vp, i32, vp, i32, vp]),
     "t2i_op_ln_modulate": (i32, [i32, i32, i32, vp, vp, vp, f32, vp, vp]),
     "t2i_op_dma_read": (i32, [vp, sz, vp, vp]),
     "t2i_op_lora_merge_batch": (i32, [i32, i32, i32, i32, i32, f32, C.POINTER(vp), i32,

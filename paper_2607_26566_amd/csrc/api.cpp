@@ -416,6 +416,30 @@ Epi make_epi() {
   return e;
 }
 
+// The fused query projection + cross-attention's view of a cross-attention
+// map (text K row-major with stride ldk, V^T with stride ldvt, output o);
+// a map with second key segments gets n = 0, which the launcher rejects.
+XAttnArgs make_xattn(const AttnMap& m, const void* k, int ldk, const void* vt, int ldvt, void* o,
+                     int ldo) {
+  XAttnArgs a;
+  std::memset(&a, 0, sizeof(a));
+  a.K = (const bf16*)k;
+  a.ldk = ldk;
+  a.Vt = (const bf16*)vt;
+  a.ldvt = ldvt;
+  a.O = (bf16*)o;
+  a.ldo = ldo;
+  a.n = m.n;
+  for (int s = 0; s < m.n; ++s) {
+    a.q_start[s] = m.q_start[s];
+    a.q_len[s] = m.q_len[s];
+    a.k_start[s] = m.k_start[s];
+    a.k_len[s] = m.k_len[s];
+    if (m.k2_len[s]) a.n = 0;
+  }
+  return a;
+}
+
 // y = A W^T + b with the config's operand type.  allow_split lets a
 // short-M, long-K layer split K (MMDiT text stream).
 hipError_t linear(t2i_dit* h, const void* A, int lda, int wi, int M, int N, int K, int kind,
@@ -687,18 +711,30 @@ t2i_status run_blocks_cross(t2i_dit* h, const Plan& P, int nb, hipStream_t st) {
       e.qscale = attn_q_scale(c.head_dim);
       e.qcols = D;
     }
-    TIMED(h, T2I_K_GEMM_XQ, st,
-          linear(h, bf ? (const void*)xb : (const void*)x, D, wb + X_XQ, R, D, D, EPI_STORE, e, st));
     const char* kv = h->at<char>(h->L.kv) + (size_t)b * txt_rows_max * 2 * D * A;
-    if (bf)
-      TIMED(h, T2I_K_ATTN_CROSS, st,
-            launch_attention(bf, 1, c.heads, c.head_dim, P.cross, qkv, D, kv, D,
-                             h->at<bf16>(h->L.vtt) + (size_t)b * D * h->L.ldvt_txt,
-                             h->L.ldvt_txt, o, D, st, true));
-    else
+    if (bf) {
+      // one kernel for the query projection and the cross-attention where
+      // the shapes fit it (same bits as the two launches below)
+      const bf16* vtt = h->at<bf16>(h->L.vtt) + (size_t)b * D * h->L.ldvt_txt;
+      const XAttnArgs xa = make_xattn(P.cross, kv, D, vtt, h->L.ldvt_txt, o, D);
+      const bf16* wq = (const bf16*)h->w[wb + X_XQ];
+      const bf16* bq = (const bf16*)h->w[wb + X_XQ + 1];
+      if (launch_gemm_xattn(xb, D, wq, D, bq, R, D, D, e, c.heads, c.head_dim, xa, st, true) ==
+          hipSuccess) {
+        TIMED(h, T2I_K_GEMM_XQ, st,
+              launch_gemm_xattn(xb, D, wq, D, bq, R, D, D, e, c.heads, c.head_dim, xa, st));
+      } else {
+        TIMED(h, T2I_K_GEMM_XQ, st, linear(h, xb, D, wb + X_XQ, R, D, D, EPI_STORE, e, st));
+        TIMED(h, T2I_K_ATTN_CROSS, st,
+              launch_attention(bf, 1, c.heads, c.head_dim, P.cross, qkv, D, kv, D, vtt,
+                               h->L.ldvt_txt, o, D, st, true));
+      }
+    } else {
+      TIMED(h, T2I_K_GEMM_XQ, st, linear(h, x, D, wb + X_XQ, R, D, D, EPI_STORE, e, st));
       TIMED(h, T2I_K_ATTN_CROSS, st,
             launch_attention(bf, 1, c.heads, c.head_dim, P.cross, qkv, D, kv, 2 * D, kv + D * A,
                              2 * D, o, D, st, false));
+    }
     e = make_epi();
     e.x = x;
     e.ldx = D;
@@ -1497,6 +1533,79 @@ t2i_status t2i_op_cross_attention(int32_t dtype, int32_t heads, int32_t head_dim
   attention_tiles(m, true, heads, 1);
   hipError_t err = launch_attention(true, 1, heads, head_dim, m, q, ldq, k, ldk, v, ldv, o, ldo,
                                     (hipStream_t)stream, false);
+  if (err != hipSuccess) return ops_fail(T2I_ERR_DEVICE, hipGetErrorString(err));
+  return T2I_OK;
+}
+
+t2i_status t2i_op_linear_cross_attention(int32_t fused, int32_t heads, int32_t head_dim,
+                                         int32_t n_seq, const int32_t* q_start,
+                                         const int32_t* q_len, const int32_t* k_start,
+                                         const int32_t* k_len, int32_t K, const void* A,
+                                         int32_t lda, const void* W, int32_t ldw, const void* bias,
+                                         const void* k, int32_t ldk, const void* v, int32_t ldv,
+                                         void* q_buf, int32_t ldq, void* o, int32_t ldo,
+                                         void* stream) {
+  if (fused != 0 && fused != 1) return ops_fail(T2I_ERR_INVALID_ARG, "fused must be 0 or 1");
+  if (heads < 1 || (head_dim != 8 && head_dim != 32 && head_dim != 64 && head_dim != 72 &&
+                    head_dim != 128))
+    return ops_fail(T2I_ERR_SHAPE, "unsupported head_dim");
+  if (n_seq < 1 || n_seq > kMaxSeq) return ops_fail(T2I_ERR_SHAPE, "bad n_seq");
+  if (!q_start || !q_len || !k_start || !k_len || !A || !W || !bias || !k || !v || !o)
+    return ops_fail(T2I_ERR_INVALID_ARG, "NULL pointer");
+  if (!fused && !q_buf) return ops_fail(T2I_ERR_INVALID_ARG, "NULL q_buf (needed when fused == 0)");
+  const int w = heads * head_dim;
+  if (K < 64 || K % 64 || lda < K || ldw < K || lda % 8 || ldw % 8)
+    return ops_fail(T2I_ERR_SHAPE, "bf16 GEMM needs K % 64 == 0 and lda, ldw >= K, % 8 == 0");
+  if (ldk < w || ldo < w || ldk % 8 || ldv % 8 || ldo % 8 || (!fused && (ldq < w || ldq % 8)))
+    return ops_fail(T2I_ERR_SHAPE, "bad leading dimension");
+  AttnMap m;
+  std::memset(&m, 0, sizeof(m));
+  m.n = n_seq;
+  long k_rows = 0;
+  int M = 0;
+  for (int s = 0; s < n_seq; ++s) {
+    if (q_start[s] < 0 || q_len[s] < 0 || k_start[s] < 0 || k_len[s] < 1 || k_len[s] > 128)
+      return ops_fail(T2I_ERR_SHAPE, "bad sequence bounds (text of 1 .. 128 keys)");
+    if (k_start[s] % 8 || (long)k_start[s] + k_len[s] > ldv)
+      return ops_fail(T2I_ERR_SHAPE, "bf16 attention needs key starts % 8 == 0 and keys within ldv");
+    m.q_start[s] = q_start[s];
+    m.q_len[s] = q_len[s];
+    m.k_start[s] = k_start[s];
+    m.k_len[s] = k_len[s];
+    k_rows = std::max(k_rows, (long)k_start[s] + k_len[s]);
+    M = std::max(M, q_start[s] + q_len[s]);
+  }
+  if (M < 1) return ops_fail(T2I_ERR_SHAPE, "no query rows");
+  if ((size_t)2 * heads * head_dim * ldv > 0x7fffffff || (size_t)2 * (k_rows + 64) * ldk > 0x7fffffff)
+    return ops_fail(T2I_ERR_SHAPE, "bf16 attention operands exceed 2 GiB of addressing");
+  // the query projection's epilogue: softmax scale folded in, one rounding
+  Epi e = make_epi();
+  e.out = q_buf;
+  e.ldo = ldq;
+  e.qscale = attn_q_scale(head_dim);
+  e.qcols = w;
+  hipStream_t st = (hipStream_t)stream;
+  hipError_t err;
+  if (fused) {
+    const XAttnArgs xa = make_xattn(m, k, ldk, v, ldv, o, ldo);
+    err = launch_gemm_xattn((const bf16*)A, lda, (const bf16*)W, ldw, (const bf16*)bias, M, w, K, e,
+                            heads, head_dim, xa, st, true);
+    if (err == hipErrorNotSupported)
+      return ops_fail(T2I_ERR_SHAPE,
+                      "shapes outside the fused kernel (head_dim 72, K % 192 == 0, sequences "
+                      "contiguous from row 0 with lengths % 256 == 0, 16-byte aligned operands)");
+    if (err == hipSuccess)
+      err = launch_gemm_xattn((const bf16*)A, lda, (const bf16*)W, ldw, (const bf16*)bias, M, w, K,
+                              e, heads, head_dim, xa, st);
+  } else {
+    err = launch_gemm_bf16((const bf16*)A, lda, (const bf16*)W, ldw, (const bf16*)bias, M, w, K,
+                           EPI_STORE, e, nullptr, 0, st);
+    if (err == hipSuccess) {
+      attention_tiles(m, true, heads, 1);
+      err = launch_attention(true, 1, heads, head_dim, m, q_buf, ldq, k, ldk, v, ldv, o, ldo, st,
+                             true);
+    }
+  }
   if (err != hipSuccess) return ops_fail(T2I_ERR_DEVICE, hipGetErrorString(err));
   return T2I_OK;
 }

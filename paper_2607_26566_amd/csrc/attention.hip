@@ -31,6 +31,7 @@
 #include <algorithm>
 
 #include "t2i_internal.h"
+#include "xattn_tile.h"
 
 namespace t2i {
 
@@ -42,16 +43,6 @@ __device__ __forceinline__ int xcd_remap_attn(int b, int nb) {
   const int q = nb >> 3, r = nb & 7;
   const int x = b & 7, j = b >> 3;
   return (x < r ? x * (q + 1) : r * (q + 1) + (x - r) * q) + j;
-}
-
-// Key order inside a staged K tile.  The P V MFMA's B operand is the lane's
-// own probabilities: for 16-key chunk q a lane of half h holds S^T rows
-// 16q + 8a + 4h + j (a in 0..1, j in 0..3), which the MFMA consumes as k-index
-// 8h + 4a + j.  Staging key swap23(r) in K row r (bits 2 and 3 swapped) makes
-// that k-index the natural key order, so V^T tiles stay in key order and can
-// be copied to LDS unchanged.
-__device__ __forceinline__ int swap23(int r) {
-  return (r & ~12) | ((r & 4) << 1) | ((r & 8) >> 1);
 }
 
 // s_waitcnt vmcnt(N), lgkmcnt / expcnt untouched
@@ -574,18 +565,11 @@ __global__ __launch_bounds__(NW * 64, (R > 1 ? 8 : (HD <= 72 ? 16 : 12)) / NW) v
     AttnMap map, int heads, const bf16* __restrict__ Q, int ldq, const bf16* __restrict__ K,
     int ldk, const bf16* __restrict__ Vt, int ldvt, bf16* __restrict__ O, int ldo,
     float scale_log2) {
-  constexpr int BQ = NW * 32, BKV = 64;
-  constexpr int DC = (HD + 15) / 16;   // 16-wide d chunks of S^T = K Q^T
-  constexpr int DT = (HD + 31) / 32, HDO = DT * 32;
-  constexpr bool ONES = HD < HDO;
-  constexpr int CPR = HD / 8, PK = 2 * HD, NI = 2 * CPR;
-  constexpr int KRS = (CPR == 4 || CPR == 8 || CPR == 16) ? 16 / CPR : 0;
-  // V^T rows kept per stage: the data and the ones row.  The P V MFMAs also
-  // read the padding rows up to HDO - 1, which only feed O^T rows that are
-  // never used: for stage 0 they are stage 1's K rows, for stage 1 a pad.
-  constexpr int VROWS = ONES ? HD + 1 : HDO;
-  constexpr int KSTAGE = BKV * PK, VSTAGE = VROWS * 128, VPAD = (HDO - VROWS) * 128;
-  static_assert(HD % 8 == 0 && KSTAGE % 1024 == 0, "head dim");
+  using X = XTile<HD>;
+  constexpr int BQ = NW * 32, BKV = X::BKV, DC = X::DC, NI = X::NI;
+  constexpr int KSTAGE = X::KSTAGE, VSTAGE = X::VSTAGE;
+  // stage 0's V^T padding rows read stage 1's K rows, stage 1's this pad
+  constexpr int VPAD = (X::HDO - X::VROWS) * 128;
   __shared__ __attribute__((aligned(1024))) char smem[2 * (KSTAGE + VSTAGE) + VPAD];
 
   const int tid = threadIdx.x, lane = tid & 63;
@@ -603,9 +587,8 @@ __global__ __launch_bounds__(NW * 64, (R > 1 ? 8 : (HD <= 72 ? 16 : 12)) / NW) v
     return s;
   };
 
-  // K / V^T tile loads of sequence s (as in attn_bf16_kernel; keys past the
-  // sequence clamped to its last key, V^T chunks wholly past it read from the
-  // tile's first chunk)
+  // K / V^T tile loads of sequence s, the NI instructions of a tile spread
+  // over the waves
   const __amdgpu_buffer_rsrc_t rk =
       __builtin_amdgcn_make_buffer_rsrc((void*)K, 0, 0x7fffffff, kBufWord3);
   const __amdgpu_buffer_rsrc_t rv =
@@ -614,43 +597,18 @@ __global__ __launch_bounds__(NW * 64, (R > 1 ? 8 : (HD <= 72 ? 16 : 12)) / NW) v
     const int k0 = map.k_start[s], k_end = k0 + map.k_len[s];
     const int nt = (map.k_len[s] + BKV - 1) / BKV;   // 1 or 2 (the launcher checks)
     for (int t = 0; t < nt; ++t) {
-      const int kv0 = k0 + t * BKV;
 #pragma unroll
       for (int ii = 0; ii < (NI + NW - 1) / NW; ++ii) {
         const int i = wave + NW * ii;
         if (i >= NI) break;
-        if (i < CPR) {
-          const int o = i * 1024 + lane * 16, r = o / PK, slot = (o - r * PK) / 16;
-          const int c = KRS ? slot ^ ((r / KRS) & (CPR - 1)) : slot;
-          const int key = min(kv0 + swap23(r), k_end - 1);
-          __builtin_amdgcn_raw_ptr_buffer_load_lds(
-              rk, (__attribute__((address_space(3))) void*)(kst(t) + i * 1024), 16,
-              2u * (uint32_t)(key * ldk + hh * HD + c * 8), 0, 0, 0);
-        } else {
-          const int o = (i - CPR) * 1024 + lane * 16, d = o / 128;
-          const int gk = kv0 + 8 * ((lane & 7) ^ ((d >> 1) & 7));
-          __builtin_amdgcn_raw_ptr_buffer_load_lds(
-              rv, (__attribute__((address_space(3))) void*)(vst(t) + (i - CPR) * 1024), 16,
-              2u * (uint32_t)((hh * HD + d) * ldvt + (gk < k_end ? gk : kv0)), 0, 0, 0);
-        }
+        xattn_dma<HD>(rk, rv, i, k0 + t * BKV, k_end, hh, ldk, ldvt, kst(t), vst(t));
       }
     }
   };
-  // after the loads of sequence s have landed: a chunk the sequence ends
-  // inside holds bytes from beyond it; zero the columns past the sequence
-  // (their probabilities are 0)
+  // after the loads of sequence s have landed
   auto fix_ragged = [&](int s) {
-    const int k_end = map.k_start[s] + map.k_len[s];
-    if (k_end & 7) {
-      const int t = (map.k_len[s] + BKV - 1) / BKV - 1, c0 = k_end - (map.k_start[s] + t * BKV);
-      char* vb = vst(t);
-      for (int i = tid; i < HD * 64; i += NW * 64) {
-        const int d = i >> 6, col = i & 63;
-        if (col >= c0)
-          *(bf16*)(vb + d * 128 + (((col >> 3) ^ ((d >> 1) & 7)) << 4) + (col & 7) * 2) = (bf16)0.f;
-      }
-      attn_barrier();
-    }
+    const int nkeys = map.k_len[s];
+    if (xattn_fix_ragged<HD>(vst((nkeys - 1) / BKV), nkeys, tid, NW * 64)) attn_barrier();
   };
   // Q fragments of query tile t (as stored): exactly DC loads per lane, from
   // a clamped row and column, so the vmcnt thresholds below can count them;
@@ -683,8 +641,8 @@ __global__ __launch_bounds__(NW * 64, (R > 1 ? 8 : (HD <= 72 ? 16 : 12)) / NW) v
   bf16x8 qa[DC];
   if (pre) load_q(t_first + 1, qa);
   // the ones rows of both stages (the tile loads never write them)
-  if constexpr (ONES)
-    for (int i = tid; i < 2 * 64; i += NW * 64) ((bf16*)(vst(i >> 6) + HD * 128))[i & 63] = (bf16)1.f;
+  xattn_ones<HD>(vst(0), tid, NW * 64);
+  xattn_ones<HD>(vst(1), tid, NW * 64);
   if (pre) wait_vmcnt<DC>();   // all but the next tile's Q
   else wait_vmcnt<0>();
   attn_barrier();
@@ -712,104 +670,8 @@ __global__ __launch_bounds__(NW * 64, (R > 1 ? 8 : (HD <= 72 ? 16 : 12)) / NW) v
     const int s = s_cur;
     const int q_end = map.q_start[s] + map.q_len[s];
     const int qr = map.q_start[s] + (tq - map.tile_start[s]) * BQ + wave * 32 + ql;
-    const int k0 = map.k_start[s], k_end = k0 + map.k_len[s];
-    const int nt = (map.k_len[s] + BKV - 1) / BKV;
-
-    // S^T of both tiles (the first MFMA of each sum takes a zero accumulator)
-    f32x16 sc_[2][2];
-#pragma unroll
-    for (int t = 0; t < 2; ++t) {
-      if (t >= nt) break;
-#pragma unroll
-      for (int c = 0; c < DC; ++c) {
-#pragma unroll
-        for (int kb = 0; kb < 2; ++kb) {
-          const int rr = 32 * kb + ql, cc = 2 * c + hl;
-          bf16x8 kf = bf16x8{};
-          if (cc < CPR) {
-            const int slot = KRS ? cc ^ ((rr / KRS) & (CPR - 1)) : cc;
-            kf = *(const bf16x8*)(kst(t) + rr * PK + slot * 16);
-          }
-          sc_[t][kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[c],
-                                                               c == 0 ? f32x16{} : sc_[t][kb], 0, 0, 0);
-        }
-      }
-    }
-    // Element e of key block kb is key swap23(32 kb + 8 (e >> 2) + (e & 3)) + 8 hl
-    // of its tile (swap23 moves the lane-half bit 2 to bit 3): only the ragged
-    // last tile is masked, against a per-lane threshold and compile-time offsets
-    float mx = -INFINITY;
-#pragma unroll
-    for (int t = 0; t < 2; ++t) {
-      if (t >= nt) break;
-      const int valid = k_end - (k0 + t * BKV);
-      if (valid < BKV) {
-        const int thr = valid - 8 * hl;
-#pragma unroll
-        for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-          for (int e = 0; e < 16; ++e)
-            if (swap23(32 * kb + 8 * (e >> 2) + (e & 3)) >= thr) sc_[t][kb][e] = -INFINITY;
-      }
-#pragma unroll
-      for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-        for (int e = 0; e < 16; ++e) mx = fmaxf(mx, sc_[t][kb][e]);
-    }
-    mx = fmaxf(mx, __shfl_xor(mx, 32, 64));   // the query's keys sit in lanes ql and ql + 32
-    // probabilities exp2(sc * (s - mx)): a subtraction, or one fma per score
-    const float sc = QS ? 1.0f : scale_log2;
-    const float mxs = mx * sc;
-
-    // P V over both tiles; row sums from the ones row or per lane
-    f32x16 o[DT];
-    float psum = 0.f;
-#pragma unroll
-    for (int t = 0; t < 2; ++t) {
-      if (t >= nt) break;
-      const char* vb = vst(t);
-#pragma unroll
-      for (int q = 0; q < 4; ++q) {
-        bf16x8 pf;
-#pragma unroll
-        for (int e = 0; e < 8; ++e) {
-          const float x = sc_[t][q >> 1][8 * (q & 1) + e];
-          const float p = __builtin_amdgcn_exp2f(QS ? x - mx : fmaf(x, sc, -mxs));
-          if (!ONES) psum += p;
-          pf[e] = (bf16)p;
-        }
-#pragma unroll
-        for (int dt = 0; dt < DT; ++dt) {
-          const int row = dt * 32 + ql;
-          const bf16x8 vf =
-              *(const bf16x8*)(vb + row * 128 + (((2 * q + hl) ^ ((row >> 1) & 7)) << 4));
-          o[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf, pf, t == 0 && q == 0 ? f32x16{} : o[dt],
-                                                          0, 0, 0);
-        }
-      }
-    }
-    float l;
-    if (ONES) {
-      constexpr int RR = HD % 32;
-      l = __shfl(o[HD / 32][4 * (RR / 8) + (RR % 4)], ((RR % 8) / 4) * 32 + ql, 64);
-    } else {
-      l = psum + __shfl_xor(psum, 32, 64);
-    }
-    if (qr < q_end) {
-      const float inv = 1.0f / l;
-#pragma unroll
-      for (int dt = 0; dt < DT; ++dt)
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          const int d = dt * 32 + i * 8 + hl * 4;
-          if (d < HD) {
-            bf16x4 w;
-#pragma unroll
-            for (int jj = 0; jj < 4; ++jj) w[jj] = (bf16)(o[dt][4 * i + jj] * inv);
-            *(bf16x4*)(O + (size_t)qr * ldo + hh * HD + d) = w;
-          }
-        }
-    }
+    xattn_wave<HD, QS>(kst(0), kst(1), vst(0), vst(1), map.k_len[s], qf, scale_log2,
+                       qr < q_end ? O + (size_t)qr * ldo + hh * HD : nullptr);
   }
 }
 

@@ -32,7 +32,10 @@
 // lane four consecutive output columns of one row, stored with one 8-byte
 // (bf16) or 16-byte (fp32 residual) access; the split q|k|v store keeps the C
 // layout and writes V^T four tokens at a time.
+#include <algorithm>
+
 #include "t2i_internal.h"
+#include "xattn_tile.h"
 
 namespace t2i {
 
@@ -118,11 +121,18 @@ __device__ __forceinline__ void dma_epi4(const Epi& e, int m, int nb, const floa
   }
 }
 
-template <int BM, int BN, int WGM, int WGN, int ST, int KIND, int AUX>
+// No cross-attention after the projection.
+struct XNone {
+  static constexpr bool on = false;
+};
+
+// XT: XNone, or XAttnArgs for the cross-attention query projection with the
+// cross-attention fused in (256 x 144 tiles, EPI_STORE; launch_gemm_xattn)
+template <int BM, int BN, int WGM, int WGN, int ST, int KIND, int AUX, class XT>
 __global__ __launch_bounds__(64 * WGM * WGN, 1) void gemm_dma_kernel(
     const bf16* __restrict__ A, int lda, const bf16* __restrict__ W, int ldw,
     const bf16* __restrict__ bias, int M, int N, int K, Epi epi, int tiles_n, int group_m,
-    int vec_ok) {
+    int vec_ok, XT xa) {
   constexpr int NW = WGM * WGN;
   constexpr int WM = BM / WGM, WN = BN / WGN;
   constexpr int TM = WM / 16, TN = WN / 16;
@@ -252,6 +262,47 @@ __global__ __launch_bounds__(64 * WGM * WGN, 1) void gemm_dma_kernel(
       }
   }
 
+  // Cross-attention after the projection (gemm_dma_kernel with XAttnArgs): this tile's
+  // two heads (72 columns each) attend to the text of the sequence its rows
+  // belong to.  The text's K / V^T tiles go into the first XKV bytes of the
+  // ring once the last K step's barrier has passed (that step reads the last
+  // stage, the host makes K / 64 a multiple of ST), so they load under that
+  // step's MFMAs; the queries are staged at XQ_OFF after the loop.
+  constexpr int XHD = 72;
+  using XX = XTile<XHD>;
+  constexpr int XKV = 4 * (XX::KSTAGE + XX::VSTAGE);
+  constexpr int XQ_OFF = ((XKV + (XX::HDO - XX::VROWS) * 128) + 1023) / 1024 * 1024;
+  auto xk = [&](int hd, int t) { return (char*)smem + (2 * hd + t) * (XX::KSTAGE + XX::VSTAGE); };
+  auto xv = [&](int hd, int t) { return xk(hd, t) + XX::KSTAGE; };
+  int xs = 0;
+  if constexpr (XT::on) {
+    static_assert(BM == 256 && BN == 2 * XHD && WGN == 1 && (ST - 1) * STAGE * 2 >= XKV &&
+                      XQ_OFF + NW * 32 * BN * 2 <= ST * STAGE * 2,
+                  "fused cross-attention tile");
+#pragma unroll 1
+    for (int i = 1; i < xa.n; ++i) xs += (m0 >= xa.q_start[i]) ? 1 : 0;
+  }
+  auto xattn_prefetch = [&]() {
+    if constexpr (XT::on) {
+      const int nkeys = xa.k_len[xs], k0 = xa.k_start[xs];
+      const int nt = (nkeys + XX::BKV - 1) / XX::BKV;
+      const __amdgpu_buffer_rsrc_t rk =
+          __builtin_amdgcn_make_buffer_rsrc((void*)xa.K, 0, 0x7fffffff, 0x00020000);
+      const __amdgpu_buffer_rsrc_t rv =
+          __builtin_amdgcn_make_buffer_rsrc((void*)xa.Vt, 0, 0x7fffffff, 0x00020000);
+      // (head, tile, instruction) triples spread over the waves
+#pragma unroll 1
+      for (int idx = __builtin_amdgcn_readfirstlane(wave); idx < 4 * XX::NI; idx += NW) {
+        const int hd = idx / (2 * XX::NI), t = (idx / XX::NI) % 2, i = idx % XX::NI;
+        if (t < nt)
+          xattn_dma<XHD>(rk, rv, i, k0 + t * XX::BKV, k0 + nkeys, n0 / XHD + hd, xa.ldk, xa.ldvt,
+                         xk(hd, t), xv(hd, t));
+      }
+#pragma unroll
+      for (int f = 0; f < 4; ++f) xattn_ones<XHD>(xv(f >> 1, f & 1), tid, NW * 64);
+    }
+  };
+
   const int KT = K / 64;
   // The small-M tiles (fewer rows per wave, spare registers) meet at the
   // barrier for stage t + 1 halfway through stage t: the fragment reads of a
@@ -319,6 +370,7 @@ __global__ __launch_bounds__(64 * WGM * WGN, 1) void gemm_dma_kernel(
         wait_rounds<BPW>(min(ST - 2, KT - 1 - t));
         block_barrier();
         if (t + ST - 1 < KT) issue(t + ST - 1, (i + ST - 1) % ST);
+        if (XT::on && t == KT - 1) xattn_prefetch();
         compute(i);
       }
     }
@@ -331,6 +383,54 @@ __global__ __launch_bounds__(64 * WGM * WGN, 1) void gemm_dma_kernel(
       if (GATED && one_seq) *(float4*)&egate[4 * tid] = sgate;
     }
     block_barrier();
+  }
+
+  if constexpr (XT::on) {
+    // Fused cross-attention (whole tile, whole_n: the host checks).  Each
+    // wave rounds its 32 rows of queries exactly as the plain projection
+    // stores them (bias, softmax scale, one rounding to bf16) into its part
+    // of the ring, then attends with them, head by head, to the text tiles.
+    constexpr int QROW = BN * 2;   // staged query row (bytes)
+    char* const qst = (char*)smem + XQ_OFF + wave * 32 * QROW;
+#pragma unroll
+    for (int i = 0; i < TM; ++i)
+#pragma unroll
+      for (int j = 0; j < TN; ++j) {
+        const int col = j * 16 + g * 4;
+        const float4 b4 = *(const float4*)&ebias[col];
+        const float v[4] = {acc[i][j][0] + b4.x, acc[i][j][1] + b4.y, acc[i][j][2] + b4.z,
+                            acc[i][j][3] + b4.w};
+        const float qs = n0 + col < epi.qcols ? epi.qscale : 1.f;
+        bf16x4 w;
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          float y = v[r];
+          y *= qs;
+          w[r] = (bf16)y;
+        }
+        *(bf16x4*)(qst + (i * 16 + fr) * QROW + col * 2) = w;
+      }
+    wait_vmcnt<0>();   // this wave's text tile loads
+    block_barrier();
+    const int nkeys = xa.k_len[xs];
+    bool ragged = false;
+#pragma unroll
+    for (int hd = 0; hd < 2; ++hd)
+      ragged = xattn_fix_ragged<XHD>(xv(hd, (nkeys - 1) / XX::BKV), nkeys, tid, NW * 64);
+    if (ragged) block_barrier();
+    const int ql = lane & 31, hl = lane >> 5;
+#pragma unroll 1
+    for (int hd = 0; hd < 2; ++hd) {
+      bf16x8 qf[XX::DC];
+#pragma unroll
+      for (int c = 0; c < XX::DC; ++c) {
+        const int d = c * 16 + hl * 8;
+        qf[c] = d < XHD ? *(const bf16x8*)(qst + ql * QROW + (hd * XHD + d) * 2) : bf16x8{};
+      }
+      xattn_wave<XHD, true>(xk(hd, 0), xk(hd, 1), xv(hd, 0), xv(hd, 1), nkeys, qf, 1.f,
+                            xa.O + (size_t)(m0 + wave * 32 + ql) * xa.ldo + n0 + hd * XHD);
+    }
+    return;
   }
 
   if (CT) {
@@ -737,8 +837,8 @@ hipError_t gemm_dma_dispatch(const bf16* A, int lda, const bf16* W, int ldw, con
   dim3 grid(tm * tn), block(64 * WGM * WGN);
 #define T2I_DMA_CASE(K_)                                                                      \
   case K_:                                                                                    \
-    hipLaunchKernelGGL((gemm_dma_kernel<BM, BN, WGM, WGN, ST, K_, AUX>), grid, block, 0, st, A, lda, \
-                       W, ldw, bias, M, N, K, epi, tn, group_m, vec_ok);                      \
+    hipLaunchKernelGGL((gemm_dma_kernel<BM, BN, WGM, WGN, ST, K_, AUX, XNone>), grid, block, 0, st, \
+                       A, lda, W, ldw, bias, M, N, K, epi, tn, group_m, vec_ok, XNone{});     \
     break;
   switch (kind) {
     T2I_DMA_CASE(EPI_STORE)
@@ -831,6 +931,44 @@ hipError_t launch_gemm_dma(const bf16* A, int lda, const bf16* W, int ldw, const
                                                    8, st);
   return gemm_dma_dispatch<256, 128, 4, 2, 3, 1>(A, lda, W, ldw, bias, M, N, K, kind, epi, vec_ok, 8,
                                                  st);
+}
+
+// The cross-attention query projection with the cross-attention fused in
+// (gemm_dma_kernel with XAttnArgs), where the shapes fit it: head dimension 72 (a 144-
+// wide tile holds two heads), K a multiple of 3 x 64 (the text tiles load
+// during the last K step), every sequence's query rows a whole number of
+// 256-row tiles, texts of 1 .. 128 keys in one segment.  Otherwise
+// hipErrorNotSupported, launching nothing: the caller then runs the
+// projection and attn_cross_kernel separately, which give the same bits.
+// check_only: the checks alone (hipSuccess where the fused kernel applies).
+hipError_t launch_gemm_xattn(const bf16* A, int lda, const bf16* W, int ldw, const bf16* bias,
+                             int M, int N, int K, const Epi& epi, int heads, int head_dim,
+                             const XAttnArgs& xa, hipStream_t st, bool check_only) {
+  auto al = [](const void* p, int a) { return ((uintptr_t)p % a) == 0; };
+  if (head_dim != 72 || N != heads * 72 || N % 144 || M < 256 || M % 256 || K < 192 || K % 192 ||
+      lda % 8 || ldw % 8 || !al(A, 16) || !al(W, 16) || !al(bias, 8) || !al(xa.O, 8) ||
+      xa.ldo % 4 || xa.ldo < N || xa.ldk % 8 || xa.ldvt % 8 || xa.n < 1 || xa.n > kMaxSeq)
+    return hipErrorNotSupported;
+  if ((size_t)2 * M * lda >= 0x7fffffff || (size_t)2 * N * ldw >= 0x7fffffff)
+    return hipErrorNotSupported;
+  int next = 0, k_rows = 0;
+  for (int s = 0; s < xa.n; ++s) {
+    if (xa.q_start[s] != next || xa.q_len[s] <= 0 || xa.q_len[s] % 256 || xa.k_len[s] < 1 ||
+        xa.k_len[s] > 128 || xa.k_start[s] < 0 || xa.k_start[s] % 8)
+      return hipErrorNotSupported;
+    next += xa.q_len[s];
+    k_rows = std::max(k_rows, xa.k_start[s] + xa.k_len[s]);
+  }
+  if (next != M) return hipErrorNotSupported;
+  // text tile loads address K and V^T with byte offsets below 2^31
+  if ((size_t)2 * heads * head_dim * xa.ldvt > 0x7fffffff ||
+      (size_t)2 * (k_rows + 64) * xa.ldk > 0x7fffffff)
+    return hipErrorNotSupported;
+  if (check_only) return hipSuccess;
+  const int tn = N / 144, tm = M / 256;
+  hipLaunchKernelGGL((gemm_dma_kernel<256, 144, 8, 1, 3, EPI_STORE, 1, XAttnArgs>), dim3(tm * tn),
+                     dim3(512), 0, st, A, lda, W, ldw, bias, M, N, K, epi, tn, 8, 1, xa);
+  return hipGetLastError();
 }
 
 // Counter calibration: read `chunks` KB of src once through the same direct

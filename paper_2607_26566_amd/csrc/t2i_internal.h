@@ -41,6 +41,24 @@ struct AttnMap {
   int tile_start[kMaxSeq + 1];
 };
 
+// Cross-attention fused into its query projection (gemm_dma_kernel with XAttnArgs): the
+// query rows of sequence s are [q_start[s], +q_len[s]) (multiples of 256, so
+// that a 256-row tile lies in one sequence); its text is K rows
+// [k_start[s], +k_len[s]) (row-major, stride ldk, 1 .. 128 rows) and the
+// same columns of V^T (stride ldvt); the attention output goes to O (stride
+// ldo), the queries themselves are not stored.
+struct XAttnArgs {
+  static constexpr bool on = true;
+  const bf16* K;
+  int ldk;
+  const bf16* Vt;
+  int ldvt;
+  bf16* O;
+  int ldo;
+  int n;
+  int q_start[kMaxSeq], q_len[kMaxSeq], k_start[kMaxSeq], k_len[kMaxSeq];
+};
+
 // Per-request geometry for the image-side kernels.
 struct ReqMap {
   int n;                    // requests
@@ -211,6 +229,13 @@ hipError_t launch_linear_rows(const float* A, int lda, const void* W, int ldw, b
 // q_prescaled (bf16 only): Q was written multiplied by log2(e)/sqrt(head_dim)
 // (Epi::qscale), so scores come out of the MFMA in log2 units; otherwise the
 // kernel applies that scale to each score in fp32.
+// The cross-attention query projection (epi: EPI_STORE's query scaling)
+// followed in the same kernel by the cross-attention of xa; the queries are
+// not stored.  hipErrorNotSupported (nothing launched) where the shapes do
+// not fit the fused kernel; check_only: only those checks.
+hipError_t launch_gemm_xattn(const bf16* A, int lda, const bf16* W, int ldw, const bf16* bias,
+                             int M, int N, int K, const Epi& epi, int heads, int head_dim,
+                             const XAttnArgs& xa, hipStream_t st, bool check_only = false);
 hipError_t launch_attention(bool bf16_io, int role, int heads, int head_dim, const AttnMap& map,
                             const void* q, int ldq, const void* k, int ldk, const void* v,
                             int ldv, void* o, int ldo, hipStream_t st, bool q_prescaled);

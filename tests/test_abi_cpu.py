@@ -239,6 +239,24 @@ def test_op_argument_errors():
                                       0x3000, 64, 0x4000, 96, None) == 2
     assert lib.t2i_op_cross_attention(1, 2, 72, 1, qs, ql, qs, ql, None, 144, 0x2000, 144,
                                       0x3000, 64, 0x4000, 144, None) == 1
+    # query projection + cross-attention: the fused setting only where its
+    # kernel applies (checked on the host, nothing launched)
+    q256 = (C.c_int32 * 1)(256)
+    k120 = (C.c_int32 * 1)(120)
+    k129 = (C.c_int32 * 1)(129)
+    args = lambda fused, hd, qlen, klen, K, qbuf: (
+        fused, 16, hd, 1, qs, qlen, qs, klen, K, 0x10000, K, 0x20000, K, 0x30000, 0x40000,
+        16 * hd, 0x50000, 128, qbuf, 16 * hd, 0x60000, 16 * hd, None)
+    assert lib.t2i_op_linear_cross_attention(*args(2, 72, q256, k120, 1152, None)) == 1
+    assert lib.t2i_op_linear_cross_attention(*args(0, 72, q256, k120, 1152, None)) == 1
+    assert b"q_buf" in lib.t2i_ops_last_error()
+    assert lib.t2i_op_linear_cross_attention(*args(1, 72, q256, k129, 1152, None)) == 2
+    assert lib.t2i_op_linear_cross_attention(*args(1, 72, q256, k120, 1000, None)) == 2
+    assert lib.t2i_op_linear_cross_attention(*args(1, 72, ql, k120, 1152, None)) == 2
+    assert b"fused kernel" in lib.t2i_ops_last_error()
+    assert lib.t2i_op_linear_cross_attention(*args(1, 64, q256, k120, 1152, None)) == 2
+    assert lib.t2i_op_linear_cross_attention(*args(1, 72, q256, k120, 1088, None)) == 2
+    assert b"fused kernel" in lib.t2i_ops_last_error()
 
 
 @pytest.mark.parametrize("name", ["dit1024_cfg", "mmdit1024", "tiny_f32"])

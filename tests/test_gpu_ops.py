@@ -254,6 +254,66 @@ def test_cross_attention_bf16(name, H, q_lens, k_lens):
     assert row_err.max() < 3e-2
 
 
+def run_linear_cross_attention(fused, heads, d, seqs, A, W, b, k, v):
+    """The query projection + cross-attention op (bf16, V passed transposed)."""
+    lib = t2i.load()
+    n = len(seqs)
+    qs, ql, ks, kl = ((C.c_int32 * n)(*[s[i] for s in seqs]) for i in range(4))
+    w = heads * d
+    M, K = A.shape
+    ldv = (v.shape[0] + 63) // 64 * 64
+    vt = np.zeros((w, ldv), dtype=np.float32)
+    vt[:, :v.shape[0]] = v.T
+    vt[:, v.shape[0]:] = np.nan              # padding must never be read into results
+    dA, dW, db = to_dev(A, "bf16"), to_dev(W, "bf16"), to_dev(b, "bf16")
+    dk, dv = to_dev(k, "bf16"), to_dev(vt, "bf16")
+    qbuf = None if fused else torch.zeros((M, w), dtype=torch.bfloat16, device=DEV)
+    o = torch.zeros((M, w), dtype=torch.bfloat16, device=DEV)
+    st = lib.t2i_op_linear_cross_attention(
+        fused, heads, d, n, qs, ql, ks, kl, K, dA.data_ptr(), K, dW.data_ptr(), K, db.data_ptr(),
+        dk.data_ptr(), w, dv.data_ptr(), ldv, qbuf.data_ptr() if qbuf is not None else None, w,
+        o.data_ptr(), w, _stream())
+    _lib.check(st)
+    torch.cuda.synchronize()
+    return o
+
+
+# (name, heads, query lengths, text lengths, K): the 1024-px guided shape
+# (16 heads, 2 x 4096 queries, 120 text keys, K = 1152); packed sequences of
+# 256-row multiples with texts of 77 keys (a ragged last chunk), 1 key and a
+# full 128; a narrow projection with K = 192 (one pass of the 3-stage ring)
+# and one with K = 576
+XQ_CASES = [
+    ("guided-1024px", 16, [4096, 4096], [120, 120], 1152),
+    ("packed-texts", 16, [256, 512, 1024, 256], [120, 77, 1, 128], 1152),
+    ("narrow-k192", 4, [256, 768], [64, 8], 192),
+    ("k576", 2, [512], [13], 576),
+]
+
+
+@pytest.mark.parametrize("name,H,q_lens,k_lens,K", XQ_CASES, ids=[c[0] for c in XQ_CASES])
+def test_linear_cross_attention_fused_equals_two_launches(name, H, q_lens, k_lens, K):
+    """The fused query projection + cross-attention kernel gives the bits of
+    the projection and the cross-attention kernel run one after the other,
+    and both match the oracle's projection and attention."""
+    say(f"query projection + cross-attention {name}")
+    d = 72
+    seqs, nq, nk = _text_seqs(q_lens, k_lens)
+    A, W, b = rnd(50, (nq, K)), rnd(51, (H * d, K), 0.05), rnd(52, (H * d,), 0.1)
+    k, v = rnd(53, (nk, H * d)), rnd(54, (nk, H * d))
+    fused = run_linear_cross_attention(1, H, d, seqs, A, W, b, k, v)
+    two = run_linear_cross_attention(0, H, d, seqs, A, W, b, k, v)
+    assert torch.equal(fused, two)
+    q = dit.linear(A.astype(np.float64), W.astype(np.float64), b.astype(np.float64))
+    ref = attention_ref(seqs, q, k, v, H)
+    got = to_host(fused)
+    err = rel_l2(got, ref)
+    row_err = np.linalg.norm(got - ref, axis=1) / np.linalg.norm(ref, axis=1)
+    say(f"  bitwise equal to two launches; rel_l2 {err:.2e}, worst row {row_err.max():.2e}")
+    assert err < 6e-3
+    assert row_err.max() < 3e-2
+
+
 def attention_ref(seqs, q, k, v, heads):
     out = np.zeros(q.shape)
     for (q0, nq, k0, nk) in seqs:
