@@ -670,8 +670,9 @@ __global__ __launch_bounds__(NW * 64, (R > 1 ? 8 : (HD <= 72 ? 16 : 12)) / NW) v
     const int s = s_cur;
     const int q_end = map.q_start[s] + map.q_len[s];
     const int qr = map.q_start[s] + (tq - map.tile_start[s]) * BQ + wave * 32 + ql;
-    xattn_wave<HD, QS>(kst(0), kst(1), vst(0), vst(1), map.k_len[s], qf, scale_log2,
-                       qr < q_end ? O + (size_t)qr * ldo + hh * HD : nullptr);
+    bf16* const orow = O + (size_t)qr * ldo + hh * HD;
+    xattn_wave<HD, QS>(kst(0), kst(1), vst(0), vst(1), map.k_len[s], qf, scale_log2, qr < q_end,
+                       [&](int d, bf16x4 w) { *(bf16x4*)(orow + d) = w; });
   }
 }
 

@@ -427,8 +427,21 @@ __global__ __launch_bounds__(64 * WGM * WGN, 1) void gemm_dma_kernel(
         const int d = c * 16 + hl * 8;
         qf[c] = d < XHD ? *(const bf16x8*)(qst + ql * QROW + (hd * XHD + d) * 2) : bf16x8{};
       }
-      xattn_wave<XHD, true>(xk(hd, 0), xk(hd, 1), xv(hd, 0), xv(hd, 1), nkeys, qf, 1.f,
-                            xa.O + (size_t)(m0 + wave * 32 + ql) * xa.ldo + n0 + hd * XHD);
+      // the head's outputs replace its queries in the wave's rows, then go
+      // out along the rows, 16 bytes per lane (faster than the lanes' own
+      // 8-byte pieces of 32 rows); the wave's LDS accesses execute in order
+      xattn_wave<XHD, true>(xk(hd, 0), xk(hd, 1), xv(hd, 0), xv(hd, 1), nkeys, qf, 1.f, true,
+                            [&](int d, bf16x4 w) {
+                              *(bf16x4*)(qst + ql * QROW + (hd * XHD + d) * 2) = w;
+                            });
+      constexpr int CPH = XHD * 2 / 16, NCH = 32 * CPH;   // 16-byte chunks per head row, per wave
+#pragma unroll
+      for (int c0 = 0; c0 < NCH; c0 += 64) {
+        const int c = c0 + lane, row = c / CPH, ch = c - row * CPH;
+        if (NCH % 64 == 0 || c < NCH)
+          *(uint4*)(xa.O + (size_t)(m0 + wave * 32 + row) * xa.ldo + n0 + hd * XHD + ch * 8) =
+              *(const uint4*)(qst + row * QROW + hd * XHD * 2 + ch * 16);
+      }
     }
     return;
   }
@@ -946,8 +959,8 @@ hipError_t launch_gemm_xattn(const bf16* A, int lda, const bf16* W, int ldw, con
                              const XAttnArgs& xa, hipStream_t st, bool check_only) {
   auto al = [](const void* p, int a) { return ((uintptr_t)p % a) == 0; };
   if (head_dim != 72 || N != heads * 72 || N % 144 || M < 256 || M % 256 || K < 192 || K % 192 ||
-      lda % 8 || ldw % 8 || !al(A, 16) || !al(W, 16) || !al(bias, 8) || !al(xa.O, 8) ||
-      xa.ldo % 4 || xa.ldo < N || xa.ldk % 8 || xa.ldvt % 8 || xa.n < 1 || xa.n > kMaxSeq)
+      lda % 8 || ldw % 8 || !al(A, 16) || !al(W, 16) || !al(bias, 8) || !al(xa.O, 16) ||
+      xa.ldo % 8 || xa.ldo < N || xa.ldk % 8 || xa.ldvt % 8 || xa.n < 1 || xa.n > kMaxSeq)
     return hipErrorNotSupported;
   if ((size_t)2 * M * lda >= 0x7fffffff || (size_t)2 * N * ldw >= 0x7fffffff)
     return hipErrorNotSupported;

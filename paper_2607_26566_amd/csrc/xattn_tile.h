@@ -100,13 +100,13 @@ __device__ __forceinline__ bool xattn_fix_ragged(char* vt, int nkeys, int tid, i
 // the B operand of S^T = K Q^T (d = 16c + 8hl .. +7, zero past HD).  All
 // scores are computed first and the softmax takes the exact row maximum;
 // probabilities exp2(sc (s - max)), sc = 1 for a pre-scaled Q (QS), else
-// scale_log2.  orow: the query's output row (head_dim values), or nullptr
-// for a lane whose query lies outside the sequence.
-template <int HD, bool QS>
+// scale_log2.  Lanes whose query lies inside the sequence (valid) hand
+// their output, four consecutive values d .. d+3 at a time, to out(d, w).
+template <int HD, bool QS, class Out>
 __device__ __forceinline__ void xattn_wave(const char* k0, const char* k1, const char* v0,
                                            const char* v1, int nkeys,
                                            const bf16x8 (&qf)[XTile<HD>::DC], float scale_log2,
-                                           bf16* orow) {
+                                           bool valid, Out&& out) {
   using X = XTile<HD>;
   constexpr int DC = X::DC, DT = X::DT, CPR = X::CPR, PK = X::PK, KRS = X::KRS;
   const int lane = threadIdx.x & 63, ql = lane & 31, hl = lane >> 5;
@@ -194,7 +194,7 @@ __device__ __forceinline__ void xattn_wave(const char* k0, const char* k1, const
   } else {
     l = psum + __shfl_xor(psum, 32, 64);
   }
-  if (orow) {
+  if (valid) {
     const float inv = 1.0f / l;
 #pragma unroll
     for (int dt = 0; dt < DT; ++dt)
@@ -205,7 +205,7 @@ __device__ __forceinline__ void xattn_wave(const char* k0, const char* k1, const
           bf16x4 w;
 #pragma unroll
           for (int jj = 0; jj < 4; ++jj) w[jj] = (bf16)(o[dt][4 * i + jj] * inv);
-          *(bf16x4*)(orow + d) = w;
+          out(d, w);
         }
       }
   }
