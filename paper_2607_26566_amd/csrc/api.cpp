@@ -714,13 +714,17 @@ t2i_status run_blocks_cross(t2i_dit* h, const Plan& P, int nb, hipStream_t st) {
     const char* kv = h->at<char>(h->L.kv) + (size_t)b * txt_rows_max * 2 * D * A;
     if (bf) {
       // one kernel for the query projection and the cross-attention where
-      // the shapes fit it (same bits as the two launches below)
+      // the shapes fit it (same bits as the two launches below) and the
+      // projection would run on 256-row tiles anyway (from 2048 rows; below,
+      // the narrower tiles of the separate projection keep more CUs busy:
+      // the 512-px model's 1024 rows make 32 fused workgroups)
       const bf16* vtt = h->at<bf16>(h->L.vtt) + (size_t)b * D * h->L.ldvt_txt;
       const XAttnArgs xa = make_xattn(P.cross, kv, D, vtt, h->L.ldvt_txt, o, D);
       const bf16* wq = (const bf16*)h->w[wb + X_XQ];
       const bf16* bq = (const bf16*)h->w[wb + X_XQ + 1];
-      if (launch_gemm_xattn(xb, D, wq, D, bq, R, D, D, e, c.heads, c.head_dim, xa, st, true) ==
-          hipSuccess) {
+      if (R >= 2048 &&
+          launch_gemm_xattn(xb, D, wq, D, bq, R, D, D, e, c.heads, c.head_dim, xa, st, true) ==
+              hipSuccess) {
         TIMED(h, T2I_K_GEMM_XQ, st,
               launch_gemm_xattn(xb, D, wq, D, bq, R, D, D, e, c.heads, c.head_dim, xa, st));
       } else {
