@@ -40,7 +40,7 @@ WORKLOAD = "dit1024_cfg"
 # blank lines removed, see code_digest): reported only while the code is
 # unchanged.
 MEASURED_TRAFFIC = {
-    ("dit1024_cfg", "attn_self"): (107.1e6, "paper_2607_26566_amd/csrc/attention.hip", "a913cdae73da4790"),
+    ("dit1024_cfg", "attn_self"): (107.1e6, "paper_2607_26566_amd/csrc/attention.hip", "bc062e227b23bc04"),
 }
 
 
