@@ -262,8 +262,8 @@ __global__ __launch_bounds__(64 * WGM * WGN, 1) void gemm_dma_kernel(
       }
   }
 
-  // Cross-attention after the projection (gemm_dma_kernel with XAttnArgs): this tile's
-  // two heads (72 columns each) attend to the text of the sequence its rows
+  // Cross-attention after the projection (XT = XAttnArgs): this tile's two
+  // heads (72 columns each) attend to the text of the sequence its rows
   // belong to.  The text's K / V^T tiles go into the first XKV bytes of the
   // ring once the last K step's barrier has passed (that step reads the last
   // stage, the host makes K / 64 a multiple of ST), so they load under that
@@ -947,10 +947,11 @@ hipError_t launch_gemm_dma(const bf16* A, int lda, const bf16* W, int ldw, const
 }
 
 // The cross-attention query projection with the cross-attention fused in
-// (gemm_dma_kernel with XAttnArgs), where the shapes fit it: head dimension 72 (a 144-
-// wide tile holds two heads), K a multiple of 3 x 64 (the text tiles load
-// during the last K step), every sequence's query rows a whole number of
-// 256-row tiles, texts of 1 .. 128 keys in one segment.  Otherwise
+// (gemm_dma_kernel with XAttnArgs), where the shapes fit it: head dimension
+// 72 (a 144-wide tile holds two heads), K a multiple of 3 x 64 (the text
+// tiles load during the last K step), every sequence's query rows a whole
+// number of 256-row tiles, texts of 1 .. 128 keys within V^T's row length,
+// 16-byte aligned operands.  Otherwise
 // hipErrorNotSupported, launching nothing: the caller then runs the
 // projection and attn_cross_kernel separately, which give the same bits.
 // check_only: the checks alone (hipSuccess where the fused kernel applies).
@@ -960,14 +961,16 @@ hipError_t launch_gemm_xattn(const bf16* A, int lda, const bf16* W, int ldw, con
   auto al = [](const void* p, int a) { return ((uintptr_t)p % a) == 0; };
   if (head_dim != 72 || N != heads * 72 || N % 144 || M < 256 || M % 256 || K < 192 || K % 192 ||
       lda % 8 || ldw % 8 || !al(A, 16) || !al(W, 16) || !al(bias, 8) || !al(xa.O, 16) ||
-      xa.ldo % 8 || xa.ldo < N || xa.ldk % 8 || xa.ldvt % 8 || xa.n < 1 || xa.n > kMaxSeq)
+      !al(xa.K, 16) || !al(xa.Vt, 16) || xa.ldo % 8 || xa.ldo < N || xa.ldk < N || xa.ldk % 8 ||
+      xa.ldvt % 8 || xa.n < 1 || xa.n > kMaxSeq)
     return hipErrorNotSupported;
   if ((size_t)2 * M * lda >= 0x7fffffff || (size_t)2 * N * ldw >= 0x7fffffff)
     return hipErrorNotSupported;
   int next = 0, k_rows = 0;
   for (int s = 0; s < xa.n; ++s) {
     if (xa.q_start[s] != next || xa.q_len[s] <= 0 || xa.q_len[s] % 256 || xa.k_len[s] < 1 ||
-        xa.k_len[s] > 128 || xa.k_start[s] < 0 || xa.k_start[s] % 8)
+        xa.k_len[s] > 128 || xa.k_start[s] < 0 || xa.k_start[s] % 8 ||
+        xa.k_start[s] + xa.k_len[s] > xa.ldvt)
       return hipErrorNotSupported;
     next += xa.q_len[s];
     k_rows = std::max(k_rows, xa.k_start[s] + xa.k_len[s]);
