@@ -74,10 +74,12 @@ t2i_status t2i_op_attention(int32_t dtype, int32_t heads, int32_t head_dim,
  * Cross-attention of image queries to their request's text (Sec. 4's model
  * `forward`, the DiT block's attention to the caption): the operation of
  * t2i_op_attention with one key segment per sequence, bf16 only (else
- * T2I_ERR_INVALID_ARG), run by the kernels the model uses for it -- texts
- * of at most 128 keys (k_len 1..128) by the two-tile kernel that keeps them
- * in LDS across query tiles, longer texts by the pipelined one.  Arguments,
- * layouts (V given transposed) and limits are those of t2i_op_attention.
+ * T2I_ERR_INVALID_ARG), run by the kernels the model uses for it where it
+ * does not fuse it into the query projection (t2i_op_linear_cross_attention)
+ * -- texts of at most 128 keys (k_len 1..128) by the two-tile kernel that
+ * keeps them in LDS across query tiles, longer texts by the pipelined one.
+ * Arguments, layouts (V given transposed) and limits are those of
+ * t2i_op_attention.
  */
 t2i_status t2i_op_cross_attention(int32_t dtype, int32_t heads, int32_t head_dim,
                                   int32_t n_seq, const int32_t* q_start,
