@@ -105,7 +105,7 @@ t2i_status t2i_op_cross_attention(int32_t dtype, int32_t heads, int32_t head_dim
  *   reads them: two launches.
  * fused = 1: one kernel; the queries never leave the chip (q_buf unused, may
  *   be NULL).  Needs head_dim 72, K % 192 == 0, sequences contiguous from
- *   row 0 whose lengths are multiples of 256, 16-byte aligned A, W and o,
+ *   row 0 whose lengths are multiples of 256, 16-byte aligned A, W, K, V and o,
  *   8-byte aligned bias, else T2I_ERR_SHAPE.  Both settings give the
  *   same bits; the model takes the fused one wherever it applies.
  */
