@@ -107,7 +107,8 @@ t2i_status t2i_op_cross_attention(int32_t dtype, int32_t heads, int32_t head_dim
  *   be NULL).  Needs head_dim 72, K % 192 == 0, sequences contiguous from
  *   row 0 whose lengths are multiples of 256, 16-byte aligned A, W, K, V and o,
  *   8-byte aligned bias, else T2I_ERR_SHAPE.  Both settings give the
- *   same bits; the model takes the fused one wherever it applies.
+ *   same bits; the model takes the fused one from 2048 rows wherever it
+ *   applies.
  */
 t2i_status t2i_op_linear_cross_attention(int32_t fused, int32_t heads, int32_t head_dim,
                                          int32_t n_seq, const int32_t* q_start,
