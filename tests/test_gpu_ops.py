@@ -441,6 +441,53 @@ def test_attention_bf16_eight_wave_pipeline_edges(d):
     assert err < 6e-3
 
 
+@pytest.mark.parametrize("d", [64, 72])
+def test_attention_bf16_packed_sequences_equal_each_alone(d):
+    """16 heads, 11 sequences packed into one launch of 512 eight-wave
+    workgroups.  Query counts give odd and even tile counts and ragged query
+    tails (one query in a last tile); key counts run from 1 to 460 (ragged,
+    single tile, several tiles); a second call splits the keys into two
+    segments.  A sequence run on its own (a launch of two-wave workgroups,
+    too few tiles to fill the chip with eight) gives the same bits, since a
+    query's arithmetic does not depend on the workgroup size or on the other
+    sequences of the launch."""
+    H = 16
+    q_lens = [600, 513, 1024, 256, 300, 777, 512, 1000, 260, 900, 520]
+    k_lens = [1, 63, 130, 200, 64, 333, 460, 65, 8, 129, 256]
+    q_starts = np.cumsum([0] + q_lens[:-1]).tolist()
+    nq = sum(q_lens)
+    starts, nk = _packed_keys(k_lens)
+    q = rnd(70 + d, (nq, H * d))
+    k, v = rnd(71 + d, (nk, H * d)), rnd(72 + d, (nk, H * d))
+    seqs = [(q_starts[i], q_lens[i], starts[i], k_lens[i]) for i in range(len(q_lens))]
+    say(f"attention bf16 packed sequences d={d}")
+    got = run_attention(_lib.T2I_BF16, H, d, seqs, q, k, v)
+    err = rel_l2(got, attention_ref(seqs, q, k, v, H))
+    say(f"  one segment rel_l2 {err:.2e}")
+    assert err < 6e-3
+    for i in (0, 1, 5, 9):
+        q0, n_q, k0, n_k = seqs[i]
+        alone = run_attention(_lib.T2I_BF16, H, d, [(0, n_q, k0, n_k)], q[q0:q0 + n_q], k, v)
+        assert np.array_equal(alone, got[q0:q0 + n_q]), i
+    n1 = [1, 40, 65, 100, 129, 7, 200, 64, 33, 250, 8]
+    n2 = [64, 100, 1, 13, 129, 300, 70, 192, 1, 210, 56]
+    st1, tot1 = _packed_keys(n1)
+    st2, tot2 = _packed_keys(n2)
+    k = rnd(73 + d, (tot1 + tot2, H * d))
+    v = rnd(74 + d, (tot1 + tot2, H * d))
+    seqs = [(q_starts[i], q_lens[i], st1[i], n1[i]) for i in range(len(q_lens))]
+    seg2 = [(tot1 + st2[i], n2[i]) for i in range(len(q_lens))]
+    got = run_attention(_lib.T2I_BF16, H, d, seqs, q, k, v, seg2)
+    ref = np.zeros(q.shape)
+    for (q0, n_q, k0, n_k), (k20, n_k2) in zip(seqs, seg2):
+        idx = np.r_[np.arange(k0, k0 + n_k), np.arange(k20, k20 + n_k2)]
+        ref[q0:q0 + n_q] = dit.attention(q[q0:q0 + n_q].astype(np.float64),
+                                         k[idx].astype(np.float64), v[idx].astype(np.float64), H)
+    err = rel_l2(got, ref)
+    say(f"  two segments rel_l2 {err:.2e}")
+    assert err < 6e-3
+
+
 JOINT_CASES = [
     # (name, H, d, [(q_start, q_len, k_start, k_len)], [(k2_start, k2_len)], nq, nk)
     ("txt+img", 2, 128, [(0, 64, 0, 64), (64, 256, 0, 64)], [(64, 256), (64, 256)], 320, 320),
