@@ -539,6 +539,31 @@ def test_ln_modulate(dtype, rows, D):
     assert rel_l2(to_host(out), ref) < (3e-3 if dtype == 1 else 1e-6)
 
 
+def test_ln_modulate_bf16_row_count_does_not_change_bits():
+    """Width 1152, bf16: launches of 1 .. 4104 rows (two rows per wave, odd
+    counts leaving a wave one row) give the same bits on the same rows: a
+    row's result does not depend on the batch; the rows match the oracle."""
+    lib = t2i.load()
+    D, rows = 1152, 4104
+    x = rnd(42, (rows, D), bf=False) * 2 + 0.5
+    mod = rnd(43, (2, D), 0.3, bf=False)
+    dx = torch.from_numpy(x.astype(np.float32)).to(DEV)
+    dm = torch.from_numpy(mod.astype(np.float32)).to(DEV)
+
+    def run(n):
+        out = torch.zeros((n, D), dtype=torch.bfloat16, device=DEV)
+        _lib.check(lib.t2i_op_ln_modulate(1, n, D, dx.data_ptr(), dm.data_ptr(),
+                                          dm.data_ptr() + 4 * D, 1e-6, out.data_ptr(), _stream()))
+        torch.cuda.synchronize()
+        return out
+
+    big = run(rows)
+    for n in (1, 255, 1024, 4095):
+        assert torch.equal(run(n), big[:n]), n
+    ref = dit.modulate(dit.layer_norm(x.astype(np.float64), 1e-6), mod[0], mod[1])
+    assert rel_l2(to_host(big), ref) < 3e-3
+
+
 @pytest.mark.parametrize("dtype,n_out,n_in,rank", [(1, 3072, 3072, 64), (1, 1152, 4608, 16),
                                                     (1, 1000, 1160, 40), (1, 77, 304, 128),
                                                     (1, 77, 300, 128), (0, 200, 130, 8)])
